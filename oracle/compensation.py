@@ -1,0 +1,52 @@
+"""Low-overhead compensation (oracle, fp64) -- Sec. IV-C.
+
+Test infrastructure only; see the package docstring.
+
+Step 1 masks every expert outside A_trans; step 2 takes a top-k of what is
+left, so the weight of pruned experts moves onto experts that are executed
+anyway.  Reading taken: a token keeps every expert of its own K_t that
+survived pruning, and only the freed slots are refilled, from A_trans minus
+K_t, best router key first (ties to the lower index), with no group limit.
+This keeps a layer without pruning identical to the plain layer, and never
+drops a token's expert whose gate weight reached the threshold.  When
+A_trans has fewer than k experts the token gets fewer than k (padded with
+id -1, weight 0).  Final weights are the router scores renormalised over
+K_final and multiplied by the routed scaling factor, so the gate mass is
+conserved.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+
+def compensate_token(key: np.ndarray, s: np.ndarray, orig_ids, trans: np.ndarray,
+                     k: int, routed_scaling: float):
+    """Return (ids, w) for one token: K_final in rank order (key desc, index
+    asc) and w_e = routed_scaling * s_e / sum_{K_final} s (float64)."""
+    orig = list(orig_ids)
+    keep = [e for e in orig if trans[e]]
+    pool = [e for e in np.flatnonzero(trans).tolist() if e not in orig]
+    pool.sort(key=lambda e: (-float(key[e]), e))
+    refill = pool[:max(0, k - len(keep))]
+    final = sorted(keep + refill, key=lambda e: (-float(key[e]), e))
+    total = 0.0
+    for e in final:
+        total += float(s[e])
+    w = [float(routed_scaling) * (float(s[e]) / total) for e in final]
+    return final, w, len(refill)
+
+
+def compensate_batch(keys: np.ndarray, s: np.ndarray, orig_ids: np.ndarray,
+                     trans: np.ndarray, k: int, routed_scaling: float):
+    """Compensation for every token.  Returns (ids [T][k] int, -1 padded;
+    w [T][k] float64, 0 padded; total refilled slots)."""
+    T = orig_ids.shape[0]
+    ids = -np.ones((T, k), dtype=np.int64)
+    w = np.zeros((T, k), dtype=np.float64)
+    n_refill = 0
+    for t in range(T):
+        fid, fw, nr = compensate_token(keys[t], s[t], orig_ids[t], trans, k, routed_scaling)
+        ids[t, :len(fid)] = fid
+        w[t, :len(fw)] = fw
+        n_refill += nr
+    return ids, w, n_refill

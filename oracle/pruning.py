@@ -1,0 +1,104 @@
+"""Cost-aware pruning (oracle, fp64) -- Sec. IV-B, steps 1-4, using the
+layer cost of Sec. IV-A.
+
+Test infrastructure only; see the package docstring.
+
+Cost model (Sec. IV-A): each expert e placed on device d costs R(e,d)*C(e,d);
+the layer cost is the maximum over devices of the summed cost of its active
+experts.  Here the product R*C is one non-negative number per expert,
+``cost[e]`` (0 for an expert that is already resident), and devices are
+``n_bins`` bins given by ``bins[e]`` (None: one bin).
+
+Readings taken where the paper is silent or inconsistent:
+  * importance I(e) is the largest normalised gate weight that any token of
+    the batch gives e (the paper leaves I(e) open in Sec. IV-B and uses other
+    definitions in Sec. V; this one makes "no expert whose gate weight reaches
+    the threshold is pruned" hold token by token);
+  * the candidate set is the activated experts that are not mandatory (the
+    text writes the complement in all experts, but the final set must lie in
+    the activated set);
+  * every token's own top expert is mandatory, so no token loses all its
+    experts;
+  * expansion visits candidates by importance, highest first, ties to the
+    lower index, and keeps F_base fixed at its step-2 value while bin loads
+    grow; "does not increase above F_base" is tested as load + cost <= F_base.
+Bin sums are float64 additions in a fixed order: ascending expert index for
+the step-2 loads, visiting order for the expansion.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+
+def importance_max(orig_ids: np.ndarray, g: np.ndarray, E: int):
+    """A_act = union of the tokens' K_t; I(e) = max over tokens t with
+    e in K_t of G(t)_e (0 for inactive experts).  Also returns each token's
+    top expert (largest G, ties to the lower index)."""
+    act = np.zeros(E, dtype=bool)
+    imp = np.zeros(E, dtype=np.float64)
+    top1 = []
+    for t in range(orig_ids.shape[0]):
+        best_e, best_g = None, None
+        for e, gv in zip(orig_ids[t].tolist(), g[t].tolist()):
+            act[e] = True
+            imp[e] = max(imp[e], gv)
+            if best_g is None or gv > best_g or (gv == best_g and e < best_e):
+                best_e, best_g = e, gv
+        top1.append(best_e)
+    return act, imp, top1
+
+
+def mandatory_split(act: np.ndarray, imp: np.ndarray, tau: float, top1):
+    """Step 1: A_must = {e in A_act : I(e) >= tau} plus each token's top
+    expert; A_cand = A_act minus A_must."""
+    must = act & (imp >= float(tau))
+    for e in top1:
+        must[e] = True
+    cand = act & ~must
+    return must, cand
+
+
+def bin_loads(member: np.ndarray, cost: np.ndarray, bins, n_bins: int) -> np.ndarray:
+    """Per-bin load: sum over e in ``member`` placed in bin b of cost[e],
+    added in ascending e (float64)."""
+    loads = np.zeros(n_bins, dtype=np.float64)
+    for e in range(member.shape[0]):
+        if member[e]:
+            b = 0 if bins is None else int(bins[e])
+            loads[b] = loads[b] + float(cost[e])
+    return loads
+
+
+def cost_aware_greedy(must: np.ndarray, cand: np.ndarray, imp: np.ndarray,
+                      cost: np.ndarray, bins, n_bins: int):
+    """Steps 2-4.  F_base = max_b load_b(A_must).  Each candidate, in
+    (importance desc, index asc) order, is promoted iff the load of its bin
+    plus its cost stays <= F_base; the bin load then grows by its cost.
+    Returns (trans, promoted, must_loads, final_loads, F_base, order)."""
+    must_loads = bin_loads(must, cost, bins, n_bins)
+    f_base = float(must_loads.max()) if n_bins > 0 else 0.0
+    loads = must_loads.copy()
+    order = sorted(np.flatnonzero(cand).tolist(), key=lambda e: (-float(imp[e]), e))
+    promoted = np.zeros_like(must)
+    for e in order:
+        b = 0 if bins is None else int(bins[e])
+        if loads[b] + float(cost[e]) <= f_base:
+            promoted[e] = True
+            loads[b] = loads[b] + float(cost[e])
+    trans = must | promoted
+    return trans, promoted, must_loads, loads, f_base, order
+
+
+def prune_batch(orig_ids: np.ndarray, g: np.ndarray, E: int, tau: float,
+                cost: np.ndarray, bins, n_bins: int) -> dict:
+    """Steps 1-4 for a routed batch.  Returns every set as a bool[E] mask
+    plus the loads and F_base."""
+    act, imp, top1 = importance_max(orig_ids, g, E)
+    must, cand = mandatory_split(act, imp, tau, top1)
+    trans, promoted, must_loads, final_loads, f_base, order = cost_aware_greedy(
+        must, cand, imp, cost, bins, n_bins)
+    return dict(act=act, imp=imp, top1=top1, must=must, cand=cand,
+                promoted=promoted, trans=trans, pruned=act & ~trans,
+                act_loads=bin_loads(act, cost, bins, n_bins),
+                must_loads=must_loads, trans_loads=final_loads,
+                f_base=f_base, cand_order=order)

@@ -1,0 +1,146 @@
+"""Pins for the oracle's cost-aware pruning (Sec. IV-B): a hand-computed
+example, the paper's literal expansion test re-evaluated from scratch,
+invariants and special cases."""
+import math
+
+import numpy as np
+import pytest
+
+from oracle import cost_aware_greedy, mandatory_split, prune_batch, route_batch
+
+
+def _mask(E, ids):
+    m = np.zeros(E, dtype=bool)
+    m[list(ids)] = True
+    return m
+
+
+def test_hand_example(golden):
+    g = golden("greedy_hand_example.json")
+    E = g["E"]
+    act = _mask(E, g["act"])
+    imp = np.array(g["importance"])
+    cost = np.array(g["cost"], dtype=np.float32)
+    bins = np.array(g["bins"], dtype=np.int32)
+    must, cand = mandatory_split(act, imp, g["tau"], [])
+    assert np.flatnonzero(must).tolist() == g["expected_must"]
+    trans, promoted, must_loads, loads, f_base, order = cost_aware_greedy(
+        must, cand, imp, cost, bins, g["n_bins"])
+    assert must_loads.tolist() == g["expected_must_loads"]
+    assert f_base == g["expected_f_base"]
+    assert order == g["expected_order"]
+    assert np.flatnonzero(promoted).tolist() == g["expected_promoted"]
+    assert np.flatnonzero(trans).tolist() == g["expected_trans"]
+    assert np.flatnonzero(act & ~trans).tolist() == g["expected_pruned"]
+    assert loads.tolist() == g["expected_final_loads"]
+    trans1, *_ = cost_aware_greedy(must, cand, imp, cost, None, 1)
+    assert np.flatnonzero(trans1).tolist() == g["expected_trans_one_bin"]
+
+
+def _literal_expansion(must, cand, imp, cost, bins, n_bins):
+    """The expansion test as the paper writes it, recomputed from the sets
+    each time with exact sums: promote e iff max over devices of the summed
+    cost of (A_must + {e}) on that device equals F_base."""
+    def f_cost(members):
+        per = [[] for _ in range(n_bins)]
+        for e in np.flatnonzero(members):
+            per[0 if bins is None else bins[e]].append(float(cost[e]))
+        return max(math.fsum(p) for p in per)
+    cur = must.copy()
+    f_base = f_cost(cur)
+    for e in sorted(np.flatnonzero(cand), key=lambda e: (-imp[e], e)):
+        trial = cur.copy()
+        trial[e] = True
+        if f_cost(trial) == f_base:
+            cur = trial
+    return cur, f_base
+
+
+def _random_batch(rng, T, E, G, tg, k):
+    logits = rng.standard_normal((T, E)).astype(np.float32)
+    return route_batch(logits, None, G, tg, k)
+
+
+@pytest.mark.parametrize("seed", range(6))
+@pytest.mark.parametrize("n_bins", [1, 2, 4])
+def test_literal_form_and_invariants(seed, n_bins):
+    rng = np.random.default_rng(seed)
+    E = 16
+    s, keys, ids, g = _random_batch(rng, 12, E, 4, 2, 4)
+    # integer costs: every sum is exact, so the literal form is unambiguous
+    cost = rng.integers(0, 9, E).astype(np.float32)
+    bins = None if n_bins == 1 else (np.arange(E) // (E // n_bins)).astype(np.int32)
+    tau = [0.0, 0.15, 0.2, 0.3][seed % 4]
+    pr = prune_batch(ids, g, E, tau, cost, bins, n_bins)
+    lit, f_base = _literal_expansion(pr["must"], pr["cand"], pr["imp"], cost, bins, n_bins)
+    assert np.array_equal(lit, pr["trans"])
+    assert f_base == pr["f_base"]
+    act, must, trans = pr["act"], pr["must"], pr["trans"]
+    assert np.all(must <= trans) and np.all(trans <= act)
+    assert pr["trans_loads"].max() == pr["f_base"]
+    for e in np.flatnonzero(pr["pruned"]):
+        b = 0 if bins is None else bins[e]
+        assert pr["trans_loads"][b] + cost[e] > pr["f_base"]
+    # no expert whose gate weight reaches tau is pruned
+    for t in range(ids.shape[0]):
+        for e, gv in zip(ids[t], g[t]):
+            if gv >= tau:
+                assert trans[e]
+
+
+def test_special_cases():
+    rng = np.random.default_rng(7)
+    E = 16
+    s, keys, ids, g = _random_batch(rng, 10, E, 4, 2, 4)
+    cost = rng.uniform(1, 5, E).astype(np.float32)
+    bins = (np.arange(E) // 4).astype(np.int32)
+    # tau = 0 prunes nothing
+    assert not prune_batch(ids, g, E, 0.0, cost, bins, 4)["pruned"].any()
+    # all experts resident prunes nothing
+    assert not prune_batch(ids, g, E, 0.5, np.zeros(E, np.float32), bins, 4)["pruned"].any()
+    # one bin: only zero-cost candidates survive
+    c2 = cost.copy()
+    c2[::3] = 0
+    pr = prune_batch(ids, g, E, 0.3, c2, None, 1)
+    assert np.array_equal(pr["promoted"], pr["cand"] & (c2 == 0))
+    # uniform cost with one bin is plain threshold pruning
+    pr = prune_batch(ids, g, E, 0.3, np.full(E, 3.0, np.float32), None, 1)
+    assert np.array_equal(pr["pruned"], pr["cand"])
+    # scaling every cost by a power of two changes no decision
+    base = prune_batch(ids, g, E, 0.3, cost, bins, 4)
+    for j in (-7, 3, 20):
+        sc = prune_batch(ids, g, E, 0.3, (cost * np.float32(2.0 ** j)).astype(np.float32), bins, 4)
+        assert np.array_equal(sc["trans"], base["trans"])
+
+
+def test_top1_always_kept():
+    rng = np.random.default_rng(8)
+    E = 16
+    s, keys, ids, g = _random_batch(rng, 6, E, 4, 2, 4)
+    pr = prune_batch(ids, g, E, 2.0, np.ones(E, np.float32), None, 1)   # tau above any weight
+    for t in range(6):
+        assert pr["trans"][ids[t][int(np.argmax(g[t]))]]
+    assert np.array_equal(pr["must"], _mask(E, pr["top1"]))
+
+
+def test_loads_exact_under_dynamic_range():
+    # fp32 costs whose max/min ratio stays below 2^20 sum exactly in float64,
+    # so the fixed-order loads equal the exactly rounded sums.
+    rng = np.random.default_rng(9)
+    cost = (rng.uniform(0.56, 26.9, 256) * 88080384).astype(np.float32)
+    member = rng.random(256) < 0.7
+    from oracle import bin_loads
+    bins = (np.arange(256) // 32).astype(np.int32)
+    loads = bin_loads(member, cost, bins, 8)
+    for b in range(8):
+        sel = [float(cost[e]) for e in range(256) if member[e] and bins[e] == b]
+        assert loads[b] == math.fsum(sel)
+
+
+def test_threshold_is_inclusive():
+    # Sec. IV-B step 1: importance at or above the threshold is mandatory
+    act = np.ones(4, dtype=bool)
+    imp = np.array([0.25, 0.125, 0.5, 0.0625])
+    must, cand = mandatory_split(act, imp, 0.125, [])
+    assert must.tolist() == [True, True, True, False]
+    assert cand.tolist() == [False, False, False, True]
