@@ -1,0 +1,183 @@
+/*
+ * caee.h -- C ABI of the Cost-Aware Expert Execution (CAEE) MoE-layer
+ * library for AMD Instinct MI355X (gfx950).
+ *
+ * One MoE layer per call, following "Beyond Uniform Experts: Cost-Aware
+ * Expert Execution for Efficient Multi-Device MoE Inference" (arxiv
+ * 2606.29982):
+ *   1. router scores and group-limited top-k K_t per token (Sec. II-A);
+ *   2. cost-aware pruning of the activated set A_act into A_trans:
+ *      importance threshold, baseline cost F_base as the maximum over bins
+ *      (devices) of the summed expert cost, cost-invariant expansion
+ *      (Sec. IV-A cost model, Sec. IV-B steps 1-4);
+ *   3. compensation: pruned experts are masked and each token's freed slots
+ *      are re-filled from A_trans (Sec. IV-C), weights renormalised;
+ *   4. the surviving experts (plus shared experts) run as a grouped SwiGLU
+ *      FFN and their outputs are combined with the gate weights (the MoE
+ *      output equation of Sec. II-A).
+ *
+ * Conventions shared by every entry point
+ *   - Every tensor pointer is caller-owned DEVICE memory (hipMalloc'd or a
+ *     torch CUDA tensor), row-major and densely packed, 16-byte aligned.
+ *     Sizes are in elements unless stated.  The library allocates no device
+ *     memory: scratch space comes from the caller's workspace `ws`.
+ *   - Calls are asynchronous on `stream` (a hipStream_t; NULL = the null
+ *     stream).  Inputs must stay valid and unmodified, and outputs must not
+ *     be read, until the stream has reached the end of the call.
+ *   - All arguments are validated on the host before anything is launched.
+ *     On any error nothing is launched, outputs are untouched, and
+ *     caee_last_error() returns a message for the calling thread.
+ *   - Device contents cannot be checked on the host.  Preconditions that
+ *     the caller must guarantee: logits, bias and costs are finite; costs
+ *     are >= 0; bin[e] is in [0, n_bins).  Violations give unspecified
+ *     (but memory-safe) results.
+ *   - Decisions (selection, importance threshold, cost comparisons) are
+ *     computed in float64, ties going to the lower expert or group index,
+ *     so results are deterministic and independent of launch shape.
+ */
+#ifndef CAEE_H
+#define CAEE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define CAEE_ABI_VERSION 1
+
+typedef enum caee_status {
+    CAEE_OK = 0,
+    CAEE_ERR_INVALID_ARG = 1,  /* bad descriptor field, NULL or misaligned pointer */
+    CAEE_ERR_UNSUPPORTED = 2,  /* well-formed but outside this build's limits */
+    CAEE_ERR_WORKSPACE = 3,    /* ws NULL or ws_bytes < caee_workspace_size() */
+    CAEE_ERR_HIP = 4           /* a HIP runtime call or a kernel launch failed */
+} caee_status_t;
+
+typedef enum caee_dtype {
+    CAEE_F32 = 0,       /* IEEE binary32 */
+    CAEE_BF16 = 1,      /* bfloat16 */
+    CAEE_FP8_E4M3 = 2   /* OCP FP8 E4M3 (max 448), used with fp32 block scales */
+} caee_dtype_t;
+
+typedef enum caee_importance {
+    /* I(e) = largest normalised gate weight any token of the batch gives e.
+     * Sec. IV-B leaves I(e) open; with this choice no (token, expert) pair
+     * whose gate weight reaches tau is pruned. */
+    CAEE_IMPORTANCE_MAX = 0
+} caee_importance_t;
+
+/* Shape and hyper-parameters of one MoE layer call. */
+typedef struct caee_layer_desc {
+    int32_t T;            /* tokens in the batch, >= 0 (0: the call does nothing) */
+    int32_t d;            /* hidden size, multiple of 128 */
+    int32_t f;            /* expert intermediate size, multiple of 128 */
+    int32_t E;            /* routed experts, 1..256 */
+    int32_t n_group;      /* expert groups (group g = experts [g*E/n_group, (g+1)*E/n_group)) */
+    int32_t topk_group;   /* groups kept per token, 1..n_group */
+    int32_t k;            /* experts per token, 1..16 and <= topk_group*E/n_group */
+    int32_t n_shared;     /* shared experts added to every token with weight 1, 0..4 */
+    float routed_scaling; /* factor on the renormalised routed weights, finite and > 0 */
+    float tau;            /* importance threshold theta of Sec. IV-B, finite and >= 0; 0 disables pruning */
+    int32_t n_bins;       /* devices/links of the max-aggregated layer cost (Sec. IV-A), 1..256 */
+    int32_t importance;   /* caee_importance_t */
+    int32_t x_dtype;      /* hidden-state dtype: CAEE_F32 with f32 weights, else CAEE_BF16 */
+    int32_t w_dtype;      /* expert weight dtype: CAEE_F32, CAEE_BF16 or CAEE_FP8_E4M3 */
+    int32_t y_dtype;      /* output dtype: CAEE_F32 or CAEE_BF16 */
+} caee_layer_desc_t;
+
+/* Expert weights.  Expert e's gate and up matrices are stacked as
+ * w13[e] = [W1; W3] of shape [2f][d], its down matrix is w2[e] of shape
+ * [d][f]; both K-contiguous (each row is one output feature).  The expert
+ * computes W2 (silu(W1 x) * (W3 x)).
+ * FP8: w13/w2 hold E4M3 codes and *_scale hold one fp32 scale per 128x128
+ * block, w13_scale [E][2f/128][d/128] and w2_scale [E][d/128][f/128]; the
+ * weight is code * scale.  *_scale must be NULL for other dtypes.
+ * The shared experts use the same layout with n_shared in place of E. */
+typedef struct caee_expert_weights {
+    const void* w13;            /* [E][2f][d] */
+    const void* w2;             /* [E][d][f] */
+    const float* w13_scale;     /* FP8 only */
+    const float* w2_scale;      /* FP8 only */
+    const void* sh_w13;         /* [n_shared][2f][d], NULL iff n_shared == 0 */
+    const void* sh_w2;          /* [n_shared][d][f] */
+    const float* sh_w13_scale;  /* FP8 only */
+    const float* sh_w2_scale;   /* FP8 only */
+} caee_expert_weights_t;
+
+/* Routing results, all caller-owned device memory.  Lists are in rank order
+ * (router key s+bias descending, expert index ascending). */
+typedef struct caee_route_out {
+    int32_t* topk_ids;   /* [T][k] K_final after compensation; -1 in unused slots (required) */
+    float* topk_w;       /* [T][k] routed_scaling * s_e / sum_{K_final} s; 0 in unused slots (required) */
+    int32_t* orig_ids;   /* [T][k] K_t before pruning (optional, may be NULL) */
+    uint32_t* masks;     /* [4][ceil(E/32)] bitmaps A_act, A_must, A_trans, pruned; bit e%32 of word e/32 (optional) */
+    int32_t* stats;      /* [8] |A_act|, |A_must|, |A_cand|, promoted, pruned, |A_trans|,
+                            refilled slots, empty slots (optional) */
+    double* bin_loads;   /* [3][n_bins] per-bin summed cost of A_act, of A_must (max = F_base)
+                            and of A_trans (optional) */
+} caee_route_out_t;
+
+/* Bytes of workspace the three compute entry points need for `desc`
+ * (the same value serves all three).  Host-only, launches nothing. */
+caee_status_t caee_workspace_size(const caee_layer_desc_t* desc, size_t* bytes);
+
+/* Routing, cost-aware pruning and compensation (Sec. II-A, IV-B, IV-C).
+ *   logits [T][E] fp32 router logits; bias [E] fp32 selection bias or NULL;
+ *   cost [E] fp32 per-expert cost R(e)*C(e) of Sec. IV-A (0 = resident);
+ *   bin [E] int32 bin of each expert, NULL = all experts in bin 0
+ *   (then n_bins must be 1).
+ * Writes `out`.  `ws` must hold caee_workspace_size() bytes. */
+caee_status_t caee_route_prune(const caee_layer_desc_t* desc, const float* logits,
+                               const float* bias, const float* cost, const int32_t* bin,
+                               const caee_route_out_t* out, void* ws, size_t ws_bytes,
+                               void* stream);
+
+/* Grouped SwiGLU expert FFN and weighted combine (Sec. II-A output
+ * equation): y_t = sum_j topk_w[t][j] * E_{topk_ids[t][j]}(x_t) + sum_s E^sh_s(x_t).
+ *   x [T][d] (x_dtype); topk_ids/topk_w [T][k] as written by
+ *   caee_route_prune (an id outside [0,E) marks an empty slot and its
+ *   weight is ignored); y [T][d] (y_dtype), fully overwritten. */
+caee_status_t caee_expert_ffn(const caee_layer_desc_t* desc, const void* x,
+                              const int32_t* topk_ids, const float* topk_w,
+                              const caee_expert_weights_t* weights, void* y,
+                              void* ws, size_t ws_bytes, void* stream);
+
+/* The whole layer: caee_route_prune followed by caee_expert_ffn, without
+ * leaving the device.  `out` may be NULL (routing results then live in the
+ * workspace only); if given, it is filled as by caee_route_prune. */
+caee_status_t caee_moe_layer(const caee_layer_desc_t* desc, const void* x,
+                             const float* logits, const float* bias, const float* cost,
+                             const int32_t* bin, const caee_expert_weights_t* weights,
+                             void* y, const caee_route_out_t* out, void* ws,
+                             size_t ws_bytes, void* stream);
+
+/* Static description of a status code. */
+const char* caee_status_str(caee_status_t status);
+/* Message of the last error raised on the calling thread ("" if none). */
+const char* caee_last_error(void);
+/* CAEE_ABI_VERSION of the built library. */
+int caee_abi_version(void);
+
+/* Opt-in per-kernel timing.  While enabled, every kernel the library
+ * launches is bracketed by HIP events recorded on the caller's stream.
+ * caee_timing_query waits for the recorded events and returns, for kernel
+ * kind `kind`, the summed duration in milliseconds and the number of
+ * launches since the last reset.  Process-wide state, not thread-safe. */
+typedef enum caee_kernel_kind {
+    CAEE_KERNEL_ROUTE = 0,    /* routing + pruning + compensation + permutation */
+    CAEE_KERNEL_GATE_UP = 1,  /* expert gate/up products and SwiGLU */
+    CAEE_KERNEL_DOWN = 2,     /* expert down products */
+    CAEE_KERNEL_COMBINE = 3,  /* weighted combine into y */
+    CAEE_KERNEL_KINDS = 4
+} caee_kernel_kind_t;
+caee_status_t caee_timing_enable(int on);
+caee_status_t caee_timing_reset(void);
+caee_status_t caee_timing_query(int kind, double* total_ms, int64_t* launches);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CAEE_H */

@@ -1,0 +1,216 @@
+"""ctypes binding of the CAEE C ABI (include/caee.h).
+
+Argument marshalling only: every step of the layer runs in the HIP kernels
+of ``libcaee.so``.  Tensors are torch CUDA tensors (device memory); the
+current torch stream of the tensors' device is passed to the library.
+Importing this module fails loudly when the library has not been built.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Optional
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libcaee.so")
+
+CAEE_OK, CAEE_ERR_INVALID_ARG, CAEE_ERR_UNSUPPORTED, CAEE_ERR_WORKSPACE, CAEE_ERR_HIP = range(5)
+CAEE_F32, CAEE_BF16, CAEE_FP8_E4M3 = 0, 1, 2
+KERNEL_KINDS = {"route": 0, "gate_up": 1, "down": 2, "combine": 3}
+DTYPE_CODE = {"f32": CAEE_F32, "bf16": CAEE_BF16, "fp8": CAEE_FP8_E4M3}
+
+
+class CaeeError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"caee status {status}: {message}")
+        self.status = status
+
+
+class LayerDesc(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in
+                ("T", "d", "f", "E", "n_group", "topk_group", "k", "n_shared")] + [
+        ("routed_scaling", ctypes.c_float), ("tau", ctypes.c_float),
+        ("n_bins", ctypes.c_int32), ("importance", ctypes.c_int32),
+        ("x_dtype", ctypes.c_int32), ("w_dtype", ctypes.c_int32), ("y_dtype", ctypes.c_int32)]
+
+
+class ExpertWeights(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in
+                ("w13", "w2", "w13_scale", "w2_scale", "sh_w13", "sh_w2", "sh_w13_scale", "sh_w2_scale")]
+
+
+class RouteOut(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in
+                ("topk_ids", "topk_w", "orig_ids", "masks", "stats", "bin_loads")]
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
+                          "(python -c 'import __graft_entry__ as g; g.build()')")
+    lib = ctypes.CDLL(LIB_PATH)
+    st = ctypes.c_int
+    P = ctypes.c_void_p
+    desc_p = ctypes.POINTER(LayerDesc)
+    sig = {
+        "caee_workspace_size": (st, [desc_p, ctypes.POINTER(ctypes.c_size_t)]),
+        "caee_route_prune": (st, [desc_p, P, P, P, P, ctypes.POINTER(RouteOut), P, ctypes.c_size_t, P]),
+        "caee_expert_ffn": (st, [desc_p, P, P, P, ctypes.POINTER(ExpertWeights), P, P, ctypes.c_size_t, P]),
+        "caee_moe_layer": (st, [desc_p, P, P, P, P, P, ctypes.POINTER(ExpertWeights), P,
+                                ctypes.POINTER(RouteOut), P, ctypes.c_size_t, P]),
+        "caee_status_str": (ctypes.c_char_p, [st]),
+        "caee_last_error": (ctypes.c_char_p, []),
+        "caee_abi_version": (ctypes.c_int, []),
+        "caee_timing_enable": (st, [ctypes.c_int]),
+        "caee_timing_reset": (st, []),
+        "caee_timing_query": (st, [ctypes.c_int, ctypes.POINTER(ctypes.c_double),
+                                   ctypes.POINTER(ctypes.c_int64)]),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    return lib
+
+
+lib = _load()
+EXPORTED = ("caee_workspace_size", "caee_route_prune", "caee_expert_ffn", "caee_moe_layer",
+            "caee_status_str", "caee_last_error", "caee_abi_version", "caee_timing_enable",
+            "caee_timing_reset", "caee_timing_query")
+
+
+def _check(status: int):
+    if status != CAEE_OK:
+        raise CaeeError(status, lib.caee_last_error().decode())
+
+
+def abi_version() -> int:
+    return lib.caee_abi_version()
+
+
+@dataclass
+class Layer:
+    """Descriptor fields of one MoE layer call (see caee_layer_desc_t)."""
+
+    T: int
+    d: int
+    f: int
+    E: int
+    n_group: int
+    topk_group: int
+    k: int
+    n_shared: int
+    routed_scaling: float
+    tau: float = 0.0
+    n_bins: int = 1
+    w_dtype: str = "bf16"
+    x_dtype: str = "bf16"
+    y_dtype: str = "bf16"
+
+    def desc(self) -> LayerDesc:
+        return LayerDesc(self.T, self.d, self.f, self.E, self.n_group, self.topk_group, self.k,
+                         self.n_shared, self.routed_scaling, self.tau, self.n_bins, 0,
+                         DTYPE_CODE[self.x_dtype], DTYPE_CODE[self.w_dtype], DTYPE_CODE[self.y_dtype])
+
+    @classmethod
+    def from_shape(cls, shape, **over) -> "Layer":
+        kw = dict(T=shape.T, d=shape.d, f=shape.f, E=shape.E, n_group=shape.n_group,
+                  topk_group=shape.topk_group, k=shape.k, n_shared=shape.n_shared,
+                  routed_scaling=shape.routed_scaling, tau=shape.tau, n_bins=shape.n_bins,
+                  w_dtype=shape.w_dtype, x_dtype=shape.x_dtype, y_dtype=shape.y_dtype)
+        kw.update(over)
+        return cls(**kw)
+
+
+def workspace_size(layer: Layer) -> int:
+    n = ctypes.c_size_t(0)
+    d = layer.desc()
+    _check(lib.caee_workspace_size(ctypes.byref(d), ctypes.byref(n)))
+    return int(n.value)
+
+
+def _ptr(t) -> Optional[int]:
+    return None if t is None else int(t.data_ptr())
+
+
+def _stream(*tensors) -> Optional[int]:
+    import torch
+    for t in tensors:
+        if t is not None:
+            return int(torch.cuda.current_stream(t.device).cuda_stream)
+    return None
+
+
+def _weights(w: dict) -> ExpertWeights:
+    g = lambda n: _ptr(w.get(n))  # noqa: E731
+    return ExpertWeights(g("w13"), g("w2"), g("w13_scale"), g("w2_scale"),
+                         g("sh_w13"), g("sh_w2"), g("sh_w13_scale"), g("sh_w2_scale"))
+
+
+def _route_out(out: Optional[dict]) -> Optional[RouteOut]:
+    if out is None:
+        return None
+    g = lambda n: _ptr(out.get(n))  # noqa: E731
+    return RouteOut(g("topk_ids"), g("topk_w"), g("orig_ids"), g("masks"), g("stats"), g("bin_loads"))
+
+
+def alloc_workspace(layer: Layer, device):
+    import torch
+    return torch.empty(max(workspace_size(layer), 256), dtype=torch.uint8, device=device)
+
+
+def alloc_route_out(layer: Layer, device, full: bool = True) -> dict:
+    """Device buffers for the routing results of ``layer``."""
+    import torch
+    T, k = layer.T, layer.k
+    out = {"topk_ids": torch.empty((T, k), dtype=torch.int32, device=device),
+           "topk_w": torch.empty((T, k), dtype=torch.float32, device=device)}
+    if full:
+        words = (layer.E + 31) // 32
+        out["orig_ids"] = torch.empty((T, k), dtype=torch.int32, device=device)
+        out["masks"] = torch.empty((4, words), dtype=torch.int32, device=device)
+        out["stats"] = torch.empty(8, dtype=torch.int32, device=device)
+        out["bin_loads"] = torch.empty((3, layer.n_bins), dtype=torch.float64, device=device)
+    return out
+
+
+def route_prune(layer: Layer, logits, bias, cost, bins, out: dict, ws) -> dict:
+    d = layer.desc()
+    ro = _route_out(out)
+    _check(lib.caee_route_prune(ctypes.byref(d), _ptr(logits), _ptr(bias), _ptr(cost), _ptr(bins),
+                                ctypes.byref(ro), _ptr(ws), ws.numel(), _stream(logits)))
+    return out
+
+
+def expert_ffn(layer: Layer, x, topk_ids, topk_w, weights: dict, y, ws):
+    d = layer.desc()
+    w = _weights(weights)
+    _check(lib.caee_expert_ffn(ctypes.byref(d), _ptr(x), _ptr(topk_ids), _ptr(topk_w), ctypes.byref(w),
+                               _ptr(y), _ptr(ws), ws.numel(), _stream(x)))
+    return y
+
+
+def moe_layer(layer: Layer, x, logits, bias, cost, bins, weights: dict, y, ws, out: Optional[dict] = None):
+    d = layer.desc()
+    w = _weights(weights)
+    ro = _route_out(out)
+    _check(lib.caee_moe_layer(ctypes.byref(d), _ptr(x), _ptr(logits), _ptr(bias), _ptr(cost), _ptr(bins),
+                              ctypes.byref(w), _ptr(y), None if ro is None else ctypes.byref(ro),
+                              _ptr(ws), ws.numel(), _stream(x)))
+    return y
+
+
+def timing_enable(on: bool = True):
+    _check(lib.caee_timing_enable(1 if on else 0))
+
+
+def timing_reset():
+    _check(lib.caee_timing_reset())
+
+
+def timing_query(kind: str):
+    ms = ctypes.c_double(0)
+    n = ctypes.c_int64(0)
+    _check(lib.caee_timing_query(KERNEL_KINDS[kind], ctypes.byref(ms), ctypes.byref(n)))
+    return float(ms.value), int(n.value)

@@ -1,0 +1,406 @@
+// Host side of the CAEE C ABI: argument validation, workspace carving,
+// launch order and opt-in per-kernel timing.  No device memory is allocated
+// here; every buffer is the caller's.
+#include <math.h>
+
+#include <cstdarg>
+#include <cstdio>
+#include <string>
+#include <vector>
+
+#include "caee_internal.h"
+
+namespace caee {
+
+namespace {
+
+thread_local std::string g_last_error;
+
+caee_status_t fail(caee_status_t st, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+    return st;
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+int experts_per_lane(int E) { return E <= 64 ? 1 : E <= 128 ? 2 : 4; }
+
+caee_status_t check_desc(const caee_layer_desc_t* d) {
+    if (!d) return fail(CAEE_ERR_INVALID_ARG, "desc is NULL");
+    if (d->T < 0) return fail(CAEE_ERR_INVALID_ARG, "T=%d must be >= 0", d->T);
+    if (d->d <= 0 || d->d % 128) return fail(CAEE_ERR_INVALID_ARG, "d=%d must be a positive multiple of 128", d->d);
+    if (d->f <= 0 || d->f % 128) return fail(CAEE_ERR_INVALID_ARG, "f=%d must be a positive multiple of 128", d->f);
+    if (d->E < 1 || d->E > kMaxE) return fail(CAEE_ERR_INVALID_ARG, "E=%d must be in [1, %d]", d->E, kMaxE);
+    if (d->n_group < 1 || d->E % d->n_group)
+        return fail(CAEE_ERR_INVALID_ARG, "n_group=%d must divide E=%d", d->n_group, d->E);
+    if (d->topk_group < 1 || d->topk_group > d->n_group)
+        return fail(CAEE_ERR_INVALID_ARG, "topk_group=%d must be in [1, n_group=%d]", d->topk_group, d->n_group);
+    const int gsize = d->E / d->n_group;
+    if (d->k < 1 || d->k > kMaxK || d->k > d->topk_group * gsize)
+        return fail(CAEE_ERR_INVALID_ARG, "k=%d must be in [1, min(%d, topk_group*E/n_group=%d)]", d->k, kMaxK,
+                    d->topk_group * gsize);
+    if (d->n_shared < 0 || d->n_shared > kMaxShared)
+        return fail(CAEE_ERR_INVALID_ARG, "n_shared=%d must be in [0, %d]", d->n_shared, kMaxShared);
+    if (!(isfinite(d->routed_scaling) && d->routed_scaling > 0.0f))
+        return fail(CAEE_ERR_INVALID_ARG, "routed_scaling must be finite and > 0");
+    if (!(isfinite(d->tau) && d->tau >= 0.0f)) return fail(CAEE_ERR_INVALID_ARG, "tau must be finite and >= 0");
+    if (d->n_bins < 1 || d->n_bins > kMaxBins)
+        return fail(CAEE_ERR_INVALID_ARG, "n_bins=%d must be in [1, %d]", d->n_bins, kMaxBins);
+    if (d->importance != CAEE_IMPORTANCE_MAX) return fail(CAEE_ERR_INVALID_ARG, "unknown importance=%d", d->importance);
+    if (d->w_dtype != CAEE_F32 && d->w_dtype != CAEE_BF16 && d->w_dtype != CAEE_FP8_E4M3)
+        return fail(CAEE_ERR_INVALID_ARG, "unknown w_dtype=%d", d->w_dtype);
+    const int want_x = d->w_dtype == CAEE_F32 ? CAEE_F32 : CAEE_BF16;
+    if (d->x_dtype != want_x)
+        return fail(CAEE_ERR_INVALID_ARG, "x_dtype=%d does not match w_dtype=%d (f32 weights take f32 x, "
+                    "bf16/fp8 weights take bf16 x)", d->x_dtype, d->w_dtype);
+    if (d->y_dtype != CAEE_F32 && d->y_dtype != CAEE_BF16)
+        return fail(CAEE_ERR_INVALID_ARG, "y_dtype=%d must be CAEE_F32 or CAEE_BF16", d->y_dtype);
+    // Limits of this build.
+    const int epl = experts_per_lane(d->E);
+    const int lpg = gsize / epl;
+    if (d->E % epl || gsize % epl || (lpg & (lpg - 1)))
+        return fail(CAEE_ERR_UNSUPPORTED, "E=%d with %d experts per group needs the group size to be a "
+                    "multiple of %d with a power-of-two quotient", d->E, gsize, epl);
+    if (d->T > kFusedMaxT) return fail(CAEE_ERR_UNSUPPORTED, "T=%d exceeds %d", d->T, kFusedMaxT);
+    if (d->w_dtype == CAEE_FP8_E4M3) return fail(CAEE_ERR_UNSUPPORTED, "fp8 weights are not built yet");
+    return CAEE_OK;
+}
+
+caee_status_t check_ptr(const void* p, const char* name, bool required) {
+    if (!p) return required ? fail(CAEE_ERR_INVALID_ARG, "%s is NULL", name) : CAEE_OK;
+    if (!aligned16(p)) return fail(CAEE_ERR_INVALID_ARG, "%s is not 16-byte aligned", name);
+    return CAEE_OK;
+}
+
+#define CAEE_TRY(expr)                          \
+    do {                                        \
+        caee_status_t st_ = (expr);             \
+        if (st_ != CAEE_OK) return st_;         \
+    } while (0)
+
+caee_status_t check_ws(const caee_layer_desc_t* d, void* ws, size_t ws_bytes, WsLayout* L) {
+    *L = ws_layout(*d);
+    if (!ws) return fail(CAEE_ERR_WORKSPACE, "workspace is NULL");
+    if (((uintptr_t)ws & 255u) != 0) return fail(CAEE_ERR_WORKSPACE, "workspace is not 256-byte aligned");
+    if (ws_bytes < L->total)
+        return fail(CAEE_ERR_WORKSPACE, "workspace has %zu bytes, %zu needed", ws_bytes, L->total);
+    return CAEE_OK;
+}
+
+caee_status_t check_route_inputs(const caee_layer_desc_t* d, const float* logits, const float* bias,
+                                 const float* cost, const int32_t* bin) {
+    CAEE_TRY(check_ptr(logits, "logits", true));
+    CAEE_TRY(check_ptr(bias, "bias", false));
+    CAEE_TRY(check_ptr(cost, "cost", true));
+    CAEE_TRY(check_ptr(bin, "bin", false));
+    if (!bin && d->n_bins != 1) return fail(CAEE_ERR_INVALID_ARG, "bin is NULL but n_bins=%d", d->n_bins);
+    return CAEE_OK;
+}
+
+caee_status_t check_route_out(const caee_route_out_t* out) {
+    if (!out) return fail(CAEE_ERR_INVALID_ARG, "out is NULL");
+    CAEE_TRY(check_ptr(out->topk_ids, "out->topk_ids", true));
+    CAEE_TRY(check_ptr(out->topk_w, "out->topk_w", true));
+    CAEE_TRY(check_ptr(out->orig_ids, "out->orig_ids", false));
+    CAEE_TRY(check_ptr(out->masks, "out->masks", false));
+    CAEE_TRY(check_ptr(out->stats, "out->stats", false));
+    CAEE_TRY(check_ptr(out->bin_loads, "out->bin_loads", false));
+    return CAEE_OK;
+}
+
+caee_status_t check_weights(const caee_layer_desc_t* d, const caee_expert_weights_t* w) {
+    if (!w) return fail(CAEE_ERR_INVALID_ARG, "weights is NULL");
+    const bool fp8 = d->w_dtype == CAEE_FP8_E4M3;
+    const bool sh = d->n_shared > 0;
+    CAEE_TRY(check_ptr(w->w13, "weights->w13", true));
+    CAEE_TRY(check_ptr(w->w2, "weights->w2", true));
+    CAEE_TRY(check_ptr(w->sh_w13, "weights->sh_w13", sh));
+    CAEE_TRY(check_ptr(w->sh_w2, "weights->sh_w2", sh));
+    if (!sh && (w->sh_w13 || w->sh_w2)) return fail(CAEE_ERR_INVALID_ARG, "shared weights given with n_shared=0");
+    CAEE_TRY(check_ptr(w->w13_scale, "weights->w13_scale", fp8));
+    CAEE_TRY(check_ptr(w->w2_scale, "weights->w2_scale", fp8));
+    CAEE_TRY(check_ptr(w->sh_w13_scale, "weights->sh_w13_scale", fp8 && sh));
+    CAEE_TRY(check_ptr(w->sh_w2_scale, "weights->sh_w2_scale", fp8 && sh));
+    if (!fp8 && (w->w13_scale || w->w2_scale || w->sh_w13_scale || w->sh_w2_scale))
+        return fail(CAEE_ERR_INVALID_ARG, "block scales given for non-fp8 weights");
+    return CAEE_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Opt-in timing: events bracket each launch on the caller's stream.
+struct TimingRec {
+    int kind;
+    hipEvent_t a, b;
+};
+struct Timing {
+    bool on = false;
+    std::vector<TimingRec> pending;
+    std::vector<hipEvent_t> pool;
+    double total_ms[CAEE_KERNEL_KINDS] = {};
+    int64_t launches[CAEE_KERNEL_KINDS] = {};
+};
+Timing& timing() {
+    static Timing t;
+    return t;
+}
+
+hipEvent_t take_event() {
+    Timing& tm = timing();
+    if (!tm.pool.empty()) {
+        hipEvent_t e = tm.pool.back();
+        tm.pool.pop_back();
+        return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
+}
+
+// Runs one launch, bracketed by timing events when timing is on.
+template <class F>
+caee_status_t timed_launch(int kind, hipStream_t s, const char* what, F&& launch) {
+    Timing& tm = timing();
+    hipEvent_t a = nullptr, b = nullptr;
+    bool timed = false;
+    if (tm.on) {
+        a = take_event();
+        b = take_event();
+        timed = a && b && hipEventRecord(a, s) == hipSuccess;
+    }
+    const hipError_t err = launch();
+    if (err != hipSuccess) return fail(CAEE_ERR_HIP, "%s launch failed: %s", what, hipGetErrorString(err));
+    if (timed && hipEventRecord(b, s) == hipSuccess) {
+        tm.pending.push_back({kind, a, b});
+    } else {
+        if (a) tm.pool.push_back(a);
+        if (b) tm.pool.push_back(b);
+    }
+    return CAEE_OK;
+}
+
+hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
+
+RouteParams make_route_params(const caee_layer_desc_t* d, const float* logits, const float* bias,
+                              const float* cost, const int32_t* bin, char* ws, const WsLayout& L) {
+    RouteParams p{};
+    p.T = d->T;
+    p.E = d->E;
+    p.n_group = d->n_group;
+    p.topk_group = d->topk_group;
+    p.k = d->k;
+    p.n_shared = d->n_shared;
+    p.n_bins = d->n_bins;
+    p.epl = experts_per_lane(d->E);
+    p.gsize = d->E / d->n_group;
+    p.lpg = p.gsize / p.epl;
+    p.rs = (double)d->routed_scaling;
+    p.tau = (double)d->tau;
+    p.logits = logits;
+    p.bias = bias;
+    p.cost = cost;
+    p.bin = bin;
+    p.perm_off = (int32_t*)(ws + L.perm_off);
+    p.perm_tok = (int32_t*)(ws + L.perm_tok);
+    p.perm_pos = (int32_t*)(ws + L.perm_pos);
+    p.chunks = (int32_t*)(ws + L.chunks);
+    p.n_chunks = (int32_t*)(ws + L.n_chunks);
+    return p;
+}
+
+caee_status_t run_ffn(const caee_layer_desc_t* d, const void* x, const int32_t* ids, const float* w,
+                      const caee_expert_weights_t* W, void* y, char* ws, const WsLayout& L, hipStream_t s) {
+    FfnParams p{};
+    p.T = d->T;
+    p.d = d->d;
+    p.f = d->f;
+    p.E = d->E;
+    p.k = d->k;
+    p.n_shared = d->n_shared;
+    p.x = x;
+    p.w13 = W->w13;
+    p.w2 = W->w2;
+    p.sh_w13 = W->sh_w13;
+    p.sh_w2 = W->sh_w2;
+    p.w13_scale = W->w13_scale;
+    p.w2_scale = W->w2_scale;
+    p.sh_w13_scale = W->sh_w13_scale;
+    p.sh_w2_scale = W->sh_w2_scale;
+    p.perm_tok = (const int32_t*)(ws + L.perm_tok);
+    p.perm_pos = (const int32_t*)(ws + L.perm_pos);
+    p.chunks = (const int32_t*)(ws + L.chunks);
+    p.n_chunks = (const int32_t*)(ws + L.n_chunks);
+    p.topk_ids = ids;
+    p.topk_w = w;
+    p.h = ws + L.h;
+    p.yperm = (float*)(ws + L.y);
+    p.y = y;
+    p.y_bf16 = d->y_dtype == CAEE_BF16;
+    CAEE_TRY(timed_launch(CAEE_KERNEL_GATE_UP, s, "gate/up",
+                          [&] { return launch_gate_up(p, d->w_dtype, L.max_chunks, s); }));
+    CAEE_TRY(timed_launch(CAEE_KERNEL_DOWN, s, "down", [&] { return launch_down(p, d->w_dtype, L.max_chunks, s); }));
+    CAEE_TRY(timed_launch(CAEE_KERNEL_COMBINE, s, "combine", [&] { return launch_combine(p, s); }));
+    return CAEE_OK;
+}
+
+}  // namespace
+
+int device_cu_count() {
+    static int cached[64] = {};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+    if (!cached[dev]) {
+        int n = 0;
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+        cached[dev] = n;
+    }
+    return cached[dev];
+}
+
+}  // namespace caee
+
+using namespace caee;
+
+extern "C" {
+
+caee_status_t caee_workspace_size(const caee_layer_desc_t* desc, size_t* bytes) {
+    g_last_error.clear();
+    if (!bytes) return fail(CAEE_ERR_INVALID_ARG, "bytes is NULL");
+    CAEE_TRY(check_desc(desc));
+    *bytes = ws_layout(*desc).total;
+    return CAEE_OK;
+}
+
+caee_status_t caee_route_prune(const caee_layer_desc_t* desc, const float* logits, const float* bias,
+                               const float* cost, const int32_t* bin, const caee_route_out_t* out, void* ws,
+                               size_t ws_bytes, void* stream) {
+    g_last_error.clear();
+    CAEE_TRY(check_desc(desc));
+    CAEE_TRY(check_route_inputs(desc, logits, bias, cost, bin));
+    CAEE_TRY(check_route_out(out));
+    WsLayout L;
+    CAEE_TRY(check_ws(desc, ws, ws_bytes, &L));
+    if (desc->T == 0) return CAEE_OK;
+    RouteParams p = make_route_params(desc, logits, bias, cost, bin, (char*)ws, L);
+    p.topk_ids = out->topk_ids;
+    p.topk_w = out->topk_w;
+    p.orig_ids = out->orig_ids;
+    p.masks = out->masks;
+    p.stats = out->stats;
+    p.bin_loads = out->bin_loads;
+    p.do_route = 1;
+    p.do_permute = 0;
+    hipStream_t s = as_stream(stream);
+    return timed_launch(CAEE_KERNEL_ROUTE, s, "route", [&] { return launch_route(p, s); });
+}
+
+caee_status_t caee_expert_ffn(const caee_layer_desc_t* desc, const void* x, const int32_t* topk_ids,
+                              const float* topk_w, const caee_expert_weights_t* weights, void* y, void* ws,
+                              size_t ws_bytes, void* stream) {
+    g_last_error.clear();
+    CAEE_TRY(check_desc(desc));
+    CAEE_TRY(check_ptr(x, "x", true));
+    CAEE_TRY(check_ptr(topk_ids, "topk_ids", true));
+    CAEE_TRY(check_ptr(topk_w, "topk_w", true));
+    CAEE_TRY(check_weights(desc, weights));
+    CAEE_TRY(check_ptr(y, "y", true));
+    WsLayout L;
+    CAEE_TRY(check_ws(desc, ws, ws_bytes, &L));
+    if (desc->T == 0) return CAEE_OK;
+    RouteParams p = make_route_params(desc, nullptr, nullptr, nullptr, nullptr, (char*)ws, L);
+    p.topk_ids = const_cast<int32_t*>(topk_ids);
+    p.do_route = 0;
+    p.do_permute = 1;
+    hipStream_t s = as_stream(stream);
+    CAEE_TRY(timed_launch(CAEE_KERNEL_ROUTE, s, "permute", [&] { return launch_route(p, s); }));
+    return run_ffn(desc, x, topk_ids, topk_w, weights, y, (char*)ws, L, s);
+}
+
+caee_status_t caee_moe_layer(const caee_layer_desc_t* desc, const void* x, const float* logits, const float* bias,
+                             const float* cost, const int32_t* bin, const caee_expert_weights_t* weights, void* y,
+                             const caee_route_out_t* out, void* ws, size_t ws_bytes, void* stream) {
+    g_last_error.clear();
+    CAEE_TRY(check_desc(desc));
+    CAEE_TRY(check_ptr(x, "x", true));
+    CAEE_TRY(check_route_inputs(desc, logits, bias, cost, bin));
+    if (out) CAEE_TRY(check_route_out(out));
+    CAEE_TRY(check_weights(desc, weights));
+    CAEE_TRY(check_ptr(y, "y", true));
+    WsLayout L;
+    CAEE_TRY(check_ws(desc, ws, ws_bytes, &L));
+    if (desc->T == 0) return CAEE_OK;
+    char* wsb = (char*)ws;
+    RouteParams p = make_route_params(desc, logits, bias, cost, bin, wsb, L);
+    p.topk_ids = out ? out->topk_ids : (int32_t*)(wsb + L.ids);
+    p.topk_w = out ? out->topk_w : (float*)(wsb + L.w);
+    p.orig_ids = out ? out->orig_ids : nullptr;
+    p.masks = out ? out->masks : nullptr;
+    p.stats = out ? out->stats : nullptr;
+    p.bin_loads = out ? out->bin_loads : nullptr;
+    p.do_route = 1;
+    p.do_permute = 1;
+    hipStream_t s = as_stream(stream);
+    CAEE_TRY(timed_launch(CAEE_KERNEL_ROUTE, s, "route", [&] { return launch_route(p, s); }));
+    return run_ffn(desc, x, p.topk_ids, p.topk_w, weights, y, wsb, L, s);
+}
+
+const char* caee_status_str(caee_status_t status) {
+    switch (status) {
+        case CAEE_OK: return "ok";
+        case CAEE_ERR_INVALID_ARG: return "invalid argument";
+        case CAEE_ERR_UNSUPPORTED: return "unsupported by this build";
+        case CAEE_ERR_WORKSPACE: return "workspace missing or too small";
+        case CAEE_ERR_HIP: return "HIP runtime error";
+    }
+    return "unknown status";
+}
+
+const char* caee_last_error(void) { return g_last_error.c_str(); }
+
+int caee_abi_version(void) { return CAEE_ABI_VERSION; }
+
+caee_status_t caee_timing_enable(int on) {
+    timing().on = on != 0;
+    return CAEE_OK;
+}
+
+caee_status_t caee_timing_reset(void) {
+    Timing& tm = timing();
+    for (auto& r : tm.pending) {
+        (void)hipEventSynchronize(r.b);
+        tm.pool.push_back(r.a);
+        tm.pool.push_back(r.b);
+    }
+    tm.pending.clear();
+    for (int i = 0; i < CAEE_KERNEL_KINDS; ++i) {
+        tm.total_ms[i] = 0.0;
+        tm.launches[i] = 0;
+    }
+    return CAEE_OK;
+}
+
+caee_status_t caee_timing_query(int kind, double* total_ms, int64_t* launches) {
+    g_last_error.clear();
+    if (kind < 0 || kind >= CAEE_KERNEL_KINDS) return fail(CAEE_ERR_INVALID_ARG, "kind=%d out of range", kind);
+    if (!total_ms || !launches) return fail(CAEE_ERR_INVALID_ARG, "NULL output pointer");
+    Timing& tm = timing();
+    for (auto& r : tm.pending) {
+        if (hipEventSynchronize(r.b) != hipSuccess) return fail(CAEE_ERR_HIP, "hipEventSynchronize failed");
+        float ms = 0.f;
+        if (hipEventElapsedTime(&ms, r.a, r.b) != hipSuccess) return fail(CAEE_ERR_HIP, "hipEventElapsedTime failed");
+        tm.total_ms[r.kind] += ms;
+        tm.launches[r.kind] += 1;
+        tm.pool.push_back(r.a);
+        tm.pool.push_back(r.b);
+    }
+    tm.pending.clear();
+    *total_ms = tm.total_ms[kind];
+    *launches = tm.launches[kind];
+    return CAEE_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,67 @@
+"""GPU parity at the DeepSeek-R1 layer shape (d=7168, f=2048, 256 experts in
+8 groups, top-4 groups, top-8 experts, 1 shared expert, bf16 weights), in
+the launch configuration the benchmark times.  Routing, pruning and
+compensation are compared on every token; the layer output on sampled
+tokens, which the oracle evaluates one by one in fp64."""
+import numpy as np
+import pytest
+import torch
+
+from caee_cases import check_route, check_y, getters_dev, gpu_layer, oracle_layer
+from synth_inputs import R1_BF16, make_expert_weights_torch, make_routing_inputs
+
+pytestmark = pytest.mark.gpu
+DEV = torch.device("cuda:0")
+
+
+@pytest.fixture(scope="module")
+def r1_weights():
+    print("drawing R1-shaped bf16 expert weights on the device", flush=True)
+    W = make_expert_weights_torch(R1_BF16, seed=0, device=DEV)
+    torch.cuda.synchronize()
+    yield W
+    del W
+    torch.cuda.empty_cache()
+
+
+def _inputs(T, skewed, n_bins, seed=0):
+    return make_routing_inputs(R1_BF16, seed=seed, T=T, zipf_logit_s=1.1 if skewed else None,
+                               cost_kind="zipf" if skewed else "flat", n_bins=n_bins)
+
+
+@pytest.mark.parametrize("T", [1, 8, 32, 128])
+@pytest.mark.parametrize("skewed", [False, True])
+def test_r1_routing_sweep(T, skewed, r1_weights):
+    for tau in (0.0, 0.02, 0.05, 0.1):
+        for n_bins in (1, 8):
+            inp = _inputs(T, skewed, n_bins, seed=T)
+            print(f"route T={T} skewed={skewed} tau={tau} n_bins={n_bins}", flush=True)
+            got = gpu_layer(R1_BF16, inp, tau, n_bins, r1_weights, DEV, route_only=True)
+            ref = oracle_layer(R1_BF16, inp, tau, n_bins, with_y=False)
+            check_route(got, ref, R1_BF16.E)
+            # gate mass conserved on every token
+            np.testing.assert_allclose(got["topk_w"].sum(axis=1), R1_BF16.routed_scaling, rtol=2e-6)
+
+
+def _layer_case(W, T, skewed, tau, n_bins, tokens):
+    inp = _inputs(T, skewed, n_bins)
+    print(f"layer T={T} skewed={skewed} tau={tau} n_bins={n_bins} tokens={tokens}", flush=True)
+    got = gpu_layer(R1_BF16, inp, tau, n_bins, W, DEV)
+    get, get_sh = getters_dev(W, "bf16")
+    ref = oracle_layer(R1_BF16, inp, tau, n_bins, get, get_sh, tokens=tokens)
+    check_route(got, ref, R1_BF16.E)
+    rel = check_y(got["y"][tokens], ref["y"], 2e-2)
+    print(f"  max|err|/max|ref| = {rel:.3e}", flush=True)
+    return got, ref
+
+
+def test_r1_dense_layer_t32(r1_weights):
+    # the dense-routing baseline: no pruning
+    got, ref = _layer_case(r1_weights, 32, False, 0.0, 1, [0, 17, 31])
+    assert ref["stats"]["n_pruned"] == 0
+
+
+@pytest.mark.parametrize("T,tokens", [(1, [0]), (8, [3, 7]), (128, [0, 64, 127])])
+def test_r1_skewed_layer(T, tokens, r1_weights):
+    # Zipf-skewed popularity and cost table, 8 bins (EP8-style placement)
+    _layer_case(r1_weights, T, True, 0.1, 8, tokens)

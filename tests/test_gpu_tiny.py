@@ -1,0 +1,137 @@
+"""GPU parity on small layers: the HIP path through the C ABI against the
+fp64 oracle, element by element.  Indices, masks, counters and bin loads
+must match exactly; weights to 1e-6; outputs to 1e-5 * max|ref| (fp32) or
+2e-2 * max|ref| (bf16)."""
+import numpy as np
+import pytest
+import torch
+
+from caee_cases import (check_route, check_y, getters_np, gpu_layer, oracle_layer, to_dev,
+                        w_to_dev)
+from paper_2606_29982_amd import caee
+from synth_inputs import TINY_F32, make_expert_weights_np, make_routing_inputs
+
+pytestmark = pytest.mark.gpu
+DEV = torch.device("cuda:0")
+TINY_BF16 = TINY_F32.with_(name="tiny-bf16", w_dtype="bf16", x_dtype="bf16", y_dtype="bf16")
+TOL = {"f32": 1e-5, "bf16": 2e-2}
+
+
+def _run(shape, seed=0, tau=0.1, n_bins=4, T=None, zipf=None, cost_kind="uniform", mutate=None):
+    inp = make_routing_inputs(shape, seed=seed, T=T, zipf_logit_s=zipf, cost_kind=cost_kind,
+                              n_bins=n_bins)
+    if mutate:
+        mutate(inp)
+    W = make_expert_weights_np(shape, seed=seed)
+    print(f"case {shape.name} seed={seed} tau={tau} n_bins={n_bins} T={inp.logits.shape[0]}", flush=True)
+    got = gpu_layer(shape, inp, tau, n_bins, w_to_dev(W, DEV), DEV)
+    get, get_sh = getters_np(W, shape.w_dtype)
+    ref = oracle_layer(shape, inp, tau, n_bins, get, get_sh)
+    check_route(got, ref, shape.E)
+    check_y(got["y"], ref["y"], TOL[shape.w_dtype])
+    return got, ref
+
+
+@pytest.mark.parametrize("seed", range(5))
+@pytest.mark.parametrize("tau,n_bins", [(0.0, 1), (0.1, 4), (0.1, 1), (0.3, 4), (0.3, 2)])
+def test_tiny_fp32(seed, tau, n_bins):
+    _run(TINY_F32, seed, tau, n_bins)
+
+
+@pytest.mark.parametrize("seed", range(3))
+@pytest.mark.parametrize("tau,n_bins", [(0.0, 1), (0.2, 4)])
+def test_tiny_bf16(seed, tau, n_bins):
+    _run(TINY_BF16, seed, tau, n_bins)
+
+
+@pytest.mark.parametrize("T", [1, 2, 7, 33, 100, 128])
+def test_ragged_batches(T):
+    _run(TINY_F32, seed=11, tau=0.2, n_bins=4, T=T)
+
+
+def test_skewed_popularity_fills_token_blocks():
+    # Zipf-skewed logits send most of 128 tokens to a few experts, so experts
+    # get several 16-token MFMA column blocks.
+    got, ref = _run(TINY_BF16, seed=3, tau=0.05, n_bins=4, T=128, zipf=1.1)
+    counts = np.bincount(ref["topk_ids"][ref["topk_ids"] >= 0], minlength=16)
+    assert counts.max() > 48
+
+
+def test_equal_logits_and_resident_experts():
+    def flat(inp):
+        inp.logits[:] = 0.0
+    got, ref = _run(TINY_F32, seed=1, tau=0.3, n_bins=4, mutate=flat)
+    # every token routes to experts 0..3 with weight 1/4 < tau; expert 0 is
+    # every token's top expert (lowest index), 1..3 share its bin and are pruned
+    assert ref["orig_ids"][0].tolist() == [0, 1, 2, 3]
+    assert ref["topk_ids"][0].tolist() == [0, -1, -1, -1]
+    got, ref = _run(TINY_F32, seed=1, tau=0.3, n_bins=4, cost_kind="zero")
+    assert not ref["pruned"].any()
+
+
+def test_threshold_above_every_weight():
+    # only each token's top expert is mandatory; freed slots refill from A_trans
+    got, ref = _run(TINY_F32, seed=2, tau=0.9, n_bins=1, T=3)
+    assert ref["stats"]["n_pad"] > 0
+
+
+@pytest.mark.parametrize("E,G,tg,k", [(64, 8, 4, 6), (128, 8, 2, 8), (256, 8, 4, 8), (32, 1, 1, 16)])
+def test_expert_counts_and_lane_layouts(E, G, tg, k):
+    shape = TINY_F32.with_(E=E, n_group=G, topk_group=tg, k=k, d=128, f=128, T=24)
+    _run(shape, seed=E, tau=0.05, n_bins=4)
+
+
+def test_no_shared_expert_and_k1():
+    _run(TINY_F32.with_(n_shared=0), seed=5, tau=0.1, n_bins=4)
+    _run(TINY_F32.with_(k=1, topk_group=1), seed=6, tau=0.1, n_bins=2)
+
+
+def test_expert_ffn_with_given_ids_and_empty_slots():
+    shape = TINY_F32
+    inp = make_routing_inputs(shape, seed=4)
+    W = make_expert_weights_np(shape, seed=4)
+    rng = np.random.default_rng(0)
+    ids = -np.ones((shape.T, shape.k), np.int32)
+    w = np.zeros((shape.T, shape.k), np.float32)
+    for t in range(shape.T):
+        n = int(rng.integers(0, shape.k + 1))
+        ids[t, :n] = rng.choice(shape.E, n, replace=False)
+        w[t, :n] = rng.random(n)
+    layer = caee.Layer.from_shape(shape)
+    ws = caee.alloc_workspace(layer, DEV)
+    y = torch.empty((shape.T, shape.d), dtype=torch.float32, device=DEV)
+    caee.expert_ffn(layer, to_dev(inp.x, DEV), to_dev(ids, DEV), to_dev(w, DEV), w_to_dev(W, DEV), y, ws)
+    torch.cuda.synchronize()
+    get, get_sh = getters_np(W, "f32")
+    from oracle import swiglu_expert
+    x = inp.x.astype(np.float64)
+    ref = np.zeros((shape.T, shape.d))
+    for t in range(shape.T):
+        for j in range(shape.k):
+            if ids[t, j] >= 0:
+                w13, w2 = get(int(ids[t, j]))
+                ref[t] += float(w[t, j]) * swiglu_expert(x[t:t + 1], w13, w2)[0]
+    w13, w2 = get_sh(0)
+    ref += swiglu_expert(x, w13, w2)
+    check_y(y.cpu().numpy().astype(np.float64), ref, 1e-5)
+
+
+def test_empty_batch_leaves_output_untouched():
+    shape = TINY_F32.with_(T=0, n_bins=1)
+    layer = caee.Layer.from_shape(shape)
+    ws = caee.alloc_workspace(layer, DEV)
+    W = w_to_dev(make_expert_weights_np(TINY_F32, seed=0), DEV)
+    y = torch.full((1, shape.d), 3.0, device=DEV)
+    z = torch.zeros((1, 16), device=DEV)
+    caee.moe_layer(layer, y, z, None, z[0], None, W, y, ws)
+    torch.cuda.synchronize()
+    assert torch.all(y == 3.0)
+
+
+def test_deterministic_repeat():
+    shape = TINY_BF16.with_(T=64)
+    inp = make_routing_inputs(shape, seed=9, zipf_logit_s=1.1)
+    Wd = w_to_dev(make_expert_weights_np(shape, seed=9), DEV)
+    a = gpu_layer(shape, inp, 0.1, 4, Wd, DEV)
+    b = gpu_layer(shape, inp, 0.1, 4, Wd, DEV)
+    assert np.array_equal(a["y"], b["y"]) and np.array_equal(a["topk_w"], b["topk_w"])
