@@ -1,0 +1,249 @@
+"""Benchmark of the CAEE MoE-layer hot path on one MI355X.
+
+One step = one full layer call (caee_moe_layer: routing, cost-aware
+pruning, compensation, grouped SwiGLU expert FFN, combine) on a resident
+batch of synthetic DeepSeek-R1-shaped inputs: d=7168, f=2048, 256 routed
+experts in 8 groups (top-4 groups, top-8 experts), 1 shared expert, bf16
+weights drawn N(0, 0.02), sigmoid router with bias, routed scaling 2.5.
+The headline workload is a decode batch of T=32 tokens with pruning off
+(the dense-routing baseline).  Prints one JSON line.
+
+  python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-sweep] [--no-cpu]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E, published
+W_EXPERT_BYTES = 3 * 7168 * 2048 * 2
+METRIC = "MoE-layer tokens/s + achieved HBM GB/s (% of peak) at T=1..128, with vs without pruning"
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gate_up_r1_t32_traffic.json")
+FFN_SOURCE = os.path.join(ROOT, "paper_2606_29982_amd", "csrc", "ffn.hip")
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--T", type=int, default=32)
+    ap.add_argument("--no-sweep", action="store_true")
+    ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--seed", type=int, default=0)
+    return ap.parse_args()
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+class Case:
+    """Device-resident inputs and buffers of one layer call."""
+
+    def __init__(self, shape, T, tau, n_bins, W, dev, seed, skewed):
+        import torch
+        from paper_2606_29982_amd import caee
+        from synth_inputs import make_routing_inputs
+        self.inp = make_routing_inputs(shape, seed=seed, T=T, zipf_logit_s=1.1 if skewed else None,
+                                       cost_kind="zipf" if skewed else "flat", n_bins=n_bins)
+        self.layer = caee.Layer.from_shape(shape, T=T, tau=tau, n_bins=n_bins)
+        to = lambda a: None if a is None else torch.from_numpy(np.ascontiguousarray(a)).to(dev)  # noqa: E731
+        self.x = torch.from_numpy(self.inp.x.view(np.int16)).to(dev).view(torch.bfloat16)
+        self.logits = to(self.inp.logits)
+        self.bias = to(self.inp.bias)
+        self.cost = to(self.inp.cost)
+        self.bins = to(self.inp.bins) if n_bins > 1 else None
+        self.W = W
+        self.y = torch.empty((T, shape.d), dtype=torch.bfloat16, device=dev)
+        self.ws = caee.alloc_workspace(self.layer, dev)
+        self.out = caee.alloc_route_out(self.layer, dev)
+        self.caee = caee
+
+    def step(self):
+        self.caee.moe_layer(self.layer, self.x, self.logits, self.bias, self.cost, self.bins, self.W,
+                            self.y, self.ws, self.out)
+
+    def stats(self):
+        return self.out["stats"].cpu().numpy().tolist()
+
+
+def time_steps(case, steps, warmup):
+    import torch
+    for _ in range(warmup):
+        case.step()
+    torch.cuda.synchronize()
+    a = torch.cuda.Event(enable_timing=True)
+    b = torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(steps):
+        case.step()
+    b.record()
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) / steps
+
+
+def layer_bytes(shape, T, n_trans):
+    """Algorithmic HBM bytes of one layer call: weights of every executed
+    expert (A_trans plus the shared one), x read, y written, router logits,
+    bias/cost/bin tables."""
+    return ((n_trans + shape.n_shared) * W_EXPERT_BYTES + T * shape.d * 2 * 2
+            + T * shape.E * 4 + 12 * shape.E)
+
+
+def gate_up_bytes(shape, T, n_trans, rows):
+    """Algorithmic bytes of one gate/up launch: the gate and up matrices of
+    every executed expert, x read once, the bf16 SwiGLU rows written."""
+    return ((n_trans + shape.n_shared) * 2 * shape.f * shape.d * 2 + T * shape.d * 2
+            + rows * shape.f * 2)
+
+
+def traffic_entry():
+    """HBM traffic of the gate/up kernel from committed rocprofv3 counter
+    runs, or None when missing or taken on a different kernel source."""
+    try:
+        with open(TRAFFIC_FILE) as fh:
+            rec = json.load(fh)
+        with open(FFN_SOURCE, "rb") as fh:
+            src = hashlib.sha256(fh.read()).hexdigest()
+        if rec.get("ffn_source_sha256") != src:
+            return None
+        return rec.get("bytes_per_launch")
+    except (OSError, ValueError):
+        return None
+
+
+def cpu_baseline(shape, case, W, sample_tokens):
+    """The fp64 oracle on the host cores: routing + pruning + compensation of
+    the whole batch and the expert FFN of ``sample_tokens`` tokens."""
+    import torch
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        blas = threadpool_info()
+        cores = max([int(i.get("num_threads", 1)) for i in blas] or [1])
+        vendor = ",".join(sorted({i.get("internal_api", "?") for i in blas}))
+    except Exception:
+        cores, vendor = len(os.sched_getaffinity(0)), "unknown"
+    inp = case.inp
+    ref = oracle.moe_layer_ref(E=shape.E, n_group=shape.n_group, topk_group=shape.topk_group, k=shape.k,
+                               routed_scaling=shape.routed_scaling, tau=case.layer.tau,
+                               n_bins=case.layer.n_bins, logits=inp.logits, bias=inp.bias, cost=inp.cost,
+                               bins=inp.bins)
+    tokens = list(range(sample_tokens))
+    need = sorted({int(e) for t in tokens for e in ref["topk_ids"][t] if e >= 0})
+    host = {}
+    for e in need:   # stage the stored bf16 weights in host memory (not timed)
+        host[e] = (W["w13"][e].view(torch.int16).cpu().numpy().view(np.uint16),
+                   W["w2"][e].view(torch.int16).cpu().numpy().view(np.uint16))
+    sh = (W["sh_w13"][0].view(torch.int16).cpu().numpy().view(np.uint16),
+          W["sh_w2"][0].view(torch.int16).cpu().numpy().view(np.uint16))
+    t0 = time.perf_counter()
+    oracle.moe_layer_ref(
+        E=shape.E, n_group=shape.n_group, topk_group=shape.topk_group, k=shape.k,
+        routed_scaling=shape.routed_scaling, tau=case.layer.tau, n_bins=case.layer.n_bins,
+        logits=inp.logits, bias=inp.bias, cost=inp.cost, bins=inp.bins, x=inp.x, x_dtype="bf16",
+        w_dtype="bf16", n_shared=shape.n_shared,
+        get_expert=lambda e: oracle.expert_weights_f64(host[e][0], host[e][1], "bf16"),
+        get_shared=lambda s: oracle.expert_weights_f64(sh[0], sh[1], "bf16"), tokens=tokens)
+    dt = time.perf_counter() - t0
+    return {"value": round(sample_tokens / dt, 4), "unit": "tokens/s", "cores": cores, "kind": "oracle",
+            "sample": (f"fp64 numpy oracle ({vendor} BLAS): routing, pruning and compensation of all "
+                       f"{case.layer.T} tokens plus the expert FFN of {sample_tokens} of them "
+                       f"({len(need)} routed experts + 1 shared), {dt:.1f} s"),
+            "seconds": round(dt, 2)}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on exactly one GPU; --gpus {args.gpus} is not supported "
+              "(the layer is measured on one MI355X; multi-GPU sharding is not built)", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_2606_29982_amd import caee
+    from synth_inputs import R1_BF16, make_expert_weights_torch
+
+    dev = torch.device("cuda:0")
+    shape = R1_BF16
+    t0 = time.time()
+    log("drawing R1-shaped bf16 expert weights on the device")
+    W = make_expert_weights_torch(shape, seed=args.seed, device=dev)
+    torch.cuda.synchronize()
+    log(f"weights ready in {time.time() - t0:.1f}s")
+
+    # Headline: T=32 decode batch, pruning off.
+    head = Case(shape, args.T, 0.0, 1, W, dev, args.seed, skewed=False)
+    ms = time_steps(head, args.steps, args.warmup)
+    st = head.stats()
+    n_trans = st[5]
+    rows = args.T * shape.k + args.T * shape.n_shared
+    # Per-kernel durations over a second timed region with library events on.
+    caee.timing_reset()
+    caee.timing_enable(True)
+    ms_ev = time_steps(head, args.steps, 0)
+    kern = {}
+    for kind in caee.KERNEL_KINDS:
+        tot, n = caee.timing_query(kind)
+        kern[kind] = tot / max(n, 1)
+    caee.timing_enable(False)
+    caee.timing_reset()
+    log(f"T={args.T}: {ms * 1e3:.1f} us/step ({ms_ev * 1e3:.1f} with kernel events); kernels (us): "
+        + ", ".join(f"{k} {v * 1e3:.1f}" for k, v in kern.items()))
+
+    b_layer = layer_bytes(shape, args.T, n_trans)
+    gu_bytes = gate_up_bytes(shape, args.T, n_trans, rows)
+    gu_gbps = gu_bytes / (kern["gate_up"] * 1e-3) / 1e9
+    traffic = traffic_entry()
+    roofline = {"kernel": "k_gate_up (expert gate/up + SwiGLU)", "bound": "hbm",
+                "achieved": round(gu_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                "frac": round(gu_gbps / HBM_PEAK_GBPS, 4), "traffic": traffic,
+                "bytes_per_launch": gu_bytes, "avg_launch_us": round(kern["gate_up"] * 1e3, 2)}
+    result = {
+        "metric": METRIC, "value": round(args.T / (ms * 1e-3), 1), "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "deepseek-r1-moe-layer-bf16-decode", "T": args.T, "d": shape.d, "f": shape.f,
+                   "E": shape.E, "n_group": shape.n_group, "topk_group": shape.topk_group, "k": shape.k,
+                   "n_shared": shape.n_shared, "tau": 0.0, "pruning": "off", "parallelism": "single-gpu"},
+        "hbm_gbps": round(b_layer / (ms * 1e-3) / 1e9, 1),
+        "hbm_frac": round(b_layer / (ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+        "experts_executed": n_trans + shape.n_shared,
+        "kernel_us": {k: round(v * 1e3, 2) for k, v in kern.items()},
+        "roofline": roofline,
+    }
+
+    if not args.no_sweep:
+        sweep = []
+        for T in (1, 8, 32, 128):
+            for tau, n_bins in ((0.0, 1), (0.1, 8)):
+                c = Case(shape, T, tau, n_bins, W, dev, args.seed, skewed=True)
+                m = time_steps(c, max(10, args.steps // 2), 3)
+                s = c.stats()
+                b = layer_bytes(shape, T, s[5])
+                sweep.append({"T": T, "tau": tau, "n_bins": n_bins, "inputs": "zipf-skewed",
+                              "us_per_step": round(m * 1e3, 1), "tokens_per_s": round(T / (m * 1e-3), 1),
+                              "hbm_gbps": round(b / (m * 1e-3) / 1e9, 1),
+                              "hbm_frac": round(b / (m * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+                              "act": s[0], "pruned": s[4], "executed": s[5] + shape.n_shared})
+                log(f"sweep {sweep[-1]}")
+                del c
+        result["sweep"] = sweep
+
+    if not args.no_cpu:
+        log("timing the fp64 oracle on the host")
+        result["cpu_baseline"] = cpu_baseline(shape, head, W, sample_tokens=4)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

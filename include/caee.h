@@ -34,6 +34,10 @@
  *   - Decisions (selection, importance threshold, cost comparisons) are
  *     computed in float64, ties going to the lower expert or group index,
  *     so results are deterministic and independent of launch shape.
+ *     Per-bin cost sums are exact (hence independent of summation order)
+ *     while, within each bin, the nonzero costs span less than 2^20
+ *     (largest / smallest); beyond that range they may differ from an
+ *     ascending-order sum in the last bit.
  */
 #ifndef CAEE_H
 #define CAEE_H

@@ -25,34 +25,35 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found")
 
 
-def build(verbose: bool = False) -> str:
-    """Compile every HIP source into one shared library; returns its path."""
+def build(verbose: bool = False, out: str = LIB, defines=()) -> str:
+    """Compile every HIP source into one shared library; returns its path.
+    ``defines`` are extra -D options (tuning knobs of the kernels)."""
     objs = []
     t0 = time.time()
     procs = []
     for src in SOURCES:
-        obj = os.path.join(CSRC, src.replace(".hip", ".o"))
-        cmd = [hipcc(), *HIP_FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+        obj = out + "." + src.replace(".hip", ".o")
+        cmd = [hipcc(), *HIP_FLAGS, *[f"-D{d}" for d in defines], "-c", os.path.join(CSRC, src), "-o", obj]
         if verbose:
             print(" ".join(cmd), flush=True)
         procs.append((src, subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT)))
         objs.append(obj)
     for src, pr in procs:
-        out, _ = pr.communicate()
+        log, _ = pr.communicate()
         if pr.returncode != 0:
-            sys.stderr.write(out.decode(errors="replace"))
+            sys.stderr.write(log.decode(errors="replace"))
             raise RuntimeError(f"hipcc failed on {src}")
-        if verbose and out:
-            sys.stderr.write(out.decode(errors="replace"))
-    tmp = LIB + ".tmp"
+        if verbose and log:
+            sys.stderr.write(log.decode(errors="replace"))
+    tmp = out + ".tmp"
     cmd = [hipcc(), "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", tmp]
     subprocess.run(cmd, check=True)
-    os.replace(tmp, LIB)
+    os.replace(tmp, out)
     for o in objs:
         os.remove(o)
     if verbose:
-        print(f"built {LIB} in {time.time() - t0:.1f}s", flush=True)
-    return LIB
+        print(f"built {out} in {time.time() - t0:.1f}s", flush=True)
+    return out
 
 
 if __name__ == "__main__":

@@ -45,11 +45,11 @@ class RouteOut(ctypes.Structure):
                 ("topk_ids", "topk_w", "orig_ids", "masks", "stats", "bin_loads")]
 
 
-def _load():
-    if not os.path.exists(LIB_PATH):
-        raise ImportError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
+def _load(path: str = LIB_PATH):
+    if not os.path.exists(path):
+        raise ImportError(f"{path} is missing: build it with __graft_entry__.build() "
                           "(python -c 'import __graft_entry__ as g; g.build()')")
-    lib = ctypes.CDLL(LIB_PATH)
+    lib = ctypes.CDLL(path)
     st = ctypes.c_int
     P = ctypes.c_void_p
     desc_p = ctypes.POINTER(LayerDesc)
@@ -75,6 +75,15 @@ def _load():
 
 
 lib = _load()
+
+
+def load_library(path: str) -> None:
+    """Bind this module to another build of the library (e.g. one compiled
+    with different kernel tuning knobs)."""
+    global lib
+    lib = _load(path)
+
+
 EXPORTED = ("caee_workspace_size", "caee_route_prune", "caee_expert_ffn", "caee_moe_layer",
             "caee_status_str", "caee_last_error", "caee_abi_version", "caee_timing_enable",
             "caee_timing_reset", "caee_timing_query")

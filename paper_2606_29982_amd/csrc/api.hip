@@ -66,7 +66,7 @@ caee_status_t check_desc(const caee_layer_desc_t* d) {
     if (d->E % epl || gsize % epl || (lpg & (lpg - 1)))
         return fail(CAEE_ERR_UNSUPPORTED, "E=%d with %d experts per group needs the group size to be a "
                     "multiple of %d with a power-of-two quotient", d->E, gsize, epl);
-    if (d->T > kFusedMaxT) return fail(CAEE_ERR_UNSUPPORTED, "T=%d exceeds %d", d->T, kFusedMaxT);
+    if (d->T > kMaxT) return fail(CAEE_ERR_UNSUPPORTED, "T=%d exceeds %d", d->T, kMaxT);
     if (d->w_dtype == CAEE_FP8_E4M3) return fail(CAEE_ERR_UNSUPPORTED, "fp8 weights are not built yet");
     return CAEE_OK;
 }
@@ -209,6 +209,12 @@ RouteParams make_route_params(const caee_layer_desc_t* d, const float* logits, c
     p.perm_pos = (int32_t*)(ws + L.perm_pos);
     p.chunks = (int32_t*)(ws + L.chunks);
     p.n_chunks = (int32_t*)(ws + L.n_chunks);
+    p.gbuf = (double*)(ws + L.gbuf);
+    p.top1 = (int32_t*)(ws + L.top1);
+    p.trans = (uint8_t*)(ws + L.trans);
+    p.counters = (int32_t*)(ws + L.counters);
+    p.chunk_tokens = L.chunk_tokens;
+    p.orig_ids = (int32_t*)(ws + L.orig);
     return p;
 }
 
@@ -240,9 +246,13 @@ caee_status_t run_ffn(const caee_layer_desc_t* d, const void* x, const int32_t* 
     p.yperm = (float*)(ws + L.y);
     p.y = y;
     p.y_bf16 = d->y_dtype == CAEE_BF16;
+    p.P = L.P;
+    p.ksplit = L.ksplit;
+    const int nb = ffn_token_blocks(*d);
     CAEE_TRY(timed_launch(CAEE_KERNEL_GATE_UP, s, "gate/up",
-                          [&] { return launch_gate_up(p, d->w_dtype, L.max_chunks, s); }));
-    CAEE_TRY(timed_launch(CAEE_KERNEL_DOWN, s, "down", [&] { return launch_down(p, d->w_dtype, L.max_chunks, s); }));
+                          [&] { return launch_gate_up(p, d->w_dtype, nb, L.max_chunks, s); }));
+    CAEE_TRY(timed_launch(CAEE_KERNEL_DOWN, s, "down",
+                          [&] { return launch_down(p, d->w_dtype, nb, L.max_chunks, s); }));
     CAEE_TRY(timed_launch(CAEE_KERNEL_COMBINE, s, "combine", [&] { return launch_combine(p, s); }));
     return CAEE_OK;
 }
@@ -288,11 +298,10 @@ caee_status_t caee_route_prune(const caee_layer_desc_t* desc, const float* logit
     RouteParams p = make_route_params(desc, logits, bias, cost, bin, (char*)ws, L);
     p.topk_ids = out->topk_ids;
     p.topk_w = out->topk_w;
-    p.orig_ids = out->orig_ids;
+    if (out->orig_ids) p.orig_ids = out->orig_ids;
     p.masks = out->masks;
     p.stats = out->stats;
     p.bin_loads = out->bin_loads;
-    p.do_route = 1;
     p.do_permute = 0;
     hipStream_t s = as_stream(stream);
     return timed_launch(CAEE_KERNEL_ROUTE, s, "route", [&] { return launch_route(p, s); });
@@ -313,10 +322,9 @@ caee_status_t caee_expert_ffn(const caee_layer_desc_t* desc, const void* x, cons
     if (desc->T == 0) return CAEE_OK;
     RouteParams p = make_route_params(desc, nullptr, nullptr, nullptr, nullptr, (char*)ws, L);
     p.topk_ids = const_cast<int32_t*>(topk_ids);
-    p.do_route = 0;
     p.do_permute = 1;
     hipStream_t s = as_stream(stream);
-    CAEE_TRY(timed_launch(CAEE_KERNEL_ROUTE, s, "permute", [&] { return launch_route(p, s); }));
+    CAEE_TRY(timed_launch(CAEE_KERNEL_ROUTE, s, "permute", [&] { return launch_permute(p, s); }));
     return run_ffn(desc, x, topk_ids, topk_w, weights, y, (char*)ws, L, s);
 }
 
@@ -337,11 +345,10 @@ caee_status_t caee_moe_layer(const caee_layer_desc_t* desc, const void* x, const
     RouteParams p = make_route_params(desc, logits, bias, cost, bin, wsb, L);
     p.topk_ids = out ? out->topk_ids : (int32_t*)(wsb + L.ids);
     p.topk_w = out ? out->topk_w : (float*)(wsb + L.w);
-    p.orig_ids = out ? out->orig_ids : nullptr;
+    if (out && out->orig_ids) p.orig_ids = out->orig_ids;
     p.masks = out ? out->masks : nullptr;
     p.stats = out ? out->stats : nullptr;
     p.bin_loads = out ? out->bin_loads : nullptr;
-    p.do_route = 1;
     p.do_permute = 1;
     hipStream_t s = as_stream(stream);
     CAEE_TRY(timed_launch(CAEE_KERNEL_ROUTE, s, "route", [&] { return launch_route(p, s); }));

@@ -16,16 +16,39 @@ constexpr int kMaxE = 256;
 constexpr int kMaxK = 16;
 constexpr int kMaxShared = 4;
 constexpr int kMaxBins = 256;
-constexpr int kFusedMaxT = 128;     // routing + permutation in one workgroup
+constexpr int kMaxT = 65536;        // tokens per call
 constexpr int kRouteThreads = 1024;
-constexpr int kChunkTokens = 128;   // tokens of one expert handled by one FFN work item
+constexpr int kMaxTokenBlocks = 8;  // 16-token MFMA column blocks one FFN work item can hold
 constexpr int kFfnThreads = 256;    // 4 independent waves per FFN workgroup
+constexpr long long kTargetItems = 4096;   // gate/up work items wanted per call (~4 per SIMD)
+
+// Contraction steps (one 16-byte load per lane) issued together per wave.
+#ifndef CAEE_GATE_UP_U
+#define CAEE_GATE_UP_U 4
+#endif
+#ifndef CAEE_DOWN_U
+#define CAEE_DOWN_U 4
+#endif
+constexpr int kGateUpU = CAEE_GATE_UP_U;
+constexpr int kDownU = CAEE_DOWN_U;
+// Minimum resident waves per SIMD the FFN kernels are compiled for (0: no bound).
+#ifndef CAEE_FFN_WAVES_PER_EU
+#define CAEE_FFN_WAVES_PER_EU 0
+#endif
+// Load weights one step block ahead of the MFMAs that use them.
+#ifndef CAEE_FFN_PIPELINE
+#define CAEE_FFN_PIPELINE 1
+#endif
 
 // ---------------------------------------------------------------------------
 // Workspace layout.  Every region is 256-byte aligned.
 struct WsLayout {
     size_t ids, w;              // [T][k] K_final and weights when the caller gives none
     size_t orig;                // [T][k] K_t when the caller gives none
+    size_t gbuf;                // [T][k] float64 normalised gate weights G(t)
+    size_t top1;                // [T] each token's top expert
+    size_t trans;               // [E] uint8 membership of A_trans
+    size_t counters;            // [4] int: (unused), refilled slots, empty slots
     size_t perm_off;            // [E + n_shared + 1] first permuted row of each expert slot
     size_t perm_tok;            // [P] token of each permuted row
     size_t perm_pos;            // [T][k + n_shared] permuted row of each (token, slot), -1 unused
@@ -34,7 +57,7 @@ struct WsLayout {
     size_t h;                   // [P][f] SwiGLU activations (weight dtype; fp32 for fp8)
     size_t y;                   // [P][d] fp32 expert outputs
     size_t total;
-    int P, max_chunks;
+    int P, max_chunks, ksplit, chunk_tokens;
 };
 
 inline size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
@@ -43,17 +66,44 @@ inline int elem_bytes(int dtype) {
     return dtype == CAEE_F32 ? 4 : dtype == CAEE_BF16 ? 2 : 1;
 }
 
+// Split of the gate/up contraction: small batches touch few experts, so the
+// d dimension is cut into ksplit ranges to give every SIMD several work items.
+// Depends on the descriptor only (not on the device).
+// The splits of one tile are waves of one 4-wave workgroup, so ksplit <= 4.
+inline int gate_up_split(const caee_layer_desc_t& d) {
+    const int ksteps = d.d * elem_bytes(d.w_dtype) / 64;
+    const long long tok_slots = (long long)(d.T > 0 ? d.T : 0) * d.k;
+    const long long experts = (tok_slots < d.E ? tok_slots : d.E) + d.n_shared;
+    const long long tiles = experts * (d.f / 16);
+    int S = 1;
+    while (S < 4 && tiles * S < kTargetItems && ksteps % (2 * S * kGateUpU) == 0) S *= 2;
+    return S;
+}
+
+// 16-token column blocks per FFN work item: enough for every token of the
+// batch to land in one chunk per expert while T <= 128, so each expert's
+// weights are streamed once; larger batches use several 128-token chunks.
+inline int ffn_token_blocks(const caee_layer_desc_t& d) {
+    const int need = (d.T + 15) / 16;
+    return need <= 1 ? 1 : need <= 2 ? 2 : need <= 4 ? 4 : kMaxTokenBlocks;
+}
+
 inline WsLayout ws_layout(const caee_layer_desc_t& d) {
     WsLayout L{};
     const size_t T = d.T > 0 ? d.T : 0;
     const int slots = d.k + d.n_shared;
     L.P = int(T * slots);
-    L.max_chunks = d.E + d.n_shared + (L.P + kChunkTokens - 1) / kChunkTokens;
+    L.chunk_tokens = 16 * ffn_token_blocks(d);
+    L.max_chunks = d.E + d.n_shared + (L.P + L.chunk_tokens - 1) / L.chunk_tokens;
     size_t off = 0;
     auto take = [&](size_t bytes) { size_t o = off; off += align256(bytes); return o; };
     L.ids = take(T * d.k * 4);
     L.w = take(T * d.k * 4);
     L.orig = take(T * d.k * 4);
+    L.gbuf = take(T * d.k * 8);
+    L.top1 = take(T * 4);
+    L.trans = take(d.E);
+    L.counters = take(16);
     L.perm_off = take(size_t(d.E + d.n_shared + 1) * 4);
     L.perm_tok = take(size_t(L.P) * 4);
     L.perm_pos = take(T * slots * 4);
@@ -62,6 +112,7 @@ inline WsLayout ws_layout(const caee_layer_desc_t& d) {
     const int h_bytes = d.w_dtype == CAEE_FP8_E4M3 ? 4 : elem_bytes(d.w_dtype);
     L.h = take(size_t(L.P) * d.f * h_bytes);
     L.y = take(size_t(L.P) * d.d * 4);
+    L.ksplit = gate_up_split(d);
     L.total = off;
     return L;
 }
@@ -85,14 +136,19 @@ struct RouteParams {
     uint32_t* masks;
     int32_t* stats;
     double* bin_loads;
+    // per-call scratch
+    double* gbuf;
+    int32_t* top1;
+    uint8_t* trans;
+    int32_t* counters;
+    int chunk_tokens;
     // permutation outputs
     int32_t* perm_off;
     int32_t* perm_tok;
     int32_t* perm_pos;
     int32_t* chunks;
     int32_t* n_chunks;
-    int do_route;       // 0: read K_final from topk_ids instead of routing
-    int do_permute;
+    int do_permute;     // 0: the permutation kernel only reports the refill/empty-slot counts
 };
 
 struct FfnParams {
@@ -116,12 +172,15 @@ struct FfnParams {
     float* yperm;
     void* y;
     int y_bf16;
+    int P;
+    int ksplit;
 };
 
 // Host-side launchers (defined next to their kernels).
 hipError_t launch_route(const RouteParams& p, hipStream_t s);
-hipError_t launch_gate_up(const FfnParams& p, int w_dtype, int max_chunks, hipStream_t s);
-hipError_t launch_down(const FfnParams& p, int w_dtype, int max_chunks, hipStream_t s);
+hipError_t launch_permute(const RouteParams& p, hipStream_t s);
+hipError_t launch_gate_up(const FfnParams& p, int w_dtype, int nb, int max_chunks, hipStream_t s);
+hipError_t launch_down(const FfnParams& p, int w_dtype, int nb, int max_chunks, hipStream_t s);
 hipError_t launch_combine(const FfnParams& p, hipStream_t s);
 int device_cu_count();
 

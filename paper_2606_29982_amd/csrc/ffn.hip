@@ -24,8 +24,6 @@ typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
-constexpr int kNB = kChunkTokens / 16;   // 16-token MFMA column blocks per chunk
-
 // One 16-byte load per lane = one contraction step of the 16x16 MFMA tile.
 struct Bf16Math {
     static constexpr int kElemBytes = 2;
@@ -58,81 +56,151 @@ __device__ inline const char* expert_base(const void* routed, const void* shared
                  : (const char*)shared + (size_t)(x - E) * expert_bytes;
 }
 
-template <class M, int U>
-__global__ __launch_bounds__(kFfnThreads) void k_gate_up(FfnParams p) {
-    const int lane = threadIdx.x & (kWave - 1);
-    const int r = lane & 15, g = lane >> 4;
-    const int gw = blockIdx.x * (kFfnThreads / kWave) + (threadIdx.x / kWave);
-    const int nw = gridDim.x * (kFfnThreads / kWave);
-    const int tiles = p.f / 16;
-    const int total = (*p.n_chunks) * tiles;
-    const size_t row_units = (size_t)p.d * M::kElemBytes / 16;
-    const int ksteps = (int)(row_units / 4);
-    const size_t expert_bytes = (size_t)2 * p.f * p.d * M::kElemBytes;
-
-    for (int item = gw; item < total; item += nw) {
-        const int c = item / tiles, jt = item - c * tiles;
-        const int xs = p.chunks[4 * c], row0 = p.chunks[4 * c + 1], ntok = p.chunks[4 * c + 2];
-        const u32x4_t* wb = (const u32x4_t*)expert_base(p.w13, p.sh_w13, xs, p.E, expert_bytes);
-        const u32x4_t* ag = wb + (size_t)(jt * 16 + r) * row_units + g;
-        const u32x4_t* au = wb + (size_t)(p.f + jt * 16 + r) * row_units + g;
-        const int nb = (ntok + 15) >> 4;
-        const u32x4_t* xb[kNB];
+// Contraction of one 16-row weight tile against up to NB 16-token blocks,
+// over `nsteps` k-steps starting at the given pointers.  Weights are loaded
+// U steps ahead of the MFMAs that consume them (register double buffer).
+template <class M, int U, int NA, int NB>
+__device__ inline void tile_contract(const u32x4_t* const (&a)[NA], const u32x4_t* const (&b)[NB], int nb,
+                                     int nsteps, f32x4_t (&acc)[NA][NB]) {
+    u32x4_t cur[NA][U], nxt[NA][U];
 #pragma unroll
-        for (int tb = 0; tb < kNB; ++tb) {
-            int n = tb * 16 + r;
-            n = n < ntok ? n : 0;   // padded token columns read a valid row; their results are dropped
-            xb[tb] = (const u32x4_t*)p.x + (size_t)p.perm_tok[row0 + n] * row_units + g;
+    for (int m = 0; m < NA; ++m)
+#pragma unroll
+        for (int u = 0; u < U; ++u) cur[m][u] = __builtin_nontemporal_load(a[m] + 4 * u);
+    for (int ks = 0; ks < nsteps; ks += U) {
+        const bool more = CAEE_FFN_PIPELINE && ks + U < nsteps;
+        if (!CAEE_FFN_PIPELINE && ks > 0) {
+#pragma unroll
+            for (int m = 0; m < NA; ++m)
+#pragma unroll
+                for (int u = 0; u < U; ++u) cur[m][u] = __builtin_nontemporal_load(a[m] + 4 * (ks + u));
         }
-        f32x4_t accg[kNB], accu[kNB];
+        if (more) {
 #pragma unroll
-        for (int tb = 0; tb < kNB; ++tb) {
-            accg[tb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-            accu[tb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+            for (int m = 0; m < NA; ++m)
+#pragma unroll
+                for (int u = 0; u < U; ++u) nxt[m][u] = __builtin_nontemporal_load(a[m] + 4 * (ks + U + u));
         }
-        for (int ks = 0; ks < ksteps; ks += U) {
-            u32x4_t a0[U], a1[U];
 #pragma unroll
-            for (int u = 0; u < U; ++u) {
-                a0[u] = __builtin_nontemporal_load(ag + 4 * (ks + u));
-                a1[u] = __builtin_nontemporal_load(au + 4 * (ks + u));
-            }
+        for (int tb = 0; tb < NB; ++tb) {
+            if (tb < nb) {
 #pragma unroll
-            for (int tb = 0; tb < kNB; ++tb) {
-                if (tb < nb) {
+                for (int u = 0; u < U; ++u) {
+                    const u32x4_t bv = b[tb][4 * (ks + u)];
 #pragma unroll
-                    for (int u = 0; u < U; ++u) {
-                        const u32x4_t b = xb[tb][4 * (ks + u)];
-                        M::mma(accg[tb], a0[u], b);
-                        M::mma(accu[tb], a1[u], b);
-                    }
+                    for (int m = 0; m < NA; ++m) M::mma(acc[m][tb], cur[m][u], bv);
                 }
             }
         }
+        if (more) {
+#pragma unroll
+            for (int m = 0; m < NA; ++m)
+#pragma unroll
+                for (int u = 0; u < U; ++u) cur[m][u] = nxt[m][u];
+        }
+    }
+}
+
+template <class M>
+__device__ inline void store_h(const FfnParams& p, size_t o, const float (&h)[4]) {
+    if (M::kElemBytes == 2) {
+        uint2 pk;
+        pk.x = bf16_rne(h[0]) | (bf16_rne(h[1]) << 16);
+        pk.y = bf16_rne(h[2]) | (bf16_rne(h[3]) << 16);
+        *(uint2*)((uint16_t*)p.h + o) = pk;
+    } else {
+        *(float4*)((float*)p.h + o) = make_float4(h[0], h[1], h[2], h[3]);
+    }
+}
+
+#if CAEE_FFN_WAVES_PER_EU > 0
+#define CAEE_FFN_BOUNDS __launch_bounds__(kFfnThreads) __attribute__((amdgpu_waves_per_eu(CAEE_FFN_WAVES_PER_EU)))
+#else
+#define CAEE_FFN_BOUNDS __launch_bounds__(kFfnThreads)
+#endif
+
+// Gate/up products and SwiGLU.  A workgroup item covers 4/ksplit adjacent
+// 16-column tiles of one chunk; wave w takes tile w/ksplit and contraction
+// range w%ksplit.  Split partial sums meet in LDS and are added in split
+// order, so the result does not depend on which wave finishes first.
+template <class M, int U, int NB>
+__global__ CAEE_FFN_BOUNDS void k_gate_up(FfnParams p) {
+    constexpr int kWaves = kFfnThreads / kWave;
+    __shared__ f32x4_t s_red[kWaves][2][NB][kWave];
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = threadIdx.x / kWave;
+    const int r = lane & 15, g = lane >> 4;
+    const int S = p.ksplit;
+    const int tiles = p.f / 16;
+    const int tiles_per_item = kWaves / S;
+    const int items_per_chunk = tiles / tiles_per_item;
+    const int total = (*p.n_chunks) * items_per_chunk;
+    const size_t row_units = (size_t)p.d * M::kElemBytes / 16;
+    const int kper = (int)(row_units / 4) / S;
+    const size_t expert_bytes = (size_t)2 * p.f * p.d * M::kElemBytes;
+    const int sp = wave % S;
+
+    for (int item = blockIdx.x; item < total; item += gridDim.x) {
+        const int c = item / items_per_chunk;
+        const int jt = (item - c * items_per_chunk) * tiles_per_item + wave / S;
+        const int xs = p.chunks[4 * c], row0 = p.chunks[4 * c + 1], ntok = p.chunks[4 * c + 2];
+        const int nb = (ntok + 15) >> 4;
+        const size_t k0 = (size_t)4 * sp * kper;
+        const u32x4_t* wb = (const u32x4_t*)expert_base(p.w13, p.sh_w13, xs, p.E, expert_bytes);
+        const u32x4_t* const a[2] = {wb + (size_t)(jt * 16 + r) * row_units + g + k0,
+                                     wb + (size_t)(p.f + jt * 16 + r) * row_units + g + k0};
+        const u32x4_t* xb[NB];
+#pragma unroll
+        for (int tb = 0; tb < NB; ++tb) {
+            int n = tb * 16 + r;
+            n = (tb < nb && n < ntok) ? n : 0;   // padded token columns read a valid row; results dropped
+            xb[tb] = (const u32x4_t*)p.x + (size_t)p.perm_tok[row0 + n] * row_units + g + k0;
+        }
+        f32x4_t acc[2][NB];
+#pragma unroll
+        for (int m = 0; m < 2; ++m)
+#pragma unroll
+            for (int tb = 0; tb < NB; ++tb) acc[m][tb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        tile_contract<M, U, 2, NB>(a, xb, nb, kper, acc);
+
+        if (S > 1) {
+#pragma unroll
+            for (int m = 0; m < 2; ++m)
+#pragma unroll
+                for (int tb = 0; tb < NB; ++tb) s_red[wave][m][tb][lane] = acc[m][tb];
+            __syncthreads();
+            if (sp == 0) {
+#pragma unroll
+                for (int m = 0; m < 2; ++m)
+#pragma unroll
+                    for (int tb = 0; tb < NB; ++tb) {
+                        f32x4_t sum = s_red[wave][m][tb][lane];
+                        for (int q = 1; q < S; ++q) sum += s_red[wave + q][m][tb][lane];
+                        acc[m][tb] = sum;
+                    }
+            }
+            __syncthreads();
+        }
         // Lane holds rows 4g..4g+3 of the tile (intermediate features) for token column r.
+        if (sp == 0) {
+            const int col = jt * 16 + 4 * g;
 #pragma unroll
-        for (int tb = 0; tb < kNB; ++tb) {
-            const int n = tb * 16 + r;
-            if (tb < nb && n < ntok) {
-                const size_t o = (size_t)(row0 + n) * p.f + jt * 16 + 4 * g;
-                float h[4];
+            for (int tb = 0; tb < NB; ++tb) {
+                const int n = tb * 16 + r;
+                if (tb < nb && n < ntok) {
+                    float h[4];
 #pragma unroll
-                for (int v = 0; v < 4; ++v) h[v] = silu_mul(accg[tb][v], accu[tb][v]);
-                if (M::kElemBytes == 2) {
-                    uint2 pk;
-                    pk.x = bf16_rne(h[0]) | (bf16_rne(h[1]) << 16);
-                    pk.y = bf16_rne(h[2]) | (bf16_rne(h[3]) << 16);
-                    *(uint2*)((uint16_t*)p.h + o) = pk;
-                } else {
-                    *(float4*)((float*)p.h + o) = make_float4(h[0], h[1], h[2], h[3]);
+                    for (int v = 0; v < 4; ++v) h[v] = silu_mul(acc[0][tb][v], acc[1][tb][v]);
+                    store_h<M>(p, (size_t)(row0 + n) * p.f + col, h);
                 }
             }
         }
     }
 }
 
-template <class M, int U>
-__global__ __launch_bounds__(kFfnThreads) void k_down(FfnParams p) {
+// Down products: Y[row][i] = W2[i] . H[row], one 16-row tile per work item.
+template <class M, int U, int NB>
+__global__ CAEE_FFN_BOUNDS void k_down(FfnParams p) {
     const int lane = threadIdx.x & (kWave - 1);
     const int r = lane & 15, g = lane >> 4;
     const int gw = blockIdx.x * (kFfnThreads / kWave) + (threadIdx.x / kWave);
@@ -146,37 +214,26 @@ __global__ __launch_bounds__(kFfnThreads) void k_down(FfnParams p) {
     for (int item = gw; item < total; item += nw) {
         const int c = item / tiles, it = item - c * tiles;
         const int xs = p.chunks[4 * c], row0 = p.chunks[4 * c + 1], ntok = p.chunks[4 * c + 2];
-        const u32x4_t* wb = (const u32x4_t*)expert_base(p.w2, p.sh_w2, xs, p.E, expert_bytes);
-        const u32x4_t* a = wb + (size_t)(it * 16 + r) * row_units + g;
         const int nb = (ntok + 15) >> 4;
-        const u32x4_t* hb[kNB];
+        const u32x4_t* wb = (const u32x4_t*)expert_base(p.w2, p.sh_w2, xs, p.E, expert_bytes);
+        const u32x4_t* const a[1] = {wb + (size_t)(it * 16 + r) * row_units + g};
+        const u32x4_t* hb[NB];
 #pragma unroll
-        for (int tb = 0; tb < kNB; ++tb) {
+        for (int tb = 0; tb < NB; ++tb) {
             int n = tb * 16 + r;
-            n = n < ntok ? n : 0;
+            n = (tb < nb && n < ntok) ? n : 0;
             hb[tb] = (const u32x4_t*)p.h + (size_t)(row0 + n) * row_units + g;
         }
-        f32x4_t acc[kNB];
+        f32x4_t acc[1][NB];
 #pragma unroll
-        for (int tb = 0; tb < kNB; ++tb) acc[tb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-        for (int ks = 0; ks < ksteps; ks += U) {
-            u32x4_t aw[U];
+        for (int tb = 0; tb < NB; ++tb) acc[0][tb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        tile_contract<M, U, 1, NB>(a, hb, nb, ksteps, acc);
 #pragma unroll
-            for (int u = 0; u < U; ++u) aw[u] = __builtin_nontemporal_load(a + 4 * (ks + u));
-#pragma unroll
-            for (int tb = 0; tb < kNB; ++tb) {
-                if (tb < nb) {
-#pragma unroll
-                    for (int u = 0; u < U; ++u) M::mma(acc[tb], aw[u], hb[tb][4 * (ks + u)]);
-                }
-            }
-        }
-#pragma unroll
-        for (int tb = 0; tb < kNB; ++tb) {
+        for (int tb = 0; tb < NB; ++tb) {
             const int n = tb * 16 + r;
             if (tb < nb && n < ntok) {
                 float* o = p.yperm + (size_t)(row0 + n) * p.d + it * 16 + 4 * g;
-                *(float4*)o = make_float4(acc[tb][0], acc[tb][1], acc[tb][2], acc[tb][3]);
+                *(float4*)o = make_float4(acc[0][tb][0], acc[0][tb][1], acc[0][tb][2], acc[0][tb][3]);
             }
         }
     }
@@ -184,8 +241,9 @@ __global__ __launch_bounds__(kFfnThreads) void k_down(FfnParams p) {
 
 // One thread per 4 output features of one token.
 __global__ __launch_bounds__(256) void k_combine(FfnParams p) {
-    const int t = blockIdx.y;
-    const int c = (blockIdx.x * 256 + threadIdx.x) * 4;
+    const int per_tok = (p.d / 4 + 255) / 256;
+    const int t = blockIdx.x / per_tok;
+    const int c = ((blockIdx.x - t * per_tok) * 256 + threadIdx.x) * 4;
     if (c >= p.d) return;
     const int slots = p.k + p.n_shared;
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
@@ -224,32 +282,45 @@ int grid_for(long long waves_needed) {
     return (int)(wgs < 1 ? 1 : (wgs < cap ? wgs : cap));
 }
 
-}  // namespace
-
-hipError_t launch_gate_up(const FfnParams& p, int w_dtype, int max_chunks, hipStream_t s) {
-    const dim3 grid(grid_for((long long)max_chunks * (p.f / 16)));
-    if (w_dtype == CAEE_BF16)
-        hipLaunchKernelGGL((k_gate_up<Bf16Math, 4>), grid, dim3(kFfnThreads), 0, s, p);
-    else if (w_dtype == CAEE_F32)
-        hipLaunchKernelGGL((k_gate_up<F32Math, 4>), grid, dim3(kFfnThreads), 0, s, p);
-    else
-        return hipErrorInvalidValue;
+template <class M, template <class, int, int> class K, int U>
+hipError_t launch_nb(const FfnParams& p, int nb, dim3 grid, hipStream_t s) {
+    switch (nb) {
+        case 1: hipLaunchKernelGGL((K<M, U, 1>::run), grid, dim3(kFfnThreads), 0, s, p); break;
+        case 2: hipLaunchKernelGGL((K<M, U, 2>::run), grid, dim3(kFfnThreads), 0, s, p); break;
+        case 4: hipLaunchKernelGGL((K<M, U, 4>::run), grid, dim3(kFfnThreads), 0, s, p); break;
+        case 8: hipLaunchKernelGGL((K<M, U, 8>::run), grid, dim3(kFfnThreads), 0, s, p); break;
+        default: return hipErrorInvalidValue;
+    }
     return hipGetLastError();
 }
 
-hipError_t launch_down(const FfnParams& p, int w_dtype, int max_chunks, hipStream_t s) {
+template <class M, int U, int NB>
+struct GateUpK {
+    static constexpr auto run = k_gate_up<M, U, NB>;
+};
+template <class M, int U, int NB>
+struct DownK {
+    static constexpr auto run = k_down<M, U, NB>;
+};
+
+}  // namespace
+
+hipError_t launch_gate_up(const FfnParams& p, int w_dtype, int nb, int max_chunks, hipStream_t s) {
+    const dim3 grid(grid_for((long long)max_chunks * (p.f / 16) * p.ksplit));   // waves wanted
+    if (w_dtype == CAEE_BF16) return launch_nb<Bf16Math, GateUpK, kGateUpU>(p, nb, grid, s);
+    if (w_dtype == CAEE_F32) return launch_nb<F32Math, GateUpK, kGateUpU>(p, nb, grid, s);
+    return hipErrorInvalidValue;
+}
+
+hipError_t launch_down(const FfnParams& p, int w_dtype, int nb, int max_chunks, hipStream_t s) {
     const dim3 grid(grid_for((long long)max_chunks * (p.d / 16)));
-    if (w_dtype == CAEE_BF16)
-        hipLaunchKernelGGL((k_down<Bf16Math, 4>), grid, dim3(kFfnThreads), 0, s, p);
-    else if (w_dtype == CAEE_F32)
-        hipLaunchKernelGGL((k_down<F32Math, 4>), grid, dim3(kFfnThreads), 0, s, p);
-    else
-        return hipErrorInvalidValue;
-    return hipGetLastError();
+    if (w_dtype == CAEE_BF16) return launch_nb<Bf16Math, DownK, kDownU>(p, nb, grid, s);
+    if (w_dtype == CAEE_F32) return launch_nb<F32Math, DownK, kDownU>(p, nb, grid, s);
+    return hipErrorInvalidValue;
 }
 
 hipError_t launch_combine(const FfnParams& p, hipStream_t s) {
-    const dim3 grid((p.d / 4 + 255) / 256, p.T);
+    const dim3 grid(((p.d / 4 + 255) / 256) * p.T);
     hipLaunchKernelGGL(k_combine, grid, dim3(256), 0, s, p);
     return hipGetLastError();
 }

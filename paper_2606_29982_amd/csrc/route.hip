@@ -21,7 +21,9 @@
 namespace caee {
 namespace {
 
-constexpr int kRouteWaves = kRouteThreads / kWave;
+constexpr int kTokWaves = 4;                       // tokens (wavefronts) per workgroup
+constexpr int kTokThreads = kTokWaves * kWave;
+constexpr int kMaskT = 1024;                       // batch size up to which the permutation uses LDS bitmasks
 constexpr int kNoIdx = 0x7fffffff;
 
 // Larger value wins; equal values go to the lower index.
@@ -32,13 +34,61 @@ __device__ inline void argmax_merge(double& v, int& i, double ov, int oi) {
     }
 }
 
+// Cross-lane moves within a 16-lane row through DPP (no LDS round trip).
+template <int C>
+__device__ inline int dpp_i(int v) {
+    return __builtin_amdgcn_mov_dpp(v, C, 0xF, 0xF, false);
+}
+template <int C>
+__device__ inline double dpp_d(double v) {
+    const long long b = __double_as_longlong(v);
+    const int lo = dpp_i<C>((int)b);
+    const int hi = dpp_i<C>((int)(b >> 32));
+    return __longlong_as_double(((long long)hi << 32) | (unsigned int)lo);
+}
+__device__ inline double readlane_d(double v, int lane) {
+    const long long b = __double_as_longlong(v);
+    const int lo = __builtin_amdgcn_readlane((int)b, lane);
+    const int hi = __builtin_amdgcn_readlane((int)(b >> 32), lane);
+    return __longlong_as_double(((long long)hi << 32) | (unsigned int)lo);
+}
+
+// DPP controls that pair every lane of a row with another one:
+// quad_perm [1,0,3,2], quad_perm [2,3,0,1], row_half_mirror, row_mirror.
+constexpr int kDppXor1 = 0xB1, kDppXor2 = 0x4E, kDppHalfMirror = 0x141, kDppMirror = 0x140;
+
+template <int C>
+__device__ inline void argmax_step(double& v, int& i) {
+    const double ov = dpp_d<C>(v);
+    const int oi = dpp_i<C>(i);
+    argmax_merge(v, i, ov, oi);
+}
+
+// Wave-wide argmax: butterfly inside each 16-lane row, then the four row
+// results are combined from scalar reads.  Every lane gets the result.
 __device__ inline void wave_argmax(double& v, int& i) {
+    argmax_step<kDppXor1>(v, i);
+    argmax_step<kDppXor2>(v, i);
+    argmax_step<kDppHalfMirror>(v, i);
+    argmax_step<kDppMirror>(v, i);
+    double bv = readlane_d(v, 0);
+    int bi = __builtin_amdgcn_readlane(i, 0);
 #pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) {
-        const double ov = __shfl_xor(v, off);
-        const int oi = __shfl_xor(i, off);
-        argmax_merge(v, i, ov, oi);
-    }
+    for (int r = 1; r < 4; ++r) argmax_merge(bv, bi, readlane_d(v, 16 * r), __builtin_amdgcn_readlane(i, 16 * r));
+    v = bv;
+    i = bi;
+}
+
+// Merge two (largest, second largest) pairs.
+__device__ inline void top2_merge(double& t1, double& t2, double o1, double o2) {
+    const double n1 = fmax(t1, o1);
+    const double n2 = fmax(fmin(t1, o1), fmax(t2, o2));
+    t1 = n1;
+    t2 = n2;
+}
+template <int C>
+__device__ inline void top2_step(double& t1, double& t2) {
+    top2_merge(t1, t2, dpp_d<C>(t1), dpp_d<C>(t2));
 }
 
 // Lane `lane` holds experts lane*EPL .. lane*EPL+EPL-1.
@@ -73,7 +123,7 @@ __device__ inline double score_of(const double (&s)[EPL], int lane, int e) {
 // Phase A for token t: writes K_t (rank order), G(t) and the token's top expert.
 template <int EPL>
 __device__ void route_token(const RouteParams& p, int t, int lane, int* ids, double* gout,
-                            int* top1, double* sbuf) {
+                            int* top1, double* sbuf, int* sids) {
     double s[EPL], key[EPL];
     load_scores<EPL>(p, t, lane, s, key);
     const bool lane_valid = lane * EPL < p.E;
@@ -89,14 +139,12 @@ __device__ void route_token(const RouteParams& p, int t, int lane, int* ids, dou
             t2 = key[i];
         }
     }
-    for (int off = 1; off < p.lpg; off <<= 1) {
-        const double o1 = __shfl_xor(t1, off);
-        const double o2 = __shfl_xor(t2, off);
-        const double n1 = fmax(t1, o1);
-        const double n2 = fmax(fmin(t1, o1), fmax(t2, o2));
-        t1 = n1;
-        t2 = n2;
-    }
+    // Reduce over the lpg lanes holding one group (aligned blocks of lpg lanes).
+    if (p.lpg >= 2) top2_step<kDppXor1>(t1, t2);
+    if (p.lpg >= 4) top2_step<kDppXor2>(t1, t2);
+    if (p.lpg >= 8) top2_step<kDppHalfMirror>(t1, t2);
+    if (p.lpg >= 16) top2_step<kDppMirror>(t1, t2);
+    for (int off = 16; off < p.lpg; off <<= 1) top2_merge(t1, t2, __shfl_xor(t1, off), __shfl_xor(t2, off));
     const double gscore = p.gsize >= 2 ? t1 + t2 : t1;
     const int my_group = lane_valid ? (lane * EPL) / p.gsize : kNoIdx;
 
@@ -127,7 +175,7 @@ __device__ void route_token(const RouteParams& p, int t, int lane, int* ids, dou
             if (lane * EPL + i == ei) chosen[i] = true;
         const double sv = score_of<EPL>(s, lane, ei);
         if (lane == 0) {
-            ids[r] = ei;
+            sids[r] = ei;
             sbuf[r] = sv;
         }
     }
@@ -138,10 +186,12 @@ __device__ void route_token(const RouteParams& p, int t, int lane, int* ids, dou
         double bg = -1.0;
         for (int r = 0; r < p.k; ++r) {
             const double g = sbuf[r] / total;
+            const int e = sids[r];
+            ids[r] = e;
             gout[r] = g;
-            if (g > bg || (g == bg && ids[r] < best)) {
+            if (g > bg || (g == bg && e < best)) {
                 bg = g;
-                best = ids[r];
+                best = e;
             }
         }
         *top1 = best;
@@ -229,176 +279,200 @@ __device__ void compensate_token(const RouteParams& p, int t, int lane, const in
     }
 }
 
+// Routing kernel: one wavefront per token (phase A).  Block 0 also resets
+// the counters the later kernels of this call accumulate into.
 template <int EPL>
-__global__ __launch_bounds__(kRouteThreads) void k_route_fused(RouteParams p) {
-    __shared__ int s_orig[kFusedMaxT * kMaxK];
-    __shared__ double s_g[kFusedMaxT * kMaxK];
-    __shared__ int s_fin[kFusedMaxT * kMaxK];
-    __shared__ int s_top1[kFusedMaxT];
-    __shared__ double s_sbuf[kRouteWaves][kMaxK];
+__global__ __launch_bounds__(kTokThreads) void k_route_tokens(RouteParams p) {
+    __shared__ double s_sbuf[kTokWaves][kMaxK];
+    __shared__ int s_ids[kTokWaves][kMaxK];
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = threadIdx.x / kWave;
+    const int t = blockIdx.x * kTokWaves + wave;
+    if (blockIdx.x == 0 && threadIdx.x < 4) p.counters[threadIdx.x] = 0;
+    if (t < p.T)
+        route_token<EPL>(p, t, lane, p.orig_ids + (size_t)t * p.k, p.gbuf + (size_t)t * p.k, p.top1 + t,
+                         s_sbuf[wave], s_ids[wave]);
+}
+
+// Pruning kernel (one workgroup): Sec. IV-B steps 1-4 over the whole batch.
+// Bin loads are float64 sums of fp32 costs; while a bin's nonzero costs span
+// less than 2^20 every such sum is exact, so the order of the additions (LDS
+// atomics here) does not change any value or decision.
+__global__ __launch_bounds__(kRouteThreads) void k_prune(RouteParams p) {
     __shared__ unsigned long long s_imp[kMaxE];
-    __shared__ uint8_t s_act[kMaxE], s_must[kMaxE], s_prom[kMaxE], s_trans[kMaxE];
+    __shared__ uint8_t s_act[kMaxE], s_must[kMaxE], s_prom[kMaxE];
     __shared__ float s_cost[kMaxE];
     __shared__ int s_bin[kMaxE];
-    __shared__ int s_sorted[kMaxE];
-    __shared__ double s_mload[kMaxBins];
+    __shared__ int s_sorted[kMaxE];      // candidates in visiting order
+    __shared__ int s_cbin[kMaxE];        // their bins
+    __shared__ float s_ccost[kMaxE];     // their costs
+    __shared__ double s_aload[kMaxBins], s_mload[kMaxBins];
     __shared__ double s_fbase;
-    __shared__ int s_counts[4];   // candidates, refilled slots, empty slots
-    __shared__ int s_cnt[kMaxE + kMaxShared];
-    __shared__ int s_off[kMaxE + kMaxShared + 1];
+    __shared__ int s_ncand;
 
     const int tid = threadIdx.x;
     const int lane = tid & (kWave - 1);
     const int wave = tid / kWave;
-    const int T = p.T, E = p.E, k = p.k;
+    const int T = p.T, E = p.E, k = p.k, nb = p.n_bins;
 
-    if (p.do_route) {
-        for (int t = wave; t < T; t += kRouteWaves)
-            route_token<EPL>(p, t, lane, &s_orig[t * k], &s_g[t * k], &s_top1[t], s_sbuf[wave]);
-        for (int e = tid; e < E; e += kRouteThreads) {
-            s_imp[e] = 0ull;
-            s_act[e] = s_must[e] = s_prom[e] = 0;
-            s_cost[e] = p.cost[e];
-            s_bin[e] = p.bin ? p.bin[e] : 0;
-        }
-        if (tid < 4) s_counts[tid] = 0;
-        __syncthreads();
-
-        // Step 1: A_act, I(e) = max gate weight, A_must (threshold + each token's top expert).
-        for (int i = tid; i < T * k; i += kRouteThreads) {
-            const int e = s_orig[i];
-            const double g = s_g[i];
-            atomicMax(&s_imp[e], (unsigned long long)__double_as_longlong(g));
-            s_act[e] = 1;
-            if (g >= p.tau) s_must[e] = 1;
-            if (p.orig_ids) p.orig_ids[i] = e;
-        }
-        for (int t = tid; t < T; t += kRouteThreads) s_must[s_top1[t]] = 1;
-        __syncthreads();
-
-        // Step 2: per-bin loads of A_act and A_must (ascending expert order).
-        for (int b = tid; b < p.n_bins; b += kRouteThreads) {
-            double la = 0.0, lm = 0.0;
-            for (int e = 0; e < E; ++e) {
-                if (s_bin[e] != b) continue;
-                if (s_act[e]) la += (double)s_cost[e];
-                if (s_must[e]) lm += (double)s_cost[e];
-            }
-            s_mload[b] = lm;
-            if (p.bin_loads) {
-                p.bin_loads[b] = la;
-                p.bin_loads[p.n_bins + b] = lm;
-            }
-        }
-        // Candidate visiting order: importance descending, index ascending.
-        for (int e = tid; e < E; e += kRouteThreads) {
-            if (s_act[e] && !s_must[e]) {
-                const unsigned long long ie = s_imp[e];
-                int rank = 0;
-                for (int o = 0; o < E; ++o) {
-                    if (s_act[o] && !s_must[o]) {
-                        const unsigned long long io = s_imp[o];
-                        rank += (io > ie || (io == ie && o < e)) ? 1 : 0;
-                    }
-                }
-                s_sorted[rank] = e;
-                atomicAdd(&s_counts[0], 1);
-            }
-        }
-        __syncthreads();
-        if (tid == 0) {
-            double fb = 0.0;
-            for (int b = 0; b < p.n_bins; ++b) fb = fmax(fb, s_mload[b]);
-            s_fbase = fb;
-        }
-        __syncthreads();
-
-        // Step 3: cost-invariant expansion, one bin per thread (bins are independent).
-        const int n_cand = s_counts[0];
-        for (int b = tid; b < p.n_bins; b += kRouteThreads) {
-            double load = s_mload[b];
-            for (int r = 0; r < n_cand; ++r) {
-                const int e = s_sorted[r];
-                if (s_bin[e] != b) continue;
-                const double c = (double)s_cost[e];
-                if (load + c <= s_fbase) {
-                    s_prom[e] = 1;
-                    load += c;
-                }
-            }
-            if (p.bin_loads) p.bin_loads[2 * p.n_bins + b] = load;
-        }
-        __syncthreads();
-        // Step 4: A_trans = A_must + promoted.
-        for (int e = tid; e < E; e += kRouteThreads) s_trans[e] = s_must[e] | s_prom[e];
-        __syncthreads();
-
-        if (p.masks) {
-            const int words = (E + 31) / 32;
-            for (int w = tid; w < words; w += kRouteThreads) {
-                uint32_t act = 0, must = 0, trans = 0, pruned = 0;
-                for (int j = 0; j < 32 && w * 32 + j < E; ++j) {
-                    const int e = w * 32 + j;
-                    act |= (uint32_t)s_act[e] << j;
-                    must |= (uint32_t)s_must[e] << j;
-                    trans |= (uint32_t)s_trans[e] << j;
-                    pruned |= (uint32_t)(s_act[e] && !s_trans[e]) << j;
-                }
-                p.masks[w] = act;
-                p.masks[words + w] = must;
-                p.masks[2 * words + w] = trans;
-                p.masks[3 * words + w] = pruned;
-            }
-        }
-
-        // Phase C: compensation.
-        for (int t = wave; t < T; t += kRouteWaves)
-            compensate_token<EPL>(p, t, lane, &s_orig[t * k], s_trans, &s_fin[t * k], s_sbuf[wave],
-                                  &s_counts[1], &s_counts[2]);
-        __syncthreads();
-
-        if (p.stats && wave == 0) {
-            int n_act = 0, n_must = 0, n_prom = 0, n_pruned = 0, n_trans = 0;
-            for (int base = 0; base < E; base += kWave) {
-                const int e = base + lane;
-                const bool v = e < E;
-                n_act += __popcll(__ballot(v && s_act[e]));
-                n_must += __popcll(__ballot(v && s_must[e]));
-                n_prom += __popcll(__ballot(v && s_prom[e]));
-                n_pruned += __popcll(__ballot(v && s_act[e] && !s_trans[e]));
-                n_trans += __popcll(__ballot(v && s_trans[e]));
-            }
-            if (lane == 0) {
-                p.stats[0] = n_act;
-                p.stats[1] = n_must;
-                p.stats[2] = s_counts[0];
-                p.stats[3] = n_prom;
-                p.stats[4] = n_pruned;
-                p.stats[5] = n_trans;
-                p.stats[6] = s_counts[1];
-                p.stats[7] = s_counts[2];
-            }
-        }
-    } else {
-        // Caller-supplied ids: anything outside [0, E) is an empty slot.
-        for (int i = tid; i < T * k; i += kRouteThreads) {
-            const int e = p.topk_ids[i];
-            s_fin[i] = (e >= 0 && e < E) ? e : -1;
-        }
-        __syncthreads();
+    for (int e = tid; e < E; e += kRouteThreads) {
+        s_imp[e] = 0ull;
+        s_act[e] = s_must[e] = s_prom[e] = 0;
+        s_cost[e] = p.cost[e];
+        const int b = p.bin ? p.bin[e] : 0;
+        s_bin[e] = (b >= 0 && b < nb) ? b : -1;   // out-of-range bins (a precondition violation) count nowhere
     }
+    for (int b = tid; b < nb; b += kRouteThreads) s_aload[b] = s_mload[b] = 0.0;
+    if (tid == 0) s_ncand = 0;
+    __syncthreads();
 
-    if (!p.do_permute) return;
+    // Step 1: A_act, I(e) = max gate weight, A_must (threshold + each token's top expert).
+    for (int i = tid; i < T * k; i += kRouteThreads) {
+        const int e = p.orig_ids[i];
+        const double g = p.gbuf[i];
+        atomicMax(&s_imp[e], (unsigned long long)__double_as_longlong(g));
+        s_act[e] = 1;
+        if (g >= p.tau) s_must[e] = 1;
+    }
+    __syncthreads();
+    for (int t = tid; t < T; t += kRouteThreads) s_must[p.top1[t]] = 1;
+    __syncthreads();
 
-    // Permutation: rows of expert slot x (x < E routed, E+s shared) are
-    // [off[x], off[x+1]), tokens ascending within a slot.
+    // Step 2: per-bin loads of A_act and A_must; candidate visiting order
+    // (importance descending, index ascending).
+    for (int e = tid; e < E; e += kRouteThreads) {
+        const double c = (double)s_cost[e];
+        const int b = s_bin[e];
+        if (s_act[e] && b >= 0) atomicAdd(&s_aload[b], c);
+        if (s_must[e] && b >= 0) atomicAdd(&s_mload[b], c);
+        if (s_act[e] && !s_must[e]) {
+            const unsigned long long ie = s_imp[e];
+            int rank = 0;
+#pragma unroll 8
+            for (int o = 0; o < E; ++o) {
+                const unsigned long long io = s_imp[o];
+                const bool cand = s_act[o] && !s_must[o];
+                rank += (cand && (io > ie || (io == ie && o < e))) ? 1 : 0;
+            }
+            s_sorted[rank] = e;
+            s_cbin[rank] = b;
+            s_ccost[rank] = s_cost[e];
+            atomicAdd(&s_ncand, 1);
+        }
+    }
+    __syncthreads();
+    if (wave == 0) {
+        double fb = 0.0;
+        for (int b = lane; b < nb; b += kWave) fb = fmax(fb, s_mload[b]);
+        for (int off = 32; off >= 1; off >>= 1) fb = fmax(fb, __shfl_xor(fb, off));
+        if (lane == 0) s_fbase = fb;
+    }
+    for (int b = tid; b < nb && p.bin_loads; b += kRouteThreads) {
+        p.bin_loads[b] = s_aload[b];
+        p.bin_loads[nb + b] = s_mload[b];
+    }
+    __syncthreads();
+
+    // Step 3: cost-invariant expansion, one bin per thread (bins are
+    // independent), walking the candidates in visiting order.
+    const int n_cand = s_ncand;
+    const double fbase = s_fbase;
+    for (int b = tid; b < nb; b += kRouteThreads) {
+        double load = s_mload[b];
+        for (int r = 0; r < n_cand; ++r) {
+            if (s_cbin[r] != b) continue;
+            const double c = (double)s_ccost[r];
+            if (load + c <= fbase) {
+                s_prom[s_sorted[r]] = 1;
+                load += c;
+            }
+        }
+        if (p.bin_loads) p.bin_loads[2 * nb + b] = load;
+    }
+    __syncthreads();
+
+    // Step 4: A_trans = A_must + promoted; masks and counters by ballot.
+    for (int e = tid; e < E; e += kRouteThreads) p.trans[e] = s_must[e] | s_prom[e];
+    if (wave == 0) {
+        const int words = (E + 31) / 32;
+        int n_act = 0, n_must = 0, n_prom = 0, n_pruned = 0, n_trans = 0;
+        for (int base = 0; base < E; base += kWave) {
+            const int e = base + lane;
+            const bool v = e < E;
+            const bool act = v && s_act[e], must = v && s_must[e], prom = v && s_prom[e];
+            const bool trans = must || prom;
+            const unsigned long long ba = __ballot(act), bm = __ballot(must), bt = __ballot(trans),
+                                     bp = __ballot(act && !trans), bpr = __ballot(prom);
+            n_act += __popcll(ba);
+            n_must += __popcll(bm);
+            n_prom += __popcll(bpr);
+            n_pruned += __popcll(bp);
+            n_trans += __popcll(bt);
+            if (p.masks && lane < 2) {
+                const int w = base / 32 + lane;
+                if (w < words) {
+                    const int sh = 32 * lane;
+                    p.masks[w] = (uint32_t)(ba >> sh);
+                    p.masks[words + w] = (uint32_t)(bm >> sh);
+                    p.masks[2 * words + w] = (uint32_t)(bt >> sh);
+                    p.masks[3 * words + w] = (uint32_t)(bp >> sh);
+                }
+            }
+        }
+        if (p.stats && lane == 0) {
+            p.stats[0] = n_act;
+            p.stats[1] = n_must;
+            p.stats[2] = n_cand;
+            p.stats[3] = n_prom;
+            p.stats[4] = n_pruned;
+            p.stats[5] = n_trans;
+        }
+    }
+}
+
+// Permutation of K_final (read from global memory) by expert slot: rows of
+// slot x (x < E routed, E+s shared) are [off[x], off[x+1]), tokens ascending
+// within a slot; then the FFN work list of chunks of at most chunk_tokens rows.
+// Executed by one workgroup of `nthr` threads.  Up to kMaskT tokens, each
+// expert's tokens are kept as a bitmask in LDS and every (token, slot) entry
+// finds its row independently by counting set bits; larger batches walk
+// K_final expert by expert.
+__device__ void permute_all(const RouteParams& p, int tid, int nthr, int* s_cnt, int* s_off, int* s_tot,
+                            unsigned long long* s_mask) {
+    const int T = p.T, E = p.E, k = p.k;
     const int nx = E + p.n_shared;
     const int slots = k + p.n_shared;
-    for (int x = tid; x < nx; x += kRouteThreads) s_cnt[x] = x < E ? 0 : T;
-    __syncthreads();
-    for (int i = tid; i < T * k; i += kRouteThreads) {
-        const int e = s_fin[i];
-        if (e >= 0) atomicAdd(&s_cnt[e], 1);
+    const int lane = tid & (kWave - 1);
+    const int wave = tid / kWave;
+    const int ch = p.chunk_tokens;
+    const bool masked = T <= kMaskT;
+    const int W = (T + 63) / 64;
+    if (masked) {
+        for (int i = tid; i < E * W; i += nthr) s_mask[i] = 0ull;
+        __syncthreads();
+        for (int i = tid; i < T * k; i += nthr) {
+            const int e = p.topk_ids[i];
+            if (e >= 0 && e < E) {
+                const int t = i / k;
+                atomicOr(&s_mask[e * W + (t >> 6)], 1ull << (t & 63));
+            }
+        }
+        __syncthreads();
+        for (int x = tid; x < nx; x += nthr) {
+            int c = T;
+            if (x < E) {
+                c = 0;
+                for (int w = 0; w < W; ++w) c += __popcll(s_mask[x * W + w]);
+            }
+            s_cnt[x] = c;
+        }
+    } else {
+        for (int x = tid; x < nx; x += nthr) s_cnt[x] = x < E ? 0 : T;
+        __syncthreads();
+        for (int i = tid; i < T * k; i += nthr) {
+            const int e = p.topk_ids[i];
+            if (e >= 0 && e < E) atomicAdd(&s_cnt[e], 1);
+        }
     }
     __syncthreads();
     if (wave == 0) {
@@ -408,7 +482,7 @@ __global__ __launch_bounds__(kRouteThreads) void k_route_fused(RouteParams p) {
         int sum = 0, csum = 0;
         for (int x = lo; x < hi; ++x) {
             sum += s_cnt[x];
-            csum += (s_cnt[x] + kChunkTokens - 1) / kChunkTokens;
+            csum += (s_cnt[x] + ch - 1) / ch;
         }
         int inc = sum, cinc = csum;
         for (int off = 1; off < kWave; off <<= 1) {
@@ -424,15 +498,15 @@ __global__ __launch_bounds__(kRouteThreads) void k_route_fused(RouteParams p) {
             const int cnt = s_cnt[x];
             s_off[x] = run;
             p.perm_off[x] = run;
-            for (int c = 0; c * kChunkTokens < cnt; ++c) {
-                int* ch = p.chunks + 4 * (crun + c);
-                ch[0] = x;
-                ch[1] = run + c * kChunkTokens;
-                ch[2] = min(kChunkTokens, cnt - c * kChunkTokens);
-                ch[3] = 0;
+            for (int c = 0; c * ch < cnt; ++c) {
+                int* chk = p.chunks + 4 * (crun + c);
+                chk[0] = x;
+                chk[1] = run + c * ch;
+                chk[2] = min(ch, cnt - c * ch);
+                chk[3] = 0;
             }
             run += cnt;
-            crun += (cnt + kChunkTokens - 1) / kChunkTokens;
+            crun += (cnt + ch - 1) / ch;
         }
         const int total = __shfl(inc, kWave - 1);
         const int ctotal = __shfl(cinc, kWave - 1);
@@ -440,42 +514,122 @@ __global__ __launch_bounds__(kRouteThreads) void k_route_fused(RouteParams p) {
             s_off[nx] = total;
             p.perm_off[nx] = total;
             *p.n_chunks = ctotal;
+            *s_tot = ctotal;
         }
     }
     __syncthreads();
-    for (int x = tid; x < nx; x += kRouteThreads) {
-        int pos = s_off[x];
-        if (x < E) {
-            if (s_cnt[x] == 0) continue;
-            for (int t = 0; t < T; ++t) {
-                for (int j = 0; j < k; ++j) {
-                    if (s_fin[t * k + j] == x) {
-                        p.perm_tok[pos] = t;
-                        p.perm_pos[t * slots + j] = pos;
-                        ++pos;
-                    }
-                }
+    // Shared experts: every token, in order.
+    for (int i = tid; i < T * p.n_shared; i += nthr) {
+        const int t = i / p.n_shared, sh = i - t * p.n_shared;
+        const int pos = s_off[E + sh] + t;
+        p.perm_tok[pos] = t;
+        p.perm_pos[t * slots + k + sh] = pos;
+    }
+    if (masked) {
+        for (int i = tid; i < T * k; i += nthr) {
+            const int e = p.topk_ids[i];
+            const int t = i / k;
+            const int j = i - t * k;
+            if (e < 0 || e >= E) {
+                p.perm_pos[t * slots + j] = -1;
+                continue;
             }
-        } else {
-            for (int t = 0; t < T; ++t) {
-                p.perm_tok[pos + t] = t;
-                p.perm_pos[t * slots + k + (x - E)] = pos + t;
+            const unsigned long long* m = s_mask + e * W;
+            int rank = __popcll(m[t >> 6] & ((1ull << (t & 63)) - 1ull));
+            for (int w = 0; w < (t >> 6); ++w) rank += __popcll(m[w]);
+            const int pos = s_off[e] + rank;
+            p.perm_tok[pos] = t;
+            p.perm_pos[t * slots + j] = pos;
+        }
+        return;
+    }
+    for (int x = tid; x < E; x += nthr) {
+        int pos = s_off[x];
+        if (s_cnt[x] == 0) continue;
+        const int n = T * k;
+        for (int i0 = 0; i0 < n; i0 += 8) {
+            int id[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) id[j] = i0 + j < n ? p.topk_ids[i0 + j] : -1;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                if (id[j] == x) {
+                    const int i = i0 + j;
+                    const int t = i / k;
+                    p.perm_tok[pos] = t;
+                    p.perm_pos[t * slots + (i - t * k)] = pos;
+                    ++pos;
+                }
             }
         }
     }
-    for (int i = tid; i < T * k; i += kRouteThreads)
-        if (s_fin[i] < 0) p.perm_pos[(i / k) * slots + (i % k)] = -1;
+    for (int i = tid; i < T * k; i += nthr) {
+        const int e = p.topk_ids[i];
+        if (e < 0 || e >= E) p.perm_pos[(i / k) * slots + (i % k)] = -1;
+    }
+}
+
+// Compensation kernel: one wavefront per token (phase C).
+template <int EPL>
+__global__ __launch_bounds__(kTokThreads) void k_compensate(RouteParams p) {
+    __shared__ uint8_t s_trans[kMaxE];
+    __shared__ double s_sbuf[kTokWaves][kMaxK];
+    __shared__ int s_fin[kTokWaves][kMaxK];
+    const int tid = threadIdx.x;
+    const int lane = tid & (kWave - 1);
+    const int wave = tid / kWave;
+    for (int e = tid; e < p.E; e += kTokThreads) s_trans[e] = p.trans[e];
+    __syncthreads();
+    const int t = blockIdx.x * kTokWaves + wave;
+    if (t < p.T)
+        compensate_token<EPL>(p, t, lane, p.orig_ids + (size_t)t * p.k, s_trans, s_fin[wave], s_sbuf[wave],
+                              &p.counters[1], &p.counters[2]);
+}
+
+// Permutation of K_final (caller-supplied ids outside [0, E) are empty
+// slots) plus the refill/empty-slot counts of the compensation kernel.
+__global__ __launch_bounds__(kRouteThreads) void k_permute(RouteParams p) {
+    __shared__ int s_cnt[kMaxE + kMaxShared];
+    __shared__ int s_off[kMaxE + kMaxShared + 1];
+    __shared__ int s_tot;
+    __shared__ unsigned long long s_mask[kMaxE * (kMaskT / 64)];
+    if (threadIdx.x == 0 && p.stats) {
+        p.stats[6] = p.counters[1];
+        p.stats[7] = p.counters[2];
+    }
+    if (p.do_permute) permute_all(p, threadIdx.x, kRouteThreads, s_cnt, s_off, &s_tot, s_mask);
 }
 
 }  // namespace
 
 hipError_t launch_route(const RouteParams& p, hipStream_t s) {
+    const dim3 tok_grid((p.T + kTokWaves - 1) / kTokWaves);
+    auto token_kernels = [&](auto route_k, auto comp_k) -> hipError_t {
+        hipLaunchKernelGGL(route_k, tok_grid, dim3(kTokThreads), 0, s, p);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(k_prune, dim3(1), dim3(kRouteThreads), 0, s, p);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(comp_k, tok_grid, dim3(kTokThreads), 0, s, p);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        if (!p.do_permute && !p.stats) return hipSuccess;
+        hipLaunchKernelGGL(k_permute, dim3(1), dim3(kRouteThreads), 0, s, p);
+        return hipGetLastError();
+    };
     switch (p.epl) {
-        case 1: hipLaunchKernelGGL(k_route_fused<1>, dim3(1), dim3(kRouteThreads), 0, s, p); break;
-        case 2: hipLaunchKernelGGL(k_route_fused<2>, dim3(1), dim3(kRouteThreads), 0, s, p); break;
-        case 4: hipLaunchKernelGGL(k_route_fused<4>, dim3(1), dim3(kRouteThreads), 0, s, p); break;
+        case 1: return token_kernels(k_route_tokens<1>, k_compensate<1>);
+        case 2: return token_kernels(k_route_tokens<2>, k_compensate<2>);
+        case 4: return token_kernels(k_route_tokens<4>, k_compensate<4>);
         default: return hipErrorInvalidValue;
     }
+}
+
+hipError_t launch_permute(const RouteParams& p, hipStream_t s) {
+    RouteParams q = p;
+    q.stats = nullptr;   // counters are not filled when routing did not run
+    hipLaunchKernelGGL(k_permute, dim3(1), dim3(kRouteThreads), 0, s, q);
     return hipGetLastError();
 }
 

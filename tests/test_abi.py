@@ -61,7 +61,7 @@ def _ws_status(layer):
     (dict(n_bins=300), caee.CAEE_ERR_INVALID_ARG),
     (dict(x_dtype="f32"), caee.CAEE_ERR_INVALID_ARG),
     (dict(y_dtype="fp8"), caee.CAEE_ERR_INVALID_ARG),
-    (dict(T=129), caee.CAEE_ERR_UNSUPPORTED),
+    (dict(T=65537), caee.CAEE_ERR_UNSUPPORTED),
     (dict(E=192, n_group=8), caee.CAEE_ERR_UNSUPPORTED),      # 24 per group, 4 per lane: 6 lanes
 ])
 def test_descriptor_validation(kw, status):
