@@ -65,11 +65,21 @@ typedef enum caee_dtype {
     CAEE_FP8_E4M3 = 2   /* OCP FP8 E4M3 (max 448), used with fp32 block scales */
 } caee_dtype_t;
 
+/* Mandatory-set rule of the pruning step (Sec. IV-B step 1).  Every rule
+ * also keeps each token's own top expert, so no token loses all experts. */
 typedef enum caee_importance {
-    /* I(e) = largest normalised gate weight any token of the batch gives e.
-     * Sec. IV-B leaves I(e) open; with this choice no (token, expert) pair
-     * whose gate weight reaches tau is pruned. */
-    CAEE_IMPORTANCE_MAX = 0
+    /* I(e) = largest normalised gate weight any token of the batch gives e;
+     * A_must = {e : I(e) >= tau}.  Sec. IV-B leaves I(e) open; with this
+     * choice no (token, expert) pair whose gate weight reaches tau is pruned. */
+    CAEE_IMPORTANCE_MAX = 0,
+    /* I(e) = sum over tokens of G(t)_e, the on-device rule of Sec. V-C;
+     * A_must = {e : I(e) >= tau}.  Candidates are visited by this sum. */
+    CAEE_IMPORTANCE_SUM = 1,
+    /* Cumulative importance ratio, the offloading rule of Sec. V-B: each
+     * token keeps its shortest prefix of experts (gate weight descending)
+     * whose share of the token's gate mass reaches tau (theta_imp); A_must
+     * is the union.  Candidates are visited by their largest gate weight. */
+    CAEE_IMPORTANCE_CIR = 2
 } caee_importance_t;
 
 /* Shape and hyper-parameters of one MoE layer call. */
@@ -83,7 +93,8 @@ typedef struct caee_layer_desc {
     int32_t k;            /* experts per token, 1..16 and <= topk_group*E/n_group */
     int32_t n_shared;     /* shared experts added to every token with weight 1, 0..4 */
     float routed_scaling; /* factor on the renormalised routed weights, finite and > 0 */
-    float tau;            /* importance threshold theta of Sec. IV-B, finite and >= 0; 0 disables pruning */
+    float tau;            /* threshold of the importance rule (theta, or theta_imp for CIR), finite and >= 0;
+                             0 disables pruning for MAX and SUM */
     int32_t n_bins;       /* devices/links of the max-aggregated layer cost (Sec. IV-A), 1..256 */
     int32_t importance;   /* caee_importance_t */
     int32_t x_dtype;      /* hidden-state dtype: CAEE_F32 with f32 weights, else CAEE_BF16 */

@@ -27,8 +27,8 @@ taken in float64 here; the kernel takes them in float64 too, so selected and
 pruned expert indices are expected to match bit for bit.
 """
 from .routing import sigmoid_scores, group_limited_topk, gate_weights, route_batch  # noqa: F401
-from .pruning import (importance_max, mandatory_split, bin_loads,  # noqa: F401
-                      cost_aware_greedy, prune_batch)
+from .pruning import (importance_max, importance_sum, cir_mandatory, mandatory_split,  # noqa: F401
+                      bin_loads, cost_aware_greedy, prune_batch)
 from .compensation import compensate_token, compensate_batch  # noqa: F401
 from .ffn import (bf16_bits_to_f64, e4m3_decode, e4m3_encode_rne,  # noqa: F401
                   quantize_e4m3_blocks, swiglu_expert, expert_weights_f64)

@@ -9,11 +9,22 @@ experts.  Here the product R*C is one non-negative number per expert,
 ``cost[e]`` (0 for an expert that is already resident), and devices are
 ``n_bins`` bins given by ``bins[e]`` (None: one bin).
 
+Three mandatory rules, selected by ``rule``:
+  * "max": I(e) is the largest normalised gate weight that any token of the
+    batch gives e, and A_must = {e : I(e) >= tau}.  Sec. IV-B leaves I(e)
+    open; this reading makes "no expert whose gate weight reaches the
+    threshold is pruned" hold token by token.
+  * "sum": I(e) = sum over tokens of G(t)_e, the definition of the
+    on-device experiments (Sec. V-C), and A_must = {e : I(e) >= tau}.  The
+    sum runs over tokens in ascending order.
+  * "cir": the retention rule of the offloading experiments (Sec. V-B):
+    each token keeps its minimal number m* of top experts (by gate weight)
+    whose cumulative importance ratio CIR(m) = sum_{i<=m} G_i / sum_{j<=k} G_j
+    reaches tau (theta_imp); A_must is the union over tokens.  The ratio is
+    formed from the router scores s (G is s normalised), added in gate order.
+    Candidates are visited by their largest gate weight.
+
 Readings taken where the paper is silent or inconsistent:
-  * importance I(e) is the largest normalised gate weight that any token of
-    the batch gives e (the paper leaves I(e) open in Sec. IV-B and uses other
-    definitions in Sec. V; this one makes "no expert whose gate weight reaches
-    the threshold is pruned" hold token by token);
   * the candidate set is the activated experts that are not mandatory (the
     text writes the complement in all experts, but the final set must lie in
     the activated set);
@@ -48,12 +59,43 @@ def importance_max(orig_ids: np.ndarray, g: np.ndarray, E: int):
     return act, imp, top1
 
 
-def mandatory_split(act: np.ndarray, imp: np.ndarray, tau: float, top1):
+def importance_sum(orig_ids: np.ndarray, g: np.ndarray, E: int) -> np.ndarray:
+    """I(e) = sum over tokens t (ascending) with e in K_t of G(t)_e."""
+    imp = np.zeros(E, dtype=np.float64)
+    for t in range(orig_ids.shape[0]):
+        for e, gv in zip(orig_ids[t].tolist(), g[t].tolist()):
+            imp[e] = imp[e] + gv
+    return imp
+
+
+def cir_mandatory(orig_ids: np.ndarray, s: np.ndarray, theta_imp: float, E: int) -> np.ndarray:
+    """Per token: experts of K_t in gate order (score descending, lower index
+    first on ties); keep the shortest prefix whose cumulative ratio
+    (prefix sum of s) / (sum of s over K_t) reaches theta_imp."""
+    must = np.zeros(E, dtype=bool)
+    for t in range(orig_ids.shape[0]):
+        order = sorted(orig_ids[t].tolist(), key=lambda e: (-float(s[t, e]), e))
+        total = 0.0
+        for e in order:
+            total += float(s[t, e])
+        cum = 0.0
+        for e in order:
+            cum += float(s[t, e])
+            must[e] = True
+            if cum / total >= float(theta_imp):
+                break
+    return must
+
+
+def mandatory_split(act: np.ndarray, imp: np.ndarray, tau: float, top1, extra=None):
     """Step 1: A_must = {e in A_act : I(e) >= tau} plus each token's top
-    expert; A_cand = A_act minus A_must."""
+    expert (plus ``extra`` mandatory experts); A_cand = A_act minus A_must.
+    Pass tau = inf to skip the threshold."""
     must = act & (imp >= float(tau))
     for e in top1:
         must[e] = True
+    if extra is not None:
+        must |= extra
     cand = act & ~must
     return must, cand
 
@@ -90,11 +132,20 @@ def cost_aware_greedy(must: np.ndarray, cand: np.ndarray, imp: np.ndarray,
 
 
 def prune_batch(orig_ids: np.ndarray, g: np.ndarray, E: int, tau: float,
-                cost: np.ndarray, bins, n_bins: int) -> dict:
-    """Steps 1-4 for a routed batch.  Returns every set as a bool[E] mask
-    plus the loads and F_base."""
+                cost: np.ndarray, bins, n_bins: int, rule: str = "max", s=None) -> dict:
+    """Steps 1-4 for a routed batch under mandatory ``rule`` ("max", "sum"
+    or "cir"; "cir" needs the router scores ``s`` [T][E]).  Returns every set
+    as a bool[E] mask plus the loads and F_base."""
     act, imp, top1 = importance_max(orig_ids, g, E)
-    must, cand = mandatory_split(act, imp, tau, top1)
+    if rule == "max":
+        must, cand = mandatory_split(act, imp, tau, top1)
+    elif rule == "sum":
+        imp = importance_sum(orig_ids, g, E)
+        must, cand = mandatory_split(act, imp, tau, top1)
+    elif rule == "cir":
+        must, cand = mandatory_split(act, imp, float("inf"), top1, cir_mandatory(orig_ids, s, tau, E))
+    else:
+        raise ValueError(rule)
     trans, promoted, must_loads, final_loads, f_base, order = cost_aware_greedy(
         must, cand, imp, cost, bins, n_bins)
     return dict(act=act, imp=imp, top1=top1, must=must, cand=cand,

@@ -19,6 +19,7 @@ CAEE_OK, CAEE_ERR_INVALID_ARG, CAEE_ERR_UNSUPPORTED, CAEE_ERR_WORKSPACE, CAEE_ER
 CAEE_F32, CAEE_BF16, CAEE_FP8_E4M3 = 0, 1, 2
 KERNEL_KINDS = {"route": 0, "gate_up": 1, "down": 2, "combine": 3}
 DTYPE_CODE = {"f32": CAEE_F32, "bf16": CAEE_BF16, "fp8": CAEE_FP8_E4M3}
+IMPORTANCE_CODE = {"max": 0, "sum": 1, "cir": 2}
 
 
 class CaeeError(RuntimeError):
@@ -116,10 +117,12 @@ class Layer:
     w_dtype: str = "bf16"
     x_dtype: str = "bf16"
     y_dtype: str = "bf16"
+    importance: str = "max"     # "max" | "sum" | "cir" (caee_importance_t)
 
     def desc(self) -> LayerDesc:
         return LayerDesc(self.T, self.d, self.f, self.E, self.n_group, self.topk_group, self.k,
-                         self.n_shared, self.routed_scaling, self.tau, self.n_bins, 0,
+                         self.n_shared, self.routed_scaling, self.tau, self.n_bins,
+                         IMPORTANCE_CODE[self.importance],
                          DTYPE_CODE[self.x_dtype], DTYPE_CODE[self.w_dtype], DTYPE_CODE[self.y_dtype])
 
     @classmethod

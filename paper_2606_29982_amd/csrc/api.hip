@@ -51,7 +51,9 @@ caee_status_t check_desc(const caee_layer_desc_t* d) {
     if (!(isfinite(d->tau) && d->tau >= 0.0f)) return fail(CAEE_ERR_INVALID_ARG, "tau must be finite and >= 0");
     if (d->n_bins < 1 || d->n_bins > kMaxBins)
         return fail(CAEE_ERR_INVALID_ARG, "n_bins=%d must be in [1, %d]", d->n_bins, kMaxBins);
-    if (d->importance != CAEE_IMPORTANCE_MAX) return fail(CAEE_ERR_INVALID_ARG, "unknown importance=%d", d->importance);
+    if (d->importance != CAEE_IMPORTANCE_MAX && d->importance != CAEE_IMPORTANCE_SUM &&
+        d->importance != CAEE_IMPORTANCE_CIR)
+        return fail(CAEE_ERR_INVALID_ARG, "unknown importance=%d", d->importance);
     if (d->w_dtype != CAEE_F32 && d->w_dtype != CAEE_BF16 && d->w_dtype != CAEE_FP8_E4M3)
         return fail(CAEE_ERR_INVALID_ARG, "unknown w_dtype=%d", d->w_dtype);
     const int want_x = d->w_dtype == CAEE_F32 ? CAEE_F32 : CAEE_BF16;
@@ -212,6 +214,9 @@ RouteParams make_route_params(const caee_layer_desc_t* d, const float* logits, c
     p.gbuf = (double*)(ws + L.gbuf);
     p.top1 = (int32_t*)(ws + L.top1);
     p.trans = (uint8_t*)(ws + L.trans);
+    p.mflag = (uint8_t*)(ws + L.mflag);
+    p.imp_sum = (double*)(ws + L.imp_sum);
+    p.rule = d->importance;
     p.counters = (int32_t*)(ws + L.counters);
     p.chunk_tokens = L.chunk_tokens;
     p.orig_ids = (int32_t*)(ws + L.orig);

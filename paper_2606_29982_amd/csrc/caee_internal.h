@@ -48,6 +48,8 @@ struct WsLayout {
     size_t gbuf;                // [T][k] float64 normalised gate weights G(t)
     size_t top1;                // [T] each token's top expert
     size_t trans;               // [E] uint8 membership of A_trans
+    size_t mflag;               // [T][k] uint8: the (token, slot) pair is mandatory on its own
+    size_t imp_sum;             // [E] float64 batch-summed gate weight (SUM rule)
     size_t counters;            // [4] int: (unused), refilled slots, empty slots
     size_t perm_off;            // [E + n_shared + 1] first permuted row of each expert slot
     size_t perm_tok;            // [P] token of each permuted row
@@ -103,6 +105,8 @@ inline WsLayout ws_layout(const caee_layer_desc_t& d) {
     L.gbuf = take(T * d.k * 8);
     L.top1 = take(T * 4);
     L.trans = take(d.E);
+    L.mflag = take(T * d.k);
+    L.imp_sum = take(size_t(d.E) * 8);
     L.counters = take(16);
     L.perm_off = take(size_t(d.E + d.n_shared + 1) * 4);
     L.perm_tok = take(size_t(L.P) * 4);
@@ -125,6 +129,7 @@ struct RouteParams {
     int lpg;        // lanes per group (power of two)
     int gsize;      // experts per group
     double rs, tau;
+    int rule;       // caee_importance_t
     const float* logits;
     const float* bias;
     const float* cost;
@@ -140,6 +145,8 @@ struct RouteParams {
     double* gbuf;
     int32_t* top1;
     uint8_t* trans;
+    uint8_t* mflag;
+    double* imp_sum;
     int32_t* counters;
     int chunk_tokens;
     // permutation outputs

@@ -123,7 +123,7 @@ __device__ inline double score_of(const double (&s)[EPL], int lane, int e) {
 // Phase A for token t: writes K_t (rank order), G(t) and the token's top expert.
 template <int EPL>
 __device__ void route_token(const RouteParams& p, int t, int lane, int* ids, double* gout,
-                            int* top1, double* sbuf, int* sids) {
+                            int* top1, uint8_t* mflag, double* sbuf, int* sids) {
     double s[EPL], key[EPL];
     load_scores<EPL>(p, t, lane, s, key);
     const bool lane_valid = lane * EPL < p.E;
@@ -195,6 +195,35 @@ __device__ void route_token(const RouteParams& p, int t, int lane, int* ids, dou
             }
         }
         *top1 = best;
+        // Pairs that are mandatory on their own: the token's top expert, plus
+        // the threshold (MAX) or the cumulative-ratio prefix (CIR).
+        uint32_t flags = 0;
+        for (int r = 0; r < p.k; ++r) {
+            const bool f = sids[r] == best || (p.rule == CAEE_IMPORTANCE_MAX && sbuf[r] / total >= p.tau);
+            flags |= (uint32_t)f << r;
+        }
+        if (p.rule == CAEE_IMPORTANCE_CIR) {
+            // Slots in gate order: score descending, lower expert first on ties.
+            int ord[kMaxK];
+            for (int r = 0; r < p.k; ++r) {
+                int j = r;
+                while (j > 0 && (sbuf[ord[j - 1]] < sbuf[r] ||
+                                 (sbuf[ord[j - 1]] == sbuf[r] && sids[ord[j - 1]] > sids[r]))) {
+                    ord[j] = ord[j - 1];
+                    --j;
+                }
+                ord[j] = r;
+            }
+            double sum = 0.0;
+            for (int j = 0; j < p.k; ++j) sum += sbuf[ord[j]];
+            double cum = 0.0;
+            for (int j = 0; j < p.k; ++j) {
+                cum += sbuf[ord[j]];
+                flags |= 1u << ord[j];
+                if (cum / sum >= p.tau) break;
+            }
+        }
+        for (int r = 0; r < p.k; ++r) mflag[r] = (uint8_t)((flags >> r) & 1u);
     }
 }
 
@@ -291,7 +320,36 @@ __global__ __launch_bounds__(kTokThreads) void k_route_tokens(RouteParams p) {
     if (blockIdx.x == 0 && threadIdx.x < 4) p.counters[threadIdx.x] = 0;
     if (t < p.T)
         route_token<EPL>(p, t, lane, p.orig_ids + (size_t)t * p.k, p.gbuf + (size_t)t * p.k, p.top1 + t,
-                         s_sbuf[wave], s_ids[wave]);
+                         p.mflag + (size_t)t * p.k, s_sbuf[wave], s_ids[wave]);
+}
+
+// Batch-summed importance (SUM rule): one wavefront per expert adds the
+// expert's gate weights in ascending token order.
+__global__ __launch_bounds__(kTokThreads) void k_importance_sum(RouteParams p) {
+    const int lane = threadIdx.x & (kWave - 1);
+    const int e = blockIdx.x * kTokWaves + threadIdx.x / kWave;
+    if (e >= p.E) return;
+    double sum = 0.0;
+    for (int t0 = 0; t0 < p.T; t0 += kWave) {
+        const int t = t0 + lane;
+        double v = 0.0;
+        bool hit = false;
+        if (t < p.T) {
+            for (int r = 0; r < p.k; ++r) {
+                if (p.orig_ids[(size_t)t * p.k + r] == e) {
+                    v = p.gbuf[(size_t)t * p.k + r];
+                    hit = true;
+                }
+            }
+        }
+        unsigned long long m = __ballot(hit);
+        while (m) {
+            const int l = __ffsll((long long)m) - 1;
+            sum += readlane_d(v, l);
+            m &= m - 1;
+        }
+    }
+    if (lane == 0) p.imp_sum[e] = sum;
 }
 
 // Pruning kernel (one workgroup): Sec. IV-B steps 1-4 over the whole batch.
@@ -326,17 +384,24 @@ __global__ __launch_bounds__(kRouteThreads) void k_prune(RouteParams p) {
     if (tid == 0) s_ncand = 0;
     __syncthreads();
 
-    // Step 1: A_act, I(e) = max gate weight, A_must (threshold + each token's top expert).
+    // Step 1: A_act, importance, A_must (pairs mandatory on their own, and
+    // for the SUM rule every expert whose summed weight reaches tau).
     for (int i = tid; i < T * k; i += kRouteThreads) {
         const int e = p.orig_ids[i];
-        const double g = p.gbuf[i];
-        atomicMax(&s_imp[e], (unsigned long long)__double_as_longlong(g));
+        atomicMax(&s_imp[e], (unsigned long long)__double_as_longlong(p.gbuf[i]));
         s_act[e] = 1;
-        if (g >= p.tau) s_must[e] = 1;
+        if (p.mflag[i]) s_must[e] = 1;
     }
     __syncthreads();
-    for (int t = tid; t < T; t += kRouteThreads) s_must[p.top1[t]] = 1;
-    __syncthreads();
+    if (p.rule == CAEE_IMPORTANCE_SUM) {
+        for (int e = tid; e < E; e += kRouteThreads) {
+            if (!s_act[e]) continue;
+            const double I = p.imp_sum[e];
+            s_imp[e] = (unsigned long long)__double_as_longlong(I);
+            if (I >= p.tau) s_must[e] = 1;
+        }
+        __syncthreads();
+    }
 
     // Step 2: per-bin loads of A_act and A_must; candidate visiting order
     // (importance descending, index ascending).
@@ -608,6 +673,11 @@ hipError_t launch_route(const RouteParams& p, hipStream_t s) {
         hipLaunchKernelGGL(route_k, tok_grid, dim3(kTokThreads), 0, s, p);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
+        if (p.rule == CAEE_IMPORTANCE_SUM) {
+            hipLaunchKernelGGL(k_importance_sum, dim3((p.E + kTokWaves - 1) / kTokWaves), dim3(kTokThreads), 0, s, p);
+            e = hipGetLastError();
+            if (e != hipSuccess) return e;
+        }
         hipLaunchKernelGGL(k_prune, dim3(1), dim3(kRouteThreads), 0, s, p);
         e = hipGetLastError();
         if (e != hipSuccess) return e;

@@ -55,21 +55,23 @@ def getters_dev(Wd: dict, w_dtype: str):
     return (lambda e: fetch("", e)), (lambda s: fetch("sh_", s))
 
 
-def oracle_layer(shape, inp, tau, n_bins, get=None, get_sh=None, tokens=None, with_y=True):
+def oracle_layer(shape, inp, tau, n_bins, get=None, get_sh=None, tokens=None, with_y=True, rule="max"):
     T = inp.logits.shape[0]
+    # the C ABI carries tau and the routed scaling as fp32
     return oracle.moe_layer_ref(
         E=shape.E, n_group=shape.n_group, topk_group=shape.topk_group, k=shape.k,
-        routed_scaling=shape.routed_scaling, tau=tau, n_bins=n_bins, logits=inp.logits,
+        routed_scaling=float(np.float32(shape.routed_scaling)), tau=float(np.float32(tau)),
+        n_bins=n_bins, logits=inp.logits, rule=rule,
         bias=inp.bias, cost=inp.cost, bins=inp.bins if n_bins > 1 else None,
         x=inp.x if with_y else None, x_dtype=shape.x_dtype, w_dtype=shape.w_dtype,
         n_shared=shape.n_shared, get_expert=get if with_y else None, get_shared=get_sh,
         tokens=tokens if tokens is not None else (list(range(T)) if with_y else None))
 
 
-def gpu_layer(shape, inp, tau, n_bins, Wd, dev, route_only=False):
+def gpu_layer(shape, inp, tau, n_bins, Wd, dev, route_only=False, rule="max"):
     """Run caee_moe_layer (or caee_route_prune) and return numpy results."""
     T = inp.logits.shape[0]
-    layer = caee.Layer.from_shape(shape, T=T, tau=tau, n_bins=n_bins)
+    layer = caee.Layer.from_shape(shape, T=T, tau=tau, n_bins=n_bins, importance=rule)
     ws = caee.alloc_workspace(layer, dev)
     out = caee.alloc_route_out(layer, dev)
     logits = to_dev(inp.logits, dev)

@@ -29,26 +29,30 @@ def _inputs(T, skewed, n_bins, seed=0):
                                cost_kind="zipf" if skewed else "flat", n_bins=n_bins)
 
 
+RULE_TAUS = {"max": (0.0, 0.02, 0.05, 0.1), "sum": (0.3, 0.6, 1.2), "cir": (0.7, 0.8, 0.9)}
+
+
 @pytest.mark.parametrize("T", [1, 8, 32, 128])
 @pytest.mark.parametrize("skewed", [False, True])
-def test_r1_routing_sweep(T, skewed, r1_weights):
-    for tau in (0.0, 0.02, 0.05, 0.1):
+@pytest.mark.parametrize("rule", ["max", "sum", "cir"])
+def test_r1_routing_sweep(T, skewed, rule, r1_weights):
+    for tau in RULE_TAUS[rule]:
         for n_bins in (1, 8):
             inp = _inputs(T, skewed, n_bins, seed=T)
-            print(f"route T={T} skewed={skewed} tau={tau} n_bins={n_bins}", flush=True)
-            got = gpu_layer(R1_BF16, inp, tau, n_bins, r1_weights, DEV, route_only=True)
-            ref = oracle_layer(R1_BF16, inp, tau, n_bins, with_y=False)
+            print(f"route T={T} skewed={skewed} rule={rule} tau={tau} n_bins={n_bins}", flush=True)
+            got = gpu_layer(R1_BF16, inp, tau, n_bins, r1_weights, DEV, route_only=True, rule=rule)
+            ref = oracle_layer(R1_BF16, inp, tau, n_bins, with_y=False, rule=rule)
             check_route(got, ref, R1_BF16.E)
             # gate mass conserved on every token
             np.testing.assert_allclose(got["topk_w"].sum(axis=1), R1_BF16.routed_scaling, rtol=2e-6)
 
 
-def _layer_case(W, T, skewed, tau, n_bins, tokens):
+def _layer_case(W, T, skewed, tau, n_bins, tokens, rule="max"):
     inp = _inputs(T, skewed, n_bins)
-    print(f"layer T={T} skewed={skewed} tau={tau} n_bins={n_bins} tokens={tokens}", flush=True)
-    got = gpu_layer(R1_BF16, inp, tau, n_bins, W, DEV)
+    print(f"layer T={T} skewed={skewed} rule={rule} tau={tau} n_bins={n_bins} tokens={tokens}", flush=True)
+    got = gpu_layer(R1_BF16, inp, tau, n_bins, W, DEV, rule=rule)
     get, get_sh = getters_dev(W, "bf16")
-    ref = oracle_layer(R1_BF16, inp, tau, n_bins, get, get_sh, tokens=tokens)
+    ref = oracle_layer(R1_BF16, inp, tau, n_bins, get, get_sh, tokens=tokens, rule=rule)
     check_route(got, ref, R1_BF16.E)
     rel = check_y(got["y"][tokens], ref["y"], 2e-2)
     print(f"  max|err|/max|ref| = {rel:.3e}", flush=True)
@@ -65,3 +69,11 @@ def test_r1_dense_layer_t32(r1_weights):
 def test_r1_skewed_layer(T, tokens, r1_weights):
     # Zipf-skewed popularity and cost table, 8 bins (EP8-style placement)
     _layer_case(r1_weights, T, True, 0.1, 8, tokens)
+
+
+@pytest.mark.parametrize("rule,tau,T,tokens", [("sum", 0.6, 64, [0, 33, 63]), ("cir", 0.8, 16, [0, 15]),
+                                               ("sum", 1.2, 128, [5, 100])])
+def test_r1_pruned_layer(rule, tau, T, tokens, r1_weights):
+    # the paper's own importance rules prune at these thresholds
+    got, ref = _layer_case(r1_weights, T, True, tau, 8, tokens, rule=rule)
+    assert ref["stats"]["n_pruned"] > 0

@@ -17,16 +17,17 @@ TINY_BF16 = TINY_F32.with_(name="tiny-bf16", w_dtype="bf16", x_dtype="bf16", y_d
 TOL = {"f32": 1e-5, "bf16": 2e-2}
 
 
-def _run(shape, seed=0, tau=0.1, n_bins=4, T=None, zipf=None, cost_kind="uniform", mutate=None):
+def _run(shape, seed=0, tau=0.1, n_bins=4, T=None, zipf=None, cost_kind="uniform", mutate=None, rule="max"):
     inp = make_routing_inputs(shape, seed=seed, T=T, zipf_logit_s=zipf, cost_kind=cost_kind,
                               n_bins=n_bins)
     if mutate:
         mutate(inp)
     W = make_expert_weights_np(shape, seed=seed)
-    print(f"case {shape.name} seed={seed} tau={tau} n_bins={n_bins} T={inp.logits.shape[0]}", flush=True)
-    got = gpu_layer(shape, inp, tau, n_bins, w_to_dev(W, DEV), DEV)
+    print(f"case {shape.name} seed={seed} tau={tau} n_bins={n_bins} T={inp.logits.shape[0]} rule={rule}",
+          flush=True)
+    got = gpu_layer(shape, inp, tau, n_bins, w_to_dev(W, DEV), DEV, rule=rule)
     get, get_sh = getters_np(W, shape.w_dtype)
-    ref = oracle_layer(shape, inp, tau, n_bins, get, get_sh)
+    ref = oracle_layer(shape, inp, tau, n_bins, get, get_sh, rule=rule)
     check_route(got, ref, shape.E)
     check_y(got["y"], ref["y"], TOL[shape.w_dtype])
     return got, ref
@@ -142,3 +143,21 @@ def test_large_batches(T):
     # the shared expert has T > 128 rows, so it spans several FFN chunks;
     # 1100 tokens also takes the permutation path used above 1024 tokens
     _run(TINY_F32, seed=21, tau=0.1, n_bins=4, T=T)
+
+
+@pytest.mark.parametrize("seed", range(3))
+@pytest.mark.parametrize("rule,tau,n_bins", [("sum", 0.5, 4), ("sum", 1.5, 1), ("sum", 0.0, 4),
+                                             ("cir", 0.7, 4), ("cir", 0.9, 2), ("cir", 1.0, 4),
+                                             ("cir", 0.3, 1)])
+def test_importance_rules(seed, rule, tau, n_bins):
+    got, ref = _run(TINY_F32, seed=40 + seed, tau=tau, n_bins=n_bins, rule=rule)
+    if rule == "cir" and tau == 1.0:
+        assert not ref["pruned"].any()
+
+
+def test_sum_rule_with_equal_weights():
+    # equal logits: every token gives 1/4 to experts 0..3, so I(e) = T/4 exactly
+    def flat(inp):
+        inp.logits[:] = 0.0
+    _run(TINY_F32, seed=2, tau=4.0, n_bins=4, mutate=flat, rule="sum")
+    _run(TINY_F32, seed=2, tau=4.5, n_bins=4, mutate=flat, rule="sum")

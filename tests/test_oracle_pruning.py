@@ -144,3 +144,50 @@ def test_threshold_is_inclusive():
     must, cand = mandatory_split(act, imp, 0.125, [])
     assert must.tolist() == [True, True, True, False]
     assert cand.tolist() == [False, False, False, True]
+
+
+def test_importance_rules_hand_example(golden):
+    from oracle import cir_mandatory, gate_weights, importance_sum
+    g_ = golden("importance_rules_hand_example.json")
+    E = g_["E"]
+    ids = np.array(g_["orig_ids"])
+    s = np.array(g_["scores"])
+    g = np.array([gate_weights(s[t], ids[t]) for t in range(ids.shape[0])])
+    np.testing.assert_array_equal(g, np.array(g_["expected_g"]))
+    imp = importance_sum(ids, g, E)
+    assert imp.tolist() == g_["expected_sum_importance"]
+    pr = prune_batch(ids, g, E, g_["sum_theta"], np.ones(E, np.float32), None, 1, rule="sum")
+    assert np.flatnonzero(pr["must"]).tolist() == g_["expected_sum_must"]
+    for case in g_["cir_cases"]:
+        m = cir_mandatory(ids, s, case["theta_imp"], E)
+        assert np.flatnonzero(m).tolist() == case["expected_must"], case["note"]
+        pr = prune_batch(ids, g, E, case["theta_imp"], np.ones(E, np.float32), None, 1, rule="cir", s=s)
+        assert np.flatnonzero(pr["must"]).tolist() == case["expected_must"]
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_importance_rule_invariants(seed):
+    rng = np.random.default_rng(300 + seed)
+    E, T, k = 16, 20, 4
+    s, keys, ids, g = route_batch(rng.standard_normal((T, E)).astype(np.float32), None, 4, 2, k)
+    from oracle import importance_sum
+    imp = importance_sum(ids, g, E)
+    np.testing.assert_allclose(imp.sum(), T, rtol=1e-14)       # every token's weights sum to one
+    cost = rng.uniform(1, 4, E).astype(np.float32)
+    bins = (np.arange(E) // 4).astype(np.int32)
+    # CIR with ratio 1 keeps everything; a tiny ratio keeps only each token's top expert
+    full = prune_batch(ids, g, E, 1.0, cost, bins, 4, rule="cir", s=s)
+    assert np.array_equal(full["must"], full["act"]) and not full["pruned"].any()
+    tiny = prune_batch(ids, g, E, 1e-9, cost, bins, 4, rule="cir", s=s)
+    assert np.array_equal(tiny["must"], np.isin(np.arange(E), tiny["top1"]))
+    # SUM with a threshold above the batch total keeps only the top experts
+    top = prune_batch(ids, g, E, T + 1.0, cost, bins, 4, rule="sum")
+    assert np.array_equal(top["must"], np.isin(np.arange(E), top["top1"]))
+    # larger thresholds never grow the mandatory set
+    for rule in ("sum", "cir"):
+        prev = None
+        for th in ((0.2, 0.5, 1.0, 2.0) if rule == "sum" else (0.3, 0.6, 0.9)):
+            m = prune_batch(ids, g, E, th, cost, bins, 4, rule=rule, s=s)["must"]
+            if prev is not None:
+                assert np.all(m <= prev) if rule == "sum" else np.all(prev <= m)
+            prev = m
