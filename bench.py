@@ -50,13 +50,13 @@ def log(msg):
 class Case:
     """Device-resident inputs and buffers of one layer call."""
 
-    def __init__(self, shape, T, tau, n_bins, W, dev, seed, skewed):
+    def __init__(self, shape, T, tau, n_bins, W, dev, seed, skewed, rule="max"):
         import torch
         from paper_2606_29982_amd import caee
         from synth_inputs import make_routing_inputs
         self.inp = make_routing_inputs(shape, seed=seed, T=T, zipf_logit_s=1.1 if skewed else None,
                                        cost_kind="zipf" if skewed else "flat", n_bins=n_bins)
-        self.layer = caee.Layer.from_shape(shape, T=T, tau=tau, n_bins=n_bins)
+        self.layer = caee.Layer.from_shape(shape, T=T, tau=tau, n_bins=n_bins, importance=rule)
         to = lambda a: None if a is None else torch.from_numpy(np.ascontiguousarray(a)).to(dev)  # noqa: E731
         self.x = torch.from_numpy(self.inp.x.view(np.int16)).to(dev).view(torch.bfloat16)
         self.logits = to(self.inp.logits)
@@ -178,11 +178,13 @@ def main():
     t0 = time.time()
     log("drawing R1-shaped bf16 expert weights on the device")
     W = make_expert_weights_torch(shape, seed=args.seed, device=dev)
+    # the kernels stream the tiled layout; the row-major copy feeds the oracle
+    Wt = caee.pack_weights(W, "bf16")
     torch.cuda.synchronize()
     log(f"weights ready in {time.time() - t0:.1f}s")
 
     # Headline: T=32 decode batch, pruning off.
-    head = Case(shape, args.T, 0.0, 1, W, dev, args.seed, skewed=False)
+    head = Case(shape, args.T, 0.0, 1, Wt, dev, args.seed, skewed=False)
     ms = time_steps(head, args.steps, args.warmup)
     st = head.stats()
     n_trans = st[5]
@@ -214,7 +216,8 @@ def main():
         "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": "deepseek-r1-moe-layer-bf16-decode", "T": args.T, "d": shape.d, "f": shape.f,
                    "E": shape.E, "n_group": shape.n_group, "topk_group": shape.topk_group, "k": shape.k,
-                   "n_shared": shape.n_shared, "tau": 0.0, "pruning": "off", "parallelism": "single-gpu"},
+                   "n_shared": shape.n_shared, "tau": 0.0, "pruning": "off", "weight_layout": "tiled",
+                   "parallelism": "single-gpu"},
         "hbm_gbps": round(b_layer / (ms * 1e-3) / 1e9, 1),
         "hbm_frac": round(b_layer / (ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
         "experts_executed": n_trans + shape.n_shared,
@@ -223,14 +226,17 @@ def main():
     }
 
     if not args.no_sweep:
+        # Zipf-skewed popularity and cost table, experts placed on 8 bins
+        # (EP8-style), with and without pruning under each importance rule.
         sweep = []
         for T in (1, 8, 32, 128):
-            for tau, n_bins in ((0.0, 1), (0.1, 8)):
-                c = Case(shape, T, tau, n_bins, W, dev, args.seed, skewed=True)
+            for rule, tau, n_bins in (("max", 0.0, 8), ("max", 0.1, 8), ("sum", 0.6, 8), ("cir", 0.8, 8)):
+                c = Case(shape, T, tau, n_bins, Wt, dev, args.seed, skewed=True, rule=rule)
                 m = time_steps(c, max(10, args.steps // 2), 3)
                 s = c.stats()
                 b = layer_bytes(shape, T, s[5])
-                sweep.append({"T": T, "tau": tau, "n_bins": n_bins, "inputs": "zipf-skewed",
+                sweep.append({"T": T, "rule": rule, "tau": tau, "n_bins": n_bins, "inputs": "zipf-skewed",
+                              "pruning": "off" if tau == 0.0 else "on",
                               "us_per_step": round(m * 1e3, 1), "tokens_per_s": round(T / (m * 1e-3), 1),
                               "hbm_gbps": round(b / (m * 1e-3) / 1e9, 1),
                               "hbm_frac": round(b / (m * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
@@ -241,7 +247,7 @@ def main():
 
     if not args.no_cpu:
         log("timing the fp64 oracle on the host")
-        result["cpu_baseline"] = cpu_baseline(shape, head, W, sample_tokens=4)
+        result["cpu_baseline"] = cpu_baseline(shape, head, W, sample_tokens=args.T)
     print(json.dumps(result), flush=True)
 
 

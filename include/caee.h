@@ -49,7 +49,7 @@
 extern "C" {
 #endif
 
-#define CAEE_ABI_VERSION 1
+#define CAEE_ABI_VERSION 2
 
 typedef enum caee_status {
     CAEE_OK = 0,
@@ -102,6 +102,19 @@ typedef struct caee_layer_desc {
     int32_t y_dtype;      /* output dtype: CAEE_F32 or CAEE_BF16 */
 } caee_layer_desc_t;
 
+/* Storage order of the expert matrices. */
+typedef enum caee_layout {
+    /* Row-major: matrix [R][K], K contiguous. */
+    CAEE_LAYOUT_ROWMAJOR = 0,
+    /* Tiled, the order the FFN kernels stream: for row tile t (rows
+     * 16t..16t+15) and contraction step s (64 bytes of each row), one
+     * 1024-byte block whose 16-byte piece j (j = r + 16*q, r < 16, q < 4)
+     * is bytes [64s + 16q, 64s + 16q + 16) of row 16t + r; blocks ordered
+     * by t, then s.  Same bytes as row-major, permuted; produced by
+     * caee_pack_matrix. */
+    CAEE_LAYOUT_TILED = 1
+} caee_layout_t;
+
 /* Expert weights.  Expert e's gate and up matrices are stacked as
  * w13[e] = [W1; W3] of shape [2f][d], its down matrix is w2[e] of shape
  * [d][f]; both K-contiguous (each row is one output feature).  The expert
@@ -109,7 +122,8 @@ typedef struct caee_layer_desc {
  * FP8: w13/w2 hold E4M3 codes and *_scale hold one fp32 scale per 128x128
  * block, w13_scale [E][2f/128][d/128] and w2_scale [E][d/128][f/128]; the
  * weight is code * scale.  *_scale must be NULL for other dtypes.
- * The shared experts use the same layout with n_shared in place of E. */
+ * The shared experts use the same layout with n_shared in place of E.
+ * `layout` applies to all four matrices (scales are always row-major). */
 typedef struct caee_expert_weights {
     const void* w13;            /* [E][2f][d] */
     const void* w2;             /* [E][d][f] */
@@ -119,6 +133,7 @@ typedef struct caee_expert_weights {
     const void* sh_w2;          /* [n_shared][d][f] */
     const float* sh_w13_scale;  /* FP8 only */
     const float* sh_w2_scale;   /* FP8 only */
+    int32_t layout;             /* caee_layout_t */
 } caee_expert_weights_t;
 
 /* Routing results, all caller-owned device memory.  Lists are in rank order
@@ -167,6 +182,16 @@ caee_status_t caee_moe_layer(const caee_layer_desc_t* desc, const void* x,
                              const int32_t* bin, const caee_expert_weights_t* weights,
                              void* y, const caee_route_out_t* out, void* ws,
                              size_t ws_bytes, void* stream);
+
+/* Repack `count` consecutive row-major matrices [rows][cols] of dtype
+ * `w_dtype` from `src` into CAEE_LAYOUT_TILED order at `dst` (same size,
+ * must not overlap).  rows must be a multiple of 16 and a row a multiple of
+ * 64 bytes.  Asynchronous on `stream`; a one-time step when weights are
+ * loaded (weights are static during inference).  Tiled weights let each
+ * FFN wavefront stream one contiguous region instead of 32 rows, which is
+ * what keeps HBM near its streaming bandwidth. */
+caee_status_t caee_pack_matrix(int32_t w_dtype, const void* src, void* dst, int64_t rows, int64_t cols,
+                               int64_t count, void* stream);
 
 /* Static description of a status code. */
 const char* caee_status_str(caee_status_t status);

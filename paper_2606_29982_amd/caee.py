@@ -38,7 +38,11 @@ class LayerDesc(ctypes.Structure):
 
 class ExpertWeights(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in
-                ("w13", "w2", "w13_scale", "w2_scale", "sh_w13", "sh_w2", "sh_w13_scale", "sh_w2_scale")]
+                ("w13", "w2", "w13_scale", "w2_scale", "sh_w13", "sh_w2", "sh_w13_scale", "sh_w2_scale")] + [
+        ("layout", ctypes.c_int32)]
+
+
+LAYOUT_ROWMAJOR, LAYOUT_TILED = 0, 1
 
 
 class RouteOut(ctypes.Structure):
@@ -60,6 +64,7 @@ def _load(path: str = LIB_PATH):
         "caee_expert_ffn": (st, [desc_p, P, P, P, ctypes.POINTER(ExpertWeights), P, P, ctypes.c_size_t, P]),
         "caee_moe_layer": (st, [desc_p, P, P, P, P, P, ctypes.POINTER(ExpertWeights), P,
                                 ctypes.POINTER(RouteOut), P, ctypes.c_size_t, P]),
+        "caee_pack_matrix": (st, [ctypes.c_int32, P, P, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, P]),
         "caee_status_str": (ctypes.c_char_p, [st]),
         "caee_last_error": (ctypes.c_char_p, []),
         "caee_abi_version": (ctypes.c_int, []),
@@ -86,8 +91,8 @@ def load_library(path: str) -> None:
 
 
 EXPORTED = ("caee_workspace_size", "caee_route_prune", "caee_expert_ffn", "caee_moe_layer",
-            "caee_status_str", "caee_last_error", "caee_abi_version", "caee_timing_enable",
-            "caee_timing_reset", "caee_timing_query")
+            "caee_pack_matrix", "caee_status_str", "caee_last_error", "caee_abi_version",
+            "caee_timing_enable", "caee_timing_reset", "caee_timing_query")
 
 
 def _check(status: int):
@@ -157,7 +162,30 @@ def _stream(*tensors) -> Optional[int]:
 def _weights(w: dict) -> ExpertWeights:
     g = lambda n: _ptr(w.get(n))  # noqa: E731
     return ExpertWeights(g("w13"), g("w2"), g("w13_scale"), g("w2_scale"),
-                         g("sh_w13"), g("sh_w2"), g("sh_w13_scale"), g("sh_w2_scale"))
+                         g("sh_w13"), g("sh_w2"), g("sh_w13_scale"), g("sh_w2_scale"),
+                         int(w.get("layout", LAYOUT_ROWMAJOR)))
+
+
+def pack_matrix(w_dtype: str, src, dst, rows: int, cols: int, count: int):
+    """Repack `count` row-major [rows][cols] matrices into the tiled layout."""
+    _check(lib.caee_pack_matrix(DTYPE_CODE[w_dtype], _ptr(src), _ptr(dst), rows, cols, count, _stream(src)))
+    return dst
+
+
+def pack_weights(weights: dict, w_dtype: str) -> dict:
+    """Tiled copy of a row-major expert weight dict (scales are shared)."""
+    import torch
+    out = {k: v for k, v in weights.items() if k.endswith("_scale")}
+    for name in ("w13", "w2", "sh_w13", "sh_w2"):
+        src = weights.get(name)
+        if src is None:
+            continue
+        dst = torch.empty_like(src)
+        if src.numel():
+            pack_matrix(w_dtype, src, dst, src.shape[1], src.shape[2], src.shape[0])
+        out[name] = dst
+    out["layout"] = LAYOUT_TILED
+    return out
 
 
 def _route_out(out: Optional[dict]) -> Optional[RouteOut]:

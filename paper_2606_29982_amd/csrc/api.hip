@@ -130,6 +130,8 @@ caee_status_t check_weights(const caee_layer_desc_t* d, const caee_expert_weight
     CAEE_TRY(check_ptr(w->sh_w2_scale, "weights->sh_w2_scale", fp8 && sh));
     if (!fp8 && (w->w13_scale || w->w2_scale || w->sh_w13_scale || w->sh_w2_scale))
         return fail(CAEE_ERR_INVALID_ARG, "block scales given for non-fp8 weights");
+    if (w->layout != CAEE_LAYOUT_ROWMAJOR && w->layout != CAEE_LAYOUT_TILED)
+        return fail(CAEE_ERR_INVALID_ARG, "unknown weight layout=%d", w->layout);
     return CAEE_OK;
 }
 
@@ -253,6 +255,7 @@ caee_status_t run_ffn(const caee_layer_desc_t* d, const void* x, const int32_t* 
     p.y_bf16 = d->y_dtype == CAEE_BF16;
     p.P = L.P;
     p.ksplit = L.ksplit;
+    p.tiled = W->layout == CAEE_LAYOUT_TILED;
     const int nb = ffn_token_blocks(*d);
     CAEE_TRY(timed_launch(CAEE_KERNEL_GATE_UP, s, "gate/up",
                           [&] { return launch_gate_up(p, d->w_dtype, nb, L.max_chunks, s); }));
@@ -358,6 +361,28 @@ caee_status_t caee_moe_layer(const caee_layer_desc_t* desc, const void* x, const
     hipStream_t s = as_stream(stream);
     CAEE_TRY(timed_launch(CAEE_KERNEL_ROUTE, s, "route", [&] { return launch_route(p, s); }));
     return run_ffn(desc, x, p.topk_ids, p.topk_w, weights, y, wsb, L, s);
+}
+
+caee_status_t caee_pack_matrix(int32_t w_dtype, const void* src, void* dst, int64_t rows, int64_t cols,
+                               int64_t count, void* stream) {
+    g_last_error.clear();
+    if (w_dtype != CAEE_F32 && w_dtype != CAEE_BF16 && w_dtype != CAEE_FP8_E4M3)
+        return fail(CAEE_ERR_INVALID_ARG, "unknown w_dtype=%d", w_dtype);
+    if (rows <= 0 || rows % 16) return fail(CAEE_ERR_INVALID_ARG, "rows=%lld must be a positive multiple of 16",
+                                            (long long)rows);
+    const long long row_bytes = (long long)cols * elem_bytes(w_dtype);
+    if (cols <= 0 || row_bytes % 64)
+        return fail(CAEE_ERR_INVALID_ARG, "a row (%lld bytes) must be a positive multiple of 64 bytes", row_bytes);
+    if (count < 0) return fail(CAEE_ERR_INVALID_ARG, "count=%lld must be >= 0", (long long)count);
+    CAEE_TRY(check_ptr(src, "src", true));
+    CAEE_TRY(check_ptr(dst, "dst", true));
+    const unsigned long long bytes = (unsigned long long)count * rows * row_bytes;
+    const uintptr_t a = (uintptr_t)src, b = (uintptr_t)dst;
+    if (a < b + bytes && b < a + bytes && bytes > 0) return fail(CAEE_ERR_INVALID_ARG, "src and dst overlap");
+    if (count == 0) return CAEE_OK;
+    const hipError_t err = launch_pack(src, dst, rows, row_bytes / 16, count, as_stream(stream));
+    if (err != hipSuccess) return fail(CAEE_ERR_HIP, "pack launch failed: %s", hipGetErrorString(err));
+    return CAEE_OK;
 }
 
 const char* caee_status_str(caee_status_t status) {

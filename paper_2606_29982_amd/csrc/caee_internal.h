@@ -181,6 +181,7 @@ struct FfnParams {
     int y_bf16;
     int P;
     int ksplit;
+    int tiled;      // weights in CAEE_LAYOUT_TILED order
 };
 
 // Host-side launchers (defined next to their kernels).
@@ -189,6 +190,8 @@ hipError_t launch_permute(const RouteParams& p, hipStream_t s);
 hipError_t launch_gate_up(const FfnParams& p, int w_dtype, int nb, int max_chunks, hipStream_t s);
 hipError_t launch_down(const FfnParams& p, int w_dtype, int nb, int max_chunks, hipStream_t s);
 hipError_t launch_combine(const FfnParams& p, hipStream_t s);
+hipError_t launch_pack(const void* src, void* dst, long long rows, long long row_units, long long count,
+                       hipStream_t s);
 int device_cu_count();
 
 }  // namespace caee

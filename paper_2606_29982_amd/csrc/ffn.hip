@@ -60,26 +60,27 @@ __device__ inline const char* expert_base(const void* routed, const void* shared
 // over `nsteps` k-steps starting at the given pointers.  Weights are loaded
 // U steps ahead of the MFMAs that consume them (register double buffer).
 template <class M, int U, int NA, int NB>
-__device__ inline void tile_contract(const u32x4_t* const (&a)[NA], const u32x4_t* const (&b)[NB], int nb,
-                                     int nsteps, f32x4_t (&acc)[NA][NB]) {
+__device__ inline void tile_contract(const u32x4_t* const (&a)[NA], int astep, const u32x4_t* const (&b)[NB],
+                                     int nb, int nsteps, f32x4_t (&acc)[NA][NB]) {
     u32x4_t cur[NA][U], nxt[NA][U];
 #pragma unroll
     for (int m = 0; m < NA; ++m)
 #pragma unroll
-        for (int u = 0; u < U; ++u) cur[m][u] = __builtin_nontemporal_load(a[m] + 4 * u);
+        for (int u = 0; u < U; ++u) cur[m][u] = __builtin_nontemporal_load(a[m] + (size_t)astep * u);
     for (int ks = 0; ks < nsteps; ks += U) {
         const bool more = CAEE_FFN_PIPELINE && ks + U < nsteps;
         if (!CAEE_FFN_PIPELINE && ks > 0) {
 #pragma unroll
             for (int m = 0; m < NA; ++m)
 #pragma unroll
-                for (int u = 0; u < U; ++u) cur[m][u] = __builtin_nontemporal_load(a[m] + 4 * (ks + u));
+                for (int u = 0; u < U; ++u) cur[m][u] = __builtin_nontemporal_load(a[m] + (size_t)astep * (ks + u));
         }
         if (more) {
 #pragma unroll
             for (int m = 0; m < NA; ++m)
 #pragma unroll
-                for (int u = 0; u < U; ++u) nxt[m][u] = __builtin_nontemporal_load(a[m] + 4 * (ks + U + u));
+                for (int u = 0; u < U; ++u)
+                    nxt[m][u] = __builtin_nontemporal_load(a[m] + (size_t)astep * (ks + U + u));
         }
 #pragma unroll
         for (int tb = 0; tb < NB; ++tb) {
@@ -147,8 +148,14 @@ __global__ CAEE_FFN_BOUNDS void k_gate_up(FfnParams p) {
         const int nb = (ntok + 15) >> 4;
         const size_t k0 = (size_t)4 * sp * kper;
         const u32x4_t* wb = (const u32x4_t*)expert_base(p.w13, p.sh_w13, xs, p.E, expert_bytes);
-        const u32x4_t* const a[2] = {wb + (size_t)(jt * 16 + r) * row_units + g + k0,
-                                     wb + (size_t)(p.f + jt * 16 + r) * row_units + g + k0};
+        const size_t ksteps = row_units / 4;
+        // Tiled: block (tile, step) is 64 consecutive 16-byte pieces, one per lane.
+        const u32x4_t* const a[2] = {
+            p.tiled ? wb + ((size_t)jt * ksteps + (size_t)sp * kper) * 64 + lane
+                    : wb + (size_t)(jt * 16 + r) * row_units + g + k0,
+            p.tiled ? wb + ((size_t)(tiles + jt) * ksteps + (size_t)sp * kper) * 64 + lane
+                    : wb + (size_t)(p.f + jt * 16 + r) * row_units + g + k0};
+        const int astep = p.tiled ? 64 : 4;
         const u32x4_t* xb[NB];
 #pragma unroll
         for (int tb = 0; tb < NB; ++tb) {
@@ -161,7 +168,7 @@ __global__ CAEE_FFN_BOUNDS void k_gate_up(FfnParams p) {
         for (int m = 0; m < 2; ++m)
 #pragma unroll
             for (int tb = 0; tb < NB; ++tb) acc[m][tb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-        tile_contract<M, U, 2, NB>(a, xb, nb, kper, acc);
+        tile_contract<M, U, 2, NB>(a, astep, xb, nb, kper, acc);
 
         if (S > 1) {
 #pragma unroll
@@ -216,7 +223,9 @@ __global__ CAEE_FFN_BOUNDS void k_down(FfnParams p) {
         const int xs = p.chunks[4 * c], row0 = p.chunks[4 * c + 1], ntok = p.chunks[4 * c + 2];
         const int nb = (ntok + 15) >> 4;
         const u32x4_t* wb = (const u32x4_t*)expert_base(p.w2, p.sh_w2, xs, p.E, expert_bytes);
-        const u32x4_t* const a[1] = {wb + (size_t)(it * 16 + r) * row_units + g};
+        const u32x4_t* const a[1] = {p.tiled ? wb + (size_t)it * ksteps * 64 + lane
+                                             : wb + (size_t)(it * 16 + r) * row_units + g};
+        const int astep = p.tiled ? 64 : 4;
         const u32x4_t* hb[NB];
 #pragma unroll
         for (int tb = 0; tb < NB; ++tb) {
@@ -227,7 +236,7 @@ __global__ CAEE_FFN_BOUNDS void k_down(FfnParams p) {
         f32x4_t acc[1][NB];
 #pragma unroll
         for (int tb = 0; tb < NB; ++tb) acc[0][tb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-        tile_contract<M, U, 1, NB>(a, hb, nb, ksteps, acc);
+        tile_contract<M, U, 1, NB>(a, astep, hb, nb, ksteps, acc);
 #pragma unroll
         for (int tb = 0; tb < NB; ++tb) {
             const int n = tb * 16 + r;
@@ -236,6 +245,22 @@ __global__ CAEE_FFN_BOUNDS void k_down(FfnParams p) {
                 *(float4*)o = make_float4(acc[0][tb][0], acc[0][tb][1], acc[0][tb][2], acc[0][tb][3]);
             }
         }
+    }
+}
+
+// Row-major -> tiled repack, one thread per 16-byte piece of the destination.
+__global__ __launch_bounds__(256) void k_pack(const u32x4_t* __restrict__ src, u32x4_t* __restrict__ dst,
+                                              long long rows, long long row_units, long long count) {
+    const long long per_mat = rows * row_units;
+    const long long total = count * per_mat;
+    const long long ksteps = row_units / 4;
+    for (long long i = (long long)blockIdx.x * 256 + threadIdx.x; i < total; i += (long long)gridDim.x * 256) {
+        const long long m = i / per_mat;
+        const long long rem = i - m * per_mat;
+        const long long blk = rem >> 6;
+        const int l = (int)(rem & 63);
+        const long long t = blk / ksteps, st = blk - t * ksteps;
+        dst[i] = src[m * per_mat + (16 * t + (l & 15)) * row_units + 4 * st + (l >> 4)];
     }
 }
 
@@ -317,6 +342,18 @@ hipError_t launch_down(const FfnParams& p, int w_dtype, int nb, int max_chunks, 
     if (w_dtype == CAEE_BF16) return launch_nb<Bf16Math, DownK, kDownU>(p, nb, grid, s);
     if (w_dtype == CAEE_F32) return launch_nb<F32Math, DownK, kDownU>(p, nb, grid, s);
     return hipErrorInvalidValue;
+}
+
+hipError_t launch_pack(const void* src, void* dst, long long rows, long long row_units, long long count,
+                       hipStream_t s) {
+    const long long total = count * rows * row_units;
+    long long blocks = (total + 255) / 256;
+    const long long cap = (long long)device_cu_count() * 16;
+    if (blocks > cap) blocks = cap;
+    if (blocks < 1) blocks = 1;
+    hipLaunchKernelGGL(k_pack, dim3((unsigned)blocks), dim3(256), 0, s, (const u32x4_t*)src, (u32x4_t*)dst, rows,
+                       row_units, count);
+    return hipGetLastError();
 }
 
 hipError_t launch_combine(const FfnParams& p, hipStream_t s) {

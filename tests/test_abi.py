@@ -26,7 +26,7 @@ def test_exports_every_declared_symbol():
     for n in names:
         assert hasattr(lib, n), n
     assert set(names) == set(caee.EXPORTED)
-    assert caee.abi_version() == 1
+    assert caee.abi_version() == 2
 
 
 def _layer(**kw):
@@ -127,3 +127,18 @@ def test_status_strings_and_timing_kinds():
     ms, cnt = ctypes.c_double(), ctypes.c_int64()
     assert caee.lib.caee_timing_query(9, ctypes.byref(ms), ctypes.byref(cnt)) == caee.CAEE_ERR_INVALID_ARG
     assert caee.lib.caee_timing_query(0, ctypes.byref(ms), ctypes.byref(cnt)) == caee.CAEE_OK
+
+
+def test_pack_matrix_host_checks():
+    pk = caee.lib.caee_pack_matrix
+    assert pk(9, FAKE, FAKE * 16, 32, 64, 1, None) == caee.CAEE_ERR_INVALID_ARG
+    assert pk(caee.CAEE_BF16, FAKE, FAKE * 16, 24, 64, 1, None) == caee.CAEE_ERR_INVALID_ARG    # rows % 16
+    assert pk(caee.CAEE_BF16, FAKE, FAKE * 16, 32, 16, 1, None) == caee.CAEE_ERR_INVALID_ARG    # 32-byte rows
+    assert pk(caee.CAEE_BF16, None, FAKE * 16, 32, 64, 1, None) == caee.CAEE_ERR_INVALID_ARG
+    assert pk(caee.CAEE_BF16, FAKE, FAKE + 1024, 32, 64, 1, None) == caee.CAEE_ERR_INVALID_ARG  # overlap
+    assert pk(caee.CAEE_BF16, FAKE, FAKE * 16, 32, 64, 0, None) == caee.CAEE_OK                 # nothing to do
+    W = caee.ExpertWeights(FAKE, FAKE, None, None, FAKE, FAKE, None, None, 7)
+    d = _layer().desc()
+    n = _ws_status(_layer())[1]
+    assert caee.lib.caee_expert_ffn(ctypes.byref(d), FAKE, FAKE, FAKE, ctypes.byref(W), FAKE, FAKE, n,
+                                    None) == caee.CAEE_ERR_INVALID_ARG                          # unknown layout

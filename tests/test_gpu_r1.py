@@ -8,6 +8,7 @@ import pytest
 import torch
 
 from caee_cases import check_route, check_y, getters_dev, gpu_layer, oracle_layer
+from paper_2606_29982_amd import caee
 from synth_inputs import R1_BF16, make_expert_weights_torch, make_routing_inputs
 
 pytestmark = pytest.mark.gpu
@@ -21,6 +22,15 @@ def r1_weights():
     torch.cuda.synchronize()
     yield W
     del W
+    torch.cuda.empty_cache()
+
+
+@pytest.fixture(scope="module")
+def r1_tiled(r1_weights):
+    Wt = caee.pack_weights(r1_weights, "bf16")
+    torch.cuda.synchronize()
+    yield Wt
+    del Wt
     torch.cuda.empty_cache()
 
 
@@ -47,10 +57,12 @@ def test_r1_routing_sweep(T, skewed, rule, r1_weights):
             np.testing.assert_allclose(got["topk_w"].sum(axis=1), R1_BF16.routed_scaling, rtol=2e-6)
 
 
-def _layer_case(W, T, skewed, tau, n_bins, tokens, rule="max"):
+def _layer_case(W, T, skewed, tau, n_bins, tokens, rule="max", Wrun=None):
+    """Layer parity; ``Wrun`` (default ``W``) is what the GPU runs, ``W``
+    the row-major copy the oracle reads."""
     inp = _inputs(T, skewed, n_bins)
     print(f"layer T={T} skewed={skewed} rule={rule} tau={tau} n_bins={n_bins} tokens={tokens}", flush=True)
-    got = gpu_layer(R1_BF16, inp, tau, n_bins, W, DEV, rule=rule)
+    got = gpu_layer(R1_BF16, inp, tau, n_bins, W if Wrun is None else Wrun, DEV, rule=rule)
     get, get_sh = getters_dev(W, "bf16")
     ref = oracle_layer(R1_BF16, inp, tau, n_bins, get, get_sh, tokens=tokens, rule=rule)
     check_route(got, ref, R1_BF16.E)
@@ -77,3 +89,9 @@ def test_r1_pruned_layer(rule, tau, T, tokens, r1_weights):
     # the paper's own importance rules prune at these thresholds
     got, ref = _layer_case(r1_weights, T, True, tau, 8, tokens, rule=rule)
     assert ref["stats"]["n_pruned"] > 0
+
+
+@pytest.mark.parametrize("T,tokens,rule,tau", [(1, [0], "max", 0.0), (32, [0, 31], "max", 0.0),
+                                               (128, [1, 77], "sum", 0.6)])
+def test_r1_tiled_weights(T, tokens, rule, tau, r1_weights, r1_tiled):
+    _layer_case(r1_weights, T, T == 128, tau, 8, tokens, rule=rule, Wrun=r1_tiled)

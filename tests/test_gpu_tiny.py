@@ -17,7 +17,8 @@ TINY_BF16 = TINY_F32.with_(name="tiny-bf16", w_dtype="bf16", x_dtype="bf16", y_d
 TOL = {"f32": 1e-5, "bf16": 2e-2}
 
 
-def _run(shape, seed=0, tau=0.1, n_bins=4, T=None, zipf=None, cost_kind="uniform", mutate=None, rule="max"):
+def _run(shape, seed=0, tau=0.1, n_bins=4, T=None, zipf=None, cost_kind="uniform", mutate=None, rule="max",
+         tiled=False):
     inp = make_routing_inputs(shape, seed=seed, T=T, zipf_logit_s=zipf, cost_kind=cost_kind,
                               n_bins=n_bins)
     if mutate:
@@ -25,7 +26,10 @@ def _run(shape, seed=0, tau=0.1, n_bins=4, T=None, zipf=None, cost_kind="uniform
     W = make_expert_weights_np(shape, seed=seed)
     print(f"case {shape.name} seed={seed} tau={tau} n_bins={n_bins} T={inp.logits.shape[0]} rule={rule}",
           flush=True)
-    got = gpu_layer(shape, inp, tau, n_bins, w_to_dev(W, DEV), DEV, rule=rule)
+    Wd = w_to_dev(W, DEV)
+    if tiled:
+        Wd = caee.pack_weights(Wd, shape.w_dtype)
+    got = gpu_layer(shape, inp, tau, n_bins, Wd, DEV, rule=rule)
     get, get_sh = getters_np(W, shape.w_dtype)
     ref = oracle_layer(shape, inp, tau, n_bins, get, get_sh, rule=rule)
     check_route(got, ref, shape.E)
@@ -161,3 +165,32 @@ def test_sum_rule_with_equal_weights():
         inp.logits[:] = 0.0
     _run(TINY_F32, seed=2, tau=4.0, n_bins=4, mutate=flat, rule="sum")
     _run(TINY_F32, seed=2, tau=4.5, n_bins=4, mutate=flat, rule="sum")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_tiled_layout_order(dtype):
+    # the documented tiled order, restated with numpy: block (t, s) holds 64
+    # 16-byte pieces, piece r + 16q = bytes [64s + 16q, +16) of row 16t + r
+    rows, cols, count = 48, 128 if dtype == "bf16" else 64, 3
+    rng = np.random.default_rng(0)
+    src = rng.integers(0, 2**31, (count, rows, cols * (2 if dtype == "bf16" else 4) // 4), dtype=np.int64)
+    src = src.astype(np.uint32)
+    row_bytes = src.shape[2] * 4
+    pieces = src.reshape(count, rows, row_bytes // 16, 4)          # 16-byte pieces of each row
+    S = row_bytes // 64
+    want = np.empty((count, rows // 16, S, 64, 4), np.uint32)
+    for t in range(rows // 16):
+        for s_ in range(S):
+            for j in range(64):
+                want[:, t, s_, j] = pieces[:, 16 * t + (j % 16), 4 * s_ + j // 16]
+    dsrc = torch.from_numpy(src.view(np.int32)).to(DEV)
+    ddst = torch.empty_like(dsrc)
+    caee.pack_matrix(dtype, dsrc, ddst, rows, cols, count)
+    torch.cuda.synchronize()
+    assert np.array_equal(ddst.cpu().numpy().view(np.uint32).reshape(want.shape), want)
+
+
+@pytest.mark.parametrize("shape", [TINY_F32, TINY_BF16], ids=["f32", "bf16"])
+@pytest.mark.parametrize("T", [1, 3, 16, 70])
+def test_tiled_weights(shape, T):
+    _run(shape, seed=T, tau=0.2, n_bins=4, T=T, tiled=True)
