@@ -8,7 +8,7 @@ weights drawn N(0, 0.02), sigmoid router with bias, routed scaling 2.5.
 The headline workload is a decode batch of T=32 tokens with pruning off
 (the dense-routing baseline).  Prints one JSON line.
 
-  python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-sweep] [--no-cpu]
+  python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-sweep] [--no-cpu] [--copy-bytes N]
 """
 from __future__ import annotations
 
@@ -40,6 +40,9 @@ def parse():
     ap.add_argument("--no-sweep", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--copy-bytes", type=int, default=0,
+                    help="finish with one device-to-device copy of this many bytes (a known-size "
+                         "reference for HBM traffic counters)")
     return ap.parse_args()
 
 
@@ -245,6 +248,12 @@ def main():
                 del c
         result["sweep"] = sweep
 
+    if args.copy_bytes > 0:
+        src = torch.empty(args.copy_bytes, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     if not args.no_cpu:
         log("timing the fp64 oracle on the host")
         result["cpu_baseline"] = cpu_baseline(shape, head, W, sample_tokens=args.T)
