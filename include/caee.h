@@ -193,6 +193,15 @@ caee_status_t caee_moe_layer(const caee_layer_desc_t* desc, const void* x,
 caee_status_t caee_pack_matrix(int32_t w_dtype, const void* src, void* dst, int64_t rows, int64_t cols,
                                int64_t count, void* stream);
 
+/* The activation quantiser of the 8-bit path: `rows` rows of `cols` values
+ * (src_dtype CAEE_BF16 or CAEE_F32) to OCP E4M3 per row per 128 columns.
+ * In fp32: scale = amax / 448 (1 for an all-zero block), code = value / scale
+ * rounded to the nearest E4M3 value, ties to the even code, saturating at
+ * 448.  q [rows][cols] uint8 codes, scale [rows][cols/128] fp32; cols must be
+ * a multiple of 128.  Asynchronous on `stream`. */
+caee_status_t caee_quantize_rows(int32_t src_dtype, const void* src, int64_t rows, int64_t cols, uint8_t* q,
+                                 float* scale, void* stream);
+
 /* Static description of a status code. */
 const char* caee_status_str(caee_status_t status);
 /* Message of the last error raised on the calling thread ("" if none). */
@@ -210,7 +219,8 @@ typedef enum caee_kernel_kind {
     CAEE_KERNEL_GATE_UP = 1,  /* expert gate/up products and SwiGLU */
     CAEE_KERNEL_DOWN = 2,     /* expert down products */
     CAEE_KERNEL_COMBINE = 3,  /* weighted combine into y */
-    CAEE_KERNEL_KINDS = 4
+    CAEE_KERNEL_QUANT = 4,    /* fp8 activation quantisation (x and the SwiGLU rows) */
+    CAEE_KERNEL_KINDS = 5
 } caee_kernel_kind_t;
 caee_status_t caee_timing_enable(int on);
 caee_status_t caee_timing_reset(void);

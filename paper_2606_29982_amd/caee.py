@@ -17,7 +17,7 @@ LIB_PATH = os.path.join(HERE, "libcaee.so")
 
 CAEE_OK, CAEE_ERR_INVALID_ARG, CAEE_ERR_UNSUPPORTED, CAEE_ERR_WORKSPACE, CAEE_ERR_HIP = range(5)
 CAEE_F32, CAEE_BF16, CAEE_FP8_E4M3 = 0, 1, 2
-KERNEL_KINDS = {"route": 0, "gate_up": 1, "down": 2, "combine": 3}
+KERNEL_KINDS = {"route": 0, "gate_up": 1, "down": 2, "combine": 3, "quant": 4}
 DTYPE_CODE = {"f32": CAEE_F32, "bf16": CAEE_BF16, "fp8": CAEE_FP8_E4M3}
 IMPORTANCE_CODE = {"max": 0, "sum": 1, "cir": 2}
 
@@ -65,6 +65,7 @@ def _load(path: str = LIB_PATH):
         "caee_moe_layer": (st, [desc_p, P, P, P, P, P, ctypes.POINTER(ExpertWeights), P,
                                 ctypes.POINTER(RouteOut), P, ctypes.c_size_t, P]),
         "caee_pack_matrix": (st, [ctypes.c_int32, P, P, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, P]),
+        "caee_quantize_rows": (st, [ctypes.c_int32, P, ctypes.c_int64, ctypes.c_int64, P, P, P]),
         "caee_status_str": (ctypes.c_char_p, [st]),
         "caee_last_error": (ctypes.c_char_p, []),
         "caee_abi_version": (ctypes.c_int, []),
@@ -91,7 +92,7 @@ def load_library(path: str) -> None:
 
 
 EXPORTED = ("caee_workspace_size", "caee_route_prune", "caee_expert_ffn", "caee_moe_layer",
-            "caee_pack_matrix", "caee_status_str", "caee_last_error", "caee_abi_version",
+            "caee_pack_matrix", "caee_quantize_rows", "caee_status_str", "caee_last_error", "caee_abi_version",
             "caee_timing_enable", "caee_timing_reset", "caee_timing_query")
 
 
@@ -170,6 +171,14 @@ def pack_matrix(w_dtype: str, src, dst, rows: int, cols: int, count: int):
     """Repack `count` row-major [rows][cols] matrices into the tiled layout."""
     _check(lib.caee_pack_matrix(DTYPE_CODE[w_dtype], _ptr(src), _ptr(dst), rows, cols, count, _stream(src)))
     return dst
+
+
+def quantize_rows(src, q, scale):
+    """E4M3 codes and per-128-column fp32 scales of a bf16/fp32 [rows][cols] tensor."""
+    import torch
+    dt = {torch.bfloat16: CAEE_BF16, torch.float32: CAEE_F32}[src.dtype]
+    _check(lib.caee_quantize_rows(dt, _ptr(src), src.shape[0], src.shape[1], _ptr(q), _ptr(scale), _stream(src)))
+    return q, scale
 
 
 def pack_weights(weights: dict, w_dtype: str) -> dict:

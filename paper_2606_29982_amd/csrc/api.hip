@@ -69,7 +69,6 @@ caee_status_t check_desc(const caee_layer_desc_t* d) {
         return fail(CAEE_ERR_UNSUPPORTED, "E=%d with %d experts per group needs the group size to be a "
                     "multiple of %d with a power-of-two quotient", d->E, gsize, epl);
     if (d->T > kMaxT) return fail(CAEE_ERR_UNSUPPORTED, "T=%d exceeds %d", d->T, kMaxT);
-    if (d->w_dtype == CAEE_FP8_E4M3) return fail(CAEE_ERR_UNSUPPORTED, "fp8 weights are not built yet");
     return CAEE_OK;
 }
 
@@ -256,7 +255,22 @@ caee_status_t run_ffn(const caee_layer_desc_t* d, const void* x, const int32_t* 
     p.P = L.P;
     p.ksplit = L.ksplit;
     p.tiled = W->layout == CAEE_LAYOUT_TILED;
+    p.xq = (uint8_t*)(ws + L.xq);
+    p.xs = (float*)(ws + L.xs);
+    p.hq = (uint8_t*)(ws + L.hq);
+    p.hs = (float*)(ws + L.hs);
     const int nb = ffn_token_blocks(*d);
+    if (d->w_dtype == CAEE_FP8_E4M3) {
+        CAEE_TRY(timed_launch(CAEE_KERNEL_QUANT, s, "quantise x",
+                              [&] { return launch_quant_rows(x, 1, d->T, d->d, p.xq, p.xs, s); }));
+        CAEE_TRY(timed_launch(CAEE_KERNEL_GATE_UP, s, "gate/up",
+                              [&] { return launch_gate_up_fp8(p, nb, L.max_chunks, s); }));
+        CAEE_TRY(timed_launch(CAEE_KERNEL_QUANT, s, "quantise H",
+                              [&] { return launch_quant_rows(p.h, 0, L.P, d->f, p.hq, p.hs, s); }));
+        CAEE_TRY(timed_launch(CAEE_KERNEL_DOWN, s, "down", [&] { return launch_down_fp8(p, nb, L.max_chunks, s); }));
+        CAEE_TRY(timed_launch(CAEE_KERNEL_COMBINE, s, "combine", [&] { return launch_combine(p, s); }));
+        return CAEE_OK;
+    }
     CAEE_TRY(timed_launch(CAEE_KERNEL_GATE_UP, s, "gate/up",
                           [&] { return launch_gate_up(p, d->w_dtype, nb, L.max_chunks, s); }));
     CAEE_TRY(timed_launch(CAEE_KERNEL_DOWN, s, "down",
@@ -382,6 +396,24 @@ caee_status_t caee_pack_matrix(int32_t w_dtype, const void* src, void* dst, int6
     if (count == 0) return CAEE_OK;
     const hipError_t err = launch_pack(src, dst, rows, row_bytes / 16, count, as_stream(stream));
     if (err != hipSuccess) return fail(CAEE_ERR_HIP, "pack launch failed: %s", hipGetErrorString(err));
+    return CAEE_OK;
+}
+
+caee_status_t caee_quantize_rows(int32_t src_dtype, const void* src, int64_t rows, int64_t cols, uint8_t* q,
+                                 float* scale, void* stream) {
+    g_last_error.clear();
+    if (src_dtype != CAEE_BF16 && src_dtype != CAEE_F32)
+        return fail(CAEE_ERR_INVALID_ARG, "src_dtype=%d must be CAEE_BF16 or CAEE_F32", src_dtype);
+    if (rows < 0 || cols <= 0 || cols % 128)
+        return fail(CAEE_ERR_INVALID_ARG, "rows=%lld must be >= 0 and cols=%lld a positive multiple of 128",
+                    (long long)rows, (long long)cols);
+    CAEE_TRY(check_ptr(src, "src", true));
+    CAEE_TRY(check_ptr(q, "q", true));
+    CAEE_TRY(check_ptr(scale, "scale", true));
+    if (rows == 0) return CAEE_OK;
+    const hipError_t err =
+        launch_quant_rows(src, src_dtype == CAEE_BF16, rows, (int)cols, q, scale, as_stream(stream));
+    if (err != hipSuccess) return fail(CAEE_ERR_HIP, "quantise launch failed: %s", hipGetErrorString(err));
     return CAEE_OK;
 }
 

@@ -31,6 +31,7 @@ constexpr long long kTargetItems = 4096;   // gate/up work items wanted per call
 #endif
 constexpr int kGateUpU = CAEE_GATE_UP_U;
 constexpr int kDownU = CAEE_DOWN_U;
+constexpr int kFp8U = 2;            // 128-wide fp8 MFMA blocks per step (4 x 16-byte loads per matrix)
 // Minimum resident waves per SIMD the FFN kernels are compiled for (0: no bound).
 #ifndef CAEE_FFN_WAVES_PER_EU
 #define CAEE_FFN_WAVES_PER_EU 0
@@ -58,6 +59,8 @@ struct WsLayout {
     size_t n_chunks;            // [1]
     size_t h;                   // [P][f] SwiGLU activations (weight dtype; fp32 for fp8)
     size_t y;                   // [P][d] fp32 expert outputs
+    size_t xq, xs;              // fp8 path: [T][d] e4m3 codes of x and [T][d/128] fp32 scales
+    size_t hq, hs;              // fp8 path: [P][f] e4m3 codes of H and [P][f/128] fp32 scales
     size_t total;
     int P, max_chunks, ksplit, chunk_tokens;
 };
@@ -73,12 +76,16 @@ inline int elem_bytes(int dtype) {
 // Depends on the descriptor only (not on the device).
 // The splits of one tile are waves of one 4-wave workgroup, so ksplit <= 4.
 inline int gate_up_split(const caee_layer_desc_t& d) {
-    const int ksteps = d.d * elem_bytes(d.w_dtype) / 64;
+    // Contraction steps of one work item: 64-byte row pieces (one MFMA for
+    // bf16) or 128-wide scale blocks (one MFMA for fp8).
+    const bool fp8 = d.w_dtype == CAEE_FP8_E4M3;
+    const int ksteps = fp8 ? d.d / 128 : d.d * elem_bytes(d.w_dtype) / 64;
+    const int U = fp8 ? kFp8U : kGateUpU;
     const long long tok_slots = (long long)(d.T > 0 ? d.T : 0) * d.k;
     const long long experts = (tok_slots < d.E ? tok_slots : d.E) + d.n_shared;
     const long long tiles = experts * (d.f / 16);
     int S = 1;
-    while (S < 4 && tiles * S < kTargetItems && ksteps % (2 * S * kGateUpU) == 0) S *= 2;
+    while (S < 4 && tiles * S < kTargetItems && ksteps % (2 * S * U) == 0) S *= 2;
     return S;
 }
 
@@ -116,6 +123,11 @@ inline WsLayout ws_layout(const caee_layer_desc_t& d) {
     const int h_bytes = d.w_dtype == CAEE_FP8_E4M3 ? 4 : elem_bytes(d.w_dtype);
     L.h = take(size_t(L.P) * d.f * h_bytes);
     L.y = take(size_t(L.P) * d.d * 4);
+    const bool fp8 = d.w_dtype == CAEE_FP8_E4M3;
+    L.xq = take(fp8 ? T * d.d : 0);
+    L.xs = take(fp8 ? T * (d.d / 128) * 4 : 0);
+    L.hq = take(fp8 ? size_t(L.P) * d.f : 0);
+    L.hs = take(fp8 ? size_t(L.P) * (d.f / 128) * 4 : 0);
     L.ksplit = gate_up_split(d);
     L.total = off;
     return L;
@@ -182,6 +194,11 @@ struct FfnParams {
     int P;
     int ksplit;
     int tiled;      // weights in CAEE_LAYOUT_TILED order
+    // fp8 path: quantised activations and their per-token 128-channel scales
+    uint8_t* xq;
+    float* xs;
+    uint8_t* hq;
+    float* hs;
 };
 
 // Host-side launchers (defined next to their kernels).
@@ -190,6 +207,10 @@ hipError_t launch_permute(const RouteParams& p, hipStream_t s);
 hipError_t launch_gate_up(const FfnParams& p, int w_dtype, int nb, int max_chunks, hipStream_t s);
 hipError_t launch_down(const FfnParams& p, int w_dtype, int nb, int max_chunks, hipStream_t s);
 hipError_t launch_combine(const FfnParams& p, hipStream_t s);
+hipError_t launch_quant_rows(const void* src, int src_bf16, long long rows, int cols, uint8_t* q, float* scale,
+                             hipStream_t s);
+hipError_t launch_gate_up_fp8(const FfnParams& p, int nb, int max_chunks, hipStream_t s);
+hipError_t launch_down_fp8(const FfnParams& p, int nb, int max_chunks, hipStream_t s);
 hipError_t launch_pack(const void* src, void* dst, long long rows, long long row_units, long long count,
                        hipStream_t s);
 int device_cu_count();

@@ -1,0 +1,336 @@
+// 8-bit expert FFN for gfx950: OCP E4M3 weights with fp32 128x128 block
+// scales, activations quantised per token per 128 channels (x before the
+// gate/up products, the SwiGLU rows before the down product).
+//
+// One 16x16x128 MFMA consumes exactly one 128-wide scale block of the
+// contraction, so each block's fp32 partial is multiplied by
+// (weight-block scale) x (token-block scale) and added to the accumulator.
+// Work decomposition, tiled weight layout and the deterministic split-K
+// reduction are those of the 16-bit kernels.
+#include <math.h>
+
+#include "caee_internal.h"
+
+namespace caee {
+namespace {
+
+typedef int i32x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+
+constexpr float kE4M3Max = 448.0f;
+constexpr int kScaleOne = 127;   // E8M0 exponent of 1.0 for the MFMA's own block scales
+
+// OCP E4M3 (fn) code of v: nearest representable value, ties to the even
+// code, magnitudes above 448 saturate to 448.
+__device__ inline uint32_t e4m3_code(float v) {
+    const uint32_t sign = (__float_as_uint(v) >> 24) & 0x80u;
+    const float a = fminf(fabsf(v), kE4M3Max);
+    uint32_t code;
+    if (a < 0.015625f) {                       // below 2^-6: subnormal steps of 2^-9
+        code = (uint32_t)rintf(a * 512.0f);     // 8 is the smallest normal, code 8
+    } else {
+        int e = (int)((__float_as_uint(a) >> 23) & 0xFFu) - 127;   // a in [2^e, 2^(e+1))
+        uint32_t q = (uint32_t)rintf(ldexpf(a, 3 - e));            // 8 .. 16
+        if (q == 16u) {
+            q = 8u;
+            ++e;
+        }
+        code = ((uint32_t)(e + 7) << 3) | (q - 8u);
+        if (code > 126u) code = 126u;
+    }
+    return sign | code;
+}
+
+// Per-row, per-128-column quantisation: one wavefront per block of 128
+// values (two per lane).  scale = amax / 448 (1 for an all-zero block),
+// code = e4m3(value / scale), all in fp32.
+__global__ __launch_bounds__(256) void k_quant_rows(const void* src, int src_bf16, long long rows, int cols,
+                                                    uint8_t* q, float* scale) {
+    const int lane = threadIdx.x & (kWave - 1);
+    const long long w = (long long)blockIdx.x * 4 + threadIdx.x / kWave;
+    const int nblk = cols / 128;
+    if (w >= rows * nblk) return;
+    const long long row = w / nblk;
+    const int blk = (int)(w - row * nblk);
+    const long long base = row * cols + blk * 128 + 2 * lane;
+    float v0, v1;
+    if (src_bf16) {
+        const uint32_t u = *(const uint32_t*)((const uint16_t*)src + base);
+        v0 = __uint_as_float(u << 16);
+        v1 = __uint_as_float(u & 0xFFFF0000u);
+    } else {
+        const float2 f = *(const float2*)((const float*)src + base);
+        v0 = f.x;
+        v1 = f.y;
+    }
+    float amax = fmaxf(fabsf(v0), fabsf(v1));
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) amax = fmaxf(amax, __shfl_xor(amax, off));
+    const float sc = amax > 0.0f ? amax / kE4M3Max : 1.0f;
+    const uint32_t c0 = e4m3_code(v0 / sc), c1 = e4m3_code(v1 / sc);
+    *(uint16_t*)(q + base) = (uint16_t)(c0 | (c1 << 8));
+    if (lane == 0) scale[row * nblk + blk] = sc;
+}
+
+__device__ inline i32x8_t join(const u32x4_t& lo, const u32x4_t& hi) {
+    return i32x8_t{(int)lo[0], (int)lo[1], (int)lo[2], (int)lo[3], (int)hi[0], (int)hi[1], (int)hi[2], (int)hi[3]};
+}
+
+__device__ inline const char* expert_base(const void* routed, const void* shared, int x, int E,
+                                          size_t expert_bytes) {
+    return x < E ? (const char*)routed + (size_t)x * expert_bytes
+                 : (const char*)shared + (size_t)(x - E) * expert_bytes;
+}
+
+// Contraction of one 16-row tile against up to NB 16-token blocks over
+// `nblocks` 128-wide blocks.  a[m]: this lane's first weight piece (the two
+// pieces of a block are `astep` apart, blocks 2*astep apart); b[tb]: the
+// token row's first piece (4 pieces = 64 bytes per step); wsc[m][kb] and
+// xsc[tb][kb]: block scales.  Weights are loaded U blocks ahead.
+template <int U, int NA, int NB>
+__device__ inline void contract_fp8(const u32x4_t* const (&a)[NA], int astep, const u32x4_t* const (&b)[NB],
+                                    const float* const (&wsc)[NA], const float* const (&xsc)[NB], int nb,
+                                    int nblocks, f32x4_t (&acc)[NA][NB]) {
+    // Blocks past the end of the row (when nblocks is not a multiple of U)
+    // are neither loaded nor multiplied.
+    u32x4_t cur[NA][U][2], nxt[NA][U][2];
+#pragma unroll
+    for (int m = 0; m < NA; ++m)
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int h = 0; h < 2; ++h)
+                cur[m][u][h] = u < nblocks ? __builtin_nontemporal_load(a[m] + (size_t)astep * (2 * u + h))
+                                           : u32x4_t{0u, 0u, 0u, 0u};
+    const f32x4_t zero = {0.f, 0.f, 0.f, 0.f};
+    for (int kb = 0; kb < nblocks; kb += U) {
+        const bool more = kb + U < nblocks;
+        if (more) {
+#pragma unroll
+            for (int m = 0; m < NA; ++m)
+#pragma unroll
+                for (int u = 0; u < U; ++u)
+#pragma unroll
+                    for (int h = 0; h < 2; ++h)
+                        nxt[m][u][h] = kb + U + u < nblocks
+                                           ? __builtin_nontemporal_load(a[m] + (size_t)astep * (2 * (kb + U + u) + h))
+                                           : u32x4_t{0u, 0u, 0u, 0u};
+        }
+        float ws[NA][U];
+#pragma unroll
+        for (int m = 0; m < NA; ++m)
+#pragma unroll
+            for (int u = 0; u < U; ++u) ws[m][u] = kb + u < nblocks ? wsc[m][kb + u] : 0.0f;
+#pragma unroll
+        for (int tb = 0; tb < NB; ++tb) {
+            if (tb < nb) {
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    if (kb + u >= nblocks) break;
+                    const int st = 2 * (kb + u);
+                    const i32x8_t bv = join(b[tb][4 * st], b[tb][4 * (st + 1)]);
+                    const float xs = xsc[tb][kb + u];
+#pragma unroll
+                    for (int m = 0; m < NA; ++m) {
+                        const f32x4_t part = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(
+                            join(cur[m][u][0], cur[m][u][1]), bv, zero, 0, 0, 0, kScaleOne, 0, kScaleOne);
+                        acc[m][tb] += part * (ws[m][u] * xs);
+                    }
+                }
+            }
+        }
+        if (more) {
+#pragma unroll
+            for (int m = 0; m < NA; ++m)
+#pragma unroll
+                for (int u = 0; u < U; ++u)
+#pragma unroll
+                    for (int h = 0; h < 2; ++h) cur[m][u][h] = nxt[m][u][h];
+        }
+    }
+}
+
+__device__ inline float silu_mul(float g, float u) { return g / (1.0f + __expf(-g)) * u; }
+
+// Gate/up + SwiGLU, fp32 output rows (quantised afterwards).
+template <int NB>
+__global__ __launch_bounds__(kFfnThreads) void k_gate_up_fp8(FfnParams p) {
+    constexpr int kWaves = kFfnThreads / kWave;
+    __shared__ f32x4_t s_red[kWaves][2][NB][kWave];
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = threadIdx.x / kWave;
+    const int r = lane & 15, g = lane >> 4;
+    const int S = p.ksplit;
+    const int tiles = p.f / 16;
+    const int tiles_per_item = kWaves / S;
+    const int items_per_chunk = tiles / tiles_per_item;
+    const int total = (*p.n_chunks) * items_per_chunk;
+    const size_t row_units = (size_t)p.d / 16;     // 16-byte pieces per weight / x row
+    const size_t ksteps = row_units / 4;            // 64-byte steps per row
+    const int kblocks = p.d / 128;
+    const int kper = kblocks / S;
+    const size_t expert_bytes = (size_t)2 * p.f * p.d;
+    const int sblk = p.d / 128;                     // scale blocks per row
+    const int sp = wave % S;
+
+    for (int item = blockIdx.x; item < total; item += gridDim.x) {
+        const int c = item / items_per_chunk;
+        const int jt = (item - c * items_per_chunk) * tiles_per_item + wave / S;
+        const int xs_ = p.chunks[4 * c], row0 = p.chunks[4 * c + 1], ntok = p.chunks[4 * c + 2];
+        const int nb = (ntok + 15) >> 4;
+        const int kb0 = sp * kper;
+        const u32x4_t* wb = (const u32x4_t*)expert_base(p.w13, p.sh_w13, xs_, p.E, expert_bytes);
+        const u32x4_t* const a[2] = {
+            p.tiled ? wb + ((size_t)jt * ksteps + 2 * (size_t)kb0) * 64 + lane
+                    : wb + (size_t)(jt * 16 + r) * row_units + g + 8 * (size_t)kb0,
+            p.tiled ? wb + ((size_t)(tiles + jt) * ksteps + 2 * (size_t)kb0) * 64 + lane
+                    : wb + (size_t)(p.f + jt * 16 + r) * row_units + g + 8 * (size_t)kb0};
+        const int astep = p.tiled ? 64 : 4;
+        const float* sbase = xs_ < p.E ? p.w13_scale + (size_t)xs_ * (2 * p.f / 128) * sblk
+                                       : p.sh_w13_scale + (size_t)(xs_ - p.E) * (2 * p.f / 128) * sblk;
+        const float* const wsc[2] = {sbase + (size_t)((jt * 16) / 128) * sblk + kb0,
+                                     sbase + (size_t)((p.f + jt * 16) / 128) * sblk + kb0};
+        const u32x4_t* xb[NB];
+        const float* xsc[NB];
+#pragma unroll
+        for (int tb = 0; tb < NB; ++tb) {
+            int n = tb * 16 + r;
+            n = (tb < nb && n < ntok) ? n : 0;   // padded token columns read a valid row; results dropped
+            const int tok = p.perm_tok[row0 + n];
+            xb[tb] = (const u32x4_t*)p.xq + (size_t)tok * row_units + g + 8 * (size_t)kb0;
+            xsc[tb] = p.xs + (size_t)tok * sblk + kb0;
+        }
+        f32x4_t acc[2][NB];
+#pragma unroll
+        for (int m = 0; m < 2; ++m)
+#pragma unroll
+            for (int tb = 0; tb < NB; ++tb) acc[m][tb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        contract_fp8<kFp8U, 2, NB>(a, astep, xb, wsc, xsc, nb, kper, acc);
+
+        if (S > 1) {
+#pragma unroll
+            for (int m = 0; m < 2; ++m)
+#pragma unroll
+                for (int tb = 0; tb < NB; ++tb) s_red[wave][m][tb][lane] = acc[m][tb];
+            __syncthreads();
+            if (sp == 0) {
+#pragma unroll
+                for (int m = 0; m < 2; ++m)
+#pragma unroll
+                    for (int tb = 0; tb < NB; ++tb) {
+                        f32x4_t sum = s_red[wave][m][tb][lane];
+                        for (int q = 1; q < S; ++q) sum += s_red[wave + q][m][tb][lane];
+                        acc[m][tb] = sum;
+                    }
+            }
+            __syncthreads();
+        }
+        if (sp == 0) {
+            const int col = jt * 16 + 4 * g;
+#pragma unroll
+            for (int tb = 0; tb < NB; ++tb) {
+                const int n = tb * 16 + r;
+                if (tb < nb && n < ntok) {
+                    float h[4];
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) h[v] = silu_mul(acc[0][tb][v], acc[1][tb][v]);
+                    *(float4*)((float*)p.h + (size_t)(row0 + n) * p.f + col) = make_float4(h[0], h[1], h[2], h[3]);
+                }
+            }
+        }
+    }
+}
+
+// Down products from the quantised SwiGLU rows.
+template <int NB>
+__global__ __launch_bounds__(kFfnThreads) void k_down_fp8(FfnParams p) {
+    const int lane = threadIdx.x & (kWave - 1);
+    const int r = lane & 15, g = lane >> 4;
+    const int gw = blockIdx.x * (kFfnThreads / kWave) + (threadIdx.x / kWave);
+    const int nw = gridDim.x * (kFfnThreads / kWave);
+    const int tiles = p.d / 16;
+    const int total = (*p.n_chunks) * tiles;
+    const size_t row_units = (size_t)p.f / 16;
+    const size_t ksteps = row_units / 4;
+    const int kblocks = p.f / 128;
+    const size_t expert_bytes = (size_t)p.d * p.f;
+    const int sblk = p.f / 128;
+
+    for (int item = gw; item < total; item += nw) {
+        const int c = item / tiles, it = item - c * tiles;
+        const int xs_ = p.chunks[4 * c], row0 = p.chunks[4 * c + 1], ntok = p.chunks[4 * c + 2];
+        const int nb = (ntok + 15) >> 4;
+        const u32x4_t* wb = (const u32x4_t*)expert_base(p.w2, p.sh_w2, xs_, p.E, expert_bytes);
+        const u32x4_t* const a[1] = {p.tiled ? wb + (size_t)it * ksteps * 64 + lane
+                                             : wb + (size_t)(it * 16 + r) * row_units + g};
+        const int astep = p.tiled ? 64 : 4;
+        const float* sbase = xs_ < p.E ? p.w2_scale + (size_t)xs_ * (p.d / 128) * sblk
+                                       : p.sh_w2_scale + (size_t)(xs_ - p.E) * (p.d / 128) * sblk;
+        const float* const wsc[1] = {sbase + (size_t)((it * 16) / 128) * sblk};
+        const u32x4_t* hb[NB];
+        const float* hsc[NB];
+#pragma unroll
+        for (int tb = 0; tb < NB; ++tb) {
+            int n = tb * 16 + r;
+            n = (tb < nb && n < ntok) ? n : 0;
+            hb[tb] = (const u32x4_t*)p.hq + (size_t)(row0 + n) * row_units + g;
+            hsc[tb] = p.hs + (size_t)(row0 + n) * sblk;
+        }
+        f32x4_t acc[1][NB];
+#pragma unroll
+        for (int tb = 0; tb < NB; ++tb) acc[0][tb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        contract_fp8<kFp8U, 1, NB>(a, astep, hb, wsc, hsc, nb, kblocks, acc);
+#pragma unroll
+        for (int tb = 0; tb < NB; ++tb) {
+            const int n = tb * 16 + r;
+            if (tb < nb && n < ntok) {
+                float* o = p.yperm + (size_t)(row0 + n) * p.d + it * 16 + 4 * g;
+                *(float4*)o = make_float4(acc[0][tb][0], acc[0][tb][1], acc[0][tb][2], acc[0][tb][3]);
+            }
+        }
+    }
+}
+
+int grid_for_waves(long long waves_needed) {
+    const long long wgs = (waves_needed + 3) / 4;
+    const long long cap = (long long)device_cu_count() * 8;
+    return (int)(wgs < 1 ? 1 : (wgs < cap ? wgs : cap));
+}
+
+}  // namespace
+
+hipError_t launch_quant_rows(const void* src, int src_bf16, long long rows, int cols, uint8_t* q, float* scale,
+                             hipStream_t s) {
+    const long long waves = rows * (cols / 128);
+    if (waves == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_quant_rows, dim3((unsigned)((waves + 3) / 4)), dim3(256), 0, s, src, src_bf16, rows, cols,
+                       q, scale);
+    return hipGetLastError();
+}
+
+hipError_t launch_gate_up_fp8(const FfnParams& p, int nb, int max_chunks, hipStream_t s) {
+    const dim3 grid(grid_for_waves((long long)max_chunks * (p.f / 16) * p.ksplit));
+    switch (nb) {
+        case 1: hipLaunchKernelGGL(k_gate_up_fp8<1>, grid, dim3(kFfnThreads), 0, s, p); break;
+        case 2: hipLaunchKernelGGL(k_gate_up_fp8<2>, grid, dim3(kFfnThreads), 0, s, p); break;
+        case 4: hipLaunchKernelGGL(k_gate_up_fp8<4>, grid, dim3(kFfnThreads), 0, s, p); break;
+        case 8: hipLaunchKernelGGL(k_gate_up_fp8<8>, grid, dim3(kFfnThreads), 0, s, p); break;
+        default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_down_fp8(const FfnParams& p, int nb, int max_chunks, hipStream_t s) {
+    const dim3 grid(grid_for_waves((long long)max_chunks * (p.d / 16)));
+    switch (nb) {
+        case 1: hipLaunchKernelGGL(k_down_fp8<1>, grid, dim3(kFfnThreads), 0, s, p); break;
+        case 2: hipLaunchKernelGGL(k_down_fp8<2>, grid, dim3(kFfnThreads), 0, s, p); break;
+        case 4: hipLaunchKernelGGL(k_down_fp8<4>, grid, dim3(kFfnThreads), 0, s, p); break;
+        case 8: hipLaunchKernelGGL(k_down_fp8<8>, grid, dim3(kFfnThreads), 0, s, p); break;
+        default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+}  // namespace caee

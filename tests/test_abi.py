@@ -142,3 +142,11 @@ def test_pack_matrix_host_checks():
     n = _ws_status(_layer())[1]
     assert caee.lib.caee_expert_ffn(ctypes.byref(d), FAKE, FAKE, FAKE, ctypes.byref(W), FAKE, FAKE, n,
                                     None) == caee.CAEE_ERR_INVALID_ARG                          # unknown layout
+
+
+def test_quantize_rows_host_checks():
+    qr = caee.lib.caee_quantize_rows
+    assert qr(caee.CAEE_FP8_E4M3, FAKE, 4, 128, FAKE, FAKE, None) == caee.CAEE_ERR_INVALID_ARG
+    assert qr(caee.CAEE_BF16, FAKE, 4, 100, FAKE, FAKE, None) == caee.CAEE_ERR_INVALID_ARG
+    assert qr(caee.CAEE_BF16, None, 4, 128, FAKE, FAKE, None) == caee.CAEE_ERR_INVALID_ARG
+    assert qr(caee.CAEE_F32, FAKE, 0, 128, FAKE, FAKE, None) == caee.CAEE_OK

@@ -1,0 +1,114 @@
+"""GPU parity of the 8-bit expert path: OCP e4m3 weights with fp32 128x128
+block scales, activations quantised per token per 128 channels.  Indices
+exact, outputs within 6e-2 * max|ref| of the fp64 oracle (which quantises
+the same activations the same way)."""
+import numpy as np
+import pytest
+import torch
+
+from caee_cases import check_route, check_y, getters_dev, getters_np, gpu_layer, oracle_layer, w_to_dev
+from paper_2606_29982_amd import caee
+from synth_inputs import R1_FP8, TINY_F32, make_expert_weights_np, make_expert_weights_torch, make_routing_inputs
+
+pytestmark = pytest.mark.gpu
+DEV = torch.device("cuda:0")
+TINY_FP8 = TINY_F32.with_(name="tiny-fp8", w_dtype="fp8", x_dtype="bf16", y_dtype="bf16")
+
+
+def _tiny(seed, tau, n_bins, T=None, rule="max", tiled=False, zipf=None):
+    shape = TINY_FP8
+    inp = make_routing_inputs(shape, seed=seed, T=T, n_bins=n_bins, zipf_logit_s=zipf)
+    W = make_expert_weights_np(shape, seed=seed)
+    Wd = w_to_dev(W, DEV)
+    if tiled:
+        Wd = caee.pack_weights(Wd, "fp8")
+    print(f"fp8 tiny seed={seed} tau={tau} n_bins={n_bins} T={inp.logits.shape[0]} rule={rule} tiled={tiled}",
+          flush=True)
+    got = gpu_layer(shape, inp, tau, n_bins, Wd, DEV, rule=rule)
+    get, get_sh = getters_np(W, "fp8")
+    ref = oracle_layer(shape, inp, tau, n_bins, get, get_sh, rule=rule)
+    check_route(got, ref, shape.E)
+    return check_y(got["y"], ref["y"], 6e-2)
+
+
+@pytest.mark.parametrize("seed", range(3))
+@pytest.mark.parametrize("tiled", [False, True])
+def test_tiny_fp8(seed, tiled):
+    rel = _tiny(seed, 0.1, 4, tiled=tiled)
+    print(f"  max|err|/max|ref| = {rel:.3e}")
+
+
+@pytest.mark.parametrize("T", [1, 5, 40, 130])
+def test_tiny_fp8_batches(T):
+    _tiny(7, 0.2, 4, T=T, tiled=True, zipf=1.1 if T > 100 else None)
+
+
+def test_tiny_fp8_sum_rule():
+    _tiny(8, 0.8, 4, rule="sum", tiled=True)
+
+
+def test_e4m3_codes_match_oracle():
+    # the activation codec: quantise rows whose values hit every rounding
+    # case (ties, subnormals, the saturation edge) and compare the dequantised
+    # rows with the oracle's fp32 quantiser
+    from oracle import quantize_e4m3_blocks
+    rng = np.random.default_rng(0)
+    rows = rng.standard_normal((64, 256)).astype(np.float32) * np.float32(3.0)
+    rows[0, :128] = np.linspace(-448, 448, 128, dtype=np.float32)
+    rows[1, :128] = 2.0 ** -np.arange(128, dtype=np.float32) * 0.5
+    rows[2, :] = 0.0
+    import synth_inputs
+    bits = synth_inputs.bf16_bits_from_f32(rows)
+    x = torch.from_numpy(bits.view(np.int16)).to(DEV).view(torch.bfloat16)
+    exact = (bits.astype(np.uint32) << 16).view(np.float32)
+    _, scale_ref, deq_ref = quantize_e4m3_blocks(exact)
+    # run the quantiser through a 1-token-per-row layer: compare via a layer
+    # whose experts are identity-like is indirect, so call the path directly
+    T, d = rows.shape
+    q = torch.empty((T, d), dtype=torch.uint8, device=DEV)
+    s = torch.empty((T, d // 128), dtype=torch.float32, device=DEV)
+    caee.quantize_rows(x, q, s)
+    torch.cuda.synchronize()
+    from oracle import e4m3_decode
+    deq = e4m3_decode(q.cpu().numpy()).reshape(T, d // 128, 128) * s.cpu().numpy()[:, :, None].astype(np.float64)
+    np.testing.assert_array_equal(s.cpu().numpy(), scale_ref)
+    np.testing.assert_array_equal(deq.reshape(T, d), deq_ref)
+
+
+@pytest.fixture(scope="module")
+def r1_fp8():
+    print("drawing R1-shaped fp8 expert weights on the device", flush=True)
+    W = make_expert_weights_torch(R1_FP8, seed=0, device=DEV)
+    Wt = caee.pack_weights(W, "fp8")
+    torch.cuda.synchronize()
+    yield W, Wt
+    del W, Wt
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("T,tokens,rule,tau", [(64, [0, 31, 63], "max", 0.05), (64, [5, 60], "sum", 1.2),
+                                               (1, [0], "max", 0.0)])
+def test_r1_fp8_decode(T, tokens, rule, tau, r1_fp8):
+    W, Wt = r1_fp8
+    inp = make_routing_inputs(R1_FP8, seed=3, T=T, zipf_logit_s=1.1, cost_kind="zipf", n_bins=8)
+    print(f"fp8 R1 T={T} rule={rule} tau={tau}", flush=True)
+    got = gpu_layer(R1_FP8, inp, tau, 8, Wt, DEV, rule=rule)
+    get, get_sh = getters_dev(W, "fp8")
+    ref = oracle_layer(R1_FP8, inp, tau, 8, get, get_sh, tokens=tokens, rule=rule)
+    check_route(got, ref, R1_FP8.E)
+    rel = check_y(got["y"][tokens], ref["y"], 6e-2)
+    print(f"  max|err|/max|ref| = {rel:.3e}", flush=True)
+
+
+def test_r1_fp8_prefill(r1_fp8):
+    W, Wt = r1_fp8
+    T = 4096
+    inp = make_routing_inputs(R1_FP8, seed=4, T=T, cost_kind="zipf", n_bins=8)
+    tokens = [0, 1234, 4095]
+    print("fp8 R1 prefill T=4096", flush=True)
+    got = gpu_layer(R1_FP8, inp, 0.05, 8, Wt, DEV)
+    get, get_sh = getters_dev(W, "fp8")
+    ref = oracle_layer(R1_FP8, inp, 0.05, 8, get, get_sh, tokens=tokens)
+    check_route(got, ref, R1_FP8.E)
+    rel = check_y(got["y"][tokens], ref["y"], 6e-2)
+    print(f"  max|err|/max|ref| = {rel:.3e}", flush=True)
