@@ -25,7 +25,10 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E, published
+FP8_PEAK_TFLOPS = 5000.0        # MI355X dense fp8 MFMA, published
 W_EXPERT_BYTES = 3 * 7168 * 2048 * 2
+W_EXPERT_BYTES_FP8 = 3 * 7168 * 2048 + 4 * (2 * 2048 // 128) * (7168 // 128) + 4 * (7168 // 128) * (2048 // 128)
+PAIR_FLOPS = 6 * 7168 * 2048    # one (token, expert) pair through gate, up and down
 METRIC = "MoE-layer tokens/s + achieved HBM GB/s (% of peak) at T=1..128, with vs without pruning"
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gate_up_r1_t32_traffic.json")
 FFN_SOURCE = os.path.join(ROOT, "paper_2606_29982_amd", "csrc", "ffn.hip")
@@ -53,12 +56,14 @@ def log(msg):
 class Case:
     """Device-resident inputs and buffers of one layer call."""
 
-    def __init__(self, shape, T, tau, n_bins, W, dev, seed, skewed, rule="max"):
+    def __init__(self, shape, T, tau, n_bins, W, dev, seed, skewed, rule="max", cost_kind=None):
         import torch
         from paper_2606_29982_amd import caee
         from synth_inputs import make_routing_inputs
+        if cost_kind is None:
+            cost_kind = "zipf" if skewed else "flat"
         self.inp = make_routing_inputs(shape, seed=seed, T=T, zipf_logit_s=1.1 if skewed else None,
-                                       cost_kind="zipf" if skewed else "flat", n_bins=n_bins)
+                                       cost_kind=cost_kind, n_bins=n_bins)
         self.layer = caee.Layer.from_shape(shape, T=T, tau=tau, n_bins=n_bins, importance=rule)
         to = lambda a: None if a is None else torch.from_numpy(np.ascontiguousarray(a)).to(dev)  # noqa: E731
         self.x = torch.from_numpy(self.inp.x.view(np.int16)).to(dev).view(torch.bfloat16)
@@ -68,6 +73,7 @@ class Case:
         self.bins = to(self.inp.bins) if n_bins > 1 else None
         self.W = W
         self.y = torch.empty((T, shape.d), dtype=torch.bfloat16, device=dev)
+        self.T = T
         self.ws = caee.alloc_workspace(self.layer, dev)
         self.out = caee.alloc_route_out(self.layer, dev)
         self.caee = caee
@@ -78,6 +84,9 @@ class Case:
 
     def stats(self):
         return self.out["stats"].cpu().numpy().tolist()
+
+    def routed_pairs(self):
+        return int((self.out["topk_ids"] >= 0).sum().item())
 
 
 def time_steps(case, steps, warmup):
@@ -247,6 +256,31 @@ def main():
                 log(f"sweep {sweep[-1]}")
                 del c
         result["sweep"] = sweep
+
+    if not args.no_sweep:
+        # 8-bit expert weights (e4m3, 128x128 block scales), activations
+        # quantised per token per 128 channels: decode and prefill, tau=0.05.
+        from synth_inputs import R1_FP8
+        W8 = caee.pack_weights(make_expert_weights_torch(R1_FP8, seed=args.seed, device=dev), "fp8")
+        fp8_rows = []
+        for T, steps in ((64, max(10, args.steps // 2)), (4096, 5)):
+            c = Case(R1_FP8, T, 0.05, 8, W8, dev, args.seed, skewed=False, cost_kind="zipf")
+            m = time_steps(c, steps, 2)
+            s = c.stats()
+            pairs = c.routed_pairs() + T * R1_FP8.n_shared
+            b = (s[5] + R1_FP8.n_shared) * W_EXPERT_BYTES_FP8 + T * R1_FP8.d * 4 + T * R1_FP8.E * 4
+            tflops = pairs * PAIR_FLOPS / (m * 1e-3) / 1e12
+            fp8_rows.append({"T": T, "tau": 0.05, "n_bins": 8, "rule": "max", "weights": "e4m3 + fp32 128x128 scales",
+                             "us_per_step": round(m * 1e3, 1), "tokens_per_s": round(T / (m * 1e-3), 1),
+                             "hbm_gbps": round(b / (m * 1e-3) / 1e9, 1),
+                             "hbm_frac": round(b / (m * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+                             "mfma_tflops": round(tflops, 1), "mfma_frac": round(tflops / FP8_PEAK_TFLOPS, 4),
+                             "executed": s[5] + R1_FP8.n_shared, "pruned": s[4]})
+            log(f"fp8 {fp8_rows[-1]}")
+            del c
+        result["fp8"] = fp8_rows
+        del W8
+        torch.cuda.empty_cache()
 
     if args.copy_bytes > 0:
         src = torch.empty(args.copy_bytes, dtype=torch.uint8, device=dev)

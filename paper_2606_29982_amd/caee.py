@@ -54,6 +54,10 @@ def _load(path: str = LIB_PATH):
     if not os.path.exists(path):
         raise ImportError(f"{path} is missing: build it with __graft_entry__.build() "
                           "(python -c 'import __graft_entry__ as g; g.build()')")
+    # torch ships its own HIP runtime; importing it first makes the library
+    # bind to that same runtime (one HIP runtime per process) instead of
+    # loading a second copy that would not see the device torch opened.
+    import torch  # noqa: F401
     lib = ctypes.CDLL(path)
     st = ctypes.c_int
     P = ctypes.c_void_p
