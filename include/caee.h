@@ -49,14 +49,15 @@
 extern "C" {
 #endif
 
-#define CAEE_ABI_VERSION 2
+#define CAEE_ABI_VERSION 3
 
 typedef enum caee_status {
     CAEE_OK = 0,
     CAEE_ERR_INVALID_ARG = 1,  /* bad descriptor field, NULL or misaligned pointer */
     CAEE_ERR_UNSUPPORTED = 2,  /* well-formed but outside this build's limits */
     CAEE_ERR_WORKSPACE = 3,    /* ws NULL or ws_bytes < caee_workspace_size() */
-    CAEE_ERR_HIP = 4           /* a HIP runtime call or a kernel launch failed */
+    CAEE_ERR_HIP = 4,          /* a HIP runtime call or a kernel launch failed */
+    CAEE_ERR_CAPACITY = 5      /* an offload call needs more device slots than it was given */
 } caee_status_t;
 
 typedef enum caee_dtype {
@@ -201,6 +202,119 @@ caee_status_t caee_pack_matrix(int32_t w_dtype, const void* src, void* dst, int6
  * a multiple of 128.  Asynchronous on `stream`. */
 caee_status_t caee_quantize_rows(int32_t src_dtype, const void* src, int64_t rows, int64_t cols, uint8_t* q,
                                  float* scale, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Offload residency.
+ *
+ * In the offloading deployment (Sec. V-B) every routed expert lives in host
+ * memory and only some of them in device memory; an expert that is needed
+ * but absent costs a host-to-device transfer of its S_e bytes over a link of
+ * bandwidth B (the cost model of Sec. IV-A, where R(e,d) = 1 for such a miss
+ * and 0 for a resident expert).  A caee_offload_t holds the residency state
+ * of one layer: which expert each device cache slot holds and the last call
+ * that used it.  Each caee_offload_layer call
+ *   1. writes the cost table: 0 for a resident expert, `miss_cost` for the
+ *      others, all experts in one bin (the host link), and runs routing,
+ *      pruning and compensation with it on `stream` -- so pruning keeps the
+ *      mandatory experts, promotes the resident candidates, and prunes the
+ *      candidates that would have to be fetched;
+ *   2. waits on the host for that routing step to finish (the only host
+ *      synchronisation of the call) and reads A_trans;
+ *   3. plans the call (caee_lru_step): experts of A_trans already resident
+ *      are hits; the others are misses and go, in ascending expert order,
+ *      into empty cache slots, then into the slots of the least recently
+ *      used experts that this call does not need; once none is left, into
+ *      the staging slots, which cache nothing;
+ *   4. copies the misses host -> device with hipMemcpyAsync on
+ *      `copy_stream`, `fetch_batch` experts at a time, while `stream` runs
+ *      the FFN of the hits and shared experts and then of each batch once it
+ *      has landed; a staging slot is refilled only after the FFN that read
+ *      it has finished;
+ *   5. combines all expert outputs into y on `stream`.
+ * The result equals caee_moe_layer with the same cost table and weights.
+ *
+ * Ownership: host weights, device slots, shared weights, inputs, outputs and
+ * the workspace are the caller's.  The handle allocates a few KB of device
+ * and page-locked host memory for its tables and some HIP events, all freed
+ * by caee_offload_destroy.  A handle is not thread-safe; calls on one
+ * handle must come from one thread, in order. */
+typedef struct caee_offload caee_offload_t;
+
+typedef struct caee_offload_desc {
+    /* Routed experts in host memory: host_w13[e] and host_w2[e] point to
+     * expert e's matrices ([2f][d] and [d][f], in `layout` order), each in
+     * page-locked memory (hipHostMalloc or a pinned torch tensor) so that
+     * copies run asynchronously. */
+    const void* const* host_w13;   /* host array of E pointers */
+    const void* const* host_w2;    /* host array of E pointers */
+    /* Device slots: slot i holds one expert at slot_w13 + i*(2f*d) elements
+     * and slot_w2 + i*(d*f) elements.  Slots [0, n_cache) are the cache,
+     * slots [n_cache, n_cache + n_stage) the staging ring. */
+    void* slot_w13;
+    void* slot_w2;
+    const void* sh_w13;            /* [n_shared][2f][d] device, NULL iff n_shared == 0 */
+    const void* sh_w2;             /* [n_shared][d][f] device */
+    int32_t layout;                /* caee_layout_t of all of the above */
+    int32_t n_cache;               /* >= 0 */
+    int32_t n_stage;               /* >= 0; n_cache + n_stage >= 1 */
+    int32_t fetch_batch;           /* misses per FFN pass, >= 1 (capped at n_stage when staging is used) */
+    float miss_cost;               /* cost-table entry of a non-resident expert, finite and > 0
+                                      (e.g. alpha * S_e / B + beta, Sec. IV-A calibration) */
+} caee_offload_desc_t;
+
+/* Counters since creation or the last caee_offload_reset. */
+typedef struct caee_offload_stats {
+    int64_t calls;       /* caee_offload_layer calls with T > 0 */
+    int64_t needed;      /* routed experts of A_trans, summed over calls */
+    int64_t hits;        /* of them resident when the call began */
+    int64_t misses;      /* of them copied host -> device */
+    int64_t staged;      /* of the misses, copied into staging slots (not cached) */
+    int64_t evictions;   /* cached experts replaced by misses */
+    int64_t bytes_h2d;   /* expert bytes copied host -> device */
+    int32_t passes;      /* FFN passes of the last call (hits, then one per fetch batch) */
+    int32_t reserved;
+} caee_offload_stats_t;
+
+/* Creates a handle for layers of shape `desc` (T is ignored here; w_dtype
+ * CAEE_F32 or CAEE_BF16).  The cache starts empty.  Host pointers must be
+ * page-locked: INVALID_ARG otherwise.  Uses the current device. */
+caee_status_t caee_offload_create(const caee_layer_desc_t* desc, const caee_offload_desc_t* od,
+                                  caee_offload_t** handle);
+/* Waits for the handle's copies and frees what it allocated; NULL is a no-op. */
+void caee_offload_destroy(caee_offload_t* handle);
+/* One layer call (steps 1-5 above).  desc must match the creating one except
+ * for T, tau and importance, and must have n_bins == 1.  `out` may be NULL.
+ * `stream` and `copy_stream` must be different streams of the handle's
+ * device.  Returns CAEE_ERR_CAPACITY, with the routing outputs written, y
+ * not written and the residency unchanged, when the call needs more misses
+ * than the free cache slots can take and n_stage is 0.  Blocks the host
+ * until the routing step has run. */
+caee_status_t caee_offload_layer(caee_offload_t* handle, const caee_layer_desc_t* desc, const void* x,
+                                 const float* logits, const float* bias, void* y, const caee_route_out_t* out,
+                                 void* ws, size_t ws_bytes, void* stream, void* copy_stream);
+caee_status_t caee_offload_stats(const caee_offload_t* handle, caee_offload_stats_t* stats);
+/* slot_of [E] host: cache slot holding expert e, or -1. */
+caee_status_t caee_offload_residency(const caee_offload_t* handle, int32_t* slot_of);
+/* Empties the cache and zeroes the counters (waits for pending copies). */
+caee_status_t caee_offload_reset(caee_offload_t* handle);
+
+/* The residency plan of one call, on host arrays (what caee_offload_layer
+ * runs in step 3; exposed so it can be checked without a device).
+ *   slot_of [E]: in/out, cache slot of each expert or -1;
+ *   slot_expert [n_cache], slot_used [n_cache]: in/out, expert held by each
+ *     cache slot (-1 empty) and the call index that last needed it;
+ *   call: index of this call (larger than every slot_used entry);
+ *   need [E]: nonzero for the routed experts of A_trans.
+ * Outputs: fetch [E] the misses in copy order (cached ones first, then
+ *   staged, each part in ascending expert order), fetch_slot [E] their slot
+ *   (staged misses cycle through n_cache .. n_cache+n_stage-1), and counts[4]
+ *   = hits, misses, staged, evictions.  Victims are taken in order of
+ *   (slot_used, expert) ascending among slots whose expert is not needed;
+ *   empty slots, lowest first, before any victim.  CAEE_ERR_CAPACITY (and
+ *   nothing changed) if misses exceed the free cache slots and n_stage == 0. */
+caee_status_t caee_lru_step(int32_t E, int32_t n_cache, int32_t n_stage, int32_t* slot_of, int32_t* slot_expert,
+                            int64_t* slot_used, int64_t call, const uint8_t* need, int32_t* fetch,
+                            int32_t* fetch_slot, int32_t* counts);
 
 /* Static description of a status code. */
 const char* caee_status_str(caee_status_t status);

@@ -15,7 +15,7 @@ from typing import Optional
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libcaee.so")
 
-CAEE_OK, CAEE_ERR_INVALID_ARG, CAEE_ERR_UNSUPPORTED, CAEE_ERR_WORKSPACE, CAEE_ERR_HIP = range(5)
+CAEE_OK, CAEE_ERR_INVALID_ARG, CAEE_ERR_UNSUPPORTED, CAEE_ERR_WORKSPACE, CAEE_ERR_HIP, CAEE_ERR_CAPACITY = range(6)
 CAEE_F32, CAEE_BF16, CAEE_FP8_E4M3 = 0, 1, 2
 KERNEL_KINDS = {"route": 0, "gate_up": 1, "down": 2, "combine": 3, "quant": 4}
 DTYPE_CODE = {"f32": CAEE_F32, "bf16": CAEE_BF16, "fp8": CAEE_FP8_E4M3}
@@ -45,6 +45,20 @@ class ExpertWeights(ctypes.Structure):
 LAYOUT_ROWMAJOR, LAYOUT_TILED = 0, 1
 
 
+class OffloadDesc(ctypes.Structure):
+    _fields_ = [("host_w13", ctypes.POINTER(ctypes.c_void_p)), ("host_w2", ctypes.POINTER(ctypes.c_void_p)),
+                ("slot_w13", ctypes.c_void_p), ("slot_w2", ctypes.c_void_p),
+                ("sh_w13", ctypes.c_void_p), ("sh_w2", ctypes.c_void_p),
+                ("layout", ctypes.c_int32), ("n_cache", ctypes.c_int32), ("n_stage", ctypes.c_int32),
+                ("fetch_batch", ctypes.c_int32), ("miss_cost", ctypes.c_float)]
+
+
+class OffloadStats(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int64) for n in
+                ("calls", "needed", "hits", "misses", "staged", "evictions", "bytes_h2d")] + [
+        ("passes", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+
+
 class RouteOut(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in
                 ("topk_ids", "topk_w", "orig_ids", "masks", "stats", "bin_loads")]
@@ -70,6 +84,13 @@ def _load(path: str = LIB_PATH):
                                 ctypes.POINTER(RouteOut), P, ctypes.c_size_t, P]),
         "caee_pack_matrix": (st, [ctypes.c_int32, P, P, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, P]),
         "caee_quantize_rows": (st, [ctypes.c_int32, P, ctypes.c_int64, ctypes.c_int64, P, P, P]),
+        "caee_offload_create": (st, [desc_p, ctypes.POINTER(OffloadDesc), ctypes.POINTER(P)]),
+        "caee_offload_destroy": (None, [P]),
+        "caee_offload_layer": (st, [P, desc_p, P, P, P, P, ctypes.POINTER(RouteOut), P, ctypes.c_size_t, P, P]),
+        "caee_offload_stats": (st, [P, ctypes.POINTER(OffloadStats)]),
+        "caee_offload_residency": (st, [P, P]),
+        "caee_offload_reset": (st, [P]),
+        "caee_lru_step": (st, [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, P, P, P, ctypes.c_int64, P, P, P, P]),
         "caee_status_str": (ctypes.c_char_p, [st]),
         "caee_last_error": (ctypes.c_char_p, []),
         "caee_abi_version": (ctypes.c_int, []),
@@ -96,7 +117,9 @@ def load_library(path: str) -> None:
 
 
 EXPORTED = ("caee_workspace_size", "caee_route_prune", "caee_expert_ffn", "caee_moe_layer",
-            "caee_pack_matrix", "caee_quantize_rows", "caee_status_str", "caee_last_error", "caee_abi_version",
+            "caee_pack_matrix", "caee_quantize_rows", "caee_offload_create", "caee_offload_destroy",
+            "caee_offload_layer", "caee_offload_stats", "caee_offload_residency", "caee_offload_reset",
+            "caee_lru_step", "caee_status_str", "caee_last_error", "caee_abi_version",
             "caee_timing_enable", "caee_timing_reset", "caee_timing_query")
 
 
@@ -201,6 +224,28 @@ def pack_weights(weights: dict, w_dtype: str) -> dict:
     return out
 
 
+def pin_host_weights(weights: dict) -> dict:
+    """Page-locked host copies of the routed expert matrices (``w13``, ``w2``)
+    of a device weight dict, in its layout: the host side of an offloaded
+    layer.  Shared experts stay on the device."""
+    import torch
+    out = {"layout": int(weights.get("layout", LAYOUT_ROWMAJOR))}
+    for name in ("w13", "w2"):
+        src = weights[name]
+        dst = torch.empty(src.shape, dtype=src.dtype, pin_memory=True)
+        dst.copy_(src)
+        out[name] = dst
+    return out
+
+
+def alloc_slots(layer: Layer, n_slots: int, device) -> tuple:
+    """Device buffers for ``n_slots`` experts of ``layer`` (w13, w2)."""
+    import torch
+    dt = {"f32": torch.float32, "bf16": torch.bfloat16}[layer.w_dtype]
+    return (torch.empty((n_slots, 2 * layer.f, layer.d), dtype=dt, device=device),
+            torch.empty((n_slots, layer.d, layer.f), dtype=dt, device=device))
+
+
 def _route_out(out: Optional[dict]) -> Optional[RouteOut]:
     if out is None:
         return None
@@ -267,3 +312,93 @@ def timing_query(kind: str):
     n = ctypes.c_int64(0)
     _check(lib.caee_timing_query(KERNEL_KINDS[kind], ctypes.byref(ms), ctypes.byref(n)))
     return float(ms.value), int(n.value)
+
+
+def lru_step(E: int, n_cache: int, n_stage: int, slot_of, slot_expert, slot_used, call: int, need):
+    """One residency plan on host numpy arrays (caee_lru_step); the state
+    arrays are updated in place.  Returns (fetch, fetch_slot, counts) with
+    counts = (hits, misses, staged, evictions)."""
+    import numpy as np
+    for a, dt in ((slot_of, np.int32), (slot_expert, np.int32), (slot_used, np.int64)):
+        if a.dtype != dt or not a.flags.c_contiguous:
+            raise TypeError("state arrays must be contiguous int32/int32/int64")
+    need = np.ascontiguousarray(need, dtype=np.uint8)
+    fetch = np.zeros(E, np.int32)
+    fetch_slot = np.zeros(E, np.int32)
+    counts = np.zeros(4, np.int32)
+    p = lambda a: a.ctypes.data_as(ctypes.c_void_p)  # noqa: E731
+    _check(lib.caee_lru_step(E, n_cache, n_stage, p(slot_of), p(slot_expert), p(slot_used), call, p(need),
+                             p(fetch), p(fetch_slot), p(counts)))
+    n = int(counts[1])
+    return fetch[:n].copy(), fetch_slot[:n].copy(), tuple(int(c) for c in counts)
+
+
+class Offload:
+    """Offload residency handle (caee_offload_t) of one layer.
+
+    ``host_w13``/``host_w2``: per-expert page-locked host tensors (or one
+    pinned tensor [E][...] each); ``slot_w13``/``slot_w2``: device tensors
+    with ``n_cache + n_stage`` expert slots; ``sh_w13``/``sh_w2``: device
+    shared-expert weights (or None).  Every tensor must stay alive while the
+    handle is used; the handle keeps references to them."""
+
+    def __init__(self, layer: Layer, host_w13, host_w2, slot_w13, slot_w2, sh_w13, sh_w2, n_cache: int,
+                 n_stage: int, miss_cost: float, fetch_batch: int = 4, layout: int = LAYOUT_TILED):
+        E = layer.E
+        h13 = list(host_w13) if isinstance(host_w13, (list, tuple)) else [host_w13[e] for e in range(E)]
+        h2 = list(host_w2) if isinstance(host_w2, (list, tuple)) else [host_w2[e] for e in range(E)]
+        if len(h13) != E or len(h2) != E:
+            raise ValueError("one host tensor per routed expert is needed")
+        self._keep = (host_w13, host_w2, h13, h2, slot_w13, slot_w2, sh_w13, sh_w2)
+        self._h13 = (ctypes.c_void_p * E)(*[int(t.data_ptr()) for t in h13])
+        self._h2 = (ctypes.c_void_p * E)(*[int(t.data_ptr()) for t in h2])
+        self.od = OffloadDesc(ctypes.cast(self._h13, ctypes.POINTER(ctypes.c_void_p)),
+                              ctypes.cast(self._h2, ctypes.POINTER(ctypes.c_void_p)),
+                              _ptr(slot_w13), _ptr(slot_w2), _ptr(sh_w13), _ptr(sh_w2),
+                              int(layout), int(n_cache), int(n_stage), int(fetch_batch), float(miss_cost))
+        self.layer = layer
+        self.E = E
+        d = layer.desc()
+        h = ctypes.c_void_p(None)
+        _check(lib.caee_offload_create(ctypes.byref(d), ctypes.byref(self.od), ctypes.byref(h)))
+        self.handle = h
+
+    def __call__(self, layer: Layer, x, logits, bias, y, ws, out: Optional[dict] = None, copy_stream=None):
+        """One layer call.  ``copy_stream``: a torch stream for the host-to-device
+        copies (default: a dedicated stream of the handle)."""
+        import torch
+        if copy_stream is None:
+            if getattr(self, "_copy_stream", None) is None:
+                self._copy_stream = torch.cuda.Stream(device=x.device)
+            copy_stream = self._copy_stream
+        d = layer.desc()
+        ro = _route_out(out)
+        _check(lib.caee_offload_layer(self.handle, ctypes.byref(d), _ptr(x), _ptr(logits), _ptr(bias), _ptr(y),
+                                      None if ro is None else ctypes.byref(ro), _ptr(ws), ws.numel(), _stream(x),
+                                      int(copy_stream.cuda_stream)))
+        return y
+
+    def stats(self) -> dict:
+        st = OffloadStats()
+        _check(lib.caee_offload_stats(self.handle, ctypes.byref(st)))
+        return {n: int(getattr(st, n)) for n, _ in OffloadStats._fields_ if n != "reserved"}
+
+    def residency(self):
+        import numpy as np
+        a = np.zeros(self.E, np.int32)
+        _check(lib.caee_offload_residency(self.handle, a.ctypes.data_as(ctypes.c_void_p)))
+        return a
+
+    def reset(self):
+        _check(lib.caee_offload_reset(self.handle))
+
+    def close(self):
+        if getattr(self, "handle", None) is not None and self.handle.value:
+            lib.caee_offload_destroy(self.handle)
+        self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

@@ -13,8 +13,14 @@
 namespace caee {
 
 namespace {
-
 thread_local std::string g_last_error;
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+int experts_per_lane(int E) { return E <= 64 ? 1 : E <= 128 ? 2 : 4; }
+}  // namespace
+
+void clear_last_error() { g_last_error.clear(); }
 
 caee_status_t fail(caee_status_t st, const char* fmt, ...) {
     char buf[512];
@@ -25,10 +31,6 @@ caee_status_t fail(caee_status_t st, const char* fmt, ...) {
     g_last_error = buf;
     return st;
 }
-
-bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
-
-int experts_per_lane(int E) { return E <= 64 ? 1 : E <= 128 ? 2 : 4; }
 
 caee_status_t check_desc(const caee_layer_desc_t* d) {
     if (!d) return fail(CAEE_ERR_INVALID_ARG, "desc is NULL");
@@ -77,12 +79,6 @@ caee_status_t check_ptr(const void* p, const char* name, bool required) {
     if (!aligned16(p)) return fail(CAEE_ERR_INVALID_ARG, "%s is not 16-byte aligned", name);
     return CAEE_OK;
 }
-
-#define CAEE_TRY(expr)                          \
-    do {                                        \
-        caee_status_t st_ = (expr);             \
-        if (st_ != CAEE_OK) return st_;         \
-    } while (0)
 
 caee_status_t check_ws(const caee_layer_desc_t* d, void* ws, size_t ws_bytes, WsLayout* L) {
     *L = ws_layout(*d);
@@ -134,19 +130,6 @@ caee_status_t check_weights(const caee_layer_desc_t* d, const caee_expert_weight
     return CAEE_OK;
 }
 
-// ---------------------------------------------------------------------------
-// Opt-in timing: events bracket each launch on the caller's stream.
-struct TimingRec {
-    int kind;
-    hipEvent_t a, b;
-};
-struct Timing {
-    bool on = false;
-    std::vector<TimingRec> pending;
-    std::vector<hipEvent_t> pool;
-    double total_ms[CAEE_KERNEL_KINDS] = {};
-    int64_t launches[CAEE_KERNEL_KINDS] = {};
-};
 Timing& timing() {
     static Timing t;
     return t;
@@ -164,29 +147,9 @@ hipEvent_t take_event() {
     return e;
 }
 
-// Runs one launch, bracketed by timing events when timing is on.
-template <class F>
-caee_status_t timed_launch(int kind, hipStream_t s, const char* what, F&& launch) {
-    Timing& tm = timing();
-    hipEvent_t a = nullptr, b = nullptr;
-    bool timed = false;
-    if (tm.on) {
-        a = take_event();
-        b = take_event();
-        timed = a && b && hipEventRecord(a, s) == hipSuccess;
-    }
-    const hipError_t err = launch();
-    if (err != hipSuccess) return fail(CAEE_ERR_HIP, "%s launch failed: %s", what, hipGetErrorString(err));
-    if (timed && hipEventRecord(b, s) == hipSuccess) {
-        tm.pending.push_back({kind, a, b});
-    } else {
-        if (a) tm.pool.push_back(a);
-        if (b) tm.pool.push_back(b);
-    }
-    return CAEE_OK;
-}
-
+namespace {
 hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
+}  // namespace
 
 RouteParams make_route_params(const caee_layer_desc_t* d, const float* logits, const float* bias,
                               const float* cost, const int32_t* bin, char* ws, const WsLayout& L) {
@@ -224,8 +187,8 @@ RouteParams make_route_params(const caee_layer_desc_t* d, const float* logits, c
     return p;
 }
 
-caee_status_t run_ffn(const caee_layer_desc_t* d, const void* x, const int32_t* ids, const float* w,
-                      const caee_expert_weights_t* W, void* y, char* ws, const WsLayout& L, hipStream_t s) {
+FfnParams make_ffn_params(const caee_layer_desc_t* d, const void* x, const int32_t* ids, const float* w,
+                          const caee_expert_weights_t* W, void* y, char* ws, const WsLayout& L) {
     FfnParams p{};
     p.T = d->T;
     p.d = d->d;
@@ -234,14 +197,17 @@ caee_status_t run_ffn(const caee_layer_desc_t* d, const void* x, const int32_t* 
     p.k = d->k;
     p.n_shared = d->n_shared;
     p.x = x;
-    p.w13 = W->w13;
-    p.w2 = W->w2;
-    p.sh_w13 = W->sh_w13;
-    p.sh_w2 = W->sh_w2;
-    p.w13_scale = W->w13_scale;
-    p.w2_scale = W->w2_scale;
-    p.sh_w13_scale = W->sh_w13_scale;
-    p.sh_w2_scale = W->sh_w2_scale;
+    if (W) {
+        p.w13 = W->w13;
+        p.w2 = W->w2;
+        p.sh_w13 = W->sh_w13;
+        p.sh_w2 = W->sh_w2;
+        p.w13_scale = W->w13_scale;
+        p.w2_scale = W->w2_scale;
+        p.sh_w13_scale = W->sh_w13_scale;
+        p.sh_w2_scale = W->sh_w2_scale;
+        p.tiled = W->layout == CAEE_LAYOUT_TILED;
+    }
     p.perm_tok = (const int32_t*)(ws + L.perm_tok);
     p.perm_pos = (const int32_t*)(ws + L.perm_pos);
     p.chunks = (const int32_t*)(ws + L.chunks);
@@ -254,31 +220,53 @@ caee_status_t run_ffn(const caee_layer_desc_t* d, const void* x, const int32_t* 
     p.y_bf16 = d->y_dtype == CAEE_BF16;
     p.P = L.P;
     p.ksplit = L.ksplit;
-    p.tiled = W->layout == CAEE_LAYOUT_TILED;
     p.xq = (uint8_t*)(ws + L.xq);
     p.xs = (float*)(ws + L.xs);
     p.hq = (uint8_t*)(ws + L.hq);
     p.hs = (float*)(ws + L.hs);
+    return p;
+}
+
+caee_status_t run_ffn_products(const caee_layer_desc_t* d, const FfnParams& p, const WsLayout& L, hipStream_t s) {
     const int nb = ffn_token_blocks(*d);
     if (d->w_dtype == CAEE_FP8_E4M3) {
         CAEE_TRY(timed_launch(CAEE_KERNEL_QUANT, s, "quantise x",
-                              [&] { return launch_quant_rows(x, 1, d->T, d->d, p.xq, p.xs, s); }));
+                              [&] { return launch_quant_rows(p.x, 1, d->T, d->d, p.xq, p.xs, s); }));
         CAEE_TRY(timed_launch(CAEE_KERNEL_GATE_UP, s, "gate/up",
                               [&] { return launch_gate_up_fp8(p, nb, L.max_chunks, s); }));
         CAEE_TRY(timed_launch(CAEE_KERNEL_QUANT, s, "quantise H",
                               [&] { return launch_quant_rows(p.h, 0, L.P, d->f, p.hq, p.hs, s); }));
-        CAEE_TRY(timed_launch(CAEE_KERNEL_DOWN, s, "down", [&] { return launch_down_fp8(p, nb, L.max_chunks, s); }));
-        CAEE_TRY(timed_launch(CAEE_KERNEL_COMBINE, s, "combine", [&] { return launch_combine(p, s); }));
-        return CAEE_OK;
+        return timed_launch(CAEE_KERNEL_DOWN, s, "down", [&] { return launch_down_fp8(p, nb, L.max_chunks, s); });
     }
     CAEE_TRY(timed_launch(CAEE_KERNEL_GATE_UP, s, "gate/up",
                           [&] { return launch_gate_up(p, d->w_dtype, nb, L.max_chunks, s); }));
-    CAEE_TRY(timed_launch(CAEE_KERNEL_DOWN, s, "down",
-                          [&] { return launch_down(p, d->w_dtype, nb, L.max_chunks, s); }));
-    CAEE_TRY(timed_launch(CAEE_KERNEL_COMBINE, s, "combine", [&] { return launch_combine(p, s); }));
-    return CAEE_OK;
+    return timed_launch(CAEE_KERNEL_DOWN, s, "down", [&] { return launch_down(p, d->w_dtype, nb, L.max_chunks, s); });
 }
 
+caee_status_t run_combine(const FfnParams& p, hipStream_t s) {
+    return timed_launch(CAEE_KERNEL_COMBINE, s, "combine", [&] { return launch_combine(p, s); });
+}
+
+caee_status_t run_route_layer(const caee_layer_desc_t* d, RouteParams& p, const caee_route_out_t* out, char* ws,
+                              const WsLayout& L, hipStream_t s) {
+    p.topk_ids = out ? out->topk_ids : (int32_t*)(ws + L.ids);
+    p.topk_w = out ? out->topk_w : (float*)(ws + L.w);
+    if (out && out->orig_ids) p.orig_ids = out->orig_ids;
+    p.masks = out ? out->masks : nullptr;
+    p.stats = out ? out->stats : nullptr;
+    p.bin_loads = out ? out->bin_loads : nullptr;
+    p.do_permute = 1;
+    (void)d;
+    return timed_launch(CAEE_KERNEL_ROUTE, s, "route", [&] { return launch_route(p, s); });
+}
+
+namespace {
+caee_status_t run_ffn(const caee_layer_desc_t* d, const void* x, const int32_t* ids, const float* w,
+                      const caee_expert_weights_t* W, void* y, char* ws, const WsLayout& L, hipStream_t s) {
+    const FfnParams p = make_ffn_params(d, x, ids, w, W, y, ws, L);
+    CAEE_TRY(run_ffn_products(d, p, L, s));
+    return run_combine(p, s);
+}
 }  // namespace
 
 int device_cu_count() {
@@ -365,15 +353,8 @@ caee_status_t caee_moe_layer(const caee_layer_desc_t* desc, const void* x, const
     if (desc->T == 0) return CAEE_OK;
     char* wsb = (char*)ws;
     RouteParams p = make_route_params(desc, logits, bias, cost, bin, wsb, L);
-    p.topk_ids = out ? out->topk_ids : (int32_t*)(wsb + L.ids);
-    p.topk_w = out ? out->topk_w : (float*)(wsb + L.w);
-    if (out && out->orig_ids) p.orig_ids = out->orig_ids;
-    p.masks = out ? out->masks : nullptr;
-    p.stats = out ? out->stats : nullptr;
-    p.bin_loads = out ? out->bin_loads : nullptr;
-    p.do_permute = 1;
     hipStream_t s = as_stream(stream);
-    CAEE_TRY(timed_launch(CAEE_KERNEL_ROUTE, s, "route", [&] { return launch_route(p, s); }));
+    CAEE_TRY(run_route_layer(desc, p, out, wsb, L, s));
     return run_ffn(desc, x, p.topk_ids, p.topk_w, weights, y, wsb, L, s);
 }
 
@@ -424,6 +405,7 @@ const char* caee_status_str(caee_status_t status) {
         case CAEE_ERR_UNSUPPORTED: return "unsupported by this build";
         case CAEE_ERR_WORKSPACE: return "workspace missing or too small";
         case CAEE_ERR_HIP: return "HIP runtime error";
+        case CAEE_ERR_CAPACITY: return "more device slots needed than given";
     }
     return "unknown status";
 }

@@ -7,6 +7,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <vector>
+
 #include "../../include/caee.h"
 
 namespace caee {
@@ -194,6 +196,12 @@ struct FfnParams {
     int P;
     int ksplit;
     int tiled;      // weights in CAEE_LAYOUT_TILED order
+    // Offload residency: when wtab is set, expert slot x takes its w13 / w2
+    // base from wtab[2x] / wtab[2x+1] instead of the contiguous arrays, and
+    // when pass_of is set only chunks of slots with pass_of[x] == pass_id run.
+    const void* const* wtab;
+    const int32_t* pass_of;
+    int pass_id;
     // fp8 path: quantised activations and their per-token 128-channel scales
     uint8_t* xq;
     float* xs;
@@ -214,5 +222,71 @@ hipError_t launch_down_fp8(const FfnParams& p, int nb, int max_chunks, hipStream
 hipError_t launch_pack(const void* src, void* dst, long long rows, long long row_units, long long count,
                        hipStream_t s);
 int device_cu_count();
+
+// ---------------------------------------------------------------------------
+// Host helpers shared by the entry points (defined in api.hip).
+caee_status_t fail(caee_status_t st, const char* fmt, ...);
+caee_status_t check_desc(const caee_layer_desc_t* d);
+caee_status_t check_ptr(const void* p, const char* name, bool required);
+caee_status_t check_ws(const caee_layer_desc_t* d, void* ws, size_t ws_bytes, WsLayout* L);
+caee_status_t check_route_inputs(const caee_layer_desc_t* d, const float* logits, const float* bias,
+                                 const float* cost, const int32_t* bin);
+caee_status_t check_route_out(const caee_route_out_t* out);
+void clear_last_error();
+RouteParams make_route_params(const caee_layer_desc_t* d, const float* logits, const float* bias,
+                              const float* cost, const int32_t* bin, char* ws, const WsLayout& L);
+FfnParams make_ffn_params(const caee_layer_desc_t* d, const void* x, const int32_t* ids, const float* w,
+                          const caee_expert_weights_t* W, void* y, char* ws, const WsLayout& L);
+// Routing, pruning, compensation and permutation of a whole-layer call; the
+// routing results go to `out` when given, else to the workspace.
+caee_status_t run_route_layer(const caee_layer_desc_t* d, RouteParams& p, const caee_route_out_t* out, char* ws,
+                              const WsLayout& L, hipStream_t s);
+// Gate/up and down products of every chunk (or, with p.pass_of set, of the
+// chunks of pass p.pass_id), then optionally the combine.
+caee_status_t run_ffn_products(const caee_layer_desc_t* d, const FfnParams& p, const WsLayout& L, hipStream_t s);
+caee_status_t run_combine(const FfnParams& p, hipStream_t s);
+
+// Opt-in timing: events bracket each launch on the caller's stream.
+struct TimingRec {
+    int kind;
+    hipEvent_t a, b;
+};
+struct Timing {
+    bool on = false;
+    std::vector<TimingRec> pending;
+    std::vector<hipEvent_t> pool;
+    double total_ms[CAEE_KERNEL_KINDS] = {};
+    int64_t launches[CAEE_KERNEL_KINDS] = {};
+};
+Timing& timing();
+hipEvent_t take_event();
+
+// Runs one launch, bracketed by timing events when timing is on.
+template <class F>
+caee_status_t timed_launch(int kind, hipStream_t s, const char* what, F&& launch) {
+    Timing& tm = timing();
+    hipEvent_t a = nullptr, b = nullptr;
+    bool timed = false;
+    if (tm.on) {
+        a = take_event();
+        b = take_event();
+        timed = a && b && hipEventRecord(a, s) == hipSuccess;
+    }
+    const hipError_t err = launch();
+    if (err != hipSuccess) return fail(CAEE_ERR_HIP, "%s launch failed: %s", what, hipGetErrorString(err));
+    if (timed && hipEventRecord(b, s) == hipSuccess) {
+        tm.pending.push_back({kind, a, b});
+    } else {
+        if (a) tm.pool.push_back(a);
+        if (b) tm.pool.push_back(b);
+    }
+    return CAEE_OK;
+}
+
+#define CAEE_TRY(expr)                          \
+    do {                                        \
+        caee_status_t st_ = (expr);             \
+        if (st_ != CAEE_OK) return st_;         \
+    } while (0)
 
 }  // namespace caee

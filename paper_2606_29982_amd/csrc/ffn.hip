@@ -145,9 +145,11 @@ __global__ CAEE_FFN_BOUNDS void k_gate_up(FfnParams p) {
         const int c = item / items_per_chunk;
         const int jt = (item - c * items_per_chunk) * tiles_per_item + wave / S;
         const int xs = p.chunks[4 * c], row0 = p.chunks[4 * c + 1], ntok = p.chunks[4 * c + 2];
+        if (p.pass_of && p.pass_of[xs] != p.pass_id) continue;   // uniform over the workgroup
         const int nb = (ntok + 15) >> 4;
         const size_t k0 = (size_t)4 * sp * kper;
-        const u32x4_t* wb = (const u32x4_t*)expert_base(p.w13, p.sh_w13, xs, p.E, expert_bytes);
+        const u32x4_t* wb = (const u32x4_t*)(p.wtab ? (const char*)p.wtab[2 * xs]
+                                                    : expert_base(p.w13, p.sh_w13, xs, p.E, expert_bytes));
         const size_t ksteps = row_units / 4;
         // Tiled: block (tile, step) is 64 consecutive 16-byte pieces, one per lane.
         const u32x4_t* const a[2] = {
@@ -221,8 +223,10 @@ __global__ CAEE_FFN_BOUNDS void k_down(FfnParams p) {
     for (int item = gw; item < total; item += nw) {
         const int c = item / tiles, it = item - c * tiles;
         const int xs = p.chunks[4 * c], row0 = p.chunks[4 * c + 1], ntok = p.chunks[4 * c + 2];
+        if (p.pass_of && p.pass_of[xs] != p.pass_id) continue;
         const int nb = (ntok + 15) >> 4;
-        const u32x4_t* wb = (const u32x4_t*)expert_base(p.w2, p.sh_w2, xs, p.E, expert_bytes);
+        const u32x4_t* wb = (const u32x4_t*)(p.wtab ? (const char*)p.wtab[2 * xs + 1]
+                                                    : expert_base(p.w2, p.sh_w2, xs, p.E, expert_bytes));
         const u32x4_t* const a[1] = {p.tiled ? wb + (size_t)it * ksteps * 64 + lane
                                              : wb + (size_t)(it * 16 + r) * row_units + g};
         const int astep = p.tiled ? 64 : 4;

@@ -13,6 +13,7 @@ from .layers import (  # noqa: F401
     WORKLOADS,
     RoutingInputs,
     make_routing_inputs,
+    make_call_sequence,
     make_cost_table,
     make_bins,
     make_expert_weights_np,

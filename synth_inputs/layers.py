@@ -154,6 +154,31 @@ def make_routing_inputs(shape: LayerShape, seed: int = 0, T: Optional[int] = Non
     )
 
 
+def make_call_sequence(shape: LayerShape, seed: int, n_calls: int, T: Optional[int] = None,
+                       zipf_logit_s: float = 1.2) -> list:
+    """Inputs of ``n_calls`` consecutive layer calls (decode steps) that share
+    one expert-popularity law: call i draws fresh hidden states ~N(0,1)
+    (stream (0, i)) and logits ~N(0,1) (stream (1, i)), plus the fixed offset
+    ln(E * p_rank(e)) of a Zipf(``zipf_logit_s``) law over a rank permutation
+    drawn once (stream 4).  The bias is fixed across calls; the cost table is
+    left at zero (an offloading caller derives it from residency)."""
+    T = shape.T if T is None else int(T)
+    perm = _rng(seed, 4).permutation(shape.E)
+    mu = np.log(shape.E * _zipf_probs(shape.E, zipf_logit_s)[perm]).astype(np.float32)
+    bias = None
+    if shape.bias_std > 0:
+        bias = (_rng(seed, 2).standard_normal(shape.E, dtype=np.float32)
+                * np.float32(shape.bias_std)).astype(np.float32)
+    calls = []
+    for i in range(int(n_calls)):
+        x = _rng(seed, 0, i).standard_normal((T, shape.d), dtype=np.float32)
+        logits = _rng(seed, 1, i).standard_normal((T, shape.E), dtype=np.float32) + mu[None, :]
+        calls.append(RoutingInputs(x=_encode(x, shape.x_dtype),
+                                   logits=np.ascontiguousarray(logits, dtype=np.float32), bias=bias,
+                                   cost=np.zeros(shape.E, np.float32), bins=None))
+    return calls
+
+
 def make_cost_table(shape: LayerShape, seed: int = 0, kind: str = "uniform") -> np.ndarray:
     """Per-expert data-movement cost in bytes-equivalent units.
 

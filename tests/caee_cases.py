@@ -124,3 +124,72 @@ def check_y(y_got, y_ref, rel_tol):
     scale = np.abs(y_ref).max()
     assert err <= rel_tol * scale, f"max|err| {err:.4e} > {rel_tol} * max|ref| {scale:.4e}"
     return err / scale
+
+
+def run_offload_sequence(shape, calls, Wl, dev, n_cache, n_stage, fetch_batch, tau, rule, miss_cost,
+                         get, get_sh, y_tokens=None, y_tol=None):
+    """Runs ``calls`` through one caee_offload handle (weights ``Wl`` on the
+    device, in their layout, copied to pinned host memory for it) and checks
+    every call against the oracle's LRU sequence and against caee_moe_layer
+    given the same residency cost table.  ``y_tokens(i)`` names the tokens
+    whose output the oracle evaluates at call i (None: none)."""
+    import dataclasses
+
+    from oracle import offload as off
+
+    T = calls[0].logits.shape[0]
+    layer = caee.Layer.from_shape(shape, T=T, tau=tau, n_bins=1, importance=rule)
+    host = caee.pin_host_weights(Wl)
+    slot13, slot2 = caee.alloc_slots(layer, n_cache + n_stage, dev)
+    h = caee.Offload(layer, host["w13"], host["w2"], slot13, slot2, Wl.get("sh_w13"), Wl.get("sh_w2"),
+                     n_cache, n_stage, miss_cost, fetch_batch, Wl.get("layout", caee.LAYOUT_ROWMAJOR))
+    ws = caee.alloc_workspace(layer, dev)
+    ws2 = caee.alloc_workspace(layer, dev)
+    out = caee.alloc_route_out(layer, dev)
+    out2 = caee.alloc_route_out(layer, dev)
+    ydt = torch.float32 if shape.y_dtype == "f32" else torch.bfloat16
+    want = {"hits": 0, "misses": 0, "staged": 0, "evictions": 0, "needed": 0}
+
+    def route(i, cost):
+        toks = y_tokens(i) if y_tokens else None
+        inp = dataclasses.replace(calls[i], cost=cost)
+        return oracle_layer(shape, inp, tau, 1, get, get_sh, tokens=toks, with_y=bool(toks), rule=rule)
+
+    try:
+        for i, step in enumerate(off.offload_sequence(route, shape.E, n_cache, miss_cost, len(calls))):
+            inp = calls[i]
+            print(f"offload call {i}: T={T} tau={tau} rule={rule} n_cache={n_cache} n_stage={n_stage} "
+                  f"batch={fetch_batch}", flush=True)
+            x, logits, bias = to_dev(inp.x, dev), to_dev(inp.logits, dev), to_dev(inp.bias, dev)
+            yfull = torch.full((T + 2, shape.d), 7.0, dtype=ydt, device=dev)
+            h(layer, x, logits, bias, yfull[1:T + 1], ws, out)
+            # the same call through caee_moe_layer with the same cost table
+            y2 = torch.empty((T, shape.d), dtype=ydt, device=dev)
+            caee.moe_layer(layer, x, logits, bias, to_dev(step["cost"], dev), None, Wl, y2, ws2, out2)
+            torch.cuda.synchronize()
+            assert torch.all(yfull[0] == 7.0) and torch.all(yfull[T + 1] == 7.0), "write outside y"
+            got = {k: v.cpu().numpy() for k, v in out.items()}
+            check_route(got, step["ref"], shape.E)
+            assert torch.equal(yfull[1:T + 1], y2), "offloaded layer differs from caee_moe_layer"
+            for k_ in out:
+                assert torch.equal(out[k_], out2[k_]), k_
+            assert set(np.flatnonzero(h.residency() >= 0).tolist()) == step["resident_after"]
+            lru = step["lru"]
+            want["hits"] += len(lru["hits"])
+            want["misses"] += len(lru["cached"]) + len(lru["staged"])
+            want["staged"] += len(lru["staged"])
+            want["evictions"] += len(lru["evicted"])
+            want["needed"] += len(lru["hits"]) + len(lru["cached"]) + len(lru["staged"])
+            if y_tokens and y_tokens(i):
+                toks = y_tokens(i)
+                y_got = yfull[1:T + 1].float().cpu().numpy().astype(np.float64)[toks]
+                check_y(y_got, step["ref"]["y"], y_tol)
+        st = h.stats()
+        for k_, v in want.items():
+            assert st[k_] == v, (k_, st[k_], v)
+        assert st["calls"] == len(calls)
+        wbytes = 3 * shape.f * shape.d * (4 if shape.w_dtype == "f32" else 2)
+        assert st["bytes_h2d"] == want["misses"] * wbytes
+        return st
+    finally:
+        h.close()

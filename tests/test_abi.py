@@ -26,7 +26,7 @@ def test_exports_every_declared_symbol():
     for n in names:
         assert hasattr(lib, n), n
     assert set(names) == set(caee.EXPORTED)
-    assert caee.abi_version() == 2
+    assert caee.abi_version() == 3
 
 
 def _layer(**kw):
@@ -150,3 +150,43 @@ def test_quantize_rows_host_checks():
     assert qr(caee.CAEE_BF16, FAKE, 4, 100, FAKE, FAKE, None) == caee.CAEE_ERR_INVALID_ARG
     assert qr(caee.CAEE_BF16, None, 4, 128, FAKE, FAKE, None) == caee.CAEE_ERR_INVALID_ARG
     assert qr(caee.CAEE_F32, FAKE, 0, 128, FAKE, FAKE, None) == caee.CAEE_OK
+
+
+def _offload_status(layer=None, **kw):
+    layer = layer or _layer(T=0, n_bins=1)
+    E = layer.E
+    arr = (ctypes.c_void_p * E)(*([FAKE] * E))
+    fields = dict(host_w13=ctypes.cast(arr, ctypes.POINTER(ctypes.c_void_p)),
+                  host_w2=ctypes.cast(arr, ctypes.POINTER(ctypes.c_void_p)),
+                  slot_w13=FAKE, slot_w2=FAKE, sh_w13=FAKE, sh_w2=FAKE, layout=1, n_cache=4, n_stage=2,
+                  fetch_batch=2, miss_cost=1.0)
+    fields.update(kw)
+    od = caee.OffloadDesc(**fields)
+    d = layer.desc()
+    h = ctypes.c_void_p(None)
+    st = caee.lib.caee_offload_create(ctypes.byref(d), ctypes.byref(od), ctypes.byref(h))
+    assert not h.value
+    return st
+
+
+@pytest.mark.parametrize("kw", [dict(n_cache=0, n_stage=0), dict(n_cache=-1), dict(fetch_batch=0),
+                                dict(miss_cost=0.0), dict(miss_cost=float("nan")), dict(layout=7),
+                                dict(slot_w13=None), dict(slot_w2=FAKE + 4), dict(sh_w13=None),
+                                dict(host_w13=None)])
+def test_offload_create_rejects_bad_arguments(kw):
+    assert _offload_status(**kw) == caee.CAEE_ERR_INVALID_ARG
+
+
+def test_offload_create_rejects_fp8_and_bad_layer():
+    assert _offload_status(_layer(T=0, n_bins=1, w_dtype="fp8")) == caee.CAEE_ERR_UNSUPPORTED
+    assert _offload_status(_layer(T=0, n_bins=1, E=192)) == caee.CAEE_ERR_UNSUPPORTED
+    assert _offload_status(_layer(T=0, n_bins=1, k=0)) == caee.CAEE_ERR_INVALID_ARG
+
+
+def test_offload_null_handle():
+    d = _layer(T=4, n_bins=1).desc()
+    st = caee.lib.caee_offload_layer(None, ctypes.byref(d), FAKE, FAKE, None, FAKE, None, FAKE, 1 << 20, None,
+                                     None)
+    assert st == caee.CAEE_ERR_INVALID_ARG
+    caee.lib.caee_offload_destroy(None)
+    assert caee.lib.caee_offload_reset(None) == caee.CAEE_ERR_INVALID_ARG
