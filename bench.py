@@ -43,6 +43,9 @@ def parse():
     ap.add_argument("--no-sweep", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-offload", action="store_true")
+    ap.add_argument("--offload-calls", type=int, default=256,
+                    help="decode calls of the offloading sequence (T=16 each)")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="finish with one device-to-device copy of this many bytes (a known-size "
                          "reference for HBM traffic counters)")
@@ -175,6 +178,91 @@ def cpu_baseline(shape, case, W, sample_tokens):
             "seconds": round(dt, 2)}
 
 
+def pinned_h2d_gbps(dev, nbytes, reps=8):
+    """Peak host-to-device bandwidth of page-locked memory: one expert-sized
+    copy repeated on its own stream, timed with events."""
+    import torch
+    src = torch.empty(nbytes, dtype=torch.uint8, pin_memory=True)
+    src.fill_(1)
+    dst = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    s = torch.cuda.Stream(device=dev)
+    with torch.cuda.stream(s):
+        dst.copy_(src, non_blocking=True)
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(s)
+        for _ in range(reps):
+            dst.copy_(src, non_blocking=True)
+        b.record(s)
+    b.synchronize()
+    gbps = reps * nbytes / (a.elapsed_time(b) * 1e-3) / 1e9
+    del src, dst
+    return gbps
+
+
+def offload_rows(args, shape, Wt, dev):
+    """The offloading deployment: all 256 bf16 experts in page-locked host
+    memory, a 64-expert LRU device cache plus a 16-slot staging ring, misses
+    copied on a side stream while resident experts compute.  A sequence of
+    T=16 decode calls with Zipf(1.2) expert popularity, cache cold at the
+    start, for several pruning thresholds."""
+    import torch
+    from paper_2606_29982_amd import caee
+    from synth_inputs import make_call_sequence
+
+    T, n_cache, n_stage, batch = 16, 64, 16, 4
+    t0 = time.time()
+    host = caee.pin_host_weights(Wt)
+    torch.cuda.synchronize()
+    log(f"offload: experts copied to page-locked host memory in {time.time() - t0:.1f}s")
+    b_pcie = pinned_h2d_gbps(dev, W_EXPERT_BYTES)
+    miss_us = W_EXPERT_BYTES / (b_pcie * 1e9) * 1e6    # alpha = 1, beta = 0
+    log(f"offload: pinned H2D peak {b_pcie:.1f} GB/s, miss cost {miss_us:.0f} us per expert")
+    calls = make_call_sequence(shape, seed=args.seed + 5, n_calls=args.offload_calls, T=T, zipf_logit_s=1.2)
+    dev_calls = [(torch.from_numpy(c.x.view(np.int16)).to(dev).view(torch.bfloat16),
+                  torch.from_numpy(c.logits).to(dev), torch.from_numpy(c.bias).to(dev)) for c in calls]
+    rows = []
+    # MAX rule at the workload's thresholds, then the offloading rule of the
+    # paper (cumulative importance ratio) at its three retention thresholds.
+    for rule, tau in (("max", 0.0), ("max", 0.05), ("max", 0.1), ("cir", 0.9), ("cir", 0.8), ("cir", 0.7)):
+        layer = caee.Layer.from_shape(shape, T=T, tau=tau, n_bins=1, importance=rule)
+        s13, s2 = caee.alloc_slots(layer, n_cache + n_stage, dev)
+        h = caee.Offload(layer, host["w13"], host["w2"], s13, s2, Wt["sh_w13"], Wt["sh_w2"], n_cache, n_stage,
+                         miss_us, batch, caee.LAYOUT_TILED)
+        ws = caee.alloc_workspace(layer, dev)
+        out = caee.alloc_route_out(layer, dev)
+        y = torch.empty((T, shape.d), dtype=torch.bfloat16, device=dev)
+        acc = torch.zeros(8, dtype=torch.int64, device=dev)
+        for x, logits, bias in dev_calls[:4]:        # warm-up, then a cold cache
+            h(layer, x, logits, bias, y, ws, out)
+        torch.cuda.synchronize()
+        h.reset()
+        t1 = time.perf_counter()
+        for x, logits, bias in dev_calls:
+            h(layer, x, logits, bias, y, ws, out)
+            acc += out["stats"]
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t1
+        st = h.stats()
+        a = acc.cpu().tolist()
+        n = len(dev_calls)
+        gbps = st["bytes_h2d"] / wall / 1e9
+        rows.append({"T": T, "calls": n, "tau": tau, "rule": rule, "n_bins": 1, "cache_slots": n_cache,
+                     "staging_slots": n_stage, "fetch_batch": batch,
+                     "tokens_per_s": round(T * n / wall, 1), "ms_per_call": round(wall / n * 1e3, 3),
+                     "h2d_gbps": round(gbps, 2), "h2d_peak_gbps": round(b_pcie, 2),
+                     "h2d_frac": round(gbps / b_pcie, 4),
+                     "hit_rate": round(st["hits"] / max(st["needed"], 1), 4),
+                     "fetched_per_call": round(st["misses"] / n, 2), "staged_per_call": round(st["staged"] / n, 2),
+                     "act_per_call": round(a[0] / n, 2), "pruned_per_call": round(a[4] / n, 2),
+                     "executed_per_call": round(st["needed"] / n + shape.n_shared, 2)})
+        log(f"offload {rows[-1]}")
+        h.close()
+        del s13, s2, ws
+        torch.cuda.empty_cache()
+    del host
+    return {"b_pcie_gbps": round(b_pcie, 2), "miss_cost_us": round(miss_us, 1), "rows": rows}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -281,6 +369,9 @@ def main():
         result["fp8"] = fp8_rows
         del W8
         torch.cuda.empty_cache()
+
+    if not args.no_offload:
+        result["offload"] = offload_rows(args, shape, Wt, dev)
 
     if args.copy_bytes > 0:
         src = torch.empty(args.copy_bytes, dtype=torch.uint8, device=dev)

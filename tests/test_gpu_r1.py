@@ -97,7 +97,8 @@ def test_r1_tiled_weights(T, tokens, rule, tau, r1_weights, r1_tiled):
     _layer_case(r1_weights, T, T == 128, tau, 8, tokens, rule=rule, Wrun=r1_tiled)
 
 
-def test_r1_offload_sequence(r1_weights, r1_tiled):
+@pytest.mark.parametrize("rule,tau", [("max", 0.05), ("cir", 0.8)])
+def test_r1_offload_sequence(r1_weights, r1_tiled, rule, tau):
     """The offloading layer at the R1 shape: 256 bf16 experts in pinned host
     memory, a 16-slot device cache and an 8-slot staging ring, T=16 decode
     calls with Zipf(1.2) popularity."""
@@ -105,7 +106,7 @@ def test_r1_offload_sequence(r1_weights, r1_tiled):
     from synth_inputs import make_call_sequence
     calls = make_call_sequence(R1_BF16, seed=11, n_calls=4, T=16, zipf_logit_s=1.2)
     get, get_sh = getters_dev(r1_weights, "bf16")
-    st = run_offload_sequence(R1_BF16, calls, r1_tiled, DEV, n_cache=16, n_stage=8, fetch_batch=4, tau=0.05,
-                              rule="max", miss_cost=1760.0, get=get, get_sh=get_sh,
+    st = run_offload_sequence(R1_BF16, calls, r1_tiled, DEV, n_cache=16, n_stage=8, fetch_batch=4, tau=tau,
+                              rule=rule, miss_cost=1760.0, get=get, get_sh=get_sh,
                               y_tokens=lambda i: [0, 15] if i in (0, 3) else None, y_tol=2e-2)
     assert st["misses"] > 0 and st["hits"] > 0
