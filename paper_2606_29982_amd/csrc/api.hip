@@ -182,7 +182,7 @@ RouteParams make_route_params(const caee_layer_desc_t* d, const float* logits, c
     p.imp_sum = (double*)(ws + L.imp_sum);
     p.rule = d->importance;
     p.counters = (int32_t*)(ws + L.counters);
-    p.chunk_tokens = L.chunk_tokens;
+    p.chunk_small = L.chunk_small;
     p.orig_ids = (int32_t*)(ws + L.orig);
     return p;
 }
@@ -227,20 +227,85 @@ FfnParams make_ffn_params(const caee_layer_desc_t* d, const void* x, const int32
     return p;
 }
 
-caee_status_t run_ffn_products(const caee_layer_desc_t* d, const FfnParams& p, const WsLayout& L, hipStream_t s) {
-    const int nb = ffn_token_blocks(*d);
+namespace {
+// A second stream per device and host thread, with the two events that fork
+// work onto it and join it back.  Created on first use, kept until the
+// process ends; default priority.
+struct SideStream {
+    hipStream_t stream = nullptr;
+    hipEvent_t fork = nullptr, join = nullptr;
+};
+
+caee_status_t side_stream(SideStream** out) {
+    thread_local SideStream per_dev[64];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return fail(CAEE_ERR_HIP, "hipGetDevice failed");
+    SideStream& ss = per_dev[dev];
+    if (!ss.stream) {
+        hipError_t e = hipStreamCreateWithFlags(&ss.stream, hipStreamNonBlocking);
+        if (e == hipSuccess) e = hipEventCreateWithFlags(&ss.fork, hipEventDisableTiming);
+        if (e == hipSuccess) e = hipEventCreateWithFlags(&ss.join, hipEventDisableTiming);
+        if (e != hipSuccess) {
+            ss = SideStream{};
+            return fail(CAEE_ERR_HIP, "side stream creation failed: %s", hipGetErrorString(e));
+        }
+    }
+    *out = &ss;
+    return CAEE_OK;
+}
+}  // namespace
+
+caee_status_t run_ffn_products(const caee_layer_desc_t* d, const FfnParams& p0, const WsLayout& L, hipStream_t s) {
+    // Small chunks, then (when the batch can have any) big chunks; each launch
+    // is compiled for its own number of 16-token blocks.
+    const int nb_small = small_token_blocks(*d), nb_big = big_token_blocks(*d);
+    FfnParams ps = p0, pb = p0;
+    ps.list = 0;
+    pb.list = 1;
     if (d->w_dtype == CAEE_FP8_E4M3) {
         CAEE_TRY(timed_launch(CAEE_KERNEL_QUANT, s, "quantise x",
-                              [&] { return launch_quant_rows(p.x, 1, d->T, d->d, p.xq, p.xs, s); }));
+                              [&] { return launch_quant_rows(p0.x, 1, d->T, d->d, p0.xq, p0.xs, s); }));
         CAEE_TRY(timed_launch(CAEE_KERNEL_GATE_UP, s, "gate/up",
-                              [&] { return launch_gate_up_fp8(p, nb, L.max_chunks, s); }));
+                              [&] { return launch_gate_up_fp8(ps, nb_small, L.max_chunks, s); }));
+        if (nb_big)
+            CAEE_TRY(timed_launch(CAEE_KERNEL_GATE_UP, s, "gate/up",
+                                  [&] { return launch_gate_up_fp8(pb, nb_big, L.max_chunks, s); }));
         CAEE_TRY(timed_launch(CAEE_KERNEL_QUANT, s, "quantise H",
-                              [&] { return launch_quant_rows(p.h, 0, L.P, d->f, p.hq, p.hs, s); }));
-        return timed_launch(CAEE_KERNEL_DOWN, s, "down", [&] { return launch_down_fp8(p, nb, L.max_chunks, s); });
+                              [&] { return launch_quant_rows(p0.h, 0, L.P, d->f, p0.hq, p0.hs, s); }));
+        CAEE_TRY(timed_launch(CAEE_KERNEL_DOWN, s, "down",
+                              [&] { return launch_down_fp8(ps, nb_small, L.max_chunks, s); }));
+        if (nb_big)
+            CAEE_TRY(timed_launch(CAEE_KERNEL_DOWN, s, "down",
+                                  [&] { return launch_down_fp8(pb, nb_big, L.max_chunks, s); }));
+        return CAEE_OK;
+    }
+    // The two chains touch disjoint rows of H and Y: the big chunks (few,
+    // long, latency-bound work items) run on a second stream next to the
+    // small ones (many, bandwidth-bound), then join back.
+    SideStream* ss = nullptr;
+    if (nb_big && kBigConcurrent) {
+        CAEE_TRY(side_stream(&ss));
+        hipError_t e = hipEventRecord(ss->fork, s);
+        if (e == hipSuccess) e = hipStreamWaitEvent(ss->stream, ss->fork, 0);
+        if (e != hipSuccess) return fail(CAEE_ERR_HIP, "fork to the side stream failed: %s", hipGetErrorString(e));
+    }
+    hipStream_t sb = ss ? ss->stream : s;
+    if (nb_big) {
+        CAEE_TRY(timed_launch(CAEE_KERNEL_GATE_UP, sb, "gate/up",
+                              [&] { return launch_gate_up(pb, d->w_dtype, nb_big, L.max_chunks, sb); }));
+        CAEE_TRY(timed_launch(CAEE_KERNEL_DOWN, sb, "down",
+                              [&] { return launch_down(pb, d->w_dtype, nb_big, L.max_chunks, sb); }));
     }
     CAEE_TRY(timed_launch(CAEE_KERNEL_GATE_UP, s, "gate/up",
-                          [&] { return launch_gate_up(p, d->w_dtype, nb, L.max_chunks, s); }));
-    return timed_launch(CAEE_KERNEL_DOWN, s, "down", [&] { return launch_down(p, d->w_dtype, nb, L.max_chunks, s); });
+                          [&] { return launch_gate_up(ps, d->w_dtype, nb_small, L.max_chunks, s); }));
+    CAEE_TRY(timed_launch(CAEE_KERNEL_DOWN, s, "down",
+                          [&] { return launch_down(ps, d->w_dtype, nb_small, L.max_chunks, s); }));
+    if (ss) {
+        hipError_t e = hipEventRecord(ss->join, ss->stream);
+        if (e == hipSuccess) e = hipStreamWaitEvent(s, ss->join, 0);
+        if (e != hipSuccess) return fail(CAEE_ERR_HIP, "join from the side stream failed: %s", hipGetErrorString(e));
+    }
+    return CAEE_OK;
 }
 
 caee_status_t run_combine(const FfnParams& p, hipStream_t s) {

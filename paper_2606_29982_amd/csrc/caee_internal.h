@@ -20,9 +20,18 @@ constexpr int kMaxShared = 4;
 constexpr int kMaxBins = 256;
 constexpr int kMaxT = 65536;        // tokens per call
 constexpr int kRouteThreads = 1024;
-constexpr int kMaxTokenBlocks = 8;  // 16-token MFMA column blocks one FFN work item can hold
+// 16-token MFMA column blocks one FFN work item can hold (1, 2, 4 or 8).
+#ifndef CAEE_MAX_TOKEN_BLOCKS
+#define CAEE_MAX_TOKEN_BLOCKS 4
+#endif
+constexpr int kMaxTokenBlocks = CAEE_MAX_TOKEN_BLOCKS;
 constexpr int kFfnThreads = 256;    // 4 independent waves per FFN workgroup
-constexpr long long kTargetItems = 4096;   // gate/up work items wanted per call (~4 per SIMD)
+// Gate/up wave work items wanted per call before the contraction is split
+// (about 32 per SIMD: short items keep the tail of the launch short).
+#ifndef CAEE_TARGET_ITEMS
+#define CAEE_TARGET_ITEMS 32768
+#endif
+constexpr long long kTargetItems = CAEE_TARGET_ITEMS;
 
 // Contraction steps (one 16-byte load per lane) issued together per wave.
 #ifndef CAEE_GATE_UP_U
@@ -33,6 +42,18 @@ constexpr long long kTargetItems = 4096;   // gate/up work items wanted per call
 #endif
 constexpr int kGateUpU = CAEE_GATE_UP_U;
 constexpr int kDownU = CAEE_DOWN_U;
+// Big chunks: contraction steps staged in LDS per stage, and whether the
+// LDS-staged kernels run them (0: the direct kernels, compiled for 128 rows).
+constexpr int kBigU = 4;
+#ifndef CAEE_BIG_STAGED
+#define CAEE_BIG_STAGED 1
+#endif
+constexpr bool kBigStaged = CAEE_BIG_STAGED != 0;
+// Run the big-chunk launches on a second stream, concurrently with the small ones.
+#ifndef CAEE_BIG_CONCURRENT
+#define CAEE_BIG_CONCURRENT 1
+#endif
+constexpr bool kBigConcurrent = CAEE_BIG_CONCURRENT != 0;
 constexpr int kFp8U = 2;            // 128-wide fp8 MFMA blocks per step (4 x 16-byte loads per matrix)
 // Minimum resident waves per SIMD the FFN kernels are compiled for (0: no bound).
 #ifndef CAEE_FFN_WAVES_PER_EU
@@ -57,14 +78,15 @@ struct WsLayout {
     size_t perm_off;            // [E + n_shared + 1] first permuted row of each expert slot
     size_t perm_tok;            // [P] token of each permuted row
     size_t perm_pos;            // [T][k + n_shared] permuted row of each (token, slot), -1 unused
-    size_t chunks;              // [max_chunks][4] (expert slot, first row, rows, 0)
-    size_t n_chunks;            // [1]
+    size_t chunks;              // [max_chunks][4] (expert slot, first row, rows, 0): small chunks, then big
+    size_t n_chunks;            // [2] small and big chunk counts
     size_t h;                   // [P][f] SwiGLU activations (weight dtype; fp32 for fp8)
     size_t y;                   // [P][d] fp32 expert outputs
     size_t xq, xs;              // fp8 path: [T][d] e4m3 codes of x and [T][d/128] fp32 scales
     size_t hq, hs;              // fp8 path: [P][f] e4m3 codes of H and [P][f/128] fp32 scales
     size_t total;
-    int P, max_chunks, ksplit, chunk_tokens;
+    int P, max_chunks, ksplit;
+    int chunk_small;            // an expert slot with at most this many rows is one small chunk
 };
 
 inline size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
@@ -73,30 +95,47 @@ inline int elem_bytes(int dtype) {
     return dtype == CAEE_F32 ? 4 : dtype == CAEE_BF16 ? 2 : 1;
 }
 
-// Split of the gate/up contraction: small batches touch few experts, so the
-// d dimension is cut into ksplit ranges to give every SIMD several work items.
-// Depends on the descriptor only (not on the device).
-// The splits of one tile are waves of one 4-wave workgroup, so ksplit <= 4.
+// Split of the gate/up contraction: when a call has few chunks, the d
+// dimension is cut into up to 4 ranges (the waves of one workgroup) so that
+// every SIMD gets several work items.  The host fixes the largest split the
+// row length allows; the kernels take the split for the number of chunks the
+// call actually has (gate_up_split_for), which routing decides on the device.
 inline int gate_up_split(const caee_layer_desc_t& d) {
     // Contraction steps of one work item: 64-byte row pieces (one MFMA for
     // bf16) or 128-wide scale blocks (one MFMA for fp8).
     const bool fp8 = d.w_dtype == CAEE_FP8_E4M3;
     const int ksteps = fp8 ? d.d / 128 : d.d * elem_bytes(d.w_dtype) / 64;
     const int U = fp8 ? kFp8U : kGateUpU;
-    const long long tok_slots = (long long)(d.T > 0 ? d.T : 0) * d.k;
-    const long long experts = (tok_slots < d.E ? tok_slots : d.E) + d.n_shared;
-    const long long tiles = experts * (d.f / 16);
     int S = 1;
-    while (S < 4 && tiles * S < kTargetItems && ksteps % (2 * S * U) == 0) S *= 2;
+    while (S < 4 && ksteps % (2 * S * U) == 0) S *= 2;
     return S;
 }
 
-// 16-token column blocks per FFN work item: enough for every token of the
-// batch to land in one chunk per expert while T <= 128, so each expert's
-// weights are streamed once; larger batches use several 128-token chunks.
-inline int ffn_token_blocks(const caee_layer_desc_t& d) {
+__host__ __device__ inline int gate_up_split_for(int n_chunks, int tiles, int s_max) {
+    int S = s_max;
+    while (S > 1 && (long long)n_chunks * tiles * (S / 2) >= kTargetItems) S >>= 1;
+    return S;
+}
+
+// Work list of the FFN kernels.  An expert slot with at most
+// 16 * small_token_blocks rows of the call is one "small" chunk; a slot with
+// more rows is cut into ceil(rows / kBigChunk) near-equal "big" chunks.  The
+// two kinds run in separate launches, each compiled for its own token-block
+// count: most experts of a decode batch carry a handful of tokens, and
+// compiling their work items for the hot experts' 128 tokens would cost them
+// occupancy.  Each big chunk streams its expert's weights once.
+constexpr int kBigChunk = 16 * kMaxTokenBlocks;
+
+// 16-token column blocks of the small-chunk kernels (1 or 2).
+inline int small_token_blocks(const caee_layer_desc_t& d) { return d.T <= 16 ? 1 : 2; }
+
+// 16-token column blocks of the big-chunk kernels (0: the call has no big
+// chunks since no slot can have more rows than T).
+inline int big_token_blocks(const caee_layer_desc_t& d) {
+    if (d.T <= 16 * small_token_blocks(d)) return 0;
     const int need = (d.T + 15) / 16;
-    return need <= 1 ? 1 : need <= 2 ? 2 : need <= 4 ? 4 : kMaxTokenBlocks;
+    const int nb = need <= 4 ? 4 : 8;
+    return nb < kMaxTokenBlocks ? nb : kMaxTokenBlocks;
 }
 
 inline WsLayout ws_layout(const caee_layer_desc_t& d) {
@@ -104,8 +143,10 @@ inline WsLayout ws_layout(const caee_layer_desc_t& d) {
     const size_t T = d.T > 0 ? d.T : 0;
     const int slots = d.k + d.n_shared;
     L.P = int(T * slots);
-    L.chunk_tokens = 16 * ffn_token_blocks(d);
-    L.max_chunks = d.E + d.n_shared + (L.P + L.chunk_tokens - 1) / L.chunk_tokens;
+    L.chunk_small = 16 * small_token_blocks(d);
+    // Every expert slot gives one small chunk or ceil(rows / kBigChunk) big
+    // ones, so the count is at most (slots) + P / kBigChunk.
+    L.max_chunks = d.E + d.n_shared + (L.P + kBigChunk - 1) / kBigChunk;
     size_t off = 0;
     auto take = [&](size_t bytes) { size_t o = off; off += align256(bytes); return o; };
     L.ids = take(T * d.k * 4);
@@ -162,7 +203,7 @@ struct RouteParams {
     uint8_t* mflag;
     double* imp_sum;
     int32_t* counters;
-    int chunk_tokens;
+    int chunk_small;
     // permutation outputs
     int32_t* perm_off;
     int32_t* perm_tok;
@@ -187,6 +228,7 @@ struct FfnParams {
     const int32_t* perm_pos;
     const int32_t* chunks;
     const int32_t* n_chunks;
+    int list;       // 0: the small chunks, 1: the big chunks
     const int32_t* topk_ids;
     const float* topk_w;
     void* h;

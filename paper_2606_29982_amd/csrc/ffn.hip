@@ -131,11 +131,13 @@ __global__ CAEE_FFN_BOUNDS void k_gate_up(FfnParams p) {
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = threadIdx.x / kWave;
     const int r = lane & 15, g = lane >> 4;
-    const int S = p.ksplit;
     const int tiles = p.f / 16;
+    const int n_chunks = p.n_chunks[p.list];
+    const int32_t* chunks = p.chunks + (p.list ? 4 * p.n_chunks[0] : 0);
+    const int S = gate_up_split_for(n_chunks, tiles, p.ksplit);
     const int tiles_per_item = kWaves / S;
     const int items_per_chunk = tiles / tiles_per_item;
-    const int total = (*p.n_chunks) * items_per_chunk;
+    const int total = n_chunks * items_per_chunk;
     const size_t row_units = (size_t)p.d * M::kElemBytes / 16;
     const int kper = (int)(row_units / 4) / S;
     const size_t expert_bytes = (size_t)2 * p.f * p.d * M::kElemBytes;
@@ -144,7 +146,7 @@ __global__ CAEE_FFN_BOUNDS void k_gate_up(FfnParams p) {
     for (int item = blockIdx.x; item < total; item += gridDim.x) {
         const int c = item / items_per_chunk;
         const int jt = (item - c * items_per_chunk) * tiles_per_item + wave / S;
-        const int xs = p.chunks[4 * c], row0 = p.chunks[4 * c + 1], ntok = p.chunks[4 * c + 2];
+        const int xs = chunks[4 * c], row0 = chunks[4 * c + 1], ntok = chunks[4 * c + 2];
         if (p.pass_of && p.pass_of[xs] != p.pass_id) continue;   // uniform over the workgroup
         const int nb = (ntok + 15) >> 4;
         const size_t k0 = (size_t)4 * sp * kper;
@@ -215,14 +217,16 @@ __global__ CAEE_FFN_BOUNDS void k_down(FfnParams p) {
     const int gw = blockIdx.x * (kFfnThreads / kWave) + (threadIdx.x / kWave);
     const int nw = gridDim.x * (kFfnThreads / kWave);
     const int tiles = p.d / 16;
-    const int total = (*p.n_chunks) * tiles;
+    const int n_chunks = p.n_chunks[p.list];
+    const int32_t* chunks = p.chunks + (p.list ? 4 * p.n_chunks[0] : 0);
+    const int total = n_chunks * tiles;
     const size_t row_units = (size_t)p.f * M::kElemBytes / 16;
     const int ksteps = (int)(row_units / 4);
     const size_t expert_bytes = (size_t)p.d * p.f * M::kElemBytes;
 
     for (int item = gw; item < total; item += nw) {
         const int c = item / tiles, it = item - c * tiles;
-        const int xs = p.chunks[4 * c], row0 = p.chunks[4 * c + 1], ntok = p.chunks[4 * c + 2];
+        const int xs = chunks[4 * c], row0 = chunks[4 * c + 1], ntok = chunks[4 * c + 2];
         if (p.pass_of && p.pass_of[xs] != p.pass_id) continue;
         const int nb = (ntok + 15) >> 4;
         const u32x4_t* wb = (const u32x4_t*)(p.wtab ? (const char*)p.wtab[2 * xs + 1]
@@ -249,6 +253,208 @@ __global__ CAEE_FFN_BOUNDS void k_down(FfnParams p) {
                 *(float4*)o = make_float4(acc[0][tb][0], acc[0][tb][1], acc[0][tb][2], acc[0][tb][3]);
             }
         }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Big chunks (more than 32 rows of one expert).  With many token columns per
+// weight tile the activation rows, not the weights, dominate the load
+// traffic: read by every wave from L2 they would cost each wave NB times its
+// weight bytes.  Here a workgroup stages the chunk's rows for U contraction
+// steps in LDS once (double buffered, one barrier per stage) and its four
+// waves, each on its own weight tiles, read their MFMA fragments from LDS.
+// LDS stage layout: [token block][step][lane] 16-byte pieces, i.e. exactly
+// the B fragment of lane l (token 16*tb + l%16, bytes 16*(l/16) of the step),
+// so every fragment read is one conflict-free 16-byte LDS load.
+
+// Staging of one stage: thread `tid` moves 16-byte piece q = tid % (4U) of
+// token (tid / (4U)) + (256 / 4U) * j for j < NB * 4U / 16 ... written for the
+// case 4U == 16 (U = 4): token tid/16 + 16 j is block j, lane tid/16 + 16 (q%4),
+// step q/4.
+template <int U, int NB>
+struct BigStage {
+    static_assert(U == 4, "staging map assumes 16 pieces per token and stage");
+    static constexpr int kPer = NB;                 // pieces per thread per stage
+    const u32x4_t* src[NB];                         // this thread's token rows (+ its piece)
+    int q;
+    __device__ inline void init(const u32x4_t* const (&rows)[NB], int tid) {
+        q = tid & 15;
+#pragma unroll
+        for (int j = 0; j < NB; ++j) src[j] = rows[j] + q;
+    }
+    __device__ inline void load(u32x4_t (&v)[NB], int kb, int nb) const {
+#pragma unroll
+        for (int j = 0; j < NB; ++j)
+            if (j < nb) v[j] = src[j][(size_t)kb * (4 * U)];
+    }
+    __device__ inline void store(u32x4_t (*sb)[U][kWave], const u32x4_t (&v)[NB], int tid, int nb) const {
+        const int l = (tid >> 4) + 16 * (q & 3), u = q >> 2;
+#pragma unroll
+        for (int j = 0; j < NB; ++j)
+            if (j < nb) sb[j][u][l] = v[j];
+    }
+};
+
+// Contraction of NA weight-tile fragments per wave against a chunk's staged
+// rows over `nkb` stages of U steps.  a[m]: this lane's first weight piece of
+// tile m (consecutive steps `astep` pieces apart); rows[j]: token row of
+// staged block j for this thread's staging slot.
+template <class M, int U, int NA, int NB>
+__device__ inline void big_contract(u32x4_t (*sb)[NB][U][kWave], const u32x4_t* const (&a)[NA], int astep,
+                                    const u32x4_t* const (&rows)[NB], int nb, int nkb, f32x4_t (&acc)[NA][NB]) {
+    const int tid = threadIdx.x, lane = tid & (kWave - 1);
+    BigStage<U, NB> st;
+    st.init(rows, tid);
+    u32x4_t bv[NB];
+    u32x4_t cur[NA][U], nxt[NA][U];
+    st.load(bv, 0, nb);
+#pragma unroll
+    for (int m = 0; m < NA; ++m)
+#pragma unroll
+        for (int u = 0; u < U; ++u) cur[m][u] = __builtin_nontemporal_load(a[m] + (size_t)astep * u);
+    st.store(sb[0], bv, tid, nb);
+    __syncthreads();
+    for (int kb = 0; kb < nkb; ++kb) {
+        const bool more = kb + 1 < nkb;
+        if (more) {
+            st.load(bv, kb + 1, nb);
+#pragma unroll
+            for (int m = 0; m < NA; ++m)
+#pragma unroll
+                for (int u = 0; u < U; ++u)
+                    nxt[m][u] = __builtin_nontemporal_load(a[m] + (size_t)astep * ((kb + 1) * U + u));
+        }
+        u32x4_t (*cb)[U][kWave] = sb[kb & 1];
+#pragma unroll
+        for (int tb = 0; tb < NB; ++tb) {
+            if (tb < nb) {
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    const u32x4_t b = cb[tb][u][lane];
+#pragma unroll
+                    for (int m = 0; m < NA; ++m) M::mma(acc[m][tb], cur[m][u], b);
+                }
+            }
+        }
+        if (more) {
+            st.store(sb[(kb + 1) & 1], bv, tid, nb);
+#pragma unroll
+            for (int m = 0; m < NA; ++m)
+#pragma unroll
+                for (int u = 0; u < U; ++u) cur[m][u] = nxt[m][u];
+        }
+        __syncthreads();
+    }
+}
+
+// Gate/up of big chunks: a workgroup item is 4 adjacent 16-feature tiles of
+// one chunk, one per wave, over the whole contraction.
+template <class M, int U, int NB>
+__global__ __launch_bounds__(kFfnThreads) void k_gate_up_big(FfnParams p) {
+    constexpr int kWaves = kFfnThreads / kWave;
+    __shared__ u32x4_t s_b[2][NB][U][kWave];
+    const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+    const int r = lane & 15, g = lane >> 4;
+    const int n_chunks = p.n_chunks[p.list];
+    const int32_t* chunks = p.chunks + (p.list ? 4 * p.n_chunks[0] : 0);
+    const int tiles = p.f / 16;
+    const int items_per_chunk = tiles / kWaves;
+    const int total = n_chunks * items_per_chunk;
+    const size_t row_units = (size_t)p.d * M::kElemBytes / 16;
+    const int ksteps = (int)(row_units / 4);
+    const size_t expert_bytes = (size_t)2 * p.f * p.d * M::kElemBytes;
+    for (int item = blockIdx.x; item < total; item += gridDim.x) {
+        const int c = item / items_per_chunk;
+        const int jt = (item - c * items_per_chunk) * kWaves + wave;
+        const int xs = chunks[4 * c], row0 = chunks[4 * c + 1], ntok = chunks[4 * c + 2];
+        if (p.pass_of && p.pass_of[xs] != p.pass_id) continue;   // uniform over the workgroup
+        const int nb = (ntok + 15) >> 4;
+        const u32x4_t* wb = (const u32x4_t*)(p.wtab ? (const char*)p.wtab[2 * xs]
+                                                    : expert_base(p.w13, p.sh_w13, xs, p.E, expert_bytes));
+        const u32x4_t* const a[2] = {
+            p.tiled ? wb + (size_t)jt * ksteps * 64 + lane : wb + (size_t)(jt * 16 + r) * row_units + g,
+            p.tiled ? wb + (size_t)(tiles + jt) * ksteps * 64 + lane
+                    : wb + (size_t)(p.f + jt * 16 + r) * row_units + g};
+        const u32x4_t* rows[NB];
+#pragma unroll
+        for (int j = 0; j < NB; ++j) {
+            int n = (tid >> 4) + 16 * j;
+            n = n < ntok ? n : 0;   // padded token columns read a valid row; results dropped
+            rows[j] = (const u32x4_t*)p.x + (size_t)p.perm_tok[row0 + n] * row_units;
+        }
+        f32x4_t acc[2][NB];
+#pragma unroll
+        for (int m = 0; m < 2; ++m)
+#pragma unroll
+            for (int tb = 0; tb < NB; ++tb) acc[m][tb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        big_contract<M, U, 2, NB>(s_b, a, p.tiled ? 64 : 4, rows, nb, ksteps / U, acc);
+        const int col = jt * 16 + 4 * g;
+#pragma unroll
+        for (int tb = 0; tb < NB; ++tb) {
+            const int n = tb * 16 + r;
+            if (tb < nb && n < ntok) {
+                float h[4];
+#pragma unroll
+                for (int v = 0; v < 4; ++v) h[v] = silu_mul(acc[0][tb][v], acc[1][tb][v]);
+                store_h<M>(p, (size_t)(row0 + n) * p.f + col, h);
+            }
+        }
+    }
+}
+
+// Down products of big chunks: a workgroup item is 8 adjacent 16-row tiles
+// of W2 (two per wave) of one chunk.
+template <class M, int U, int NB>
+__global__ __launch_bounds__(kFfnThreads) void k_down_big(FfnParams p) {
+    constexpr int kWaves = kFfnThreads / kWave;
+    constexpr int kTW = 2;
+    __shared__ u32x4_t s_b[2][NB][U][kWave];
+    const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+    const int r = lane & 15, g = lane >> 4;
+    const int n_chunks = p.n_chunks[p.list];
+    const int32_t* chunks = p.chunks + (p.list ? 4 * p.n_chunks[0] : 0);
+    const int tiles = p.d / 16;
+    const int items_per_chunk = tiles / (kWaves * kTW);
+    const int total = n_chunks * items_per_chunk;
+    const size_t row_units = (size_t)p.f * M::kElemBytes / 16;
+    const int ksteps = (int)(row_units / 4);
+    const size_t expert_bytes = (size_t)p.d * p.f * M::kElemBytes;
+    for (int item = blockIdx.x; item < total; item += gridDim.x) {
+        const int c = item / items_per_chunk;
+        const int it0 = ((item - c * items_per_chunk) * kWaves + wave) * kTW;
+        const int xs = chunks[4 * c], row0 = chunks[4 * c + 1], ntok = chunks[4 * c + 2];
+        if (p.pass_of && p.pass_of[xs] != p.pass_id) continue;
+        const int nb = (ntok + 15) >> 4;
+        const u32x4_t* wb = (const u32x4_t*)(p.wtab ? (const char*)p.wtab[2 * xs + 1]
+                                                    : expert_base(p.w2, p.sh_w2, xs, p.E, expert_bytes));
+        const u32x4_t* a[kTW];
+#pragma unroll
+        for (int m = 0; m < kTW; ++m)
+            a[m] = p.tiled ? wb + (size_t)(it0 + m) * ksteps * 64 + lane
+                           : wb + (size_t)((it0 + m) * 16 + r) * row_units + g;
+        const u32x4_t* rows[NB];
+#pragma unroll
+        for (int j = 0; j < NB; ++j) {
+            int n = (tid >> 4) + 16 * j;
+            n = n < ntok ? n : 0;
+            rows[j] = (const u32x4_t*)p.h + (size_t)(row0 + n) * row_units;
+        }
+        f32x4_t acc[kTW][NB];
+#pragma unroll
+        for (int m = 0; m < kTW; ++m)
+#pragma unroll
+            for (int tb = 0; tb < NB; ++tb) acc[m][tb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        big_contract<M, U, kTW, NB>(s_b, a, p.tiled ? 64 : 4, rows, nb, ksteps / U, acc);
+#pragma unroll
+        for (int m = 0; m < kTW; ++m)
+#pragma unroll
+            for (int tb = 0; tb < NB; ++tb) {
+                const int n = tb * 16 + r;
+                if (tb < nb && n < ntok) {
+                    float* o = p.yperm + (size_t)(row0 + n) * p.d + (it0 + m) * 16 + 4 * g;
+                    *(float4*)o = make_float4(acc[m][tb][0], acc[m][tb][1], acc[m][tb][2], acc[m][tb][3]);
+                }
+            }
     }
 }
 
@@ -332,9 +538,32 @@ struct DownK {
     static constexpr auto run = k_down<M, U, NB>;
 };
 
+template <class M>
+hipError_t launch_big(const FfnParams& p, bool gate_up, int nb, dim3 grid, hipStream_t s) {
+    constexpr int U = kBigU;
+    switch (nb) {
+        case 4:
+            if (gate_up) hipLaunchKernelGGL((k_gate_up_big<M, U, 4>), grid, dim3(kFfnThreads), 0, s, p);
+            else hipLaunchKernelGGL((k_down_big<M, U, 4>), grid, dim3(kFfnThreads), 0, s, p);
+            break;
+        case 8:
+            if (gate_up) hipLaunchKernelGGL((k_gate_up_big<M, U, 8>), grid, dim3(kFfnThreads), 0, s, p);
+            else hipLaunchKernelGGL((k_down_big<M, U, 8>), grid, dim3(kFfnThreads), 0, s, p);
+            break;
+        default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
 }  // namespace
 
 hipError_t launch_gate_up(const FfnParams& p, int w_dtype, int nb, int max_chunks, hipStream_t s) {
+    if (p.list == 1 && kBigStaged) {
+        const dim3 grid(grid_for((long long)max_chunks * (p.f / 16)));
+        if (w_dtype == CAEE_BF16) return launch_big<Bf16Math>(p, true, nb, grid, s);
+        if (w_dtype == CAEE_F32) return launch_big<F32Math>(p, true, nb, grid, s);
+        return hipErrorInvalidValue;
+    }
     const dim3 grid(grid_for((long long)max_chunks * (p.f / 16) * p.ksplit));   // waves wanted
     if (w_dtype == CAEE_BF16) return launch_nb<Bf16Math, GateUpK, kGateUpU>(p, nb, grid, s);
     if (w_dtype == CAEE_F32) return launch_nb<F32Math, GateUpK, kGateUpU>(p, nb, grid, s);
@@ -342,6 +571,12 @@ hipError_t launch_gate_up(const FfnParams& p, int w_dtype, int nb, int max_chunk
 }
 
 hipError_t launch_down(const FfnParams& p, int w_dtype, int nb, int max_chunks, hipStream_t s) {
+    if (p.list == 1 && kBigStaged) {
+        const dim3 grid(grid_for((long long)max_chunks * (p.d / 16) / 2));
+        if (w_dtype == CAEE_BF16) return launch_big<Bf16Math>(p, false, nb, grid, s);
+        if (w_dtype == CAEE_F32) return launch_big<F32Math>(p, false, nb, grid, s);
+        return hipErrorInvalidValue;
+    }
     const dim3 grid(grid_for((long long)max_chunks * (p.d / 16)));
     if (w_dtype == CAEE_BF16) return launch_nb<Bf16Math, DownK, kDownU>(p, nb, grid, s);
     if (w_dtype == CAEE_F32) return launch_nb<F32Math, DownK, kDownU>(p, nb, grid, s);

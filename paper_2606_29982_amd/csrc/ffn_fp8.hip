@@ -161,11 +161,13 @@ __global__ __launch_bounds__(kFfnThreads) void k_gate_up_fp8(FfnParams p) {
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = threadIdx.x / kWave;
     const int r = lane & 15, g = lane >> 4;
-    const int S = p.ksplit;
     const int tiles = p.f / 16;
+    const int n_chunks = p.n_chunks[p.list];
+    const int32_t* chunks = p.chunks + (p.list ? 4 * p.n_chunks[0] : 0);
+    const int S = gate_up_split_for(n_chunks, tiles, p.ksplit);
     const int tiles_per_item = kWaves / S;
     const int items_per_chunk = tiles / tiles_per_item;
-    const int total = (*p.n_chunks) * items_per_chunk;
+    const int total = n_chunks * items_per_chunk;
     const size_t row_units = (size_t)p.d / 16;     // 16-byte pieces per weight / x row
     const size_t ksteps = row_units / 4;            // 64-byte steps per row
     const int kblocks = p.d / 128;
@@ -177,7 +179,7 @@ __global__ __launch_bounds__(kFfnThreads) void k_gate_up_fp8(FfnParams p) {
     for (int item = blockIdx.x; item < total; item += gridDim.x) {
         const int c = item / items_per_chunk;
         const int jt = (item - c * items_per_chunk) * tiles_per_item + wave / S;
-        const int xs_ = p.chunks[4 * c], row0 = p.chunks[4 * c + 1], ntok = p.chunks[4 * c + 2];
+        const int xs_ = chunks[4 * c], row0 = chunks[4 * c + 1], ntok = chunks[4 * c + 2];
         const int nb = (ntok + 15) >> 4;
         const int kb0 = sp * kper;
         const u32x4_t* wb = (const u32x4_t*)expert_base(p.w13, p.sh_w13, xs_, p.E, expert_bytes);
@@ -250,7 +252,9 @@ __global__ __launch_bounds__(kFfnThreads) void k_down_fp8(FfnParams p) {
     const int gw = blockIdx.x * (kFfnThreads / kWave) + (threadIdx.x / kWave);
     const int nw = gridDim.x * (kFfnThreads / kWave);
     const int tiles = p.d / 16;
-    const int total = (*p.n_chunks) * tiles;
+    const int n_chunks = p.n_chunks[p.list];
+    const int32_t* chunks = p.chunks + (p.list ? 4 * p.n_chunks[0] : 0);
+    const int total = n_chunks * tiles;
     const size_t row_units = (size_t)p.f / 16;
     const size_t ksteps = row_units / 4;
     const int kblocks = p.f / 128;
@@ -259,7 +263,7 @@ __global__ __launch_bounds__(kFfnThreads) void k_down_fp8(FfnParams p) {
 
     for (int item = gw; item < total; item += nw) {
         const int c = item / tiles, it = item - c * tiles;
-        const int xs_ = p.chunks[4 * c], row0 = p.chunks[4 * c + 1], ntok = p.chunks[4 * c + 2];
+        const int xs_ = chunks[4 * c], row0 = chunks[4 * c + 1], ntok = chunks[4 * c + 2];
         const int nb = (ntok + 15) >> 4;
         const u32x4_t* wb = (const u32x4_t*)expert_base(p.w2, p.sh_w2, xs_, p.E, expert_bytes);
         const u32x4_t* const a[1] = {p.tiled ? wb + (size_t)it * ksteps * 64 + lane

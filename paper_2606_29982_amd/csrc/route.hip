@@ -497,7 +497,9 @@ __global__ __launch_bounds__(kRouteThreads) void k_prune(RouteParams p) {
 
 // Permutation of K_final (read from global memory) by expert slot: rows of
 // slot x (x < E routed, E+s shared) are [off[x], off[x+1]), tokens ascending
-// within a slot; then the FFN work list of chunks of at most chunk_tokens rows.
+// within a slot; then the FFN work list: one small chunk per slot with at
+// most chunk_small rows, then ceil(rows / kBigChunk) near-equal big chunks per
+// larger slot.
 // Executed by one workgroup of `nthr` threads.  Up to kMaskT tokens, each
 // expert's tokens are kept as a bitmask in LDS and every (token, slot) entry
 // finds its row independently by counting set bits; larger batches walk
@@ -509,7 +511,7 @@ __device__ void permute_all(const RouteParams& p, int tid, int nthr, int* s_cnt,
     const int slots = k + p.n_shared;
     const int lane = tid & (kWave - 1);
     const int wave = tid / kWave;
-    const int ch = p.chunk_tokens;
+    const int cs = p.chunk_small;
     const bool masked = T <= kMaskT;
     const int W = (T + 63) / 64;
     if (masked) {
@@ -541,45 +543,63 @@ __device__ void permute_all(const RouteParams& p, int tid, int nthr, int* s_cnt,
     }
     __syncthreads();
     if (wave == 0) {
+        // Exclusive scans of rows, small chunks and big chunks over the slots;
+        // small chunks are listed first, big ones after all of them.
         const int per = (nx + kWave - 1) / kWave;
         const int lo = lane * per;
         const int hi = min(lo + per, nx);
-        int sum = 0, csum = 0;
+        int sum = 0, ssum = 0, bsum = 0;
         for (int x = lo; x < hi; ++x) {
-            sum += s_cnt[x];
-            csum += (s_cnt[x] + ch - 1) / ch;
+            const int n = s_cnt[x];
+            sum += n;
+            ssum += (n > 0 && n <= cs) ? 1 : 0;
+            bsum += n > cs ? (n + kBigChunk - 1) / kBigChunk : 0;
         }
-        int inc = sum, cinc = csum;
+        int inc = sum, sinc = ssum, binc = bsum;
         for (int off = 1; off < kWave; off <<= 1) {
             const int o = __shfl_up(inc, off);
-            const int co = __shfl_up(cinc, off);
+            const int so = __shfl_up(sinc, off);
+            const int bo = __shfl_up(binc, off);
             if (lane >= off) {
                 inc += o;
-                cinc += co;
+                sinc += so;
+                binc += bo;
             }
         }
-        int run = inc - sum, crun = cinc - csum;
+        const int stotal = __shfl(sinc, kWave - 1);
+        int run = inc - sum, srun = sinc - ssum, brun = stotal + binc - bsum;
         for (int x = lo; x < hi; ++x) {
             const int cnt = s_cnt[x];
             s_off[x] = run;
             p.perm_off[x] = run;
-            for (int c = 0; c * ch < cnt; ++c) {
-                int* chk = p.chunks + 4 * (crun + c);
+            if (cnt > 0 && cnt <= cs) {
+                int* chk = p.chunks + 4 * srun++;
                 chk[0] = x;
-                chk[1] = run + c * ch;
-                chk[2] = min(ch, cnt - c * ch);
+                chk[1] = run;
+                chk[2] = cnt;
                 chk[3] = 0;
+            } else if (cnt > cs) {
+                const int pieces = (cnt + kBigChunk - 1) / kBigChunk;
+                const int size = (cnt + pieces - 1) / pieces;
+                for (int c = 0; c < pieces; ++c) {
+                    int* chk = p.chunks + 4 * (brun + c);
+                    chk[0] = x;
+                    chk[1] = run + c * size;
+                    chk[2] = min(size, cnt - c * size);
+                    chk[3] = 0;
+                }
+                brun += pieces;
             }
             run += cnt;
-            crun += (cnt + ch - 1) / ch;
         }
         const int total = __shfl(inc, kWave - 1);
-        const int ctotal = __shfl(cinc, kWave - 1);
+        const int btotal = __shfl(binc, kWave - 1);
         if (lane == 0) {
             s_off[nx] = total;
             p.perm_off[nx] = total;
-            *p.n_chunks = ctotal;
-            *s_tot = ctotal;
+            p.n_chunks[0] = stotal;
+            p.n_chunks[1] = btotal;
+            *s_tot = stotal + btotal;
         }
     }
     __syncthreads();
