@@ -228,9 +228,9 @@ FfnParams make_ffn_params(const caee_layer_desc_t* d, const void* x, const int32
 }
 
 namespace {
-// A second stream per device and host thread, with the two events that fork
-// work onto it and join it back.  Created on first use, kept until the
-// process ends; default priority.
+// A second stream per device and host thread, with the events that fork work
+// onto it and join it back.  Created on first use,
+// kept until the process ends; default priority.
 struct SideStream {
     hipStream_t stream = nullptr;
     hipEvent_t fork = nullptr, join = nullptr;
@@ -253,86 +253,99 @@ caee_status_t side_stream(SideStream** out) {
     *out = &ss;
     return CAEE_OK;
 }
-}  // namespace
 
-caee_status_t run_ffn_products(const caee_layer_desc_t* d, const FfnParams& p0, const WsLayout& L, hipStream_t s) {
-    // Small chunks, then (when the batch can have any) big chunks; each launch
-    // is compiled for its own number of 16-token blocks.
-    const int nb_small = small_token_blocks(*d), nb_big = big_token_blocks(*d);
-    FfnParams ps = p0, pb = p0;
-    ps.list = 0;
-    pb.list = 1;
-    if (d->w_dtype == CAEE_FP8_E4M3) {
-        CAEE_TRY(timed_launch(CAEE_KERNEL_QUANT, s, "quantise x",
-                              [&] { return launch_quant_rows(p0.x, 1, d->T, d->d, p0.xq, p0.xs, s); }));
-        CAEE_TRY(timed_launch(CAEE_KERNEL_GATE_UP, s, "gate/up",
-                              [&] { return launch_gate_up_fp8(ps, nb_small, L.max_chunks, s); }));
-        if (nb_big)
-            CAEE_TRY(timed_launch(CAEE_KERNEL_GATE_UP, s, "gate/up",
-                                  [&] { return launch_gate_up_fp8(pb, nb_big, L.max_chunks, s); }));
-        CAEE_TRY(timed_launch(CAEE_KERNEL_QUANT, s, "quantise H",
-                              [&] { return launch_quant_rows(p0.h, 0, L.P, d->f, p0.hq, p0.hs, s); }));
-        CAEE_TRY(timed_launch(CAEE_KERNEL_DOWN, s, "down",
-                              [&] { return launch_down_fp8(ps, nb_small, L.max_chunks, s); }));
-        if (nb_big)
-            CAEE_TRY(timed_launch(CAEE_KERNEL_DOWN, s, "down",
-                                  [&] { return launch_down_fp8(pb, nb_big, L.max_chunks, s); }));
-        return CAEE_OK;
-    }
-    // The two chains touch disjoint rows of H and Y: the big chunks (few,
-    // long, latency-bound work items) run on a second stream next to the
-    // small ones (many, bandwidth-bound), then join back.
-    SideStream* ss = nullptr;
-    if (nb_big && kBigConcurrent) {
-        CAEE_TRY(side_stream(&ss));
-        hipError_t e = hipEventRecord(ss->fork, s);
-        if (e == hipSuccess) e = hipStreamWaitEvent(ss->stream, ss->fork, 0);
-        if (e != hipSuccess) return fail(CAEE_ERR_HIP, "fork to the side stream failed: %s", hipGetErrorString(e));
-    }
-    hipStream_t sb = ss ? ss->stream : s;
-    if (nb_big) {
-        CAEE_TRY(timed_launch(CAEE_KERNEL_GATE_UP, sb, "gate/up",
-                              [&] { return launch_gate_up(pb, d->w_dtype, nb_big, L.max_chunks, sb); }));
-        CAEE_TRY(timed_launch(CAEE_KERNEL_DOWN, sb, "down",
-                              [&] { return launch_down(pb, d->w_dtype, nb_big, L.max_chunks, sb); }));
-    }
-    CAEE_TRY(timed_launch(CAEE_KERNEL_GATE_UP, s, "gate/up",
-                          [&] { return launch_gate_up(ps, d->w_dtype, nb_small, L.max_chunks, s); }));
-    CAEE_TRY(timed_launch(CAEE_KERNEL_DOWN, s, "down",
-                          [&] { return launch_down(ps, d->w_dtype, nb_small, L.max_chunks, s); }));
-    if (ss) {
-        hipError_t e = hipEventRecord(ss->join, ss->stream);
-        if (e == hipSuccess) e = hipStreamWaitEvent(s, ss->join, 0);
-        if (e != hipSuccess) return fail(CAEE_ERR_HIP, "join from the side stream failed: %s", hipGetErrorString(e));
-    }
+caee_status_t order(hipEvent_t ev, hipStream_t from, hipStream_t to, const char* what) {
+    hipError_t e = hipEventRecord(ev, from);
+    if (e == hipSuccess) e = hipStreamWaitEvent(to, ev, 0);
+    if (e != hipSuccess) return fail(CAEE_ERR_HIP, "%s failed: %s", what, hipGetErrorString(e));
     return CAEE_OK;
 }
 
-caee_status_t run_combine(const FfnParams& p, hipStream_t s) {
-    return timed_launch(CAEE_KERNEL_COMBINE, s, "combine", [&] { return launch_combine(p, s); });
+caee_status_t gate_up_list(const caee_layer_desc_t* d, FfnParams p, int list, int nb, int max_chunks,
+                           hipStream_t s) {
+    p.list = list;
+    if (d->w_dtype == CAEE_FP8_E4M3)
+        return timed_launch(CAEE_KERNEL_GATE_UP, s, "gate/up", [&] { return launch_gate_up_fp8(p, nb, max_chunks, s); });
+    return timed_launch(CAEE_KERNEL_GATE_UP, s, "gate/up",
+                        [&] { return launch_gate_up(p, d->w_dtype, nb, max_chunks, s); });
 }
 
-caee_status_t run_route_layer(const caee_layer_desc_t* d, RouteParams& p, const caee_route_out_t* out, char* ws,
-                              const WsLayout& L, hipStream_t s) {
+caee_status_t down_list(const caee_layer_desc_t* d, FfnParams p, int list, int nb, int max_chunks, hipStream_t s) {
+    p.list = list;
+    if (d->w_dtype == CAEE_FP8_E4M3)
+        return timed_launch(CAEE_KERNEL_DOWN, s, "down", [&] { return launch_down_fp8(p, nb, max_chunks, s); });
+    return timed_launch(CAEE_KERNEL_DOWN, s, "down", [&] { return launch_down(p, d->w_dtype, nb, max_chunks, s); });
+}
+
+}  // namespace
+
+caee_status_t ffn_begin(const caee_layer_desc_t* d, const FfnParams& p, const WsLayout& L, hipStream_t s,
+                        FfnCall* call) {
+    (void)L;
+    *call = FfnCall{};
+    call->main = s;
+    call->side = s;
+    if (d->w_dtype == CAEE_FP8_E4M3)
+        CAEE_TRY(timed_launch(CAEE_KERNEL_QUANT, s, "quantise x",
+                              [&] { return launch_quant_rows(p.x, 1, d->T, d->d, p.xq, p.xs, s); }));
+    return CAEE_OK;
+}
+
+caee_status_t ffn_routed(const caee_layer_desc_t* d, const FfnParams& p, const WsLayout& L, FfnCall* call,
+                         bool big_on_side) {
+    const int nb_small = small_token_blocks(*d), nb_big = big_token_blocks(*d);
+    hipStream_t s = call->main;
+    if (d->w_dtype == CAEE_FP8_E4M3) {
+        CAEE_TRY(gate_up_list(d, p, 0, nb_small, L.max_chunks, s));
+        if (nb_big) CAEE_TRY(gate_up_list(d, p, 1, nb_big, L.max_chunks, s));
+        CAEE_TRY(timed_launch(CAEE_KERNEL_QUANT, s, "quantise H",
+                              [&] { return launch_quant_rows(p.h, 0, L.P, d->f, p.hq, p.hs, s); }));
+        CAEE_TRY(down_list(d, p, 0, nb_small, L.max_chunks, s));
+        if (nb_big) CAEE_TRY(down_list(d, p, 1, nb_big, L.max_chunks, s));
+        return CAEE_OK;
+    }
+    // The big chunks (few, long, latency-bound work items) run on a side
+    // stream next to the small ones (many, bandwidth-bound): disjoint rows.
+    hipStream_t sb = s;
+    if (nb_big && big_on_side && kBigConcurrent) {
+        if (call->side == s) {
+            SideStream* ss = nullptr;
+            CAEE_TRY(side_stream(&ss));
+            call->side = ss->stream;
+            call->ev_join = ss->join;
+            CAEE_TRY(order(ss->fork, s, ss->stream, "fork to the side stream"));
+        }
+        sb = call->side;
+    }
+    if (nb_big) {
+        CAEE_TRY(gate_up_list(d, p, 1, nb_big, L.max_chunks, sb));
+        CAEE_TRY(down_list(d, p, 1, nb_big, L.max_chunks, sb));
+    }
+    CAEE_TRY(gate_up_list(d, p, 0, nb_small, L.max_chunks, s));
+    return down_list(d, p, 0, nb_small, L.max_chunks, s);
+}
+
+caee_status_t ffn_end(const FfnParams& p, FfnCall* call) {
+    if (call->side != call->main) CAEE_TRY(order(call->ev_join, call->side, call->main, "join from the side stream"));
+    return timed_launch(CAEE_KERNEL_COMBINE, call->main, "combine", [&] { return launch_combine(p, call->main); });
+}
+
+void set_route_outputs(RouteParams& p, const caee_route_out_t* out, char* ws, const WsLayout& L) {
     p.topk_ids = out ? out->topk_ids : (int32_t*)(ws + L.ids);
     p.topk_w = out ? out->topk_w : (float*)(ws + L.w);
     if (out && out->orig_ids) p.orig_ids = out->orig_ids;
     p.masks = out ? out->masks : nullptr;
     p.stats = out ? out->stats : nullptr;
     p.bin_loads = out ? out->bin_loads : nullptr;
+}
+
+caee_status_t run_route_layer(const caee_layer_desc_t* d, RouteParams& p, const caee_route_out_t* out, char* ws,
+                              const WsLayout& L, hipStream_t s) {
+    set_route_outputs(p, out, ws, L);
     p.do_permute = 1;
     (void)d;
     return timed_launch(CAEE_KERNEL_ROUTE, s, "route", [&] { return launch_route(p, s); });
 }
-
-namespace {
-caee_status_t run_ffn(const caee_layer_desc_t* d, const void* x, const int32_t* ids, const float* w,
-                      const caee_expert_weights_t* W, void* y, char* ws, const WsLayout& L, hipStream_t s) {
-    const FfnParams p = make_ffn_params(d, x, ids, w, W, y, ws, L);
-    CAEE_TRY(run_ffn_products(d, p, L, s));
-    return run_combine(p, s);
-}
-}  // namespace
 
 int device_cu_count() {
     static int cached[64] = {};
@@ -399,8 +412,12 @@ caee_status_t caee_expert_ffn(const caee_layer_desc_t* desc, const void* x, cons
     p.topk_ids = const_cast<int32_t*>(topk_ids);
     p.do_permute = 1;
     hipStream_t s = as_stream(stream);
+    const FfnParams fp = make_ffn_params(desc, x, topk_ids, topk_w, weights, y, (char*)ws, L);
+    FfnCall call;
+    CAEE_TRY(ffn_begin(desc, fp, L, s, &call));
     CAEE_TRY(timed_launch(CAEE_KERNEL_ROUTE, s, "permute", [&] { return launch_permute(p, s); }));
-    return run_ffn(desc, x, topk_ids, topk_w, weights, y, (char*)ws, L, s);
+    CAEE_TRY(ffn_routed(desc, fp, L, &call, true));
+    return ffn_end(fp, &call);
 }
 
 caee_status_t caee_moe_layer(const caee_layer_desc_t* desc, const void* x, const float* logits, const float* bias,
@@ -419,8 +436,13 @@ caee_status_t caee_moe_layer(const caee_layer_desc_t* desc, const void* x, const
     char* wsb = (char*)ws;
     RouteParams p = make_route_params(desc, logits, bias, cost, bin, wsb, L);
     hipStream_t s = as_stream(stream);
+    set_route_outputs(p, out, wsb, L);
+    const FfnParams fp = make_ffn_params(desc, x, p.topk_ids, p.topk_w, weights, y, wsb, L);
+    FfnCall call;
+    CAEE_TRY(ffn_begin(desc, fp, L, s, &call));
     CAEE_TRY(run_route_layer(desc, p, out, wsb, L, s));
-    return run_ffn(desc, x, p.topk_ids, p.topk_w, weights, y, wsb, L, s);
+    CAEE_TRY(ffn_routed(desc, fp, L, &call, true));
+    return ffn_end(fp, &call);
 }
 
 caee_status_t caee_pack_matrix(int32_t w_dtype, const void* src, void* dst, int64_t rows, int64_t cols,

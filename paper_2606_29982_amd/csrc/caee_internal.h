@@ -228,7 +228,7 @@ struct FfnParams {
     const int32_t* perm_pos;
     const int32_t* chunks;
     const int32_t* n_chunks;
-    int list;       // 0: the small chunks, 1: the big chunks
+    int list;         // 0: the small chunks, 1: the big chunks
     const int32_t* topk_ids;
     const float* topk_w;
     void* h;
@@ -250,6 +250,41 @@ struct FfnParams {
     uint8_t* hq;
     float* hs;
 };
+
+// ---------------------------------------------------------------------------
+// FFN work items: chunk c of the list a launch runs (the small chunks are
+// listed first, then the big ones).
+struct ChunkRef {
+    int xs, row0, ntok;
+};
+
+__device__ inline int ffn_list_size(const FfnParams& p) { return p.n_chunks[p.list]; }
+
+__device__ inline ChunkRef ffn_chunk(const FfnParams& p, int c) {
+    const int32_t* ch = p.chunks + 4 * ((p.list ? p.n_chunks[0] : 0) + c);
+    return {ch[0], ch[1], ch[2]};
+}
+
+// Token of permuted row `row` (of expert slot xs).
+__device__ inline int ffn_token(const FfnParams& p, int xs, int row) {
+    (void)xs;
+    return p.perm_tok[row];
+}
+
+// Offload passes: only the chunks of experts in pass p.pass_id run.
+__device__ inline bool ffn_skip(const FfnParams& p, int xs) { return p.pass_of && p.pass_of[xs] != p.pass_id; }
+
+// First byte of matrix w13 (w2 = false) or w2 of expert slot xs.
+__device__ inline const char* ffn_weights(const FfnParams& p, int xs, bool w2, size_t expert_bytes) {
+    if (xs >= p.E) return (const char*)(w2 ? p.sh_w2 : p.sh_w13) + (size_t)(xs - p.E) * expert_bytes;
+    if (p.wtab) return (const char*)p.wtab[2 * xs + (w2 ? 1 : 0)];
+    return (const char*)(w2 ? p.w2 : p.w13) + (size_t)xs * expert_bytes;
+}
+
+__device__ inline const float* ffn_scales(const FfnParams& p, int xs, bool w2, size_t per_expert) {
+    if (xs >= p.E) return (w2 ? p.sh_w2_scale : p.sh_w13_scale) + (size_t)(xs - p.E) * per_expert;
+    return (w2 ? p.w2_scale : p.w13_scale) + (size_t)xs * per_expert;
+}
 
 // Host-side launchers (defined next to their kernels).
 hipError_t launch_route(const RouteParams& p, hipStream_t s);
@@ -283,10 +318,23 @@ FfnParams make_ffn_params(const caee_layer_desc_t* d, const void* x, const int32
 // routing results go to `out` when given, else to the workspace.
 caee_status_t run_route_layer(const caee_layer_desc_t* d, RouteParams& p, const caee_route_out_t* out, char* ws,
                               const WsLayout& L, hipStream_t s);
-// Gate/up and down products of every chunk (or, with p.pass_of set, of the
-// chunks of pass p.pass_id), then optionally the combine.
-caee_status_t run_ffn_products(const caee_layer_desc_t* d, const FfnParams& p, const WsLayout& L, hipStream_t s);
-caee_status_t run_combine(const FfnParams& p, hipStream_t s);
+void set_route_outputs(RouteParams& p, const caee_route_out_t* out, char* ws, const WsLayout& L);
+
+// The FFN of one layer call, in three parts:
+//   ffn_begin   (fp8) quantises x;
+//   ffn_routed  after the permutation, runs the small chunks on the main
+//               stream and (big_on_side) the big chunks on a side stream
+//               forked from it; with p.pass_of set only pass p.pass_id runs;
+//   ffn_end     joins the side stream and combines into y.
+struct FfnCall {
+    hipStream_t main = nullptr, side = nullptr;   // side == main until forked
+    hipEvent_t ev_join = nullptr;
+};
+caee_status_t ffn_begin(const caee_layer_desc_t* d, const FfnParams& p, const WsLayout& L, hipStream_t s,
+                        FfnCall* call);
+caee_status_t ffn_routed(const caee_layer_desc_t* d, const FfnParams& p, const WsLayout& L, FfnCall* call,
+                         bool big_on_side);
+caee_status_t ffn_end(const FfnParams& p, FfnCall* call);
 
 // Opt-in timing: events bracket each launch on the caller's stream.
 struct TimingRec {

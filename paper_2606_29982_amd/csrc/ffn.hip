@@ -50,12 +50,6 @@ __device__ inline uint32_t bf16_rne(float v) {
 
 __device__ inline float silu_mul(float g, float u) { return g / (1.0f + __expf(-g)) * u; }
 
-__device__ inline const char* expert_base(const void* routed, const void* shared, int x, int E,
-                                          size_t expert_bytes) {
-    return x < E ? (const char*)routed + (size_t)x * expert_bytes
-                 : (const char*)shared + (size_t)(x - E) * expert_bytes;
-}
-
 // Contraction of one 16-row weight tile against up to NB 16-token blocks,
 // over `nsteps` k-steps starting at the given pointers.  Weights are loaded
 // U steps ahead of the MFMAs that consume them (register double buffer).
@@ -132,8 +126,7 @@ __global__ CAEE_FFN_BOUNDS void k_gate_up(FfnParams p) {
     const int wave = threadIdx.x / kWave;
     const int r = lane & 15, g = lane >> 4;
     const int tiles = p.f / 16;
-    const int n_chunks = p.n_chunks[p.list];
-    const int32_t* chunks = p.chunks + (p.list ? 4 * p.n_chunks[0] : 0);
+    const int n_chunks = ffn_list_size(p);
     const int S = gate_up_split_for(n_chunks, tiles, p.ksplit);
     const int tiles_per_item = kWaves / S;
     const int items_per_chunk = tiles / tiles_per_item;
@@ -146,12 +139,12 @@ __global__ CAEE_FFN_BOUNDS void k_gate_up(FfnParams p) {
     for (int item = blockIdx.x; item < total; item += gridDim.x) {
         const int c = item / items_per_chunk;
         const int jt = (item - c * items_per_chunk) * tiles_per_item + wave / S;
-        const int xs = chunks[4 * c], row0 = chunks[4 * c + 1], ntok = chunks[4 * c + 2];
-        if (p.pass_of && p.pass_of[xs] != p.pass_id) continue;   // uniform over the workgroup
+        const ChunkRef ck = ffn_chunk(p, c);
+        const int xs = ck.xs, row0 = ck.row0, ntok = ck.ntok;
+        if (ffn_skip(p, xs)) continue;   // uniform over the workgroup
         const int nb = (ntok + 15) >> 4;
         const size_t k0 = (size_t)4 * sp * kper;
-        const u32x4_t* wb = (const u32x4_t*)(p.wtab ? (const char*)p.wtab[2 * xs]
-                                                    : expert_base(p.w13, p.sh_w13, xs, p.E, expert_bytes));
+        const u32x4_t* wb = (const u32x4_t*)ffn_weights(p, xs, false, expert_bytes);
         const size_t ksteps = row_units / 4;
         // Tiled: block (tile, step) is 64 consecutive 16-byte pieces, one per lane.
         const u32x4_t* const a[2] = {
@@ -165,7 +158,7 @@ __global__ CAEE_FFN_BOUNDS void k_gate_up(FfnParams p) {
         for (int tb = 0; tb < NB; ++tb) {
             int n = tb * 16 + r;
             n = (tb < nb && n < ntok) ? n : 0;   // padded token columns read a valid row; results dropped
-            xb[tb] = (const u32x4_t*)p.x + (size_t)p.perm_tok[row0 + n] * row_units + g + k0;
+            xb[tb] = (const u32x4_t*)p.x + (size_t)ffn_token(p, xs, row0 + n) * row_units + g + k0;
         }
         f32x4_t acc[2][NB];
 #pragma unroll
@@ -217,8 +210,7 @@ __global__ CAEE_FFN_BOUNDS void k_down(FfnParams p) {
     const int gw = blockIdx.x * (kFfnThreads / kWave) + (threadIdx.x / kWave);
     const int nw = gridDim.x * (kFfnThreads / kWave);
     const int tiles = p.d / 16;
-    const int n_chunks = p.n_chunks[p.list];
-    const int32_t* chunks = p.chunks + (p.list ? 4 * p.n_chunks[0] : 0);
+    const int n_chunks = ffn_list_size(p);
     const int total = n_chunks * tiles;
     const size_t row_units = (size_t)p.f * M::kElemBytes / 16;
     const int ksteps = (int)(row_units / 4);
@@ -226,11 +218,11 @@ __global__ CAEE_FFN_BOUNDS void k_down(FfnParams p) {
 
     for (int item = gw; item < total; item += nw) {
         const int c = item / tiles, it = item - c * tiles;
-        const int xs = chunks[4 * c], row0 = chunks[4 * c + 1], ntok = chunks[4 * c + 2];
-        if (p.pass_of && p.pass_of[xs] != p.pass_id) continue;
+        const ChunkRef ck = ffn_chunk(p, c);
+        const int xs = ck.xs, row0 = ck.row0, ntok = ck.ntok;
+        if (ffn_skip(p, xs)) continue;
         const int nb = (ntok + 15) >> 4;
-        const u32x4_t* wb = (const u32x4_t*)(p.wtab ? (const char*)p.wtab[2 * xs + 1]
-                                                    : expert_base(p.w2, p.sh_w2, xs, p.E, expert_bytes));
+        const u32x4_t* wb = (const u32x4_t*)ffn_weights(p, xs, true, expert_bytes);
         const u32x4_t* const a[1] = {p.tiled ? wb + (size_t)it * ksteps * 64 + lane
                                              : wb + (size_t)(it * 16 + r) * row_units + g};
         const int astep = p.tiled ? 64 : 4;
@@ -355,8 +347,7 @@ __global__ __launch_bounds__(kFfnThreads) void k_gate_up_big(FfnParams p) {
     __shared__ u32x4_t s_b[2][NB][U][kWave];
     const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
     const int r = lane & 15, g = lane >> 4;
-    const int n_chunks = p.n_chunks[p.list];
-    const int32_t* chunks = p.chunks + (p.list ? 4 * p.n_chunks[0] : 0);
+    const int n_chunks = ffn_list_size(p);
     const int tiles = p.f / 16;
     const int items_per_chunk = tiles / kWaves;
     const int total = n_chunks * items_per_chunk;
@@ -366,11 +357,11 @@ __global__ __launch_bounds__(kFfnThreads) void k_gate_up_big(FfnParams p) {
     for (int item = blockIdx.x; item < total; item += gridDim.x) {
         const int c = item / items_per_chunk;
         const int jt = (item - c * items_per_chunk) * kWaves + wave;
-        const int xs = chunks[4 * c], row0 = chunks[4 * c + 1], ntok = chunks[4 * c + 2];
-        if (p.pass_of && p.pass_of[xs] != p.pass_id) continue;   // uniform over the workgroup
+        const ChunkRef ck = ffn_chunk(p, c);
+        const int xs = ck.xs, row0 = ck.row0, ntok = ck.ntok;
+        if (ffn_skip(p, xs)) continue;   // uniform over the workgroup
         const int nb = (ntok + 15) >> 4;
-        const u32x4_t* wb = (const u32x4_t*)(p.wtab ? (const char*)p.wtab[2 * xs]
-                                                    : expert_base(p.w13, p.sh_w13, xs, p.E, expert_bytes));
+        const u32x4_t* wb = (const u32x4_t*)ffn_weights(p, xs, false, expert_bytes);
         const u32x4_t* const a[2] = {
             p.tiled ? wb + (size_t)jt * ksteps * 64 + lane : wb + (size_t)(jt * 16 + r) * row_units + g,
             p.tiled ? wb + (size_t)(tiles + jt) * ksteps * 64 + lane
@@ -380,7 +371,7 @@ __global__ __launch_bounds__(kFfnThreads) void k_gate_up_big(FfnParams p) {
         for (int j = 0; j < NB; ++j) {
             int n = (tid >> 4) + 16 * j;
             n = n < ntok ? n : 0;   // padded token columns read a valid row; results dropped
-            rows[j] = (const u32x4_t*)p.x + (size_t)p.perm_tok[row0 + n] * row_units;
+            rows[j] = (const u32x4_t*)p.x + (size_t)ffn_token(p, xs, row0 + n) * row_units;
         }
         f32x4_t acc[2][NB];
 #pragma unroll
@@ -411,8 +402,7 @@ __global__ __launch_bounds__(kFfnThreads) void k_down_big(FfnParams p) {
     __shared__ u32x4_t s_b[2][NB][U][kWave];
     const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
     const int r = lane & 15, g = lane >> 4;
-    const int n_chunks = p.n_chunks[p.list];
-    const int32_t* chunks = p.chunks + (p.list ? 4 * p.n_chunks[0] : 0);
+    const int n_chunks = ffn_list_size(p);
     const int tiles = p.d / 16;
     const int items_per_chunk = tiles / (kWaves * kTW);
     const int total = n_chunks * items_per_chunk;
@@ -422,11 +412,11 @@ __global__ __launch_bounds__(kFfnThreads) void k_down_big(FfnParams p) {
     for (int item = blockIdx.x; item < total; item += gridDim.x) {
         const int c = item / items_per_chunk;
         const int it0 = ((item - c * items_per_chunk) * kWaves + wave) * kTW;
-        const int xs = chunks[4 * c], row0 = chunks[4 * c + 1], ntok = chunks[4 * c + 2];
-        if (p.pass_of && p.pass_of[xs] != p.pass_id) continue;
+        const ChunkRef ck = ffn_chunk(p, c);
+        const int xs = ck.xs, row0 = ck.row0, ntok = ck.ntok;
+        if (ffn_skip(p, xs)) continue;
         const int nb = (ntok + 15) >> 4;
-        const u32x4_t* wb = (const u32x4_t*)(p.wtab ? (const char*)p.wtab[2 * xs + 1]
-                                                    : expert_base(p.w2, p.sh_w2, xs, p.E, expert_bytes));
+        const u32x4_t* wb = (const u32x4_t*)ffn_weights(p, xs, true, expert_bytes);
         const u32x4_t* a[kTW];
 #pragma unroll
         for (int m = 0; m < kTW; ++m)
@@ -558,7 +548,7 @@ hipError_t launch_big(const FfnParams& p, bool gate_up, int nb, dim3 grid, hipSt
 }  // namespace
 
 hipError_t launch_gate_up(const FfnParams& p, int w_dtype, int nb, int max_chunks, hipStream_t s) {
-    if (p.list == 1 && kBigStaged) {
+    if (nb >= 4 && kBigStaged) {
         const dim3 grid(grid_for((long long)max_chunks * (p.f / 16)));
         if (w_dtype == CAEE_BF16) return launch_big<Bf16Math>(p, true, nb, grid, s);
         if (w_dtype == CAEE_F32) return launch_big<F32Math>(p, true, nb, grid, s);
@@ -571,7 +561,7 @@ hipError_t launch_gate_up(const FfnParams& p, int w_dtype, int nb, int max_chunk
 }
 
 hipError_t launch_down(const FfnParams& p, int w_dtype, int nb, int max_chunks, hipStream_t s) {
-    if (p.list == 1 && kBigStaged) {
+    if (nb >= 4 && kBigStaged) {
         const dim3 grid(grid_for((long long)max_chunks * (p.d / 16) / 2));
         if (w_dtype == CAEE_BF16) return launch_big<Bf16Math>(p, false, nb, grid, s);
         if (w_dtype == CAEE_F32) return launch_big<F32Math>(p, false, nb, grid, s);

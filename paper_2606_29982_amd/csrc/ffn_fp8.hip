@@ -77,12 +77,6 @@ __device__ inline i32x8_t join(const u32x4_t& lo, const u32x4_t& hi) {
     return i32x8_t{(int)lo[0], (int)lo[1], (int)lo[2], (int)lo[3], (int)hi[0], (int)hi[1], (int)hi[2], (int)hi[3]};
 }
 
-__device__ inline const char* expert_base(const void* routed, const void* shared, int x, int E,
-                                          size_t expert_bytes) {
-    return x < E ? (const char*)routed + (size_t)x * expert_bytes
-                 : (const char*)shared + (size_t)(x - E) * expert_bytes;
-}
-
 // Contraction of one 16-row tile against up to NB 16-token blocks over
 // `nblocks` 128-wide blocks.  a[m]: this lane's first weight piece (the two
 // pieces of a block are `astep` apart, blocks 2*astep apart); b[tb]: the
@@ -162,8 +156,7 @@ __global__ __launch_bounds__(kFfnThreads) void k_gate_up_fp8(FfnParams p) {
     const int wave = threadIdx.x / kWave;
     const int r = lane & 15, g = lane >> 4;
     const int tiles = p.f / 16;
-    const int n_chunks = p.n_chunks[p.list];
-    const int32_t* chunks = p.chunks + (p.list ? 4 * p.n_chunks[0] : 0);
+    const int n_chunks = ffn_list_size(p);
     const int S = gate_up_split_for(n_chunks, tiles, p.ksplit);
     const int tiles_per_item = kWaves / S;
     const int items_per_chunk = tiles / tiles_per_item;
@@ -179,18 +172,18 @@ __global__ __launch_bounds__(kFfnThreads) void k_gate_up_fp8(FfnParams p) {
     for (int item = blockIdx.x; item < total; item += gridDim.x) {
         const int c = item / items_per_chunk;
         const int jt = (item - c * items_per_chunk) * tiles_per_item + wave / S;
-        const int xs_ = chunks[4 * c], row0 = chunks[4 * c + 1], ntok = chunks[4 * c + 2];
+        const ChunkRef ck = ffn_chunk(p, c);
+        const int xs_ = ck.xs, row0 = ck.row0, ntok = ck.ntok;
         const int nb = (ntok + 15) >> 4;
         const int kb0 = sp * kper;
-        const u32x4_t* wb = (const u32x4_t*)expert_base(p.w13, p.sh_w13, xs_, p.E, expert_bytes);
+        const u32x4_t* wb = (const u32x4_t*)ffn_weights(p, xs_, false, expert_bytes);
         const u32x4_t* const a[2] = {
             p.tiled ? wb + ((size_t)jt * ksteps + 2 * (size_t)kb0) * 64 + lane
                     : wb + (size_t)(jt * 16 + r) * row_units + g + 8 * (size_t)kb0,
             p.tiled ? wb + ((size_t)(tiles + jt) * ksteps + 2 * (size_t)kb0) * 64 + lane
                     : wb + (size_t)(p.f + jt * 16 + r) * row_units + g + 8 * (size_t)kb0};
         const int astep = p.tiled ? 64 : 4;
-        const float* sbase = xs_ < p.E ? p.w13_scale + (size_t)xs_ * (2 * p.f / 128) * sblk
-                                       : p.sh_w13_scale + (size_t)(xs_ - p.E) * (2 * p.f / 128) * sblk;
+        const float* sbase = ffn_scales(p, xs_, false, (size_t)(2 * p.f / 128) * sblk);
         const float* const wsc[2] = {sbase + (size_t)((jt * 16) / 128) * sblk + kb0,
                                      sbase + (size_t)((p.f + jt * 16) / 128) * sblk + kb0};
         const u32x4_t* xb[NB];
@@ -199,7 +192,7 @@ __global__ __launch_bounds__(kFfnThreads) void k_gate_up_fp8(FfnParams p) {
         for (int tb = 0; tb < NB; ++tb) {
             int n = tb * 16 + r;
             n = (tb < nb && n < ntok) ? n : 0;   // padded token columns read a valid row; results dropped
-            const int tok = p.perm_tok[row0 + n];
+            const int tok = ffn_token(p, xs_, row0 + n);
             xb[tb] = (const u32x4_t*)p.xq + (size_t)tok * row_units + g + 8 * (size_t)kb0;
             xsc[tb] = p.xs + (size_t)tok * sblk + kb0;
         }
@@ -252,8 +245,7 @@ __global__ __launch_bounds__(kFfnThreads) void k_down_fp8(FfnParams p) {
     const int gw = blockIdx.x * (kFfnThreads / kWave) + (threadIdx.x / kWave);
     const int nw = gridDim.x * (kFfnThreads / kWave);
     const int tiles = p.d / 16;
-    const int n_chunks = p.n_chunks[p.list];
-    const int32_t* chunks = p.chunks + (p.list ? 4 * p.n_chunks[0] : 0);
+    const int n_chunks = ffn_list_size(p);
     const int total = n_chunks * tiles;
     const size_t row_units = (size_t)p.f / 16;
     const size_t ksteps = row_units / 4;
@@ -263,14 +255,14 @@ __global__ __launch_bounds__(kFfnThreads) void k_down_fp8(FfnParams p) {
 
     for (int item = gw; item < total; item += nw) {
         const int c = item / tiles, it = item - c * tiles;
-        const int xs_ = chunks[4 * c], row0 = chunks[4 * c + 1], ntok = chunks[4 * c + 2];
+        const ChunkRef ck = ffn_chunk(p, c);
+        const int xs_ = ck.xs, row0 = ck.row0, ntok = ck.ntok;
         const int nb = (ntok + 15) >> 4;
-        const u32x4_t* wb = (const u32x4_t*)expert_base(p.w2, p.sh_w2, xs_, p.E, expert_bytes);
+        const u32x4_t* wb = (const u32x4_t*)ffn_weights(p, xs_, true, expert_bytes);
         const u32x4_t* const a[1] = {p.tiled ? wb + (size_t)it * ksteps * 64 + lane
                                              : wb + (size_t)(it * 16 + r) * row_units + g};
         const int astep = p.tiled ? 64 : 4;
-        const float* sbase = xs_ < p.E ? p.w2_scale + (size_t)xs_ * (p.d / 128) * sblk
-                                       : p.sh_w2_scale + (size_t)(xs_ - p.E) * (p.d / 128) * sblk;
+        const float* sbase = ffn_scales(p, xs_, true, (size_t)(p.d / 128) * sblk);
         const float* const wsc[1] = {sbase + (size_t)((it * 16) / 128) * sblk};
         const u32x4_t* hb[NB];
         const float* hsc[NB];

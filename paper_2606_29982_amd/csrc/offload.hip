@@ -310,30 +310,49 @@ caee_status_t caee_offload_layer(caee_offload_t* h, const caee_layer_desc_t* des
     for (int e = 0; e < E; ++e) hcost[e] = h->slot_of[e] >= 0 ? 0.0f : h->miss_cost;
     HIP_TRY(hipMemcpyAsync(h->dev_tab, hcost, (size_t)E * 4, hipMemcpyHostToDevice, s), "cost table copy");
     RouteParams rp = make_route_params(desc, logits, bias, (const float*)h->dev_tab, nullptr, wsb, L);
-    CAEE_TRY(run_route_layer(desc, rp, out, wsb, L, s));
+    set_route_outputs(rp, out, wsb, L);
+    FfnParams fp = make_ffn_params(desc, x, rp.topk_ids, rp.topk_w, nullptr, y, wsb, L);
+    fp.sh_w13 = h->sh_w13;
+    fp.sh_w2 = h->sh_w2;
+    fp.tiled = h->layout == CAEE_LAYOUT_TILED;
+    fp.wtab = (const void* const*)(h->dev_tab + h->off_wtab);
+    fp.pass_of = (const int32_t*)(h->dev_tab + h->off_pass);
+    fp.pass_id = 0;
+    FfnCall fc;
+    CAEE_TRY(ffn_begin(desc, fp, L, s, &fc));
+    // Any return below must first bring the side stream back into `stream`.
+    auto joined = [&](caee_status_t st) {
+        if (fc.side != fc.main && hipEventRecord(fc.ev_join, fc.side) == hipSuccess)
+            (void)hipStreamWaitEvent(fc.main, fc.ev_join, 0);
+        return st;
+    };
+    caee_status_t st = run_route_layer(desc, rp, out, wsb, L, s);
+    if (st != CAEE_OK) return joined(st);
     // 2. read A_trans back.
-    HIP_TRY(hipMemcpyAsync(h->host_trans, wsb + L.trans, E, hipMemcpyDeviceToHost, s), "A_trans read-back");
-    HIP_TRY(hipEventRecord(h->ev_route, s), "hipEventRecord");
-    HIP_TRY(hipEventSynchronize(h->ev_route), "hipEventSynchronize");
+    hipError_t he = hipMemcpyAsync(h->host_trans, wsb + L.trans, E, hipMemcpyDeviceToHost, s);
+    if (he == hipSuccess) he = hipEventRecord(h->ev_route, s);
+    if (he == hipSuccess) he = hipEventSynchronize(h->ev_route);
+    if (he != hipSuccess) return joined(hip_fail(he, "A_trans read-back"));
 
     // 3. plan.
     std::vector<int32_t> fetch(E), fetch_slot(E);
     int32_t counts[4];
     const int64_t call = h->call;
-    CAEE_TRY(lru_plan(E, h->n_cache, h->n_stage, h->slot_of.data(), h->slot_expert.data(), h->slot_used.data(), call,
-                      h->host_trans, fetch.data(), fetch_slot.data(), counts));
+    st = lru_plan(E, h->n_cache, h->n_stage, h->slot_of.data(), h->slot_expert.data(), h->slot_used.data(), call,
+                  h->host_trans, fetch.data(), fetch_slot.data(), counts);
+    if (st != CAEE_OK) return joined(st);
     const int misses = counts[1], staged = counts[2];
     const int batch = staged > 0 ? std::min(h->fetch_batch, h->n_stage) : h->fetch_batch;
     const int n_batches = (misses + batch - 1) / batch;
     // Undo the residency of this call's cached misses if anything below fails.
-    auto rollback = [&](caee_status_t st) {
+    auto rollback = [&](caee_status_t st_) {
         for (int i = 0; i < misses - staged; ++i) {
             const int sl = fetch_slot[i];
             h->slot_of[fetch[i]] = -1;
             h->slot_expert[sl] = -1;
             h->slot_used[sl] = -1;
         }
-        return st;
+        return joined(st_);
     };
 
     // Tables: weight addresses and the pass of every expert slot.
@@ -359,8 +378,8 @@ caee_status_t caee_offload_layer(caee_offload_t* h, const caee_layer_desc_t* des
     (void)X;
     if (ensure_events(h->ev_fetch, n_batches) != CAEE_OK || ensure_events(h->ev_pass, n_batches + 1) != CAEE_OK)
         return rollback(CAEE_ERR_HIP);
-    hipError_t he = hipMemcpyAsync(h->dev_tab + h->off_wtab, h->host_tab + h->off_wtab, h->tab_bytes - h->off_wtab,
-                                   hipMemcpyHostToDevice, s);
+    he = hipMemcpyAsync(h->dev_tab + h->off_wtab, h->host_tab + h->off_wtab, h->tab_bytes - h->off_wtab,
+                        hipMemcpyHostToDevice, s);
     if (he != hipSuccess) return rollback(hip_fail(he, "table copy"));
 
     // 4. copies and FFN passes.  Slots overwritten here were last read by an
@@ -369,12 +388,7 @@ caee_status_t caee_offload_layer(caee_offload_t* h, const caee_layer_desc_t* des
         he = hipStreamWaitEvent(cs, h->ev_done, 0);
         if (he != hipSuccess) return rollback(hip_fail(he, "hipStreamWaitEvent"));
     }
-    FfnParams fp = make_ffn_params(desc, x, rp.topk_ids, rp.topk_w, nullptr, y, wsb, L);
-    fp.tiled = h->layout == CAEE_LAYOUT_TILED;
-    fp.wtab = (const void* const*)(h->dev_tab + h->off_wtab);
-    fp.pass_of = (const int32_t*)(h->dev_tab + h->off_pass);
-    fp.pass_id = 0;
-    caee_status_t st = run_ffn_products(desc, fp, L, s);
+    st = ffn_routed(desc, fp, L, &fc, false);
     if (st != CAEE_OK) return rollback(st);
     const int cached = misses - staged;
     for (int b = 0; b < n_batches; ++b) {
@@ -397,13 +411,13 @@ caee_status_t caee_offload_layer(caee_offload_t* h, const caee_layer_desc_t* des
         if (he == hipSuccess) he = hipStreamWaitEvent(s, h->ev_fetch[b], 0);
         if (he != hipSuccess) return rollback(hip_fail(he, "fetch event"));
         fp.pass_id = 1 + b;
-        st = run_ffn_products(desc, fp, L, s);
+        st = ffn_routed(desc, fp, L, &fc, false);
         if (st != CAEE_OK) return rollback(st);
         he = hipEventRecord(h->ev_pass[1 + b], s);
         if (he != hipSuccess) return rollback(hip_fail(he, "pass event"));
     }
-    // 5. combine.
-    st = run_combine(fp, s);
+    // 5. join and combine.
+    st = ffn_end(fp, &fc);
     if (st != CAEE_OK) return rollback(st);
     he = hipEventRecord(h->ev_done, s);
     if (he != hipSuccess) return rollback(hip_fail(he, "hipEventRecord"));
