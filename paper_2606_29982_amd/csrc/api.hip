@@ -173,6 +173,7 @@ RouteParams make_route_params(const caee_layer_desc_t* d, const float* logits, c
     p.perm_off = (int32_t*)(ws + L.perm_off);
     p.perm_tok = (int32_t*)(ws + L.perm_tok);
     p.perm_pos = (int32_t*)(ws + L.perm_pos);
+    p.perm_blk = (int32_t*)(ws + L.perm_blk);
     p.chunks = (int32_t*)(ws + L.chunks);
     p.n_chunks = (int32_t*)(ws + L.n_chunks);
     p.gbuf = (double*)(ws + L.gbuf);
@@ -295,15 +296,6 @@ caee_status_t ffn_routed(const caee_layer_desc_t* d, const FfnParams& p, const W
                          bool big_on_side) {
     const int nb_small = small_token_blocks(*d), nb_big = big_token_blocks(*d);
     hipStream_t s = call->main;
-    if (d->w_dtype == CAEE_FP8_E4M3) {
-        CAEE_TRY(gate_up_list(d, p, 0, nb_small, L.max_chunks, s));
-        if (nb_big) CAEE_TRY(gate_up_list(d, p, 1, nb_big, L.max_chunks, s));
-        CAEE_TRY(timed_launch(CAEE_KERNEL_QUANT, s, "quantise H",
-                              [&] { return launch_quant_rows(p.h, 0, L.P, d->f, p.hq, p.hs, s); }));
-        CAEE_TRY(down_list(d, p, 0, nb_small, L.max_chunks, s));
-        if (nb_big) CAEE_TRY(down_list(d, p, 1, nb_big, L.max_chunks, s));
-        return CAEE_OK;
-    }
     // The big chunks (few, long, latency-bound work items) run on a side
     // stream next to the small ones (many, bandwidth-bound): disjoint rows.
     hipStream_t sb = s;
@@ -317,12 +309,19 @@ caee_status_t ffn_routed(const caee_layer_desc_t* d, const FfnParams& p, const W
         }
         sb = call->side;
     }
-    if (nb_big) {
-        CAEE_TRY(gate_up_list(d, p, 1, nb_big, L.max_chunks, sb));
-        CAEE_TRY(down_list(d, p, 1, nb_big, L.max_chunks, sb));
-    }
-    CAEE_TRY(gate_up_list(d, p, 0, nb_small, L.max_chunks, s));
-    return down_list(d, p, 0, nb_small, L.max_chunks, s);
+    // One list's chain: gate/up, (fp8) quantisation of its SwiGLU rows, down.
+    auto chain = [&](int list, int nb, hipStream_t st) -> caee_status_t {
+        CAEE_TRY(gate_up_list(d, p, list, nb, L.max_chunks, st));
+        if (d->w_dtype == CAEE_FP8_E4M3) {
+            FfnParams q = p;
+            q.list = list;
+            CAEE_TRY(timed_launch(CAEE_KERNEL_QUANT, st, "quantise H",
+                                  [&] { return launch_quant_list(q, nb, L.max_chunks, st); }));
+        }
+        return down_list(d, p, list, nb, L.max_chunks, st);
+    };
+    if (nb_big) CAEE_TRY(chain(1, nb_big, sb));
+    return chain(0, nb_small, s);
 }
 
 caee_status_t ffn_end(const FfnParams& p, FfnCall* call) {

@@ -19,6 +19,7 @@ constexpr int kMaxK = 16;
 constexpr int kMaxShared = 4;
 constexpr int kMaxBins = 256;
 constexpr int kMaxT = 65536;        // tokens per call
+constexpr int kMaskT = 1024;        // token block of the permutation (one LDS bitmask per expert)
 constexpr int kRouteThreads = 1024;
 // 16-token MFMA column blocks one FFN work item can hold (1, 2, 4 or 8).
 #ifndef CAEE_MAX_TOKEN_BLOCKS
@@ -42,9 +43,7 @@ constexpr long long kTargetItems = CAEE_TARGET_ITEMS;
 #endif
 constexpr int kGateUpU = CAEE_GATE_UP_U;
 constexpr int kDownU = CAEE_DOWN_U;
-// Big chunks: contraction steps staged in LDS per stage, and whether the
-// LDS-staged kernels run them (0: the direct kernels, compiled for 128 rows).
-constexpr int kBigU = 4;
+// Whether the LDS-staged kernels run the big chunks (0: the direct kernels).
 #ifndef CAEE_BIG_STAGED
 #define CAEE_BIG_STAGED 1
 #endif
@@ -78,6 +77,7 @@ struct WsLayout {
     size_t perm_off;            // [E + n_shared + 1] first permuted row of each expert slot
     size_t perm_tok;            // [P] token of each permuted row
     size_t perm_pos;            // [T][k + n_shared] permuted row of each (token, slot), -1 unused
+    size_t perm_blk;            // [ceil(T / kMaskT)][E] per token block: expert counts, then first rows
     size_t chunks;              // [max_chunks][4] (expert slot, first row, rows, 0): small chunks, then big
     size_t n_chunks;            // [2] small and big chunk counts
     size_t h;                   // [P][f] SwiGLU activations (weight dtype; fp32 for fp8)
@@ -161,6 +161,7 @@ inline WsLayout ws_layout(const caee_layer_desc_t& d) {
     L.perm_off = take(size_t(d.E + d.n_shared + 1) * 4);
     L.perm_tok = take(size_t(L.P) * 4);
     L.perm_pos = take(T * slots * 4);
+    L.perm_blk = take(((T + kMaskT - 1) / kMaskT) * size_t(d.E) * 4);
     L.chunks = take(size_t(L.max_chunks) * 16);
     L.n_chunks = take(16);
     const int h_bytes = d.w_dtype == CAEE_FP8_E4M3 ? 4 : elem_bytes(d.w_dtype);
@@ -208,6 +209,7 @@ struct RouteParams {
     int32_t* perm_off;
     int32_t* perm_tok;
     int32_t* perm_pos;
+    int32_t* perm_blk;
     int32_t* chunks;
     int32_t* n_chunks;
     int do_permute;     // 0: the permutation kernel only reports the refill/empty-slot counts
@@ -295,6 +297,7 @@ hipError_t launch_combine(const FfnParams& p, hipStream_t s);
 hipError_t launch_quant_rows(const void* src, int src_bf16, long long rows, int cols, uint8_t* q, float* scale,
                              hipStream_t s);
 hipError_t launch_gate_up_fp8(const FfnParams& p, int nb, int max_chunks, hipStream_t s);
+hipError_t launch_quant_list(const FfnParams& p, int nb, int max_chunks, hipStream_t s);
 hipError_t launch_down_fp8(const FfnParams& p, int nb, int max_chunks, hipStream_t s);
 hipError_t launch_pack(const void* src, void* dst, long long rows, long long row_units, long long count,
                        hipStream_t s);

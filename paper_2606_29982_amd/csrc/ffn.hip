@@ -16,13 +16,13 @@
 //   down:    Y[row][i] = W2[i] . H[row]                   (fp32)
 //   combine: y[t] = sum_j w[t][j] Y[pos(t,j)] + sum_s Y[pos(t,k+s)]
 #include "caee_internal.h"
+#include "ffn_stage.h"
 
 namespace caee {
 namespace {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 // One 16-byte load per lane = one contraction step of the 16x16 MFMA tile.
 struct Bf16Math {
@@ -259,57 +259,32 @@ __global__ CAEE_FFN_BOUNDS void k_down(FfnParams p) {
 // the B fragment of lane l (token 16*tb + l%16, bytes 16*(l/16) of the step),
 // so every fragment read is one conflict-free 16-byte LDS load.
 
-// Staging of one stage: thread `tid` moves 16-byte piece q = tid % (4U) of
-// token (tid / (4U)) + (256 / 4U) * j for j < NB * 4U / 16 ... written for the
-// case 4U == 16 (U = 4): token tid/16 + 16 j is block j, lane tid/16 + 16 (q%4),
-// step q/4.
-template <int U, int NB>
-struct BigStage {
-    static_assert(U == 4, "staging map assumes 16 pieces per token and stage");
-    static constexpr int kPer = NB;                 // pieces per thread per stage
-    const u32x4_t* src[NB];                         // this thread's token rows (+ its piece)
-    int q;
-    __device__ inline void init(const u32x4_t* const (&rows)[NB], int tid) {
-        q = tid & 15;
-#pragma unroll
-        for (int j = 0; j < NB; ++j) src[j] = rows[j] + q;
-    }
-    __device__ inline void load(u32x4_t (&v)[NB], int kb, int nb) const {
-#pragma unroll
-        for (int j = 0; j < NB; ++j)
-            if (j < nb) v[j] = src[j][(size_t)kb * (4 * U)];
-    }
-    __device__ inline void store(u32x4_t (*sb)[U][kWave], const u32x4_t (&v)[NB], int tid, int nb) const {
-        const int l = (tid >> 4) + 16 * (q & 3), u = q >> 2;
-#pragma unroll
-        for (int j = 0; j < NB; ++j)
-            if (j < nb) sb[j][u][l] = v[j];
-    }
-};
-
 // Contraction of NA weight-tile fragments per wave against a chunk's staged
 // rows over `nkb` stages of U steps.  a[m]: this lane's first weight piece of
 // tile m (consecutive steps `astep` pieces apart); rows[j]: token row of
 // staged block j for this thread's staging slot.
-template <class M, int U, int NA, int NB>
-__device__ inline void big_contract(u32x4_t (*sb)[NB][U][kWave], const u32x4_t* const (&a)[NA], int astep,
-                                    const u32x4_t* const (&rows)[NB], int nb, int nkb, f32x4_t (&acc)[NA][NB]) {
+template <class M, int NA, int NB>
+__device__ inline void big_contract(u32x4_t (*sb)[NB][kStageSteps][kWave], const u32x4_t* const (&a)[NA],
+                                    int astep, const u32x4_t* const (&rows)[NB], int nb, int nkb,
+                                    f32x4_t (&acc)[NA][NB]) {
+    constexpr int U = kStageSteps;
     const int tid = threadIdx.x, lane = tid & (kWave - 1);
-    BigStage<U, NB> st;
+    const int row_pieces = nkb * kStagePieces;
+    RowStage<NB> st;
     st.init(rows, tid);
     u32x4_t bv[NB];
     u32x4_t cur[NA][U], nxt[NA][U];
-    st.load(bv, 0, nb);
+    st.load(bv, 0, nb, row_pieces);
 #pragma unroll
     for (int m = 0; m < NA; ++m)
 #pragma unroll
         for (int u = 0; u < U; ++u) cur[m][u] = __builtin_nontemporal_load(a[m] + (size_t)astep * u);
-    st.store(sb[0], bv, tid, nb);
+    st.store(sb[0], bv, tid, nb, 0, row_pieces);
     __syncthreads();
     for (int kb = 0; kb < nkb; ++kb) {
         const bool more = kb + 1 < nkb;
         if (more) {
-            st.load(bv, kb + 1, nb);
+            st.load(bv, kb + 1, nb, row_pieces);
 #pragma unroll
             for (int m = 0; m < NA; ++m)
 #pragma unroll
@@ -329,7 +304,7 @@ __device__ inline void big_contract(u32x4_t (*sb)[NB][U][kWave], const u32x4_t* 
             }
         }
         if (more) {
-            st.store(sb[(kb + 1) & 1], bv, tid, nb);
+            st.store(sb[(kb + 1) & 1], bv, tid, nb, kb + 1, row_pieces);
 #pragma unroll
             for (int m = 0; m < NA; ++m)
 #pragma unroll
@@ -341,10 +316,10 @@ __device__ inline void big_contract(u32x4_t (*sb)[NB][U][kWave], const u32x4_t* 
 
 // Gate/up of big chunks: a workgroup item is 4 adjacent 16-feature tiles of
 // one chunk, one per wave, over the whole contraction.
-template <class M, int U, int NB>
+template <class M, int NB>
 __global__ __launch_bounds__(kFfnThreads) void k_gate_up_big(FfnParams p) {
     constexpr int kWaves = kFfnThreads / kWave;
-    __shared__ u32x4_t s_b[2][NB][U][kWave];
+    __shared__ u32x4_t s_b[2][NB][kStageSteps][kWave];
     const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
     const int r = lane & 15, g = lane >> 4;
     const int n_chunks = ffn_list_size(p);
@@ -378,7 +353,7 @@ __global__ __launch_bounds__(kFfnThreads) void k_gate_up_big(FfnParams p) {
         for (int m = 0; m < 2; ++m)
 #pragma unroll
             for (int tb = 0; tb < NB; ++tb) acc[m][tb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-        big_contract<M, U, 2, NB>(s_b, a, p.tiled ? 64 : 4, rows, nb, ksteps / U, acc);
+        big_contract<M, 2, NB>(s_b, a, p.tiled ? 64 : 4, rows, nb, ksteps / kStageSteps, acc);
         const int col = jt * 16 + 4 * g;
 #pragma unroll
         for (int tb = 0; tb < NB; ++tb) {
@@ -395,11 +370,11 @@ __global__ __launch_bounds__(kFfnThreads) void k_gate_up_big(FfnParams p) {
 
 // Down products of big chunks: a workgroup item is 8 adjacent 16-row tiles
 // of W2 (two per wave) of one chunk.
-template <class M, int U, int NB>
+template <class M, int NB>
 __global__ __launch_bounds__(kFfnThreads) void k_down_big(FfnParams p) {
     constexpr int kWaves = kFfnThreads / kWave;
     constexpr int kTW = 2;
-    __shared__ u32x4_t s_b[2][NB][U][kWave];
+    __shared__ u32x4_t s_b[2][NB][kStageSteps][kWave];
     const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
     const int r = lane & 15, g = lane >> 4;
     const int n_chunks = ffn_list_size(p);
@@ -434,7 +409,7 @@ __global__ __launch_bounds__(kFfnThreads) void k_down_big(FfnParams p) {
         for (int m = 0; m < kTW; ++m)
 #pragma unroll
             for (int tb = 0; tb < NB; ++tb) acc[m][tb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-        big_contract<M, U, kTW, NB>(s_b, a, p.tiled ? 64 : 4, rows, nb, ksteps / U, acc);
+        big_contract<M, kTW, NB>(s_b, a, p.tiled ? 64 : 4, rows, nb, ksteps / kStageSteps, acc);
 #pragma unroll
         for (int m = 0; m < kTW; ++m)
 #pragma unroll
@@ -530,15 +505,14 @@ struct DownK {
 
 template <class M>
 hipError_t launch_big(const FfnParams& p, bool gate_up, int nb, dim3 grid, hipStream_t s) {
-    constexpr int U = kBigU;
     switch (nb) {
         case 4:
-            if (gate_up) hipLaunchKernelGGL((k_gate_up_big<M, U, 4>), grid, dim3(kFfnThreads), 0, s, p);
-            else hipLaunchKernelGGL((k_down_big<M, U, 4>), grid, dim3(kFfnThreads), 0, s, p);
+            if (gate_up) hipLaunchKernelGGL((k_gate_up_big<M, 4>), grid, dim3(kFfnThreads), 0, s, p);
+            else hipLaunchKernelGGL((k_down_big<M, 4>), grid, dim3(kFfnThreads), 0, s, p);
             break;
         case 8:
-            if (gate_up) hipLaunchKernelGGL((k_gate_up_big<M, U, 8>), grid, dim3(kFfnThreads), 0, s, p);
-            else hipLaunchKernelGGL((k_down_big<M, U, 8>), grid, dim3(kFfnThreads), 0, s, p);
+            if (gate_up) hipLaunchKernelGGL((k_gate_up_big<M, 8>), grid, dim3(kFfnThreads), 0, s, p);
+            else hipLaunchKernelGGL((k_down_big<M, 8>), grid, dim3(kFfnThreads), 0, s, p);
             break;
         default: return hipErrorInvalidValue;
     }

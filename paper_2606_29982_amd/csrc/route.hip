@@ -23,7 +23,6 @@ namespace {
 
 constexpr int kTokWaves = 4;                       // tokens (wavefronts) per workgroup
 constexpr int kTokThreads = kTokWaves * kWave;
-constexpr int kMaskT = 1024;                       // batch size up to which the permutation uses LDS bitmasks
 constexpr int kNoIdx = 0x7fffffff;
 
 // Larger value wins; equal values go to the lower index.
@@ -495,163 +494,228 @@ __global__ __launch_bounds__(kRouteThreads) void k_prune(RouteParams p) {
     }
 }
 
-// Permutation of K_final (read from global memory) by expert slot: rows of
-// slot x (x < E routed, E+s shared) are [off[x], off[x+1]), tokens ascending
-// within a slot; then the FFN work list: one small chunk per slot with at
-// most chunk_small rows, then ceil(rows / kBigChunk) near-equal big chunks per
-// larger slot.
-// Executed by one workgroup of `nthr` threads.  Up to kMaskT tokens, each
-// expert's tokens are kept as a bitmask in LDS and every (token, slot) entry
-// finds its row independently by counting set bits; larger batches walk
-// K_final expert by expert.
-__device__ void permute_all(const RouteParams& p, int tid, int nthr, int* s_cnt, int* s_off, int* s_tot,
-                            unsigned long long* s_mask) {
-    const int T = p.T, E = p.E, k = p.k;
-    const int nx = E + p.n_shared;
-    const int slots = k + p.n_shared;
-    const int lane = tid & (kWave - 1);
-    const int wave = tid / kWave;
+// Row offsets of every expert slot and the FFN work lists, from the slot
+// row counts in s_cnt (run by one wavefront).  Slot x (x < E routed, E+s
+// shared) owns rows [off[x], off[x] + count); then one small chunk per slot
+// with at most chunk_small rows, and ceil(rows / kBigChunk) near-equal big
+// chunks per larger slot, the small chunks listed first.
+__device__ void build_lists(const RouteParams& p, const int* s_cnt, int* s_off, int lane) {
+    const int nx = p.E + p.n_shared;
     const int cs = p.chunk_small;
-    const bool masked = T <= kMaskT;
-    const int W = (T + 63) / 64;
-    if (masked) {
-        for (int i = tid; i < E * W; i += nthr) s_mask[i] = 0ull;
-        __syncthreads();
-        for (int i = tid; i < T * k; i += nthr) {
-            const int e = p.topk_ids[i];
-            if (e >= 0 && e < E) {
-                const int t = i / k;
-                atomicOr(&s_mask[e * W + (t >> 6)], 1ull << (t & 63));
-            }
-        }
-        __syncthreads();
-        for (int x = tid; x < nx; x += nthr) {
-            int c = T;
-            if (x < E) {
-                c = 0;
-                for (int w = 0; w < W; ++w) c += __popcll(s_mask[x * W + w]);
-            }
-            s_cnt[x] = c;
-        }
-    } else {
-        for (int x = tid; x < nx; x += nthr) s_cnt[x] = x < E ? 0 : T;
-        __syncthreads();
-        for (int i = tid; i < T * k; i += nthr) {
-            const int e = p.topk_ids[i];
-            if (e >= 0 && e < E) atomicAdd(&s_cnt[e], 1);
+    const int per = (nx + kWave - 1) / kWave;
+    const int lo = lane * per;
+    const int hi = min(lo + per, nx);
+    int sum = 0, ssum = 0, bsum = 0;
+    for (int x = lo; x < hi; ++x) {
+        const int n = s_cnt[x];
+        sum += n;
+        ssum += (n > 0 && n <= cs) ? 1 : 0;
+        bsum += n > cs ? (n + kBigChunk - 1) / kBigChunk : 0;
+    }
+    int inc = sum, sinc = ssum, binc = bsum;
+    for (int off = 1; off < kWave; off <<= 1) {
+        const int o = __shfl_up(inc, off);
+        const int so = __shfl_up(sinc, off);
+        const int bo = __shfl_up(binc, off);
+        if (lane >= off) {
+            inc += o;
+            sinc += so;
+            binc += bo;
         }
     }
-    __syncthreads();
-    if (wave == 0) {
-        // Exclusive scans of rows, small chunks and big chunks over the slots;
-        // small chunks are listed first, big ones after all of them.
-        const int per = (nx + kWave - 1) / kWave;
-        const int lo = lane * per;
-        const int hi = min(lo + per, nx);
-        int sum = 0, ssum = 0, bsum = 0;
-        for (int x = lo; x < hi; ++x) {
-            const int n = s_cnt[x];
-            sum += n;
-            ssum += (n > 0 && n <= cs) ? 1 : 0;
-            bsum += n > cs ? (n + kBigChunk - 1) / kBigChunk : 0;
-        }
-        int inc = sum, sinc = ssum, binc = bsum;
-        for (int off = 1; off < kWave; off <<= 1) {
-            const int o = __shfl_up(inc, off);
-            const int so = __shfl_up(sinc, off);
-            const int bo = __shfl_up(binc, off);
-            if (lane >= off) {
-                inc += o;
-                sinc += so;
-                binc += bo;
-            }
-        }
-        const int stotal = __shfl(sinc, kWave - 1);
-        int run = inc - sum, srun = sinc - ssum, brun = stotal + binc - bsum;
-        for (int x = lo; x < hi; ++x) {
-            const int cnt = s_cnt[x];
-            s_off[x] = run;
-            p.perm_off[x] = run;
-            if (cnt > 0 && cnt <= cs) {
-                int* chk = p.chunks + 4 * srun++;
+    const int stotal = __shfl(sinc, kWave - 1);
+    int run = inc - sum, srun = sinc - ssum, brun = stotal + binc - bsum;
+    for (int x = lo; x < hi; ++x) {
+        const int cnt = s_cnt[x];
+        s_off[x] = run;
+        p.perm_off[x] = run;
+        if (cnt > 0 && cnt <= cs) {
+            int* chk = p.chunks + 4 * srun++;
+            chk[0] = x;
+            chk[1] = run;
+            chk[2] = cnt;
+            chk[3] = 0;
+        } else if (cnt > cs) {
+            const int pieces = (cnt + kBigChunk - 1) / kBigChunk;
+            const int size = (cnt + pieces - 1) / pieces;
+            for (int c = 0; c < pieces; ++c) {
+                int* chk = p.chunks + 4 * (brun + c);
                 chk[0] = x;
-                chk[1] = run;
-                chk[2] = cnt;
+                chk[1] = run + c * size;
+                chk[2] = min(size, cnt - c * size);
                 chk[3] = 0;
-            } else if (cnt > cs) {
-                const int pieces = (cnt + kBigChunk - 1) / kBigChunk;
-                const int size = (cnt + pieces - 1) / pieces;
-                for (int c = 0; c < pieces; ++c) {
-                    int* chk = p.chunks + 4 * (brun + c);
-                    chk[0] = x;
-                    chk[1] = run + c * size;
-                    chk[2] = min(size, cnt - c * size);
-                    chk[3] = 0;
-                }
-                brun += pieces;
             }
-            run += cnt;
+            brun += pieces;
         }
-        const int total = __shfl(inc, kWave - 1);
-        const int btotal = __shfl(binc, kWave - 1);
-        if (lane == 0) {
-            s_off[nx] = total;
-            p.perm_off[nx] = total;
-            p.n_chunks[0] = stotal;
-            p.n_chunks[1] = btotal;
-            *s_tot = stotal + btotal;
+        run += cnt;
+    }
+    const int total = __shfl(inc, kWave - 1);
+    const int btotal = __shfl(binc, kWave - 1);
+    if (lane == 0) {
+        s_off[nx] = total;
+        p.perm_off[nx] = total;
+        p.n_chunks[0] = stotal;
+        p.n_chunks[1] = btotal;
+    }
+}
+
+// Token-block bitmasks: bit (t - t0) of word (x, (t - t0) / 64) is set when
+// token t of [t0, t0 + tn) chose routed expert x.  W words per expert.
+__device__ void fill_masks(const RouteParams& p, int t0, int tn, int W, int tid, int nthr,
+                           unsigned long long* s_mask) {
+    const int E = p.E, k = p.k;
+    for (int i = tid; i < E * W; i += nthr) s_mask[i] = 0ull;
+    __syncthreads();
+    for (int i = tid; i < tn * k; i += nthr) {
+        const int e = p.topk_ids[(size_t)t0 * k + i];
+        if (e >= 0 && e < E) {
+            const int tl = i / k;
+            atomicOr(&s_mask[e * W + (tl >> 6)], 1ull << (tl & 63));
         }
     }
     __syncthreads();
-    // Shared experts: every token, in order.
+}
+
+// Rows of the (token, slot) entries of tokens [t0, t0 + tn): routed entry
+// of expert e goes to row base[e] + (number of earlier tokens of the block
+// that chose e); caller-supplied ids outside [0, E) are empty slots.
+__device__ void place_entries(const RouteParams& p, int t0, int tn, int W, const int* base, int tid, int nthr,
+                              const unsigned long long* s_mask) {
+    const int E = p.E, k = p.k, slots = k + p.n_shared;
+    for (int i = tid; i < tn * k; i += nthr) {
+        const int tl = i / k, j = i - tl * k;
+        const int t = t0 + tl;
+        const int e = p.topk_ids[(size_t)t * k + j];
+        if (e < 0 || e >= E) {
+            p.perm_pos[(size_t)t * slots + j] = -1;
+            continue;
+        }
+        const unsigned long long* m = s_mask + e * W;
+        int rank = __popcll(m[tl >> 6] & ((1ull << (tl & 63)) - 1ull));
+        for (int w = 0; w < (tl >> 6); ++w) rank += __popcll(m[w]);
+        const int pos = base[e] + rank;
+        p.perm_tok[pos] = t;
+        p.perm_pos[(size_t)t * slots + j] = pos;
+    }
+}
+
+// Shared experts: every token, in order.
+__device__ void place_shared(const RouteParams& p, const int* s_off, int tid, int nthr) {
+    const int T = p.T, E = p.E, k = p.k, slots = k + p.n_shared;
     for (int i = tid; i < T * p.n_shared; i += nthr) {
         const int t = i / p.n_shared, sh = i - t * p.n_shared;
         const int pos = s_off[E + sh] + t;
         p.perm_tok[pos] = t;
-        p.perm_pos[t * slots + k + sh] = pos;
+        p.perm_pos[(size_t)t * slots + k + sh] = pos;
     }
-    if (masked) {
-        for (int i = tid; i < T * k; i += nthr) {
-            const int e = p.topk_ids[i];
-            const int t = i / k;
-            const int j = i - t * k;
-            if (e < 0 || e >= E) {
-                p.perm_pos[t * slots + j] = -1;
-                continue;
-            }
-            const unsigned long long* m = s_mask + e * W;
-            int rank = __popcll(m[t >> 6] & ((1ull << (t & 63)) - 1ull));
-            for (int w = 0; w < (t >> 6); ++w) rank += __popcll(m[w]);
-            const int pos = s_off[e] + rank;
-            p.perm_tok[pos] = t;
-            p.perm_pos[t * slots + j] = pos;
+}
+
+// Permutation of K_final (read from global memory) by expert slot, tokens
+// ascending within a slot, plus the FFN work lists, for batches of at most
+// kMaskT tokens: one workgroup; each expert's tokens are a bitmask in LDS and
+// every (token, slot) entry finds its row independently by counting set bits.
+// Also reports the refill/empty-slot counts of the compensation kernel.
+__global__ __launch_bounds__(kRouteThreads) void k_permute(RouteParams p) {
+    __shared__ int s_cnt[kMaxE + kMaxShared];
+    __shared__ int s_off[kMaxE + kMaxShared + 1];
+    __shared__ unsigned long long s_mask[kMaxE * (kMaskT / 64)];
+    const int tid = threadIdx.x;
+    if (tid == 0 && p.stats) {
+        p.stats[6] = p.counters[1];
+        p.stats[7] = p.counters[2];
+    }
+    if (!p.do_permute) return;
+    const int T = p.T, E = p.E;
+    const int W = (T + 63) / 64;
+    fill_masks(p, 0, T, W, tid, kRouteThreads, s_mask);
+    for (int x = tid; x < E + p.n_shared; x += kRouteThreads) {
+        int c = T;
+        if (x < E) {
+            c = 0;
+            for (int w = 0; w < W; ++w) c += __popcll(s_mask[x * W + w]);
         }
-        return;
+        s_cnt[x] = c;
     }
-    for (int x = tid; x < E; x += nthr) {
-        int pos = s_off[x];
-        if (s_cnt[x] == 0) continue;
-        const int n = T * k;
-        for (int i0 = 0; i0 < n; i0 += 8) {
-            int id[8];
-#pragma unroll
-            for (int j = 0; j < 8; ++j) id[j] = i0 + j < n ? p.topk_ids[i0 + j] : -1;
-#pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                if (id[j] == x) {
-                    const int i = i0 + j;
-                    const int t = i / k;
-                    p.perm_tok[pos] = t;
-                    p.perm_pos[t * slots + (i - t * k)] = pos;
-                    ++pos;
-                }
-            }
+    __syncthreads();
+    if (tid < kWave) build_lists(p, s_cnt, s_off, tid);
+    __syncthreads();
+    place_shared(p, s_off, tid, kRouteThreads);
+    place_entries(p, 0, T, W, s_off, tid, kRouteThreads, s_mask);
+}
+
+// Larger batches: the tokens are cut into blocks of kMaskT.
+// (1) per block, each routed expert's token count;
+__global__ __launch_bounds__(kRouteThreads) void k_permute_count(RouteParams p) {
+    __shared__ int s_c[kMaxE];
+    const int tid = threadIdx.x, b = blockIdx.x;
+    const int t0 = b * kMaskT, tn = min(kMaskT, p.T - t0);
+    for (int e = tid; e < p.E; e += kRouteThreads) s_c[e] = 0;
+    __syncthreads();
+    for (int i = tid; i < tn * p.k; i += kRouteThreads) {
+        const int e = p.topk_ids[(size_t)t0 * p.k + i];
+        if (e >= 0 && e < p.E) atomicAdd(&s_c[e], 1);
+    }
+    __syncthreads();
+    for (int e = tid; e < p.E; e += kRouteThreads) p.perm_blk[(size_t)b * p.E + e] = s_c[e];
+}
+
+// (2) one workgroup: slot totals, offsets and work lists, each block's first
+// row per expert (replacing its count), the shared experts' rows;
+__global__ __launch_bounds__(kRouteThreads) void k_permute_scan(RouteParams p) {
+    __shared__ int s_cnt[kMaxE + kMaxShared];
+    __shared__ int s_off[kMaxE + kMaxShared + 1];
+    const int tid = threadIdx.x, E = p.E;
+    const int nblk = (p.T + kMaskT - 1) / kMaskT;
+    if (tid == 0 && p.stats) {
+        p.stats[6] = p.counters[1];
+        p.stats[7] = p.counters[2];
+    }
+    for (int x = tid; x < E + p.n_shared; x += kRouteThreads) {
+        int c = p.T;
+        if (x < E) {
+            c = 0;
+            for (int b = 0; b < nblk; ++b) c += p.perm_blk[(size_t)b * E + x];
+        }
+        s_cnt[x] = c;
+    }
+    __syncthreads();
+    if (tid < kWave) build_lists(p, s_cnt, s_off, tid);
+    __syncthreads();
+    for (int x = tid; x < E; x += kRouteThreads) {
+        int run = s_off[x];
+        for (int b = 0; b < nblk; ++b) {
+            const int c = p.perm_blk[(size_t)b * E + x];
+            p.perm_blk[(size_t)b * E + x] = run;
+            run += c;
         }
     }
-    for (int i = tid; i < T * k; i += nthr) {
-        const int e = p.topk_ids[i];
-        if (e < 0 || e >= E) p.perm_pos[(i / k) * slots + (i % k)] = -1;
+    place_shared(p, s_off, tid, kRouteThreads);
+}
+
+// (3) per block, the rows of its (token, slot) entries.
+__global__ __launch_bounds__(kRouteThreads) void k_permute_place(RouteParams p) {
+    __shared__ unsigned long long s_mask[kMaxE * (kMaskT / 64)];
+    const int tid = threadIdx.x, b = blockIdx.x;
+    const int t0 = b * kMaskT, tn = min(kMaskT, p.T - t0);
+    const int W = (tn + 63) / 64;
+    fill_masks(p, t0, tn, W, tid, kRouteThreads, s_mask);
+    place_entries(p, t0, tn, W, p.perm_blk + (size_t)b * p.E, tid, kRouteThreads, s_mask);
+}
+
+hipError_t launch_permutation(const RouteParams& p, hipStream_t s) {
+    if (!p.do_permute || p.T <= kMaskT) {
+        hipLaunchKernelGGL(k_permute, dim3(1), dim3(kRouteThreads), 0, s, p);
+        return hipGetLastError();
     }
+    const dim3 blocks((p.T + kMaskT - 1) / kMaskT);
+    hipLaunchKernelGGL(k_permute_count, blocks, dim3(kRouteThreads), 0, s, p);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_permute_scan, dim3(1), dim3(kRouteThreads), 0, s, p);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_permute_place, blocks, dim3(kRouteThreads), 0, s, p);
+    return hipGetLastError();
 }
 
 // Compensation kernel: one wavefront per token (phase C).
@@ -669,20 +733,6 @@ __global__ __launch_bounds__(kTokThreads) void k_compensate(RouteParams p) {
     if (t < p.T)
         compensate_token<EPL>(p, t, lane, p.orig_ids + (size_t)t * p.k, s_trans, s_fin[wave], s_sbuf[wave],
                               &p.counters[1], &p.counters[2]);
-}
-
-// Permutation of K_final (caller-supplied ids outside [0, E) are empty
-// slots) plus the refill/empty-slot counts of the compensation kernel.
-__global__ __launch_bounds__(kRouteThreads) void k_permute(RouteParams p) {
-    __shared__ int s_cnt[kMaxE + kMaxShared];
-    __shared__ int s_off[kMaxE + kMaxShared + 1];
-    __shared__ int s_tot;
-    __shared__ unsigned long long s_mask[kMaxE * (kMaskT / 64)];
-    if (threadIdx.x == 0 && p.stats) {
-        p.stats[6] = p.counters[1];
-        p.stats[7] = p.counters[2];
-    }
-    if (p.do_permute) permute_all(p, threadIdx.x, kRouteThreads, s_cnt, s_off, &s_tot, s_mask);
 }
 
 }  // namespace
@@ -705,8 +755,7 @@ hipError_t launch_route(const RouteParams& p, hipStream_t s) {
         e = hipGetLastError();
         if (e != hipSuccess) return e;
         if (!p.do_permute && !p.stats) return hipSuccess;
-        hipLaunchKernelGGL(k_permute, dim3(1), dim3(kRouteThreads), 0, s, p);
-        return hipGetLastError();
+        return launch_permutation(p, s);
     };
     switch (p.epl) {
         case 1: return token_kernels(k_route_tokens<1>, k_compensate<1>);
@@ -719,8 +768,7 @@ hipError_t launch_route(const RouteParams& p, hipStream_t s) {
 hipError_t launch_permute(const RouteParams& p, hipStream_t s) {
     RouteParams q = p;
     q.stats = nullptr;   // counters are not filled when routing did not run
-    hipLaunchKernelGGL(k_permute, dim3(1), dim3(kRouteThreads), 0, s, q);
-    return hipGetLastError();
+    return launch_permutation(q, s);
 }
 
 }  // namespace caee
