@@ -184,6 +184,7 @@ RouteParams make_route_params(const caee_layer_desc_t* d, const float* logits, c
     p.rule = d->importance;
     p.counters = (int32_t*)(ws + L.counters);
     p.chunk_small = L.chunk_small;
+    p.chunk_big = L.chunk_big;
     p.orig_ids = (int32_t*)(ws + L.orig);
     return p;
 }

@@ -23,9 +23,16 @@ constexpr int kMaskT = 1024;        // token block of the permutation (one LDS b
 constexpr int kRouteThreads = 1024;
 // 16-token MFMA column blocks one FFN work item can hold (1, 2, 4 or 8).
 #ifndef CAEE_MAX_TOKEN_BLOCKS
-#define CAEE_MAX_TOKEN_BLOCKS 4
+#define CAEE_MAX_TOKEN_BLOCKS 8
 #endif
 constexpr int kMaxTokenBlocks = CAEE_MAX_TOKEN_BLOCKS;
+// Batches above this many tokens use 128-row big chunks (fewer weight
+// re-reads, one wave per SIMD); others 64-row chunks (two waves per SIMD),
+// which measured faster up to the 4096-token prefill.
+#ifndef CAEE_PREFILL_T
+#define CAEE_PREFILL_T 65536
+#endif
+constexpr int kPrefillT = CAEE_PREFILL_T;
 constexpr int kFfnThreads = 256;    // 4 independent waves per FFN workgroup
 // Gate/up wave work items wanted per call before the contraction is split
 // (about 32 per SIMD: short items keep the tail of the launch short).
@@ -87,6 +94,7 @@ struct WsLayout {
     size_t total;
     int P, max_chunks, ksplit;
     int chunk_small;            // an expert slot with at most this many rows is one small chunk
+    int chunk_big;              // rows of a big chunk at most
 };
 
 inline size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
@@ -119,12 +127,12 @@ __host__ __device__ inline int gate_up_split_for(int n_chunks, int tiles, int s_
 
 // Work list of the FFN kernels.  An expert slot with at most
 // 16 * small_token_blocks rows of the call is one "small" chunk; a slot with
-// more rows is cut into ceil(rows / kBigChunk) near-equal "big" chunks.  The
-// two kinds run in separate launches, each compiled for its own token-block
-// count: most experts of a decode batch carry a handful of tokens, and
-// compiling their work items for the hot experts' 128 tokens would cost them
-// occupancy.  Each big chunk streams its expert's weights once.
-constexpr int kBigChunk = 16 * kMaxTokenBlocks;
+// more rows is cut into ceil(rows / chunk_big) near-equal "big" chunks of at
+// most chunk_big = 16 * big_token_blocks rows.  The two kinds run in
+// separate launches, each compiled for its own token-block count: most
+// experts of a decode batch carry a handful of tokens, and compiling their
+// work items for the hot experts' rows would cost them occupancy.  Each
+// chunk streams its expert's weights once.
 
 // 16-token column blocks of the small-chunk kernels (1 or 2).
 inline int small_token_blocks(const caee_layer_desc_t& d) { return d.T <= 16 ? 1 : 2; }
@@ -133,8 +141,7 @@ inline int small_token_blocks(const caee_layer_desc_t& d) { return d.T <= 16 ? 1
 // chunks since no slot can have more rows than T).
 inline int big_token_blocks(const caee_layer_desc_t& d) {
     if (d.T <= 16 * small_token_blocks(d)) return 0;
-    const int need = (d.T + 15) / 16;
-    const int nb = need <= 4 ? 4 : 8;
+    const int nb = d.T <= kPrefillT ? 4 : 8;
     return nb < kMaxTokenBlocks ? nb : kMaxTokenBlocks;
 }
 
@@ -144,9 +151,10 @@ inline WsLayout ws_layout(const caee_layer_desc_t& d) {
     const int slots = d.k + d.n_shared;
     L.P = int(T * slots);
     L.chunk_small = 16 * small_token_blocks(d);
-    // Every expert slot gives one small chunk or ceil(rows / kBigChunk) big
-    // ones, so the count is at most (slots) + P / kBigChunk.
-    L.max_chunks = d.E + d.n_shared + (L.P + kBigChunk - 1) / kBigChunk;
+    L.chunk_big = 16 * (big_token_blocks(d) > 0 ? big_token_blocks(d) : 1);
+    // Every expert slot gives one small chunk or ceil(rows / chunk_big) big
+    // ones, so the count is at most (slots) + P / chunk_big.
+    L.max_chunks = d.E + d.n_shared + (L.P + L.chunk_big - 1) / L.chunk_big;
     size_t off = 0;
     auto take = [&](size_t bytes) { size_t o = off; off += align256(bytes); return o; };
     L.ids = take(T * d.k * 4);
@@ -204,7 +212,7 @@ struct RouteParams {
     uint8_t* mflag;
     double* imp_sum;
     int32_t* counters;
-    int chunk_small;
+    int chunk_small, chunk_big;
     // permutation outputs
     int32_t* perm_off;
     int32_t* perm_tok;

@@ -497,11 +497,11 @@ __global__ __launch_bounds__(kRouteThreads) void k_prune(RouteParams p) {
 // Row offsets of every expert slot and the FFN work lists, from the slot
 // row counts in s_cnt (run by one wavefront).  Slot x (x < E routed, E+s
 // shared) owns rows [off[x], off[x] + count); then one small chunk per slot
-// with at most chunk_small rows, and ceil(rows / kBigChunk) near-equal big
+// with at most chunk_small rows, and ceil(rows / chunk_big) near-equal big
 // chunks per larger slot, the small chunks listed first.
 __device__ void build_lists(const RouteParams& p, const int* s_cnt, int* s_off, int lane) {
     const int nx = p.E + p.n_shared;
-    const int cs = p.chunk_small;
+    const int cs = p.chunk_small, cb = p.chunk_big;
     const int per = (nx + kWave - 1) / kWave;
     const int lo = lane * per;
     const int hi = min(lo + per, nx);
@@ -510,7 +510,7 @@ __device__ void build_lists(const RouteParams& p, const int* s_cnt, int* s_off, 
         const int n = s_cnt[x];
         sum += n;
         ssum += (n > 0 && n <= cs) ? 1 : 0;
-        bsum += n > cs ? (n + kBigChunk - 1) / kBigChunk : 0;
+        bsum += n > cs ? (n + cb - 1) / cb : 0;
     }
     int inc = sum, sinc = ssum, binc = bsum;
     for (int off = 1; off < kWave; off <<= 1) {
@@ -536,7 +536,7 @@ __device__ void build_lists(const RouteParams& p, const int* s_cnt, int* s_off, 
             chk[2] = cnt;
             chk[3] = 0;
         } else if (cnt > cs) {
-            const int pieces = (cnt + kBigChunk - 1) / kBigChunk;
+            const int pieces = (cnt + cb - 1) / cb;
             const int size = (cnt + pieces - 1) / pieces;
             for (int c = 0; c < pieces; ++c) {
                 int* chk = p.chunks + 4 * (brun + c);
