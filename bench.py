@@ -46,6 +46,9 @@ def parse():
     ap.add_argument("--no-offload", action="store_true")
     ap.add_argument("--offload-calls", type=int, default=256,
                     help="decode calls of the offloading sequence (T=16 each)")
+    ap.add_argument("--case", default=None,
+                    help="time one configuration only, DTYPE:T[:skewed] (e.g. bf16:128:skewed, fp8:4096), "
+                         "and print its line instead of the headline")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="finish with one device-to-device copy of this many bytes (a known-size "
                          "reference for HBM traffic counters)")
@@ -263,12 +266,39 @@ def offload_rows(args, shape, Wt, dev):
     return {"b_pcie_gbps": round(b_pcie, 2), "miss_cost_us": round(miss_us, 1), "rows": rows}
 
 
+def run_case(args, dev):
+    """One configuration (e.g. for a profiler run): the sweep's inputs for
+    bf16 (Zipf-skewed when asked, 8 bins, no pruning) or the 8-bit rows'
+    inputs (tau 0.05, 8 bins), timed over --steps calls."""
+    import torch
+    from paper_2606_29982_amd import caee
+    from synth_inputs import R1_BF16, R1_FP8, make_expert_weights_torch
+    parts = args.case.split(":")
+    dtype, T = parts[0], int(parts[1])
+    skewed = len(parts) > 2 and parts[2] == "skewed"
+    shape = {"bf16": R1_BF16, "fp8": R1_FP8}[dtype]
+    W = caee.pack_weights(make_expert_weights_torch(shape, seed=args.seed, device=dev), dtype)
+    torch.cuda.synchronize()
+    tau = 0.0 if dtype == "bf16" else 0.05
+    c = Case(shape, T, tau, 8, W, dev, args.seed, skewed=skewed, cost_kind="zipf")
+    ms = time_steps(c, args.steps, args.warmup)
+    s = c.stats()
+    b = (s[5] + shape.n_shared) * (W_EXPERT_BYTES if dtype == "bf16" else W_EXPERT_BYTES_FP8)
+    print(json.dumps({"case": args.case, "us_per_step": round(ms * 1e3, 1), "tokens_per_s": round(T / (ms * 1e-3), 1),
+                      "weight_gbps": round(b / (ms * 1e-3) / 1e9, 1), "executed": s[5] + shape.n_shared,
+                      "steps": args.steps, "warmup": args.warmup}), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
         print(f"bench.py runs on exactly one GPU; --gpus {args.gpus} is not supported "
               "(the layer is measured on one MI355X; multi-GPU sharding is not built)", file=sys.stderr)
         sys.exit(2)
+    if args.case:
+        import torch
+        run_case(args, torch.device("cuda:0"))
+        return
     import torch
     from paper_2606_29982_amd import caee
     from synth_inputs import R1_BF16, make_expert_weights_torch
