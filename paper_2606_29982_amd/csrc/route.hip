@@ -23,6 +23,11 @@ namespace {
 
 constexpr int kTokWaves = 4;                       // tokens (wavefronts) per workgroup
 constexpr int kTokThreads = kTokWaves * kWave;
+// Batches up to this many tokens are routed by one fused single-workgroup kernel.
+#ifndef CAEE_FUSED_T
+#define CAEE_FUSED_T 16
+#endif
+constexpr int kFusedT = CAEE_FUSED_T;
 constexpr int kNoIdx = 0x7fffffff;
 
 // Larger value wins; equal values go to the lower index.
@@ -234,17 +239,21 @@ __device__ void compensate_token(const RouteParams& p, int t, int lane, const in
     double s[EPL], key[EPL];
     load_scores<EPL>(p, t, lane, s, key);
     bool in_k[EPL], tr[EPL], take[EPL], fin_f[EPL], out_f[EPL];
+    // K_t: lane r < k holds its r-th expert; the list is broadcast lane by lane.
+    const int my_orig = lane < p.k ? orig[lane] : -1;
 #pragma unroll
     for (int i = 0; i < EPL; ++i) {
-        const int e = lane * EPL + i;
         in_k[i] = false;
-        for (int r = 0; r < p.k; ++r) in_k[i] |= (orig[r] == e);
-        tr[i] = e < p.E && trans[e];
+        tr[i] = lane * EPL + i < p.E && trans[lane * EPL + i];
         take[i] = false;
         out_f[i] = false;
     }
-    int n_keep = 0;
-    for (int r = 0; r < p.k; ++r) n_keep += trans[orig[r]] ? 1 : 0;
+    for (int r = 0; r < p.k; ++r) {
+        const int o = __builtin_amdgcn_readlane(my_orig, r);
+#pragma unroll
+        for (int i = 0; i < EPL; ++i) in_k[i] |= (o == lane * EPL + i);
+    }
+    const int n_keep = __popcll(__ballot(my_orig >= 0 && trans[my_orig]));
 
     int got = 0;
     for (int r = 0; r < p.k - n_keep; ++r) {
@@ -324,10 +333,7 @@ __global__ __launch_bounds__(kTokThreads) void k_route_tokens(RouteParams p) {
 
 // Batch-summed importance (SUM rule): one wavefront per expert adds the
 // expert's gate weights in ascending token order.
-__global__ __launch_bounds__(kTokThreads) void k_importance_sum(RouteParams p) {
-    const int lane = threadIdx.x & (kWave - 1);
-    const int e = blockIdx.x * kTokWaves + threadIdx.x / kWave;
-    if (e >= p.E) return;
+__device__ void importance_sum_expert(const RouteParams& p, int e, int lane) {
     double sum = 0.0;
     for (int t0 = 0; t0 < p.T; t0 += kWave) {
         const int t = t0 + lane;
@@ -351,41 +357,58 @@ __global__ __launch_bounds__(kTokThreads) void k_importance_sum(RouteParams p) {
     if (lane == 0) p.imp_sum[e] = sum;
 }
 
+__global__ __launch_bounds__(kTokThreads) void k_importance_sum(RouteParams p) {
+    const int e = blockIdx.x * kTokWaves + threadIdx.x / kWave;
+    if (e < p.E) importance_sum_expert(p, e, threadIdx.x & (kWave - 1));
+}
+
 // Pruning kernel (one workgroup): Sec. IV-B steps 1-4 over the whole batch.
 // Bin loads are float64 sums of fp32 costs; while a bin's nonzero costs span
 // less than 2^20 every such sum is exact, so the order of the additions (LDS
 // atomics here) does not change any value or decision.
-__global__ __launch_bounds__(kRouteThreads) void k_prune(RouteParams p) {
-    __shared__ unsigned long long s_imp[kMaxE];
-    __shared__ uint8_t s_act[kMaxE], s_must[kMaxE], s_prom[kMaxE];
-    __shared__ float s_cost[kMaxE];
-    __shared__ int s_bin[kMaxE];
-    __shared__ int s_sorted[kMaxE];      // candidates in visiting order
-    __shared__ int s_cbin[kMaxE];        // their bins
-    __shared__ float s_ccost[kMaxE];     // their costs
-    __shared__ double s_aload[kMaxBins], s_mload[kMaxBins];
-    __shared__ double s_fbase;
-    __shared__ int s_ncand;
+struct PruneShared {
+    unsigned long long imp[kMaxE];
+    uint8_t act[kMaxE], must[kMaxE], prom[kMaxE];
+    float cost[kMaxE];
+    int bin[kMaxE];
+    int sorted[kMaxE];      // candidates in visiting order
+    int cbin[kMaxE];        // their bins
+    float ccost[kMaxE];     // their costs
+    double aload[kMaxBins], mload[kMaxBins];
+    double fbase;
+    int ncand;
+};
 
-    const int tid = threadIdx.x;
+// Run by one workgroup of `nthr` threads (a multiple of the wave size).
+__device__ void prune_all(const RouteParams& p, int tid, int nthr, PruneShared& sh) {
+    unsigned long long* s_imp = sh.imp;
+    uint8_t *s_act = sh.act, *s_must = sh.must, *s_prom = sh.prom;
+    float* s_cost = sh.cost;
+    int* s_bin = sh.bin;
+    int* s_sorted = sh.sorted;
+    int* s_cbin = sh.cbin;
+    float* s_ccost = sh.ccost;
+    double *s_aload = sh.aload, *s_mload = sh.mload;
+    double& s_fbase = sh.fbase;
+    int& s_ncand = sh.ncand;
     const int lane = tid & (kWave - 1);
     const int wave = tid / kWave;
     const int T = p.T, E = p.E, k = p.k, nb = p.n_bins;
 
-    for (int e = tid; e < E; e += kRouteThreads) {
+    for (int e = tid; e < E; e += nthr) {
         s_imp[e] = 0ull;
         s_act[e] = s_must[e] = s_prom[e] = 0;
         s_cost[e] = p.cost[e];
         const int b = p.bin ? p.bin[e] : 0;
         s_bin[e] = (b >= 0 && b < nb) ? b : -1;   // out-of-range bins (a precondition violation) count nowhere
     }
-    for (int b = tid; b < nb; b += kRouteThreads) s_aload[b] = s_mload[b] = 0.0;
+    for (int b = tid; b < nb; b += nthr) s_aload[b] = s_mload[b] = 0.0;
     if (tid == 0) s_ncand = 0;
     __syncthreads();
 
     // Step 1: A_act, importance, A_must (pairs mandatory on their own, and
     // for the SUM rule every expert whose summed weight reaches tau).
-    for (int i = tid; i < T * k; i += kRouteThreads) {
+    for (int i = tid; i < T * k; i += nthr) {
         const int e = p.orig_ids[i];
         atomicMax(&s_imp[e], (unsigned long long)__double_as_longlong(p.gbuf[i]));
         s_act[e] = 1;
@@ -393,7 +416,7 @@ __global__ __launch_bounds__(kRouteThreads) void k_prune(RouteParams p) {
     }
     __syncthreads();
     if (p.rule == CAEE_IMPORTANCE_SUM) {
-        for (int e = tid; e < E; e += kRouteThreads) {
+        for (int e = tid; e < E; e += nthr) {
             if (!s_act[e]) continue;
             const double I = p.imp_sum[e];
             s_imp[e] = (unsigned long long)__double_as_longlong(I);
@@ -404,7 +427,7 @@ __global__ __launch_bounds__(kRouteThreads) void k_prune(RouteParams p) {
 
     // Step 2: per-bin loads of A_act and A_must; candidate visiting order
     // (importance descending, index ascending).
-    for (int e = tid; e < E; e += kRouteThreads) {
+    for (int e = tid; e < E; e += nthr) {
         const double c = (double)s_cost[e];
         const int b = s_bin[e];
         if (s_act[e] && b >= 0) atomicAdd(&s_aload[b], c);
@@ -431,7 +454,7 @@ __global__ __launch_bounds__(kRouteThreads) void k_prune(RouteParams p) {
         for (int off = 32; off >= 1; off >>= 1) fb = fmax(fb, __shfl_xor(fb, off));
         if (lane == 0) s_fbase = fb;
     }
-    for (int b = tid; b < nb && p.bin_loads; b += kRouteThreads) {
+    for (int b = tid; b < nb && p.bin_loads; b += nthr) {
         p.bin_loads[b] = s_aload[b];
         p.bin_loads[nb + b] = s_mload[b];
     }
@@ -441,7 +464,7 @@ __global__ __launch_bounds__(kRouteThreads) void k_prune(RouteParams p) {
     // independent), walking the candidates in visiting order.
     const int n_cand = s_ncand;
     const double fbase = s_fbase;
-    for (int b = tid; b < nb; b += kRouteThreads) {
+    for (int b = tid; b < nb; b += nthr) {
         double load = s_mload[b];
         for (int r = 0; r < n_cand; ++r) {
             if (s_cbin[r] != b) continue;
@@ -456,7 +479,7 @@ __global__ __launch_bounds__(kRouteThreads) void k_prune(RouteParams p) {
     __syncthreads();
 
     // Step 4: A_trans = A_must + promoted; masks and counters by ballot.
-    for (int e = tid; e < E; e += kRouteThreads) p.trans[e] = s_must[e] | s_prom[e];
+    for (int e = tid; e < E; e += nthr) p.trans[e] = s_must[e] | s_prom[e];
     if (wave == 0) {
         const int words = (E + 31) / 32;
         int n_act = 0, n_must = 0, n_prom = 0, n_pruned = 0, n_trans = 0;
@@ -492,6 +515,11 @@ __global__ __launch_bounds__(kRouteThreads) void k_prune(RouteParams p) {
             p.stats[5] = n_trans;
         }
     }
+}
+
+__global__ __launch_bounds__(kRouteThreads) void k_prune(RouteParams p) {
+    __shared__ PruneShared sh;
+    prune_all(p, threadIdx.x, kRouteThreads, sh);
 }
 
 // Row offsets of every expert slot and the FFN work lists, from the slot
@@ -615,11 +643,16 @@ __device__ void place_shared(const RouteParams& p, const int* s_off, int tid, in
 // kMaskT tokens: one workgroup; each expert's tokens are a bitmask in LDS and
 // every (token, slot) entry finds its row independently by counting set bits.
 // Also reports the refill/empty-slot counts of the compensation kernel.
-__global__ __launch_bounds__(kRouteThreads) void k_permute(RouteParams p) {
-    __shared__ int s_cnt[kMaxE + kMaxShared];
-    __shared__ int s_off[kMaxE + kMaxShared + 1];
-    __shared__ unsigned long long s_mask[kMaxE * (kMaskT / 64)];
-    const int tid = threadIdx.x;
+struct PermShared {
+    int cnt[kMaxE + kMaxShared];
+    int off[kMaxE + kMaxShared + 1];
+    unsigned long long mask[kMaxE * (kMaskT / 64)];
+};
+
+__device__ void permute_small(const RouteParams& p, int tid, int nthr, PermShared& sh) {
+    int* s_cnt = sh.cnt;
+    int* s_off = sh.off;
+    unsigned long long* s_mask = sh.mask;
     if (tid == 0 && p.stats) {
         p.stats[6] = p.counters[1];
         p.stats[7] = p.counters[2];
@@ -627,8 +660,8 @@ __global__ __launch_bounds__(kRouteThreads) void k_permute(RouteParams p) {
     if (!p.do_permute) return;
     const int T = p.T, E = p.E;
     const int W = (T + 63) / 64;
-    fill_masks(p, 0, T, W, tid, kRouteThreads, s_mask);
-    for (int x = tid; x < E + p.n_shared; x += kRouteThreads) {
+    fill_masks(p, 0, T, W, tid, nthr, s_mask);
+    for (int x = tid; x < E + p.n_shared; x += nthr) {
         int c = T;
         if (x < E) {
             c = 0;
@@ -639,8 +672,13 @@ __global__ __launch_bounds__(kRouteThreads) void k_permute(RouteParams p) {
     __syncthreads();
     if (tid < kWave) build_lists(p, s_cnt, s_off, tid);
     __syncthreads();
-    place_shared(p, s_off, tid, kRouteThreads);
-    place_entries(p, 0, T, W, s_off, tid, kRouteThreads, s_mask);
+    place_shared(p, s_off, tid, nthr);
+    place_entries(p, 0, T, W, s_off, tid, nthr, s_mask);
+}
+
+__global__ __launch_bounds__(kRouteThreads) void k_permute(RouteParams p) {
+    __shared__ PermShared sh;
+    permute_small(p, threadIdx.x, kRouteThreads, sh);
 }
 
 // Larger batches: the tokens are cut into blocks of kMaskT.
@@ -735,11 +773,51 @@ __global__ __launch_bounds__(kTokThreads) void k_compensate(RouteParams p) {
                               &p.counters[1], &p.counters[2]);
 }
 
+// Small batches: the whole routing step (phases A-C and the permutation)
+// in one workgroup of 16 wavefronts, one launch instead of four or five.
+// Phases are separated by workgroup barriers; their data passes through
+// global memory (visible across the workgroup's waves after a barrier) and
+// LDS, exactly as between the separate kernels.
+constexpr int kFusedWaves = kRouteThreads / kWave;
+
+template <int EPL>
+__global__ __launch_bounds__(kRouteThreads) void k_route_fused(RouteParams p) {
+    __shared__ double s_sbuf[kFusedWaves][kMaxK];
+    __shared__ int s_ids[kFusedWaves][kMaxK];
+    __shared__ uint8_t s_trans[kMaxE];
+    __shared__ PruneShared sp;
+    __shared__ PermShared sq;
+    const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+    const int k = p.k;
+    if (tid < 4) p.counters[tid] = 0;
+    for (int t = wave; t < p.T; t += kFusedWaves)
+        route_token<EPL>(p, t, lane, p.orig_ids + (size_t)t * k, p.gbuf + (size_t)t * k, p.top1 + t,
+                         p.mflag + (size_t)t * k, s_sbuf[wave], s_ids[wave]);
+    __syncthreads();
+    if (p.rule == CAEE_IMPORTANCE_SUM) {
+        for (int e = wave; e < p.E; e += kFusedWaves) importance_sum_expert(p, e, lane);
+        __syncthreads();
+    }
+    prune_all(p, tid, kRouteThreads, sp);
+    __syncthreads();
+    for (int e = tid; e < p.E; e += kRouteThreads) s_trans[e] = p.trans[e];
+    __syncthreads();
+    for (int t = wave; t < p.T; t += kFusedWaves)
+        compensate_token<EPL>(p, t, lane, p.orig_ids + (size_t)t * k, s_trans, s_ids[wave], s_sbuf[wave],
+                              &p.counters[1], &p.counters[2]);
+    __syncthreads();
+    if (p.do_permute || p.stats) permute_small(p, tid, kRouteThreads, sq);
+}
+
 }  // namespace
 
 hipError_t launch_route(const RouteParams& p, hipStream_t s) {
     const dim3 tok_grid((p.T + kTokWaves - 1) / kTokWaves);
-    auto token_kernels = [&](auto route_k, auto comp_k) -> hipError_t {
+    auto token_kernels = [&](auto route_k, auto comp_k, auto fused_k) -> hipError_t {
+        if (p.T <= kFusedT) {
+            hipLaunchKernelGGL(fused_k, dim3(1), dim3(kRouteThreads), 0, s, p);
+            return hipGetLastError();
+        }
         hipLaunchKernelGGL(route_k, tok_grid, dim3(kTokThreads), 0, s, p);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
@@ -758,9 +836,9 @@ hipError_t launch_route(const RouteParams& p, hipStream_t s) {
         return launch_permutation(p, s);
     };
     switch (p.epl) {
-        case 1: return token_kernels(k_route_tokens<1>, k_compensate<1>);
-        case 2: return token_kernels(k_route_tokens<2>, k_compensate<2>);
-        case 4: return token_kernels(k_route_tokens<4>, k_compensate<4>);
+        case 1: return token_kernels(k_route_tokens<1>, k_compensate<1>, k_route_fused<1>);
+        case 2: return token_kernels(k_route_tokens<2>, k_compensate<2>, k_route_fused<2>);
+        case 4: return token_kernels(k_route_tokens<4>, k_compensate<4>, k_route_fused<4>);
         default: return hipErrorInvalidValue;
     }
 }
