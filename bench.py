@@ -44,6 +44,7 @@ def parse():
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-offload", action="store_true")
+    ap.add_argument("--no-calibrate", action="store_true")
     ap.add_argument("--offload-calls", type=int, default=256,
                     help="decode calls of the offloading sequence (T=16 each)")
     ap.add_argument("--case", default=None,
@@ -202,7 +203,7 @@ def pinned_h2d_gbps(dev, nbytes, reps=8):
     return gbps
 
 
-def offload_rows(args, shape, Wt, dev):
+def offload_rows(args, shape, Wt, dev, link_model=None):
     """The offloading deployment: all 256 bf16 experts in page-locked host
     memory, a 64-expert LRU device cache plus a 16-slot staging ring, misses
     copied on a side stream while resident experts compute.  A sequence of
@@ -218,7 +219,10 @@ def offload_rows(args, shape, Wt, dev):
     torch.cuda.synchronize()
     log(f"offload: experts copied to page-locked host memory in {time.time() - t0:.1f}s")
     b_pcie = pinned_h2d_gbps(dev, W_EXPERT_BYTES)
-    miss_us = W_EXPERT_BYTES / (b_pcie * 1e9) * 1e6    # alpha = 1, beta = 0
+    if link_model is not None:      # calibrated alpha * S / B + beta
+        miss_us = float(link_model.cost_us(W_EXPERT_BYTES))
+    else:                           # alpha = 1, beta = 0 at the measured peak
+        miss_us = W_EXPERT_BYTES / (b_pcie * 1e9) * 1e6
     log(f"offload: pinned H2D peak {b_pcie:.1f} GB/s, miss cost {miss_us:.0f} us per expert")
     calls = make_call_sequence(shape, seed=args.seed + 5, n_calls=args.offload_calls, T=T, zipf_logit_s=1.2)
     dev_calls = [(torch.from_numpy(c.x.view(np.int16)).to(dev).view(torch.bfloat16),
@@ -263,7 +267,8 @@ def offload_rows(args, shape, Wt, dev):
         del s13, s2, ws
         torch.cuda.empty_cache()
     del host
-    return {"b_pcie_gbps": round(b_pcie, 2), "miss_cost_us": round(miss_us, 1), "rows": rows}
+    return {"b_pcie_gbps": round(b_pcie, 2), "miss_cost_us": round(miss_us, 1),
+            "miss_cost_source": "calibrated" if link_model is not None else "measured peak", "rows": rows}
 
 
 def run_case(args, dev):
@@ -406,8 +411,19 @@ def main():
         del W8
         torch.cuda.empty_cache()
 
+    link_model = None
+    if not args.no_calibrate:
+        # Offline cost calibration (alpha, beta of both data paths).
+        from paper_2606_29982_amd import calibrate as cal
+        cres = cal.calibrate(dev)
+        link_model = cres["link"]
+        result["calibration"] = {
+            "hbm": {**cres["hbm"].as_dict(), "expert_cost_us": round(float(cres["hbm"].cost_us(W_EXPERT_BYTES)), 2)},
+            "h2d": {**cres["link"].as_dict(), "expert_cost_us": round(float(cres["link"].cost_us(W_EXPERT_BYTES)), 1)}}
+        log(f"calibration {result['calibration']}")
+
     if not args.no_offload:
-        result["offload"] = offload_rows(args, shape, Wt, dev)
+        result["offload"] = offload_rows(args, shape, Wt, dev, link_model)
 
     if args.copy_bytes > 0:
         src = torch.empty(args.copy_bytes, dtype=torch.uint8, device=dev)

@@ -20,6 +20,9 @@ the paper (Cost-Aware Expert Execution, arxiv 2606.29982):
   ffn.py           SwiGLU expert FFN and weighted combine (Sec. II-A), and
                    the OCP e4m3 codec used for 8-bit weights/activations
   layer.py         the whole layer, chaining the above
+  offload.py       residency cost table and the LRU device cache (Sec. IV-A, V-B)
+  calibration.py   the least-squares fit of the cost model's alpha and beta
+                   (Sec. IV-A, offline calibration)
 
 Where the paper is silent or ambiguous the reading taken is stated in the
 docstring of the function that takes it.  Routing and pruning decisions are
@@ -33,3 +36,4 @@ from .compensation import compensate_token, compensate_batch  # noqa: F401
 from .ffn import (bf16_bits_to_f64, e4m3_decode, e4m3_encode_rne,  # noqa: F401
                   quantize_e4m3_blocks, swiglu_expert, expert_weights_f64)
 from .layer import moe_layer_ref  # noqa: F401
+from .calibration import fit_alpha_beta, fit_grouped, cost_of  # noqa: F401
