@@ -294,6 +294,55 @@ def run_case(args, dev):
                       "steps": args.steps, "warmup": args.warmup}), flush=True)
 
 
+def ablation_rows(args, shape, Wt, dev):
+    """Compensation ablation, a synthetic stand-in for the paper's comparison
+    of random selection with its compensation: an offloading-style layer
+    (the 32 most popular experts resident at cost 0, the others at cost 1,
+    one bin, the CIR rule) pruned at theta_imp 0.9 / 0.8 / 0.7, and the
+    relative output error ||y - y_dense|| / ||y_dense|| against the same
+    layer without pruning, for the paper's score-based refill, a random
+    refill (mean of 4 seeds) and no refill (renormalise only).  With random
+    expert weights a refilled expert's output is uncorrelated with the one it
+    replaces, so this measures how far each variant moves the output, not
+    the task accuracy the paper reports."""
+    import torch
+    from paper_2606_29982_amd import caee
+    from synth_inputs import make_call_sequence, popularity_ranks
+    ranks = popularity_ranks(shape, args.seed + 9)
+    cost = torch.from_numpy(np.where(ranks < 32, 0.0, 1.0).astype(np.float32)).to(dev)
+    rows = []
+    for T in (8, 32, 128):
+        c = make_call_sequence(shape, seed=args.seed + 9, n_calls=1, T=T, zipf_logit_s=1.2)[0]
+        x = torch.from_numpy(c.x.view(np.int16)).to(dev).view(torch.bfloat16)
+        logits = torch.from_numpy(c.logits).to(dev)
+        bias = torch.from_numpy(c.bias).to(dev)
+
+        def run(tau, refill="score", seed=0, rule="cir"):
+            layer = caee.Layer.from_shape(shape, T=T, tau=tau, n_bins=1, importance=rule, refill=refill, seed=seed)
+            ws = caee.alloc_workspace(layer, dev)
+            out = caee.alloc_route_out(layer, dev)
+            y = torch.empty((T, shape.d), dtype=torch.bfloat16, device=dev)
+            caee.moe_layer(layer, x, logits, bias, cost, None, Wt, y, ws, out)
+            return y.float(), out["stats"].cpu().tolist()
+
+        y0, _ = run(0.0, rule="max")      # tau = 0: nothing pruned
+        n0 = float(torch.linalg.norm(y0))
+        for theta in (0.9, 0.8, 0.7):
+            errs = {}
+            st = None
+            for mode in ("score", "none"):
+                y, st_m = run(theta, mode)
+                errs[mode] = float(torch.linalg.norm(y - y0)) / n0
+                st = st if st is not None else st_m
+            rnd = [float(torch.linalg.norm(run(theta, "random", sd)[0] - y0)) / n0 for sd in range(4)]
+            errs["random"] = float(np.mean(rnd))
+            rows.append({"T": T, "theta_imp": theta, "pruned": st[4], "refilled_slots": st[6],
+                         "rel_err_score": round(errs["score"], 5), "rel_err_random": round(errs["random"], 5),
+                         "rel_err_none": round(errs["none"], 5)})
+            log(f"ablation {rows[-1]}")
+    return rows
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -410,6 +459,9 @@ def main():
         result["fp8"] = fp8_rows
         del W8
         torch.cuda.empty_cache()
+
+    if not args.no_sweep:
+        result["compensation_ablation"] = ablation_rows(args, shape, Wt, dev)
 
     link_model = None
     if not args.no_calibrate:

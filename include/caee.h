@@ -49,7 +49,7 @@
 extern "C" {
 #endif
 
-#define CAEE_ABI_VERSION 3
+#define CAEE_ABI_VERSION 4
 
 typedef enum caee_status {
     CAEE_OK = 0,
@@ -83,6 +83,21 @@ typedef enum caee_importance {
     CAEE_IMPORTANCE_CIR = 2
 } caee_importance_t;
 
+/* How compensation (Sec. IV-C) fills the slots pruning freed in a token's
+ * list.  SCORE is the paper's mechanism; the other two exist for its
+ * ablation (random selection among the executed experts vs the proposed
+ * compensation). */
+typedef enum caee_refill {
+    /* Best router keys of A_trans minus K_t (no group limit). */
+    CAEE_REFILL_SCORE = 0,
+    /* No refill: K_final = K_t within A_trans, weights renormalised over it. */
+    CAEE_REFILL_NONE = 1,
+    /* The experts of A_trans minus K_t with the largest random keys: the top
+     * 53 bits of the SplitMix64 output for counter (seed << 32) | (t*E + e),
+     * t the token's index in the call; ties to the lower index. */
+    CAEE_REFILL_RANDOM = 2
+} caee_refill_t;
+
 /* Shape and hyper-parameters of one MoE layer call. */
 typedef struct caee_layer_desc {
     int32_t T;            /* tokens in the batch, >= 0 (0: the call does nothing) */
@@ -101,6 +116,8 @@ typedef struct caee_layer_desc {
     int32_t x_dtype;      /* hidden-state dtype: CAEE_F32 with f32 weights, else CAEE_BF16 */
     int32_t w_dtype;      /* expert weight dtype: CAEE_F32, CAEE_BF16 or CAEE_FP8_E4M3 */
     int32_t y_dtype;      /* output dtype: CAEE_F32 or CAEE_BF16 */
+    int32_t refill;       /* a caee_refill_t; CAEE_REFILL_SCORE is the paper's method */
+    uint32_t seed;        /* CAEE_REFILL_RANDOM: seed of the random keys; ignored otherwise */
 } caee_layer_desc_t;
 
 /* Storage order of the expert matrices. */

@@ -18,15 +18,49 @@ from __future__ import annotations
 
 import numpy as np
 
+# Ablation variants of the refill (the paper contrasts its score-based
+# compensation with a random selection among the cheap experts):
+#   "score"  - the paper's mechanism, as described above;
+#   "none"   - no refill: K_final = K_t within A_trans, weights renormalised;
+#   "random" - the freed slots take the experts of A_trans minus K_t with the
+#              largest counter-based random keys (below), lower index on ties.
+_M64 = (1 << 64) - 1
+_GOLDEN_GAMMA = 0x9E3779B97F4A7C15
+
+
+def splitmix64(state: int) -> int:
+    """The output SplitMix64 (Steele, Lea and Flood, OOPSLA 2014, in the
+    64-bit form Vigna publishes) produces from `state`: add the golden
+    gamma, then two xor-shift-multiply rounds and a final xor-shift."""
+    z = (state + _GOLDEN_GAMMA) & _M64
+    z = ((z ^ (z >> 30)) * 0xBF58476D1CE4E5B9) & _M64
+    z = ((z ^ (z >> 27)) * 0x94D049BB133111EB) & _M64
+    return z ^ (z >> 31)
+
+
+def refill_key(seed: int, t: int, e: int, E: int) -> int:
+    """53-bit random key of (token t, expert e) for the random refill: the
+    SplitMix64 output of counter (seed << 32) | (t * E + e), top 53 bits."""
+    return splitmix64(((int(seed) & 0xFFFFFFFF) << 32) | (int(t) * int(E) + int(e))) >> 11
+
 
 def compensate_token(key: np.ndarray, s: np.ndarray, orig_ids, trans: np.ndarray,
-                     k: int, routed_scaling: float):
+                     k: int, routed_scaling: float, refill: str = "score", seed: int = 0, t: int = 0):
     """Return (ids, w) for one token: K_final in rank order (key desc, index
-    asc) and w_e = routed_scaling * s_e / sum_{K_final} s (float64)."""
+    asc) and w_e = routed_scaling * s_e / sum_{K_final} s (float64).
+    `refill`, `seed` and the token index `t` select the ablation variant."""
     orig = list(orig_ids)
     keep = [e for e in orig if trans[e]]
     pool = [e for e in np.flatnonzero(trans).tolist() if e not in orig]
-    pool.sort(key=lambda e: (-float(key[e]), e))
+    if refill == "score":
+        pool.sort(key=lambda e: (-float(key[e]), e))
+    elif refill == "random":
+        E = len(trans)
+        pool.sort(key=lambda e: (-refill_key(seed, t, e, E), e))
+    elif refill == "none":
+        pool = []
+    else:
+        raise ValueError(refill)
     refill = pool[:max(0, k - len(keep))]
     final = sorted(keep + refill, key=lambda e: (-float(key[e]), e))
     total = 0.0
@@ -37,7 +71,7 @@ def compensate_token(key: np.ndarray, s: np.ndarray, orig_ids, trans: np.ndarray
 
 
 def compensate_batch(keys: np.ndarray, s: np.ndarray, orig_ids: np.ndarray,
-                     trans: np.ndarray, k: int, routed_scaling: float):
+                     trans: np.ndarray, k: int, routed_scaling: float, refill: str = "score", seed: int = 0):
     """Compensation for every token.  Returns (ids [T][k] int, -1 padded;
     w [T][k] float64, 0 padded; total refilled slots)."""
     T = orig_ids.shape[0]
@@ -45,7 +79,7 @@ def compensate_batch(keys: np.ndarray, s: np.ndarray, orig_ids: np.ndarray,
     w = np.zeros((T, k), dtype=np.float64)
     n_refill = 0
     for t in range(T):
-        fid, fw, nr = compensate_token(keys[t], s[t], orig_ids[t], trans, k, routed_scaling)
+        fid, fw, nr = compensate_token(keys[t], s[t], orig_ids[t], trans, k, routed_scaling, refill, seed, t)
         ids[t, :len(fid)] = fid
         w[t, :len(fw)] = fw
         n_refill += nr

@@ -24,7 +24,8 @@ def decode_x(x, x_dtype: str) -> np.ndarray:
 def moe_layer_ref(*, E, n_group, topk_group, k, routed_scaling, tau, n_bins,
                   logits, bias=None, cost, bins=None,
                   x=None, x_dtype="f32", w_dtype="f32", n_shared=0,
-                  get_expert=None, get_shared=None, tokens=None, rule="max") -> dict:
+                  get_expert=None, get_shared=None, tokens=None, rule="max", refill="score",
+                  seed=0) -> dict:
     """Run the layer.  Routing/pruning/compensation always run on the whole
     batch (pruning is a batch-level decision).  When ``x`` and the weight
     getters are given, the output rows y_t are computed for ``tokens``
@@ -37,7 +38,7 @@ def moe_layer_ref(*, E, n_group, topk_group, k, routed_scaling, tau, n_bins,
     T = logits.shape[0]
     s, keys, orig_ids, g = route_batch(logits, bias, n_group, topk_group, k)
     pr = prune_batch(orig_ids, g, E, tau, cost, bins, n_bins, rule=rule, s=s)
-    ids, w, n_refill = compensate_batch(keys, s, orig_ids, pr["trans"], k, routed_scaling)
+    ids, w, n_refill = compensate_batch(keys, s, orig_ids, pr["trans"], k, routed_scaling, refill, seed)
     out = dict(s=s, keys=keys, orig_ids=orig_ids, g=g, topk_ids=ids, topk_w=w, **pr)
     out["stats"] = dict(
         n_act=int(pr["act"].sum()), n_must=int(pr["must"].sum()),

@@ -20,6 +20,7 @@ CAEE_F32, CAEE_BF16, CAEE_FP8_E4M3 = 0, 1, 2
 KERNEL_KINDS = {"route": 0, "gate_up": 1, "down": 2, "combine": 3, "quant": 4}
 DTYPE_CODE = {"f32": CAEE_F32, "bf16": CAEE_BF16, "fp8": CAEE_FP8_E4M3}
 IMPORTANCE_CODE = {"max": 0, "sum": 1, "cir": 2}
+REFILL_CODE = {"score": 0, "none": 1, "random": 2}
 
 
 class CaeeError(RuntimeError):
@@ -33,7 +34,8 @@ class LayerDesc(ctypes.Structure):
                 ("T", "d", "f", "E", "n_group", "topk_group", "k", "n_shared")] + [
         ("routed_scaling", ctypes.c_float), ("tau", ctypes.c_float),
         ("n_bins", ctypes.c_int32), ("importance", ctypes.c_int32),
-        ("x_dtype", ctypes.c_int32), ("w_dtype", ctypes.c_int32), ("y_dtype", ctypes.c_int32)]
+        ("x_dtype", ctypes.c_int32), ("w_dtype", ctypes.c_int32), ("y_dtype", ctypes.c_int32),
+        ("refill", ctypes.c_int32), ("seed", ctypes.c_uint32)]
 
 
 class ExpertWeights(ctypes.Structure):
@@ -151,12 +153,15 @@ class Layer:
     x_dtype: str = "bf16"
     y_dtype: str = "bf16"
     importance: str = "max"     # "max" | "sum" | "cir" (caee_importance_t)
+    refill: str = "score"       # "score" | "none" | "random" (caee_refill_t)
+    seed: int = 0               # random refill keys
 
     def desc(self) -> LayerDesc:
         return LayerDesc(self.T, self.d, self.f, self.E, self.n_group, self.topk_group, self.k,
                          self.n_shared, self.routed_scaling, self.tau, self.n_bins,
                          IMPORTANCE_CODE[self.importance],
-                         DTYPE_CODE[self.x_dtype], DTYPE_CODE[self.w_dtype], DTYPE_CODE[self.y_dtype])
+                         DTYPE_CODE[self.x_dtype], DTYPE_CODE[self.w_dtype], DTYPE_CODE[self.y_dtype],
+                         REFILL_CODE[self.refill], self.seed & 0xFFFFFFFF)
 
     @classmethod
     def from_shape(cls, shape, **over) -> "Layer":

@@ -56,6 +56,8 @@ caee_status_t check_desc(const caee_layer_desc_t* d) {
     if (d->importance != CAEE_IMPORTANCE_MAX && d->importance != CAEE_IMPORTANCE_SUM &&
         d->importance != CAEE_IMPORTANCE_CIR)
         return fail(CAEE_ERR_INVALID_ARG, "unknown importance=%d", d->importance);
+    if (d->refill != CAEE_REFILL_SCORE && d->refill != CAEE_REFILL_NONE && d->refill != CAEE_REFILL_RANDOM)
+        return fail(CAEE_ERR_INVALID_ARG, "unknown refill=%d", d->refill);
     if (d->w_dtype != CAEE_F32 && d->w_dtype != CAEE_BF16 && d->w_dtype != CAEE_FP8_E4M3)
         return fail(CAEE_ERR_INVALID_ARG, "unknown w_dtype=%d", d->w_dtype);
     const int want_x = d->w_dtype == CAEE_F32 ? CAEE_F32 : CAEE_BF16;
@@ -182,6 +184,8 @@ RouteParams make_route_params(const caee_layer_desc_t* d, const float* logits, c
     p.mflag = (uint8_t*)(ws + L.mflag);
     p.imp_sum = (double*)(ws + L.imp_sum);
     p.rule = d->importance;
+    p.refill = d->refill;
+    p.seed = d->seed;
     p.counters = (int32_t*)(ws + L.counters);
     p.chunk_small = L.chunk_small;
     p.chunk_big = L.chunk_big;

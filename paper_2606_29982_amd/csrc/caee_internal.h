@@ -194,6 +194,8 @@ struct RouteParams {
     int gsize;      // experts per group
     double rs, tau;
     int rule;       // caee_importance_t
+    int refill;     // caee_refill_t
+    uint32_t seed;  // random refill keys
     const float* logits;
     const float* bias;
     const float* cost;

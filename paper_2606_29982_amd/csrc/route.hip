@@ -231,6 +231,15 @@ __device__ void route_token(const RouteParams& p, int t, int lane, int* ids, dou
     }
 }
 
+// SplitMix64 output for `state` (Steele, Lea and Flood 2014): golden-gamma
+// increment, two xor-shift-multiply rounds, a final xor-shift.
+__device__ inline uint64_t splitmix64(uint64_t state) {
+    uint64_t z = state + 0x9E3779B97F4A7C15ull;
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+    return z ^ (z >> 31);
+}
+
 // Phase C for token t: K_final = (K_t ∩ A_trans) refilled from A_trans \ K_t.
 template <int EPL>
 __device__ void compensate_token(const RouteParams& p, int t, int lane, const int* orig,
@@ -255,14 +264,23 @@ __device__ void compensate_token(const RouteParams& p, int t, int lane, const in
     }
     const int n_keep = __popcll(__ballot(my_orig >= 0 && trans[my_orig]));
 
+    // Refill order: router key (the paper's compensation) or, for the
+    // ablation, a 53-bit random key (exact in a double) per (token, expert).
+    double rv[EPL];
+#pragma unroll
+    for (int i = 0; i < EPL; ++i) {
+        const uint64_t ctr = ((uint64_t)p.seed << 32) | (uint64_t)(t * p.E + lane * EPL + i);
+        rv[i] = p.refill == CAEE_REFILL_RANDOM ? (double)(splitmix64(ctr) >> 11) : key[i];
+    }
+    const int to_fill = p.refill == CAEE_REFILL_NONE ? 0 : p.k - n_keep;
     int got = 0;
-    for (int r = 0; r < p.k - n_keep; ++r) {
+    for (int r = 0; r < to_fill; ++r) {
         double v = -INFINITY;
         int ei = kNoIdx;
 #pragma unroll
         for (int i = 0; i < EPL; ++i) {
-            if (tr[i] && !in_k[i] && !take[i] && key[i] > v) {
-                v = key[i];
+            if (tr[i] && !in_k[i] && !take[i] && rv[i] > v) {
+                v = rv[i];
                 ei = lane * EPL + i;
             }
         }

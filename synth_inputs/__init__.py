@@ -14,6 +14,7 @@ from .layers import (  # noqa: F401
     RoutingInputs,
     make_routing_inputs,
     make_call_sequence,
+    popularity_ranks,
     make_cost_table,
     make_bins,
     make_expert_weights_np,

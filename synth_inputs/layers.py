@@ -154,6 +154,12 @@ def make_routing_inputs(shape: LayerShape, seed: int = 0, T: Optional[int] = Non
     )
 
 
+def popularity_ranks(shape: LayerShape, seed: int) -> np.ndarray:
+    """Popularity rank of every expert (0 = most popular) under the Zipf
+    offset of make_routing_inputs / make_call_sequence (stream 4)."""
+    return _rng(seed, 4).permutation(shape.E)
+
+
 def make_call_sequence(shape: LayerShape, seed: int, n_calls: int, T: Optional[int] = None,
                        zipf_logit_s: float = 1.2) -> list:
     """Inputs of ``n_calls`` consecutive layer calls (decode steps) that share

@@ -55,7 +55,8 @@ def getters_dev(Wd: dict, w_dtype: str):
     return (lambda e: fetch("", e)), (lambda s: fetch("sh_", s))
 
 
-def oracle_layer(shape, inp, tau, n_bins, get=None, get_sh=None, tokens=None, with_y=True, rule="max"):
+def oracle_layer(shape, inp, tau, n_bins, get=None, get_sh=None, tokens=None, with_y=True, rule="max",
+                 refill="score", seed=0):
     T = inp.logits.shape[0]
     # the C ABI carries tau and the routed scaling as fp32
     return oracle.moe_layer_ref(
@@ -65,13 +66,13 @@ def oracle_layer(shape, inp, tau, n_bins, get=None, get_sh=None, tokens=None, wi
         bias=inp.bias, cost=inp.cost, bins=inp.bins if n_bins > 1 else None,
         x=inp.x if with_y else None, x_dtype=shape.x_dtype, w_dtype=shape.w_dtype,
         n_shared=shape.n_shared, get_expert=get if with_y else None, get_shared=get_sh,
-        tokens=tokens if tokens is not None else (list(range(T)) if with_y else None))
+        tokens=tokens if tokens is not None else (list(range(T)) if with_y else None), refill=refill, seed=seed)
 
 
-def gpu_layer(shape, inp, tau, n_bins, Wd, dev, route_only=False, rule="max"):
+def gpu_layer(shape, inp, tau, n_bins, Wd, dev, route_only=False, rule="max", refill="score", seed=0):
     """Run caee_moe_layer (or caee_route_prune) and return numpy results."""
     T = inp.logits.shape[0]
-    layer = caee.Layer.from_shape(shape, T=T, tau=tau, n_bins=n_bins, importance=rule)
+    layer = caee.Layer.from_shape(shape, T=T, tau=tau, n_bins=n_bins, importance=rule, refill=refill, seed=seed)
     ws = caee.alloc_workspace(layer, dev)
     out = caee.alloc_route_out(layer, dev)
     logits = to_dev(inp.logits, dev)

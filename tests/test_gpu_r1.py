@@ -110,3 +110,17 @@ def test_r1_offload_sequence(r1_weights, r1_tiled, rule, tau):
                               rule=rule, miss_cost=1760.0, get=get, get_sh=get_sh,
                               y_tokens=lambda i: [0, 15] if i in (0, 3) else None, y_tol=2e-2)
     assert st["misses"] > 0 and st["hits"] > 0
+
+
+@pytest.mark.parametrize("T", [1, 8, 32, 128])
+@pytest.mark.parametrize("refill", ["none", "random"])
+def test_r1_refill_variants(T, refill, r1_weights):
+    """Compensation ablation variants at the R1 shape: the offloading rule
+    (CIR) with one bin, where every non-mandatory candidate with a cost is
+    pruned and many slots are refilled."""
+    inp = make_routing_inputs(R1_BF16, seed=T, T=T, zipf_logit_s=1.1, cost_kind="zipf", n_bins=1)
+    for tau in (0.9, 0.7):
+        print(f"refill={refill} T={T} tau={tau}", flush=True)
+        got = gpu_layer(R1_BF16, inp, tau, 1, r1_weights, DEV, route_only=True, rule="cir", refill=refill, seed=5)
+        ref = oracle_layer(R1_BF16, inp, tau, 1, with_y=False, rule="cir", refill=refill, seed=5)
+        check_route(got, ref, R1_BF16.E)

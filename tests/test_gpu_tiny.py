@@ -18,20 +18,20 @@ TOL = {"f32": 1e-5, "bf16": 2e-2}
 
 
 def _run(shape, seed=0, tau=0.1, n_bins=4, T=None, zipf=None, cost_kind="uniform", mutate=None, rule="max",
-         tiled=False):
+         tiled=False, refill="score", rseed=0):
     inp = make_routing_inputs(shape, seed=seed, T=T, zipf_logit_s=zipf, cost_kind=cost_kind,
                               n_bins=n_bins)
     if mutate:
         mutate(inp)
     W = make_expert_weights_np(shape, seed=seed)
-    print(f"case {shape.name} seed={seed} tau={tau} n_bins={n_bins} T={inp.logits.shape[0]} rule={rule}",
-          flush=True)
+    print(f"case {shape.name} seed={seed} tau={tau} n_bins={n_bins} T={inp.logits.shape[0]} rule={rule} "
+          f"refill={refill}", flush=True)
     Wd = w_to_dev(W, DEV)
     if tiled:
         Wd = caee.pack_weights(Wd, shape.w_dtype)
-    got = gpu_layer(shape, inp, tau, n_bins, Wd, DEV, rule=rule)
+    got = gpu_layer(shape, inp, tau, n_bins, Wd, DEV, rule=rule, refill=refill, seed=rseed)
     get, get_sh = getters_np(W, shape.w_dtype)
-    ref = oracle_layer(shape, inp, tau, n_bins, get, get_sh, rule=rule)
+    ref = oracle_layer(shape, inp, tau, n_bins, get, get_sh, rule=rule, refill=refill, seed=rseed)
     check_route(got, ref, shape.E)
     check_y(got["y"], ref["y"], TOL[shape.w_dtype])
     return got, ref
@@ -194,3 +194,15 @@ def test_tiled_layout_order(dtype):
 @pytest.mark.parametrize("T", [1, 3, 16, 70])
 def test_tiled_weights(shape, T):
     _run(shape, seed=T, tau=0.2, n_bins=4, T=T, tiled=True)
+
+
+@pytest.mark.parametrize("refill", ["none", "random"])
+@pytest.mark.parametrize("T", [5, 16, 40])
+@pytest.mark.parametrize("seed", [0, 3])
+def test_tiny_refill_variants(refill, T, seed):
+    """Compensation ablation variants (no refill; random refill by
+    SplitMix64 keys) against the oracle, through both routing paths."""
+    got, ref = _run(TINY_F32, seed=seed, tau=0.7, n_bins=1, T=T, zipf=1.2, cost_kind="zipf", rule="cir",
+                    refill=refill, rseed=11 + seed)
+    if refill == "none":
+        assert got["stats"][6] == 0

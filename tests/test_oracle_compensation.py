@@ -3,6 +3,7 @@ example and the invariants it must satisfy on random batches."""
 import numpy as np
 import pytest
 
+import oracle
 from oracle import compensate_batch, compensate_token, group_limited_topk, prune_batch, route_batch
 
 
@@ -66,3 +67,72 @@ def test_refill_ignores_groups():
     assert fid[0].tolist() == [0, 5]
     assert fid[1].tolist() == [5, 6]
     assert nref == 2
+
+
+# ---- refill variants of the compensation ablation ----------------------------
+
+def test_splitmix64_published_outputs(golden):
+    from oracle.compensation import splitmix64
+    g = golden("splitmix64.json")
+    gamma = int(g["gamma"], 16)
+    got = [splitmix64(i * gamma) for i in range(3)]
+    assert got == [int(v, 16) for v in g["outputs_from_state_0"]]
+
+
+def _ablation_case(seed=0, T=16):
+    from synth_inputs import TINY_F32, make_routing_inputs
+    shape = TINY_F32
+    inp = make_routing_inputs(shape, seed=seed, T=T, zipf_logit_s=1.2, cost_kind="zipf")
+    return shape, inp
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_refill_none_keeps_only_survivors(seed):
+    shape, inp = _ablation_case(seed)
+    ref = oracle.moe_layer_ref(E=shape.E, n_group=shape.n_group, topk_group=shape.topk_group, k=shape.k,
+                               routed_scaling=1.0, tau=0.8, n_bins=1, logits=inp.logits, cost=inp.cost,
+                               rule="cir", refill="none")
+    trans = ref["trans"]
+    for t in range(inp.logits.shape[0]):
+        want = [e for e in ref["orig_ids"][t] if trans[e]]
+        got = [e for e in ref["topk_ids"][t] if e >= 0]
+        assert sorted(got) == sorted(want)
+        assert abs(sum(ref["topk_w"][t]) - 1.0) < 1e-12
+    assert ref["stats"]["n_refill"] == 0
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_refill_random_takes_top_random_keys(seed):
+    from oracle.compensation import refill_key
+    shape, inp = _ablation_case(seed)
+    kw = dict(E=shape.E, n_group=shape.n_group, topk_group=shape.topk_group, k=shape.k, routed_scaling=1.0,
+              tau=0.8, n_bins=1, logits=inp.logits, cost=inp.cost, rule="cir")
+    score = oracle.moe_layer_ref(**kw, refill="score")
+    rnd = oracle.moe_layer_ref(**kw, refill="random", seed=7)
+    trans = rnd["trans"]
+    assert np.array_equal(trans, score["trans"])   # the refill never changes the pruning
+    pool_all = set(np.flatnonzero(trans).tolist())
+    for t in range(inp.logits.shape[0]):
+        orig = set(rnd["orig_ids"][t].tolist())
+        keep = {e for e in orig if trans[e]}
+        fin = {e for e in rnd["topk_ids"][t].tolist() if e >= 0}
+        assert keep <= fin and fin <= pool_all
+        assert len(fin) == min(shape.k, len(pool_all))
+        added = fin - keep
+        rest = pool_all - orig - added
+        # every added expert's key beats every left-out candidate's key
+        if added and rest:
+            assert min(refill_key(7, t, e, shape.E) for e in added) > max(refill_key(7, t, e, shape.E) for e in rest)
+    other = oracle.moe_layer_ref(**kw, refill="random", seed=8)
+    if rnd["stats"]["n_refill"] > 0:
+        assert not np.array_equal(rnd["topk_ids"], other["topk_ids"])
+
+
+def test_refill_variants_agree_without_pruning():
+    shape, inp = _ablation_case(1)
+    kw = dict(E=shape.E, n_group=shape.n_group, topk_group=shape.topk_group, k=shape.k, routed_scaling=1.0,
+              tau=0.0, n_bins=1, logits=inp.logits, cost=inp.cost)
+    a = oracle.moe_layer_ref(**kw, refill="score")
+    for mode in ("none", "random"):
+        b = oracle.moe_layer_ref(**kw, refill=mode, seed=3)
+        assert np.array_equal(a["topk_ids"], b["topk_ids"])
