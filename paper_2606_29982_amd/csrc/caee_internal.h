@@ -33,6 +33,12 @@ constexpr int kMaxTokenBlocks = CAEE_MAX_TOKEN_BLOCKS;
 #define CAEE_PREFILL_T 65536
 #endif
 constexpr int kPrefillT = CAEE_PREFILL_T;
+// 8-bit batches above this many tokens use 128-row big chunks and the
+// LDS-pipelined GEMM kernels (0 disables them).
+#ifndef CAEE_GEMM_T
+#define CAEE_GEMM_T 256
+#endif
+constexpr int kGemmT = CAEE_GEMM_T;
 constexpr int kFfnThreads = 256;    // 4 independent waves per FFN workgroup
 // Gate/up wave work items wanted per call before the contraction is split
 // (about 32 per SIMD: short items keep the tail of the launch short).
@@ -141,7 +147,8 @@ inline int small_token_blocks(const caee_layer_desc_t& d) { return d.T <= 16 ? 1
 // chunks since no slot can have more rows than T).
 inline int big_token_blocks(const caee_layer_desc_t& d) {
     if (d.T <= 16 * small_token_blocks(d)) return 0;
-    const int nb = d.T <= kPrefillT ? 4 : 8;
+    int nb = d.T <= kPrefillT ? 4 : 8;
+    if (kGemmT > 0 && d.w_dtype == CAEE_FP8_E4M3 && d.T > kGemmT) nb = 8;
     return nb < kMaxTokenBlocks ? nb : kMaxTokenBlocks;
 }
 
@@ -308,6 +315,8 @@ hipError_t launch_quant_rows(const void* src, int src_bf16, long long rows, int 
                              hipStream_t s);
 hipError_t launch_gate_up_fp8(const FfnParams& p, int nb, int max_chunks, hipStream_t s);
 hipError_t launch_quant_list(const FfnParams& p, int nb, int max_chunks, hipStream_t s);
+bool gemm_fp8_supports(const FfnParams& p, int nb);
+hipError_t launch_gemm_fp8(const FfnParams& p, bool gate_up, int max_chunks, hipStream_t s);
 hipError_t launch_down_fp8(const FfnParams& p, int nb, int max_chunks, hipStream_t s);
 hipError_t launch_pack(const void* src, void* dst, long long rows, long long row_units, long long count,
                        hipStream_t s);

@@ -408,18 +408,26 @@ __device__ inline void big_contract_fp8(u32x4_t (*sb)[NB][kStageSteps][kWave], f
     }
 }
 
-// Gate/up of big chunks: 4 adjacent 16-feature tiles of one chunk per
-// workgroup item, one per wave, over the whole contraction; fp32 rows out.
+#ifndef CAEE_FP8_BIG_TW_GU
+#define CAEE_FP8_BIG_TW_GU 1
+#endif
+#ifndef CAEE_FP8_BIG_TW_DN
+#define CAEE_FP8_BIG_TW_DN 2
+#endif
+
+// Gate/up of big chunks: 4 * kTW adjacent 16-feature tiles of one chunk per
+// workgroup item, kTW per wave, over the whole contraction; fp32 rows out.
 template <int NB>
 __global__ __launch_bounds__(kFfnThreads) void k_gate_up_fp8_big(FfnParams p) {
     constexpr int kWaves = kFfnThreads / kWave;
+    constexpr int kTW = CAEE_FP8_BIG_TW_GU;
     __shared__ u32x4_t s_b[2][NB][kStageSteps][kWave];
     __shared__ float s_x[2][16 * NB][2];
     const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
     const int r = lane & 15, g = lane >> 4;
     const int tiles = p.f / 16;
     const int n_chunks = ffn_list_size(p);
-    const int items_per_chunk = tiles / kWaves;
+    const int items_per_chunk = tiles / (kWaves * kTW);
     const int total = n_chunks * items_per_chunk;
     const size_t row_units = (size_t)p.d / 16;
     const size_t ksteps = row_units / 4;
@@ -428,19 +436,25 @@ __global__ __launch_bounds__(kFfnThreads) void k_gate_up_fp8_big(FfnParams p) {
     const int sblk = p.d / 128;
     for (int item = blockIdx.x; item < total; item += gridDim.x) {
         const int c = item / items_per_chunk;
-        const int jt = (item - c * items_per_chunk) * kWaves + wave;
+        const int jt0 = ((item - c * items_per_chunk) * kWaves + wave) * kTW;
         const ChunkRef ck = ffn_chunk(p, c);
         const int xs_ = ck.xs, row0 = ck.row0, ntok = ck.ntok;
         if (ffn_skip(p, xs_)) continue;   // uniform over the workgroup
         const int nb = (ntok + 15) >> 4;
         const u32x4_t* wb = (const u32x4_t*)ffn_weights(p, xs_, false, expert_bytes);
-        const u32x4_t* const a[2] = {
-            p.tiled ? wb + (size_t)jt * ksteps * 64 + lane : wb + (size_t)(jt * 16 + r) * row_units + g,
-            p.tiled ? wb + (size_t)(tiles + jt) * ksteps * 64 + lane
-                    : wb + (size_t)(p.f + jt * 16 + r) * row_units + g};
         const float* sbase = ffn_scales(p, xs_, false, (size_t)(2 * p.f / 128) * sblk);
-        const float* const wsc[2] = {sbase + (size_t)((jt * 16) / 128) * sblk,
-                                     sbase + (size_t)((p.f + jt * 16) / 128) * sblk};
+        // Fragments 2m and 2m+1: gate and up rows of feature tile jt0 + m.
+        const u32x4_t* a[2 * kTW];
+        const float* wsc[2 * kTW];
+#pragma unroll
+        for (int m = 0; m < kTW; ++m) {
+            const int jt = jt0 + m;
+            a[2 * m] = p.tiled ? wb + (size_t)jt * ksteps * 64 + lane : wb + (size_t)(jt * 16 + r) * row_units + g;
+            a[2 * m + 1] = p.tiled ? wb + (size_t)(tiles + jt) * ksteps * 64 + lane
+                                   : wb + (size_t)(p.f + jt * 16 + r) * row_units + g;
+            wsc[2 * m] = sbase + (size_t)((jt * 16) / 128) * sblk;
+            wsc[2 * m + 1] = sbase + (size_t)((p.f + jt * 16) / 128) * sblk;
+        }
         const u32x4_t* rows[NB];
         const float* rsc[NB];
 #pragma unroll
@@ -451,21 +465,24 @@ __global__ __launch_bounds__(kFfnThreads) void k_gate_up_fp8_big(FfnParams p) {
             rows[j] = (const u32x4_t*)p.xq + (size_t)tok * row_units;
             rsc[j] = p.xs + (size_t)tok * sblk;
         }
-        f32x4_t acc[2][NB];
+        f32x4_t acc[2 * kTW][NB];
 #pragma unroll
-        for (int m = 0; m < 2; ++m)
+        for (int m = 0; m < 2 * kTW; ++m)
 #pragma unroll
             for (int tb = 0; tb < NB; ++tb) acc[m][tb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-        big_contract_fp8<2, NB>(s_b, s_x, a, p.tiled ? 64 : 4, wsc, rows, rsc, nb, kblocks, acc);
-        const int col = jt * 16 + 4 * g;
+        big_contract_fp8<2 * kTW, NB>(s_b, s_x, a, p.tiled ? 64 : 4, wsc, rows, rsc, nb, kblocks, acc);
 #pragma unroll
-        for (int tb = 0; tb < NB; ++tb) {
-            const int n = tb * 16 + r;
-            if (tb < nb && n < ntok) {
-                float h[4];
+        for (int m = 0; m < kTW; ++m) {
+            const int col = (jt0 + m) * 16 + 4 * g;
 #pragma unroll
-                for (int v = 0; v < 4; ++v) h[v] = silu_mul(acc[0][tb][v], acc[1][tb][v]);
-                *(float4*)((float*)p.h + (size_t)(row0 + n) * p.f + col) = make_float4(h[0], h[1], h[2], h[3]);
+            for (int tb = 0; tb < NB; ++tb) {
+                const int n = tb * 16 + r;
+                if (tb < nb && n < ntok) {
+                    float h[4];
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) h[v] = silu_mul(acc[2 * m][tb][v], acc[2 * m + 1][tb][v]);
+                    *(float4*)((float*)p.h + (size_t)(row0 + n) * p.f + col) = make_float4(h[0], h[1], h[2], h[3]);
+                }
             }
         }
     }
@@ -476,7 +493,7 @@ __global__ __launch_bounds__(kFfnThreads) void k_gate_up_fp8_big(FfnParams p) {
 template <int NB>
 __global__ __launch_bounds__(kFfnThreads) void k_down_fp8_big(FfnParams p) {
     constexpr int kWaves = kFfnThreads / kWave;
-    constexpr int kTW = 2;
+    constexpr int kTW = CAEE_FP8_BIG_TW_DN;
     __shared__ u32x4_t s_b[2][NB][kStageSteps][kWave];
     __shared__ float s_x[2][16 * NB][2];
     const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
@@ -563,8 +580,9 @@ hipError_t launch_quant_list(const FfnParams& p, int nb, int max_chunks, hipStre
 }
 
 hipError_t launch_gate_up_fp8(const FfnParams& p, int nb, int max_chunks, hipStream_t s) {
+    if (gemm_fp8_supports(p, nb)) return launch_gemm_fp8(p, true, max_chunks, s);
     if (nb >= 4 && kBigStaged) {
-        const dim3 grid(grid_for_waves((long long)max_chunks * (p.f / 16)));
+        const dim3 grid(grid_for_waves((long long)max_chunks * (p.f / 16) / CAEE_FP8_BIG_TW_GU));
         if (nb == 4) hipLaunchKernelGGL(k_gate_up_fp8_big<4>, grid, dim3(kFfnThreads), 0, s, p);
         else if (nb == 8) hipLaunchKernelGGL(k_gate_up_fp8_big<8>, grid, dim3(kFfnThreads), 0, s, p);
         else return hipErrorInvalidValue;
@@ -582,8 +600,9 @@ hipError_t launch_gate_up_fp8(const FfnParams& p, int nb, int max_chunks, hipStr
 }
 
 hipError_t launch_down_fp8(const FfnParams& p, int nb, int max_chunks, hipStream_t s) {
+    if (gemm_fp8_supports(p, nb)) return launch_gemm_fp8(p, false, max_chunks, s);
     if (nb >= 4 && kBigStaged) {
-        const dim3 grid(grid_for_waves((long long)max_chunks * (p.d / 16) / 2));
+        const dim3 grid(grid_for_waves((long long)max_chunks * (p.d / 16) / CAEE_FP8_BIG_TW_DN));
         if (nb == 4) hipLaunchKernelGGL(k_down_fp8_big<4>, grid, dim3(kFfnThreads), 0, s, p);
         else if (nb == 8) hipLaunchKernelGGL(k_down_fp8_big<8>, grid, dim3(kFfnThreads), 0, s, p);
         else return hipErrorInvalidValue;

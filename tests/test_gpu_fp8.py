@@ -38,7 +38,9 @@ def test_tiny_fp8(seed, tiled):
     print(f"  max|err|/max|ref| = {rel:.3e}")
 
 
-@pytest.mark.parametrize("T", [1, 5, 40, 130])
+# T=600 takes the prefill GEMM (128-row chunks): ragged chunk tails, a
+# one-block contraction in the down product (f=128) and two in gate/up.
+@pytest.mark.parametrize("T", [1, 5, 40, 130, 600])
 def test_tiny_fp8_batches(T):
     _tiny(7, 0.2, 4, T=T, tiled=True, zipf=1.1 if T > 100 else None)
 
