@@ -271,6 +271,18 @@ def offload_rows(args, shape, Wt, dev, link_model=None):
             "miss_cost_source": "calibrated" if link_model is not None else "measured peak", "rows": rows}
 
 
+def known_copy(args, dev):
+    """One device-to-device copy of --copy-bytes bytes: a kernel of known
+    traffic that calibrates the profiler's HBM byte counters."""
+    import torch
+    if args.copy_bytes > 0:
+        src = torch.empty(args.copy_bytes, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+
+
 def run_case(args, dev):
     """One configuration (e.g. for a profiler run): the sweep's inputs for
     bf16 (Zipf-skewed when asked, 8 bins, no pruning) or the 8-bit rows'
@@ -352,6 +364,7 @@ def main():
     if args.case:
         import torch
         run_case(args, torch.device("cuda:0"))
+        known_copy(args, torch.device("cuda:0"))
         return
     import torch
     from paper_2606_29982_amd import caee
@@ -477,12 +490,7 @@ def main():
     if not args.no_offload:
         result["offload"] = offload_rows(args, shape, Wt, dev, link_model)
 
-    if args.copy_bytes > 0:
-        src = torch.empty(args.copy_bytes, dtype=torch.uint8, device=dev)
-        dst = torch.empty_like(src)
-        dst.copy_(src)
-        torch.cuda.synchronize()
-        del src, dst
+    known_copy(args, dev)
     if not args.no_cpu:
         log("timing the fp64 oracle on the host")
         result["cpu_baseline"] = cpu_baseline(shape, head, W, sample_tokens=args.T)

@@ -230,6 +230,8 @@ FfnParams make_ffn_params(const caee_layer_desc_t* d, const void* x, const int32
     p.xs = (float*)(ws + L.xs);
     p.hq = (uint8_t*)(ws + L.hq);
     p.hs = (float*)(ws + L.hs);
+    p.xst = (float*)(ws + L.xst);
+    p.hst = (float*)(ws + L.hst);
     return p;
 }
 
@@ -299,7 +301,7 @@ caee_status_t ffn_begin(const caee_layer_desc_t* d, const FfnParams& p, const Ws
 
 caee_status_t ffn_routed(const caee_layer_desc_t* d, const FfnParams& p, const WsLayout& L, FfnCall* call,
                          bool big_on_side) {
-    const int nb_small = small_token_blocks(*d), nb_big = big_token_blocks(*d);
+    const int nb_small = small_token_blocks(*d), nb_big = call_big_blocks(*d, p.tiled);
     hipStream_t s = call->main;
     // The big chunks (few, long, latency-bound work items) run on a side
     // stream next to the small ones (many, bandwidth-bound): disjoint rows.
@@ -315,14 +317,19 @@ caee_status_t ffn_routed(const caee_layer_desc_t* d, const FfnParams& p, const W
         sb = call->side;
     }
     // One list's chain: gate/up, (fp8) quantisation of its SwiGLU rows, down.
+    // The 8-bit GEMM reads its rows' block scales transposed and in permuted
+    // row order: gathered once for x, written so by the quantiser for H.
     auto chain = [&](int list, int nb, hipStream_t st) -> caee_status_t {
+        const bool gemm = d->w_dtype == CAEE_FP8_E4M3 && nb == gemm_fp8_blocks() && gemm_fp8_applies(*d, p.tiled);
+        FfnParams q = p;
+        q.list = list;
+        if (gemm)
+            CAEE_TRY(timed_launch(CAEE_KERNEL_QUANT, st, "gather x scales",
+                                  [&] { return launch_gather_xs(q, L.max_chunks, st); }));
         CAEE_TRY(gate_up_list(d, p, list, nb, L.max_chunks, st));
-        if (d->w_dtype == CAEE_FP8_E4M3) {
-            FfnParams q = p;
-            q.list = list;
+        if (d->w_dtype == CAEE_FP8_E4M3)
             CAEE_TRY(timed_launch(CAEE_KERNEL_QUANT, st, "quantise H",
-                                  [&] { return launch_quant_list(q, nb, L.max_chunks, st); }));
-        }
+                                  [&] { return launch_quant_list(q, nb, L.max_chunks, gemm, st); }));
         return down_list(d, p, list, nb, L.max_chunks, st);
     };
     if (nb_big) CAEE_TRY(chain(1, nb_big, sb));
@@ -413,6 +420,7 @@ caee_status_t caee_expert_ffn(const caee_layer_desc_t* desc, const void* x, cons
     CAEE_TRY(check_ws(desc, ws, ws_bytes, &L));
     if (desc->T == 0) return CAEE_OK;
     RouteParams p = make_route_params(desc, nullptr, nullptr, nullptr, nullptr, (char*)ws, L);
+    p.chunk_big = call_chunk_big(*desc, weights->layout == CAEE_LAYOUT_TILED);
     p.topk_ids = const_cast<int32_t*>(topk_ids);
     p.do_permute = 1;
     hipStream_t s = as_stream(stream);
@@ -439,6 +447,7 @@ caee_status_t caee_moe_layer(const caee_layer_desc_t* desc, const void* x, const
     if (desc->T == 0) return CAEE_OK;
     char* wsb = (char*)ws;
     RouteParams p = make_route_params(desc, logits, bias, cost, bin, wsb, L);
+    p.chunk_big = call_chunk_big(*desc, weights->layout == CAEE_LAYOUT_TILED);
     hipStream_t s = as_stream(stream);
     set_route_outputs(p, out, wsb, L);
     const FfnParams fp = make_ffn_params(desc, x, p.topk_ids, p.topk_w, weights, y, wsb, L);

@@ -33,8 +33,9 @@ constexpr int kMaxTokenBlocks = CAEE_MAX_TOKEN_BLOCKS;
 #define CAEE_PREFILL_T 65536
 #endif
 constexpr int kPrefillT = CAEE_PREFILL_T;
-// 8-bit batches above this many tokens use 128-row big chunks and the
-// LDS-pipelined GEMM kernels (0 disables them).
+// 8-bit batches above this many tokens run their big chunks (as wide as the
+// GEMM's token tile) with the LDS-pipelined GEMM kernels, when the weights
+// are tiled and the sizes fit (0 disables them).
 #ifndef CAEE_GEMM_T
 #define CAEE_GEMM_T 256
 #endif
@@ -97,6 +98,7 @@ struct WsLayout {
     size_t y;                   // [P][d] fp32 expert outputs
     size_t xq, xs;              // fp8 path: [T][d] e4m3 codes of x and [T][d/128] fp32 scales
     size_t hq, hs;              // fp8 path: [P][f] e4m3 codes of H and [P][f/128] fp32 scales
+    size_t xst, hst;            // fp8 GEMM: [d/128][P] and [f/128][P] block scales of the permuted rows
     size_t total;
     int P, max_chunks, ksplit;
     int chunk_small;            // an expert slot with at most this many rows is one small chunk
@@ -152,6 +154,25 @@ inline int big_token_blocks(const caee_layer_desc_t& d) {
     return nb < kMaxTokenBlocks ? nb : kMaxTokenBlocks;
 }
 
+bool gemm_fp8_applies(const caee_layer_desc_t& d, bool tiled);
+int gemm_fp8_blocks();
+
+// 16-token column blocks of a call's big chunks: the width of the 8-bit
+// GEMM's tile when that kernel runs the call's big list (its chunks are as
+// wide as its tile), big_token_blocks otherwise.  The chunk lists and the FFN
+// launches both take it from here; the workspace is sized for
+// big_token_blocks, which never gives fewer chunks.
+inline int call_big_blocks(const caee_layer_desc_t& d, bool tiled) {
+    const int nb = big_token_blocks(d);
+    return nb > 0 && gemm_fp8_applies(d, tiled) ? gemm_fp8_blocks() : nb;
+}
+
+// Rows per big chunk of a call (16 when there are no big chunks).
+inline int call_chunk_big(const caee_layer_desc_t& d, bool tiled) {
+    const int nb = call_big_blocks(d, tiled);
+    return 16 * (nb > 0 ? nb : 1);
+}
+
 inline WsLayout ws_layout(const caee_layer_desc_t& d) {
     WsLayout L{};
     const size_t T = d.T > 0 ? d.T : 0;
@@ -187,6 +208,9 @@ inline WsLayout ws_layout(const caee_layer_desc_t& d) {
     L.xs = take(fp8 ? T * (d.d / 128) * 4 : 0);
     L.hq = take(fp8 ? size_t(L.P) * d.f : 0);
     L.hs = take(fp8 ? size_t(L.P) * (d.f / 128) * 4 : 0);
+    const bool gemm = fp8 && kGemmT > 0 && d.T > kGemmT;
+    L.xst = take(gemm ? size_t(L.P) * (d.d / 128) * 4 : 0);
+    L.hst = take(gemm ? size_t(L.P) * (d.f / 128) * 4 : 0);
     L.ksplit = gate_up_split(d);
     L.total = off;
     return L;
@@ -268,6 +292,8 @@ struct FfnParams {
     float* xs;
     uint8_t* hq;
     float* hs;
+    float* xst;       // 8-bit GEMM: block scales transposed, [block][permuted row]
+    float* hst;
 };
 
 // ---------------------------------------------------------------------------
@@ -314,7 +340,8 @@ hipError_t launch_combine(const FfnParams& p, hipStream_t s);
 hipError_t launch_quant_rows(const void* src, int src_bf16, long long rows, int cols, uint8_t* q, float* scale,
                              hipStream_t s);
 hipError_t launch_gate_up_fp8(const FfnParams& p, int nb, int max_chunks, hipStream_t s);
-hipError_t launch_quant_list(const FfnParams& p, int nb, int max_chunks, hipStream_t s);
+hipError_t launch_quant_list(const FfnParams& p, int nb, int max_chunks, bool transposed, hipStream_t s);
+hipError_t launch_gather_xs(const FfnParams& p, int max_chunks, hipStream_t s);
 bool gemm_fp8_supports(const FfnParams& p, int nb);
 hipError_t launch_gemm_fp8(const FfnParams& p, bool gate_up, int max_chunks, hipStream_t s);
 hipError_t launch_down_fp8(const FfnParams& p, int nb, int max_chunks, hipStream_t s);

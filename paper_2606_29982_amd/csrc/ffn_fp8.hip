@@ -46,8 +46,7 @@ __device__ inline uint32_t e4m3_code(float v) {
 // wavefront (two per lane): scale = amax / 448 (1 for an all-zero block),
 // code = e4m3(value / scale), all in fp32.
 __device__ inline void quant_block(const void* src, int src_bf16, long long row, int blk, int cols, uint8_t* q,
-                                   float* scale, int lane) {
-    const int nblk = cols / 128;
+                                   float* scale, long long srow, long long sblk, int lane) {
     const long long base = row * cols + blk * 128 + 2 * lane;
     float v0, v1;
     if (src_bf16) {
@@ -65,7 +64,7 @@ __device__ inline void quant_block(const void* src, int src_bf16, long long row,
     const float sc = amax > 0.0f ? amax / kE4M3Max : 1.0f;
     const uint32_t c0 = e4m3_code(v0 / sc), c1 = e4m3_code(v1 / sc);
     *(uint16_t*)(q + base) = (uint16_t)(c0 | (c1 << 8));
-    if (lane == 0) scale[row * nblk + blk] = sc;
+    if (lane == 0) scale[row * srow + blk * sblk] = sc;
 }
 
 // All blocks of `rows` consecutive rows, one wavefront per block.
@@ -76,12 +75,14 @@ __global__ __launch_bounds__(256) void k_quant_rows(const void* src, int src_bf1
     const int nblk = cols / 128;
     if (w >= rows * nblk) return;
     const long long row = w / nblk;
-    quant_block(src, src_bf16, row, (int)(w - row * nblk), cols, q, scale, lane);
+    quant_block(src, src_bf16, row, (int)(w - row * nblk), cols, q, scale, nblk, 1, lane);
 }
 
 // The fp32 SwiGLU rows of the chunks of one work list (at most rows_max
 // rows per chunk), so that each list's chain can run on its own stream.
-__global__ __launch_bounds__(256) void k_quant_list(FfnParams p, int rows_max) {
+// Scales go to hs ([row][block]), or transposed to hst ([block][row]) for
+// the 8-bit GEMM.
+__global__ __launch_bounds__(256) void k_quant_list(FfnParams p, int rows_max, int transposed) {
     const int lane = threadIdx.x & (kWave - 1);
     const int nblk = p.f / 128;
     const long long per_chunk = (long long)rows_max * nblk;
@@ -92,7 +93,8 @@ __global__ __launch_bounds__(256) void k_quant_list(FfnParams p, int rows_max) {
         const int r = rem / nblk;
         const ChunkRef ck = ffn_chunk(p, c);
         if (r >= ck.ntok) continue;
-        quant_block(p.h, 0, ck.row0 + r, rem - r * nblk, p.f, p.hq, p.hs, lane);
+        if (transposed) quant_block(p.h, 0, ck.row0 + r, rem - r * nblk, p.f, p.hq, p.hst, 1, p.P, lane);
+        else quant_block(p.h, 0, ck.row0 + r, rem - r * nblk, p.f, p.hq, p.hs, nblk, 1, lane);
     }
 }
 
@@ -569,13 +571,13 @@ hipError_t launch_quant_rows(const void* src, int src_bf16, long long rows, int 
     return hipGetLastError();
 }
 
-hipError_t launch_quant_list(const FfnParams& p, int nb, int max_chunks, hipStream_t s) {
+hipError_t launch_quant_list(const FfnParams& p, int nb, int max_chunks, bool transposed, hipStream_t s) {
     const long long waves = (long long)max_chunks * 16 * nb * (p.f / 128);
     long long blocks = (waves + 3) / 4;
     const long long cap = (long long)device_cu_count() * 16;
     if (blocks > cap) blocks = cap;
     if (blocks < 1) blocks = 1;
-    hipLaunchKernelGGL(k_quant_list, dim3((unsigned)blocks), dim3(256), 0, s, p, 16 * nb);
+    hipLaunchKernelGGL(k_quant_list, dim3((unsigned)blocks), dim3(256), 0, s, p, 16 * nb, transposed ? 1 : 0);
     return hipGetLastError();
 }
 

@@ -1,19 +1,29 @@
-// Prefill-class 8-bit expert products for big chunks (up to 128 rows).
+// Prefill-class 8-bit expert products for big chunks.
 //
-// A workgroup computes a 256-weight-row x 128-token tile of one chunk over
-// the whole contraction, one 128-wide block (one scaled 16x16x128 MFMA deep)
-// per pipeline stage.  Weights (tiled order: the 2 KB of one 16-row tile and
-// one block are contiguous), the chunk's token rows and the rows' block
-// scales go straight from global memory to LDS with the 16-byte (and 4-byte)
-// direct-to-LDS loads of gfx950, three stages in a ring, so that two stages
-// of loads are in flight while one is multiplied and no register holds
-// staged data.  Every wave issues the same number of loads per stage, so a
-// wave waits for its oldest stage with a constant vmcnt, and one barrier per
-// stage makes all waves' loads of that stage visible.
+// A workgroup of 8 waves computes a 256-weight-row x 128-token tile (or,
+// built with CAEE_GEMM_TILES=8, 128 x 256) of one chunk over the whole
+// contraction, one 128-wide block (one scaled 16x16x128
+// MFMA deep) per pipeline stage.  Weights (tiled order: the 2 KB of one
+// 16-row tile and one block are contiguous), the chunk's token rows and the
+// rows' block scales go straight from global memory to LDS with the 16-byte
+// (and 4-byte) direct-to-LDS loads of gfx950, three stages in a ring, so that
+// two stages of loads are in flight while one is multiplied and no register
+// holds staged data.  Every wave issues the same number of loads per stage,
+// so a wave waits for its oldest stage with a constant vmcnt, and one barrier
+// per stage makes all waves' loads of that stage visible.
 //
-//   gate/up: the tile is 8 features (gate and up rows of each); wave w owns
-//            features 2w, 2w+1 -> fp32 SwiGLU rows;
-//   down:    the tile is 256 rows of W2; wave w owns 4 row tiles -> fp32 Y rows.
+// The tile is as wide in tokens as a chunk can be.  Each wave owns 4 weight
+// tiles x 4 token tiles (64 x 64 outputs); two waves share a SIMD, so one
+// wave's fp32 block-scale arithmetic (VALU) overlaps the other's matrix
+// instructions.  With R = kTiles / 4 waves across the rows, wave
+// w = R * c + q takes token tiles 4c .. 4c + 3 and
+//   gate/up: features 2q, 2q + 1 of the tile's kTiles / 2 (gate and up rows
+//            of each) -> fp32 SwiGLU rows;
+//   down:    row tiles 4q .. 4q + 3 -> fp32 Y rows.
+// The rows' block scales are read transposed ([block][permuted row]), one
+// 128-byte line per wave and block.  Measured at the 4096-token prefill, the
+// 256 x 128 tile is faster than 128 x 256 (which reads each weight byte once
+// for experts with up to 256 rows, but issues twice the token-row loads).
 #include "caee_internal.h"
 
 namespace caee {
@@ -25,16 +35,33 @@ typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void lds_void_t;
 
 constexpr int kScaleOne = 127;        // E8M0 1.0: the MFMA's own block scales are unused
-constexpr int kTiles = 16;            // 16-row weight tiles per workgroup tile
-constexpr int kNT = 8;                // 16-token tiles per workgroup tile (128 tokens)
+// Workgroup tile: kTiles 16-row weight tiles x kNT 16-token tiles, 8 waves
+// of 4 x 4 tiles each.
+#ifndef CAEE_GEMM_TILES
+#define CAEE_GEMM_TILES 16
+#endif
+constexpr int kTiles = CAEE_GEMM_TILES;
+constexpr int kNT = 128 / kTiles;
+constexpr int kWaveNT = 4;            // token tiles per wave
+constexpr int kRowWaves = kTiles / 4; // waves across the weight rows
+constexpr int kXPer = 2 * kNT;        // tokens whose scales one wave loads
+static_assert(kTiles == 8 || kTiles == 16, "tile shape");
+// Whether the items are laid out by XCD (see the kernel; measured slower at
+// the 4096-token prefill, so off by default).
+#ifndef CAEE_GEMM_XCD
+#define CAEE_GEMM_XCD 0
+#endif
 constexpr int kStages = 3;
-constexpr int kLoadsPerStage = 13;    // per wave: 8 weight, 4 row, 1 scale loads
+constexpr int kGemmWaves = 8;
+constexpr int kGemmThreads = kGemmWaves * kWave;
+constexpr int kLoadsPerStage = 7;     // per wave: 2 weight, 4 row, 1 scale loads
 constexpr int kMaxKBlocks = 128;      // contraction up to 16384
+constexpr int kXcds = 8;              // accelerator complex dies, each with its own L2
 
 struct GemmStage {
     u32x4_t a[kTiles][2][kWave];      // weight fragments: [tile][half of the block][lane]
     u32x4_t b[kNT][2][kWave];         // token-row fragments: [token tile][half][lane]
-    float x[4][kWave];                // row scales: token n at [n / 32][n % 32]
+    float x[kGemmWaves][kWave];       // row scales: token n at [n / kXPer][n % kXPer]
 };
 
 __device__ inline i32x8_t join(const u32x4_t& lo, const u32x4_t& hi) {
@@ -60,8 +87,8 @@ __device__ inline void stage_barrier() {
 }
 
 template <bool kGateUp>
-__global__ __launch_bounds__(kFfnThreads) void k_gemm_fp8(FfnParams p) {
-    // The ring's stages are separate LDS objects (and the loop below names
+__global__ __launch_bounds__(kGemmThreads) void k_gemm_fp8(FfnParams p) {
+    // The ring's stages are separate LDS objects (and the code below names
     // each statically), so the compiler can tell a read of one stage from the
     // loads still filling the others and does not wait for those.
     __shared__ GemmStage st0, st1, st2;
@@ -70,6 +97,7 @@ __global__ __launch_bounds__(kFfnThreads) void k_gemm_fp8(FfnParams p) {
     // pipeline, as a global load there would make the wave drain its loads.
     __shared__ float wsl[2][kMaxKBlocks];
     const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+    const int wq = wave % kRowWaves, wc = wave / kRowWaves;   // weight rows, token columns
     const int r = lane & 15, g = lane >> 4;
     const int K = kGateUp ? p.d : p.f;                 // contraction length
     const int kblocks = K / 128;
@@ -81,7 +109,20 @@ __global__ __launch_bounds__(kFfnThreads) void k_gemm_fp8(FfnParams p) {
     const int total = n_chunks * groups;
     const size_t expert_bytes = kGateUp ? (size_t)2 * p.f * p.d : (size_t)p.d * p.f;
     const size_t scales_per_expert = (size_t)((kGateUp ? 2 * p.f : p.d) / 128) * kblocks;
-    for (int item = blockIdx.x; item < total; item += gridDim.x) {
+    const f32x4_t zero = {0.f, 0.f, 0.f, 0.f};
+    // Workgroups go to the XCDs round robin (workgroup b to XCD b % 8).  With
+    // a grid that is a multiple of 8, XCD x takes the x-th eighth of the item
+    // list, so the items of one chunk (same token rows, different weight
+    // groups) and those of one expert's consecutive chunks (same weights) run
+    // at the same time on one XCD and share its L2.
+    int item = blockIdx.x, item_end = total, item_step = gridDim.x;
+    if (CAEE_GEMM_XCD && gridDim.x % kXcds == 0) {
+        const int x = blockIdx.x % kXcds, per = gridDim.x / kXcds;
+        item = (int)((long long)x * total / kXcds) + blockIdx.x / kXcds;
+        item_end = (int)((long long)(x + 1) * total / kXcds);
+        item_step = per;
+    }
+    for (; item < item_end; item += item_step) {
         const int c = item / groups, grp = item - c * groups;
         const ChunkRef ck = ffn_chunk(p, c);
         const int xs = ck.xs, row0 = ck.row0, ntok = ck.ntok;
@@ -94,76 +135,72 @@ __global__ __launch_bounds__(kFfnThreads) void k_gemm_fp8(FfnParams p) {
             if (kGateUp) return i < kTiles / 2 ? grp * (kTiles / 2) + i : p.f / 16 + grp * (kTiles / 2) + i - kTiles / 2;
             return grp * kTiles + i;
         };
-        // This wave's loads: weight tiles 4w..4w+3 (both halves), row blocks
-        // j = 4w..4w+3 (token tile j/2, half j%2), and scales of tokens
-        // 32w..32w+31 (lanes 32..63 repeat them into padding).
-        const u32x4_t* asrc[4];
+        // This wave's loads per stage: (tile, half) pairs j = kTiles/4 * w + i
+        // of the weights, (token tile, half) pairs j = kNT/4 * w + i of the
+        // rows, and the scales of tokens kXPer * w .. + kXPer - 1 (the other
+        // lanes repeat them into padding).
+        const u32x4_t* asrc[kTiles / 4];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) asrc[i] = wb + (size_t)tile_of(4 * wave + i) * ksteps * 64 + lane;
-        const u32x4_t* bsrc[4];
+        for (int i = 0; i < kTiles / 4; ++i) {
+            const int j = kTiles / 4 * wave + i;
+            asrc[i] = wb + (size_t)tile_of(j >> 1) * ksteps * 64 + (j & 1) * 64 + lane;
+        }
+        const u32x4_t* bsrc[kNT / 4];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int j = 4 * wave + i, tb = j >> 1;
-            int n = 16 * tb + r;
+        for (int i = 0; i < kNT / 4; ++i) {
+            const int j = kNT / 4 * wave + i;
+            int n = 16 * (j >> 1) + r;
             n = n < ntok ? n : 0;          // padded token columns read a valid row; results dropped
             const int row = kGateUp ? ffn_token(p, xs, row0 + n) : row0 + n;
             bsrc[i] = (const u32x4_t*)(kGateUp ? (const void*)p.xq : (const void*)p.hq) + (size_t)row * row_units +
                       (j & 1) * 4 + g;
         }
+        // Row scales, transposed and in permuted row order ([block][row]):
+        // one 128-byte line per wave and block.
         const float* xsrc;
         {
-            int n = 32 * wave + (lane & 31);
+            int n = kXPer * wave + lane % kXPer;
             n = n < ntok ? n : 0;
-            const int row = kGateUp ? ffn_token(p, xs, row0 + n) : row0 + n;
-            xsrc = (kGateUp ? p.xs : p.hs) + (size_t)row * kblocks;
+            xsrc = (kGateUp ? p.xst : p.hst) + row0 + n;
         }
-        auto issue = [&](int kb, GemmStage& s) {
+        auto issue = [&](int kb, GemmStage& s) __attribute__((always_inline)) {
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
+            for (int i = 0; i < kTiles / 4; ++i) {
+                const int j = kTiles / 4 * wave + i;
+                __builtin_amdgcn_global_load_lds((const void*)(asrc[i] + (size_t)kb * 128),
+                                                 (lds_void_t*)&s.a[j >> 1][j & 1][0], 16, 0, 0);
+            }
 #pragma unroll
-                for (int h = 0; h < 2; ++h)
-                    __builtin_amdgcn_global_load_lds((const void*)(asrc[i] + (size_t)(2 * kb + h) * 64),
-                                                     (lds_void_t*)&s.a[4 * wave + i][h][0], 16, 0, 0);
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int j = 4 * wave + i;
+            for (int i = 0; i < kNT / 4; ++i) {
+                const int j = kNT / 4 * wave + i;
                 __builtin_amdgcn_global_load_lds((const void*)(bsrc[i] + (size_t)kb * 8),
                                                  (lds_void_t*)&s.b[j >> 1][j & 1][0], 16, 0, 0);
             }
-            __builtin_amdgcn_global_load_lds((const void*)(xsrc + kb), (lds_void_t*)&s.x[wave][0], 4, 0, 0);
+            __builtin_amdgcn_global_load_lds((const void*)(xsrc + (size_t)kb * p.P), (lds_void_t*)&s.x[wave][0], 4, 0, 0);
         };
-        // Fragments this wave multiplies: gate/up -> slots 2w, 2w+1 (gate)
-        // and 8+2w, 9+2w (up); down -> slots 4w..4w+3.
-        int aslot[4];
+        // Weight tiles this wave multiplies: gate/up -> slots 2q, 2q+1 (gate)
+        // and 4+2q, 5+2q (up); down -> slots 4q..4q+3.
+        int aslot[4], srow[4];
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-            aslot[i] = kGateUp ? (i < 2 ? 2 * wave + i : kTiles / 2 + 2 * wave + i - 2) : 4 * wave + i;
-        int srow[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) srow[i] = aslot[i] >= kTiles / 2;
-        for (int q = tid; q < 2 * kblocks; q += kFfnThreads) {
+        for (int i = 0; i < 4; ++i) {
+            aslot[i] = kGateUp ? (i < 2 ? 2 * wq + i : kTiles / 2 + 2 * wq + i - 2) : 4 * wq + i;
+            srow[i] = aslot[i] >= kTiles / 2;
+        }
+        for (int q = tid; q < 2 * kblocks; q += kGemmThreads) {
             const int h = q >= kblocks, kb = q - h * kblocks;
             const int row = (tile_of(h * (kTiles / 2)) * 16) / 128;
             wsl[h][kb] = wsc[(size_t)row * kblocks + kb];
         }
         __syncthreads();
 
-        f32x4_t acc[4][kNT];
+        f32x4_t acc[4][kWaveNT];
 #pragma unroll
         for (int i = 0; i < 4; ++i)
 #pragma unroll
-            for (int n = 0; n < kNT; ++n) acc[i][n] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-        const f32x4_t zero = {0.f, 0.f, 0.f, 0.f};
+            for (int j = 0; j < kWaveNT; ++j) acc[i][j] = zero;
 
-        // One pipeline step: wait for this wave's loads of stage kb (the
-        // loads of stage kb + 1 may stay in flight), make every wave's loads
-        // visible, refill the stage freed by step kb - 1 with block kb + 2,
-        // then multiply stage kb.
-        auto step = [&](int kb, const GemmStage& s, GemmStage& ahead) {
-            if (kb + 1 < kblocks) wait_vm<kLoadsPerStage>();
-            else wait_vm<0>();
-            stage_barrier();
-            if (kb + 2 < kblocks) issue(kb + 2, ahead);
+        // Multiplies block kb, held in stage s.
+        auto compute = [&](int kb, const GemmStage& s) __attribute__((always_inline)) {
             i32x8_t af[4];
             float ws[4];
 #pragma unroll
@@ -172,72 +209,139 @@ __global__ __launch_bounds__(kFfnThreads) void k_gemm_fp8(FfnParams p) {
                 ws[i] = wsl[srow[i]][kb];
             }
 #pragma unroll
-            for (int n = 0; n < kNT; ++n) {
+            for (int j = 0; j < kWaveNT; ++j) {
+                const int n = kWaveNT * wc + j;
                 if (n < nb) {
                     const i32x8_t bf = join(s.b[n][0][lane], s.b[n][1][lane]);
                     const int tok = 16 * n + r;
-                    const float xsv = s.x[tok >> 5][tok & 31];
+                    const float xsv = s.x[tok / kXPer][tok % kXPer];
                     f32x4_t part[4];
 #pragma unroll
                     for (int i = 0; i < 4; ++i)
                         part[i] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(af[i], bf, zero, 0, 0, 0,
                                                                                   kScaleOne, 0, kScaleOne);
 #pragma unroll
-                    for (int i = 0; i < 4; ++i) acc[i][n] += part[i] * (ws[i] * xsv);
+                    for (int i = 0; i < 4; ++i) acc[i][j] += part[i] * (ws[i] * xsv);
                 }
             }
         };
-        issue(0, st0);
-        // Always a full second stage (block 0 again when there is one block;
-        // never read), so that every path into the loop has the same loads
-        // in flight and the compiler adds no wait of its own.
-        issue(kblocks > 1 ? 1 : 0, st1);
-        for (int kb = 0; kb < kblocks; kb += kStages) {
-            step(kb, st0, st2);
-            if (kb + 1 < kblocks) step(kb + 1, st1, st0);
-            if (kb + 2 < kblocks) step(kb + 2, st2, st1);
+        // Pipeline step v (< kblocks) issues block v into stage v % 3 and
+        // multiplies block v - 2.  Before multiplying, the wave waits for its
+        // own loads of block v - 2 (those of block v - 1 may stay in flight),
+        // and a barrier makes every wave's loads visible; the same barrier
+        // guarantees that all waves are done with block v - 3, whose stage
+        // block v refills.  Waits and loads are unconditional and each stage
+        // is named statically, so the compiler's wait analysis can tell that
+        // the stage read is complete and adds no waits of its own.
+        auto step = [&](int v, GemmStage& fill, const GemmStage& use) __attribute__((always_inline)) {
+            wait_vm<kLoadsPerStage>();
+            stage_barrier();
+            issue(v, fill);
+            if (v >= 2) compute(v - 2, use);
+        };
+        // The last two blocks, held in stages s2 (block kblocks - 2) and s1.
+        auto tail = [&](const GemmStage& s2, const GemmStage& s1) __attribute__((always_inline)) {
+            if (kblocks >= 2) {
+                wait_vm<kLoadsPerStage>();
+                stage_barrier();
+                compute(kblocks - 2, s2);
+            }
+            wait_vm<0>();
+            stage_barrier();
+            compute(kblocks - 1, s1);
+        };
+        const int full = kblocks - kblocks % kStages;
+#pragma clang loop unroll(disable)
+        for (int v = 0; v < full; v += kStages) {
+            step(v, st0, st1);
+            step(v + 1, st1, st2);
+            step(v + 2, st2, st0);
+        }
+        switch (kblocks % kStages) {
+            case 0:
+                tail(st1, st2);
+                break;
+            case 1:
+                step(full, st0, st1);
+                tail(st2, st0);
+                break;
+            default:
+                step(full, st0, st1);
+                step(full + 1, st1, st2);
+                tail(st0, st1);
+                break;
         }
         // All waves are done with the ring before the next item refills it.
         stage_barrier();
 #pragma unroll
-        for (int n = 0; n < kNT; ++n) {
-            const int tn = 16 * n + r;
+        for (int j = 0; j < kWaveNT; ++j) {
+            const int n = kWaveNT * wc + j, tn = 16 * n + r;
             if (n >= nb || tn >= ntok) continue;
             if (kGateUp) {
 #pragma unroll
                 for (int i = 0; i < 2; ++i) {
-                    const int col = (grp * (kTiles / 2) + 2 * wave + i) * 16 + 4 * g;
+                    const int col = (grp * (kTiles / 2) + 2 * wq + i) * 16 + 4 * g;
                     float h[4];
 #pragma unroll
-                    for (int v = 0; v < 4; ++v) h[v] = silu_mul(acc[i][n][v], acc[i + 2][n][v]);
+                    for (int v = 0; v < 4; ++v) h[v] = silu_mul(acc[i][j][v], acc[i + 2][j][v]);
                     *(float4*)((float*)p.h + (size_t)(row0 + tn) * p.f + col) = make_float4(h[0], h[1], h[2], h[3]);
                 }
             } else {
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    float* o = p.yperm + (size_t)(row0 + tn) * p.d + (grp * kTiles + 4 * wave + i) * 16 + 4 * g;
-                    *(float4*)o = make_float4(acc[i][n][0], acc[i][n][1], acc[i][n][2], acc[i][n][3]);
+                    float* o = p.yperm + (size_t)(row0 + tn) * p.d + (grp * kTiles + 4 * wq + i) * 16 + 4 * g;
+                    *(float4*)o = make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
                 }
             }
         }
     }
 }
 
-}  // namespace
-
-bool gemm_fp8_supports(const FfnParams& p, int nb) {
-    return nb == kNT && p.tiled && p.f % 128 == 0 && p.d % 256 == 0 && p.d / 128 <= kMaxKBlocks &&
-           p.f / 128 <= kMaxKBlocks;
+// Block scales of x for the rows of the big chunks, transposed and in
+// permuted row order: xst[b][row] = xs[token of row][b].  One workgroup per
+// chunk, one thread per row (coalesced stores).
+__global__ __launch_bounds__(256) void k_gather_xs(FfnParams p) {
+    const int nblk = p.d / 128;
+    for (int c = blockIdx.x; c < ffn_list_size(p); c += gridDim.x) {
+        const ChunkRef ck = ffn_chunk(p, c);
+        for (int n = threadIdx.x; n < ck.ntok; n += blockDim.x) {
+            const int row = ck.row0 + n;
+            const float* src = p.xs + (size_t)ffn_token(p, ck.xs, row) * nblk;
+            for (int b = 0; b < nblk; ++b) p.xst[(size_t)b * p.P + row] = src[b];
+        }
+    }
 }
 
+}  // namespace
+
+hipError_t launch_gather_xs(const FfnParams& p, int max_chunks, hipStream_t s) {
+    const int blocks = max_chunks > 0 ? max_chunks : 1;
+    hipLaunchKernelGGL(k_gather_xs, dim3((unsigned)blocks), dim3(256), 0, s, p);
+    return hipGetLastError();
+}
+
+bool gemm_fp8_supports(const FfnParams& p, int nb) {
+    return nb == kNT && p.tiled && p.f % 128 == 0 && p.d % 128 == 0 && p.d % (16 * kTiles) == 0 &&
+           p.d / 128 <= kMaxKBlocks && p.f / 128 <= kMaxKBlocks;
+}
+
+bool gemm_fp8_applies(const caee_layer_desc_t& d, bool tiled) {
+    return kGemmT > 0 && d.w_dtype == CAEE_FP8_E4M3 && d.T > kGemmT && tiled && d.f % 128 == 0 &&
+           d.d % 128 == 0 && d.d % (16 * kTiles) == 0 && d.d / 128 <= kMaxKBlocks && d.f / 128 <= kMaxKBlocks;
+}
+
+int gemm_fp8_blocks() { return kNT; }
+
 hipError_t launch_gemm_fp8(const FfnParams& p, bool gate_up, int max_chunks, hipStream_t s) {
-    const int groups = gate_up ? p.f / 128 : p.d / 256;
+    const int groups = gate_up ? p.f / (16 * kTiles / 2) : p.d / (16 * kTiles);
+    // One workgroup per CU at a time (the ring fills the LDS); with the plain
+    // order, two per CU so that a CU whose items end early takes more.
     long long items = (long long)max_chunks * groups;
-    const long long cap = (long long)device_cu_count() * 2;
+    const long long cap = (long long)device_cu_count() * (CAEE_GEMM_XCD ? 1 : 2);
     if (items > cap) items = cap;
     if (items < 1) items = 1;
-    if (gate_up) hipLaunchKernelGGL(k_gemm_fp8<true>, dim3((unsigned)items), dim3(kFfnThreads), 0, s, p);
-    else hipLaunchKernelGGL(k_gemm_fp8<false>, dim3((unsigned)items), dim3(kFfnThreads), 0, s, p);
+    if (gate_up) hipLaunchKernelGGL(k_gemm_fp8<true>, dim3((unsigned)items), dim3(kGemmThreads), 0, s, p);
+    else hipLaunchKernelGGL(k_gemm_fp8<false>, dim3((unsigned)items), dim3(kGemmThreads), 0, s, p);
     return hipGetLastError();
 }
 

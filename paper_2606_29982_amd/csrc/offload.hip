@@ -310,6 +310,7 @@ caee_status_t caee_offload_layer(caee_offload_t* h, const caee_layer_desc_t* des
     for (int e = 0; e < E; ++e) hcost[e] = h->slot_of[e] >= 0 ? 0.0f : h->miss_cost;
     HIP_TRY(hipMemcpyAsync(h->dev_tab, hcost, (size_t)E * 4, hipMemcpyHostToDevice, s), "cost table copy");
     RouteParams rp = make_route_params(desc, logits, bias, (const float*)h->dev_tab, nullptr, wsb, L);
+    rp.chunk_big = call_chunk_big(d, h->layout == CAEE_LAYOUT_TILED);
     set_route_outputs(rp, out, wsb, L);
     FfnParams fp = make_ffn_params(desc, x, rp.topk_ids, rp.topk_w, nullptr, y, wsb, L);
     fp.sh_w13 = h->sh_w13;
