@@ -327,7 +327,7 @@ caee_status_t ffn_routed(const caee_layer_desc_t* d, const FfnParams& p, const W
             CAEE_TRY(timed_launch(CAEE_KERNEL_QUANT, st, "gather x scales",
                                   [&] { return launch_gather_xs(q, L.max_chunks, st); }));
         CAEE_TRY(gate_up_list(d, p, list, nb, L.max_chunks, st));
-        if (d->w_dtype == CAEE_FP8_E4M3)
+        if (d->w_dtype == CAEE_FP8_E4M3 && !(gemm && gemm_fp8_fuses_quant()))
             CAEE_TRY(timed_launch(CAEE_KERNEL_QUANT, st, "quantise H",
                                   [&] { return launch_quant_list(q, nb, L.max_chunks, gemm, st); }));
         return down_list(d, p, list, nb, L.max_chunks, st);

@@ -156,6 +156,7 @@ inline int big_token_blocks(const caee_layer_desc_t& d) {
 
 bool gemm_fp8_applies(const caee_layer_desc_t& d, bool tiled);
 int gemm_fp8_blocks();
+bool gemm_fp8_fuses_quant();   // the GEMM's gate/up writes the e4m3 H rows itself
 
 // 16-token column blocks of a call's big chunks: the width of the 8-bit
 // GEMM's tile when that kernel runs the call's big list (its chunks are as

@@ -11,6 +11,7 @@
 
 #include "caee_internal.h"
 #include "ffn_stage.h"
+#include "fp8_codec.h"
 
 namespace caee {
 namespace {
@@ -18,29 +19,7 @@ namespace {
 typedef int i32x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
-constexpr float kE4M3Max = 448.0f;
 constexpr int kScaleOne = 127;   // E8M0 exponent of 1.0 for the MFMA's own block scales
-
-// OCP E4M3 (fn) code of v: nearest representable value, ties to the even
-// code, magnitudes above 448 saturate to 448.
-__device__ inline uint32_t e4m3_code(float v) {
-    const uint32_t sign = (__float_as_uint(v) >> 24) & 0x80u;
-    const float a = fminf(fabsf(v), kE4M3Max);
-    uint32_t code;
-    if (a < 0.015625f) {                       // below 2^-6: subnormal steps of 2^-9
-        code = (uint32_t)rintf(a * 512.0f);     // 8 is the smallest normal, code 8
-    } else {
-        int e = (int)((__float_as_uint(a) >> 23) & 0xFFu) - 127;   // a in [2^e, 2^(e+1))
-        uint32_t q = (uint32_t)rintf(ldexpf(a, 3 - e));            // 8 .. 16
-        if (q == 16u) {
-            q = 8u;
-            ++e;
-        }
-        code = ((uint32_t)(e + 7) << 3) | (q - 8u);
-        if (code > 126u) code = 126u;
-    }
-    return sign | code;
-}
 
 // Per-row, per-128-column quantisation of one block of 128 values by one
 // wavefront (two per lane): scale = amax / 448 (1 for an all-zero block),

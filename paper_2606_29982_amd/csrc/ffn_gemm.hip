@@ -25,6 +25,7 @@
 // 256 x 128 tile is faster than 128 x 256 (which reads each weight byte once
 // for experts with up to 256 rows, but issues twice the token-row loads).
 #include "caee_internal.h"
+#include "fp8_codec.h"
 
 namespace caee {
 namespace {
@@ -46,6 +47,10 @@ constexpr int kWaveNT = 4;            // token tiles per wave
 constexpr int kRowWaves = kTiles / 4; // waves across the weight rows
 constexpr int kXPer = 2 * kNT;        // tokens whose scales one wave loads
 static_assert(kTiles == 8 || kTiles == 16, "tile shape");
+// With 256-row tiles a gate/up item holds 128 features, one quantisation
+// block of each of its token rows: the epilogue quantises the SwiGLU rows
+// itself (e4m3 codes and transposed block scales for the down product).
+constexpr bool kFuseQuant = kTiles == 16;
 // Whether the items are laid out by XCD (see the kernel; measured slower at
 // the 4096-token prefill, so off by default).
 #ifndef CAEE_GEMM_XCD
@@ -273,6 +278,49 @@ __global__ __launch_bounds__(kGemmThreads) void k_gemm_fp8(FfnParams p) {
         }
         // All waves are done with the ring before the next item refills it.
         stage_barrier();
+        if constexpr (kGateUp && kFuseQuant) {
+            // Per token row: amax over the item's 128 SwiGLU values (this
+            // lane's 8, the 4 lanes of the column, the row waves through
+            // LDS), scale = amax / 448 (1 if zero), codes of value / scale:
+            // the separate quantiser's arithmetic, so the codes are the same.
+            float* red = reinterpret_cast<float*>(&st0);   // [wave][64 tokens]; the ring is idle
+            float hv[kWaveNT][2][4];
+#pragma unroll
+            for (int j = 0; j < kWaveNT; ++j) {
+                float m = 0.0f;
+#pragma unroll
+                for (int i = 0; i < 2; ++i)
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) {
+                        hv[j][i][v] = silu_mul(acc[i][j][v], acc[i + 2][j][v]);
+                        m = fmaxf(m, fabsf(hv[j][i][v]));
+                    }
+                m = fmaxf(m, __shfl_xor(m, 16));
+                m = fmaxf(m, __shfl_xor(m, 32));
+                if (g == 0) red[wave * 64 + 16 * j + r] = m;
+            }
+            __syncthreads();
+#pragma unroll
+            for (int j = 0; j < kWaveNT; ++j) {
+                const int n = kWaveNT * wc + j, tn = 16 * n + r;
+                float m = 0.0f;
+#pragma unroll
+                for (int q = 0; q < kRowWaves; ++q) m = fmaxf(m, red[(kRowWaves * wc + q) * 64 + 16 * j + r]);
+                if (n >= nb || tn >= ntok) continue;
+                const float sc = m > 0.0f ? m / kE4M3Max : 1.0f;
+                const size_t row = (size_t)(row0 + tn);
+#pragma unroll
+                for (int i = 0; i < 2; ++i) {
+                    const int col = (grp * (kTiles / 2) + 2 * wq + i) * 16 + 4 * g;
+                    uint32_t word = 0;
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) word |= e4m3_code(hv[j][i][v] / sc) << (8 * v);
+                    *(uint32_t*)(p.hq + row * p.f + col) = word;
+                }
+                if (wq == 0 && g == 0) p.hst[(size_t)grp * p.P + row] = sc;
+            }
+            continue;
+        }
 #pragma unroll
         for (int j = 0; j < kWaveNT; ++j) {
             const int n = kWaveNT * wc + j, tn = 16 * n + r;
@@ -331,6 +379,8 @@ bool gemm_fp8_applies(const caee_layer_desc_t& d, bool tiled) {
 }
 
 int gemm_fp8_blocks() { return kNT; }
+
+bool gemm_fp8_fuses_quant() { return kFuseQuant; }
 
 hipError_t launch_gemm_fp8(const FfnParams& p, bool gate_up, int max_chunks, hipStream_t s) {
     const int groups = gate_up ? p.f / (16 * kTiles / 2) : p.d / (16 * kTiles);
