@@ -780,15 +780,23 @@ __global__ __launch_bounds__(kTokThreads) void k_compensate(RouteParams p) {
     __shared__ uint8_t s_trans[kMaxE];
     __shared__ double s_sbuf[kTokWaves][kMaxK];
     __shared__ int s_fin[kTokWaves][kMaxK];
+    __shared__ int s_cnt[2];   // refilled and empty slots of the workgroup's tokens
     const int tid = threadIdx.x;
     const int lane = tid & (kWave - 1);
     const int wave = tid / kWave;
     for (int e = tid; e < p.E; e += kTokThreads) s_trans[e] = p.trans[e];
+    if (tid < 2) s_cnt[tid] = 0;
     __syncthreads();
-    const int t = blockIdx.x * kTokWaves + wave;
-    if (t < p.T)
+    for (int t = blockIdx.x * kTokWaves + wave; t < p.T; t += gridDim.x * kTokWaves)
         compensate_token<EPL>(p, t, lane, p.orig_ids + (size_t)t * p.k, s_trans, s_fin[wave], s_sbuf[wave],
-                              &p.counters[1], &p.counters[2]);
+                              &s_cnt[0], &s_cnt[1]);
+    // One global update per workgroup (per-token updates of the same two
+    // words serialise in the L2).
+    __syncthreads();
+    if (tid == 0) {
+        if (s_cnt[0]) atomicAdd(&p.counters[1], s_cnt[0]);
+        if (s_cnt[1]) atomicAdd(&p.counters[2], s_cnt[1]);
+    }
 }
 
 // Small batches: the whole routing step (phases A-C and the permutation)
@@ -818,11 +826,18 @@ __global__ __launch_bounds__(kRouteThreads) void k_route_fused(RouteParams p) {
     }
     prune_all(p, tid, kRouteThreads, sp);
     __syncthreads();
+    __shared__ int s_cnt[2];
     for (int e = tid; e < p.E; e += kRouteThreads) s_trans[e] = p.trans[e];
+    if (tid < 2) s_cnt[tid] = 0;
     __syncthreads();
     for (int t = wave; t < p.T; t += kFusedWaves)
         compensate_token<EPL>(p, t, lane, p.orig_ids + (size_t)t * k, s_trans, s_ids[wave], s_sbuf[wave],
-                              &p.counters[1], &p.counters[2]);
+                              &s_cnt[0], &s_cnt[1]);
+    __syncthreads();
+    if (tid == 0) {   // the only workgroup: the call's totals
+        p.counters[1] = s_cnt[0];
+        p.counters[2] = s_cnt[1];
+    }
     __syncthreads();
     if (p.do_permute || p.stats) permute_small(p, tid, kRouteThreads, sq);
 }
