@@ -23,7 +23,15 @@ import numpy as np
 #   "score"  - the paper's mechanism, as described above;
 #   "none"   - no refill: K_final = K_t within A_trans, weights renormalised;
 #   "random" - the freed slots take the experts of A_trans minus K_t with the
-#              largest counter-based random keys (below), lower index on ties.
+#              largest counter-based random keys (below), lower index on ties;
+#   "literal" - Sec. IV-C's second step read literally: K_final is the top-k
+#              of the masked router keys, i.e. the k best keys of A_trans
+#              (ties to the lower index), whether or not they were in K_t and
+#              with no group limit.  It can drop a token's own surviving
+#              expert for a better-keyed one from a group the token did not
+#              select, so unlike "score" it does not reduce to the plain layer
+#              when nothing is pruned (unless A_trans lies within the token's
+#              groups, as at T = 1).
 _M64 = (1 << 64) - 1
 _GOLDEN_GAMMA = 0x9E3779B97F4A7C15
 
@@ -50,6 +58,13 @@ def compensate_token(key: np.ndarray, s: np.ndarray, orig_ids, trans: np.ndarray
     asc) and w_e = routed_scaling * s_e / sum_{K_final} s (float64).
     `refill`, `seed` and the token index `t` select the ablation variant."""
     orig = list(orig_ids)
+    if refill == "literal":
+        final = sorted(np.flatnonzero(trans).tolist(), key=lambda e: (-float(key[e]), e))[:k]
+        total = 0.0
+        for e in final:
+            total += float(s[e])
+        w = [float(routed_scaling) * (float(s[e]) / total) for e in final]
+        return final, w, sum(1 for e in final if e not in orig)
     keep = [e for e in orig if trans[e]]
     pool = [e for e in np.flatnonzero(trans).tolist() if e not in orig]
     if refill == "score":

@@ -69,6 +69,56 @@ def test_refill_ignores_groups():
     assert nref == 2
 
 
+# ---- literal top-k of the masked scores (Sec. IV-C read literally) -----------
+
+def test_literal_hand_example():
+    # E=4 in two groups {0,1}, {2,3}; one group per token, k=2.  Scores
+    # [0.9, 0.1, 0.8, 0.7] (bias 0, so keys = scores): group sums 1.0 and
+    # 1.5 select group 1, K_t = {2, 3}.  With A_trans = {0, 2, 3} (expert 0
+    # activated by another token) keep-and-refill keeps {2, 3}; the literal
+    # top-2 of the masked scores is {0, 2}, dropping the token's own expert 3.
+    sc = np.array([[0.9, 0.1, 0.8, 0.7]])
+    logits = np.log(sc / (1.0 - sc))
+    _, _, ids, _ = oracle.route_batch(logits, np.zeros(4), 2, 1, 2)
+    assert sorted(ids[0].tolist()) == [2, 3]
+    trans = np.array([True, False, True, True])
+    sid, sw, sn = compensate_batch(sc, sc, ids, trans, 2, 2.5, "score")
+    lid, lw, ln = compensate_batch(sc, sc, ids, trans, 2, 2.5, "literal")
+    assert sid[0].tolist() == [2, 3] and sn == 0
+    assert lid[0].tolist() == [0, 2] and ln == 1
+    np.testing.assert_allclose(lw[0], [2.5 * 0.9 / 1.7, 2.5 * 0.8 / 1.7], rtol=0, atol=1e-15)
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_literal_is_top_k_of_trans(seed):
+    # brute force: each token's K_final is the first k of A_trans ordered by
+    # (key desc, index asc), whatever its own K_t was
+    shape, inp = _ablation_case(seed)
+    ref = oracle.moe_layer_ref(E=shape.E, n_group=shape.n_group, topk_group=shape.topk_group, k=shape.k,
+                               routed_scaling=1.0, tau=0.8, n_bins=1, logits=inp.logits, cost=inp.cost,
+                               rule="cir", refill="literal")
+    trans = np.flatnonzero(ref["trans"]).tolist()
+    n_out = 0
+    for t in range(inp.logits.shape[0]):
+        order = sorted(trans, key=lambda e: (-ref["keys"][t, e], e))[:shape.k]
+        assert [e for e in ref["topk_ids"][t] if e >= 0] == order
+        assert abs(sum(ref["topk_w"][t]) - 1.0) < 1e-12
+        n_out += sum(1 for e in order if e not in ref["orig_ids"][t])
+    assert ref["stats"]["n_refill"] == n_out
+
+
+def test_literal_equals_score_for_one_token():
+    # T = 1: A_trans lies inside the token's own K_t, so both readings agree
+    shape, inp = _ablation_case(5, T=1)
+    for tau in (0.0, 0.8):
+        kw = dict(E=shape.E, n_group=shape.n_group, topk_group=shape.topk_group, k=shape.k, routed_scaling=1.0,
+                  tau=tau, n_bins=1, logits=inp.logits, cost=inp.cost, rule="cir")
+        a = oracle.moe_layer_ref(**kw, refill="score")
+        b = oracle.moe_layer_ref(**kw, refill="literal")
+        assert np.array_equal(a["topk_ids"], b["topk_ids"])
+        np.testing.assert_array_equal(a["topk_w"], b["topk_w"])
+
+
 # ---- refill variants of the compensation ablation ----------------------------
 
 def test_splitmix64_published_outputs(golden):
