@@ -313,7 +313,9 @@ def ablation_rows(args, shape, Wt, dev):
     one bin, the CIR rule) pruned at theta_imp 0.9 / 0.8 / 0.7, and the
     relative output error ||y - y_dense|| / ||y_dense|| against the same
     layer without pruning, for the paper's score-based refill, a random
-    refill (mean of 4 seeds) and no refill (renormalise only).  With random
+    refill (mean of 4 seeds), no refill (renormalise only) and the literal
+    top-k of the masked router keys (which can also replace a token's own
+    surviving experts; its row also reports its error at tau = 0).  With random
     expert weights a refilled expert's output is uncorrelated with the one it
     replaces, so this measures how far each variant moves the output, not
     the task accuracy the paper reports."""
@@ -339,10 +341,11 @@ def ablation_rows(args, shape, Wt, dev):
 
         y0, _ = run(0.0, rule="max")      # tau = 0: nothing pruned
         n0 = float(torch.linalg.norm(y0))
+        lit0 = float(torch.linalg.norm(run(0.0, "literal", rule="max")[0] - y0)) / n0
         for theta in (0.9, 0.8, 0.7):
             errs = {}
             st = None
-            for mode in ("score", "none"):
+            for mode in ("score", "none", "literal"):
                 y, st_m = run(theta, mode)
                 errs[mode] = float(torch.linalg.norm(y - y0)) / n0
                 st = st if st is not None else st_m
@@ -350,7 +353,8 @@ def ablation_rows(args, shape, Wt, dev):
             errs["random"] = float(np.mean(rnd))
             rows.append({"T": T, "theta_imp": theta, "pruned": st[4], "refilled_slots": st[6],
                          "rel_err_score": round(errs["score"], 5), "rel_err_random": round(errs["random"], 5),
-                         "rel_err_none": round(errs["none"], 5)})
+                         "rel_err_none": round(errs["none"], 5), "rel_err_literal": round(errs["literal"], 5),
+                         "rel_err_literal_tau0": round(lit0, 5)})
             log(f"ablation {rows[-1]}")
     return rows
 

@@ -49,7 +49,7 @@
 extern "C" {
 #endif
 
-#define CAEE_ABI_VERSION 4
+#define CAEE_ABI_VERSION 5
 
 typedef enum caee_status {
     CAEE_OK = 0,
@@ -84,9 +84,9 @@ typedef enum caee_importance {
 } caee_importance_t;
 
 /* How compensation (Sec. IV-C) fills the slots pruning freed in a token's
- * list.  SCORE is the paper's mechanism; the other two exist for its
+ * list.  SCORE is the paper's mechanism; NONE and RANDOM exist for its
  * ablation (random selection among the executed experts vs the proposed
- * compensation). */
+ * compensation); LITERAL is the other reading of its top-k step. */
 typedef enum caee_refill {
     /* Best router keys of A_trans minus K_t (no group limit). */
     CAEE_REFILL_SCORE = 0,
@@ -95,7 +95,12 @@ typedef enum caee_refill {
     /* The experts of A_trans minus K_t with the largest random keys: the top
      * 53 bits of the SplitMix64 output for counter (seed << 32) | (t*E + e),
      * t the token's index in the call; ties to the lower index. */
-    CAEE_REFILL_RANDOM = 2
+    CAEE_REFILL_RANDOM = 2,
+    /* Sec. IV-C's top-k of the masked scores taken literally: K_final = the
+     * k best router keys of A_trans (ties to the lower index), whether or
+     * not they were in K_t, no group limit.  May drop a token's own
+     * surviving expert; not the plain layer at tau = 0 in general. */
+    CAEE_REFILL_LITERAL = 3
 } caee_refill_t;
 
 /* Shape and hyper-parameters of one MoE layer call. */

@@ -20,7 +20,7 @@ CAEE_F32, CAEE_BF16, CAEE_FP8_E4M3 = 0, 1, 2
 KERNEL_KINDS = {"route": 0, "gate_up": 1, "down": 2, "combine": 3, "quant": 4}
 DTYPE_CODE = {"f32": CAEE_F32, "bf16": CAEE_BF16, "fp8": CAEE_FP8_E4M3}
 IMPORTANCE_CODE = {"max": 0, "sum": 1, "cir": 2}
-REFILL_CODE = {"score": 0, "none": 1, "random": 2}
+REFILL_CODE = {"score": 0, "none": 1, "random": 2, "literal": 3}
 
 
 class CaeeError(RuntimeError):
@@ -153,7 +153,7 @@ class Layer:
     x_dtype: str = "bf16"
     y_dtype: str = "bf16"
     importance: str = "max"     # "max" | "sum" | "cir" (caee_importance_t)
-    refill: str = "score"       # "score" | "none" | "random" (caee_refill_t)
+    refill: str = "score"       # "score" | "none" | "random" | "literal" (caee_refill_t)
     seed: int = 0               # random refill keys
 
     def desc(self) -> LayerDesc:

@@ -56,7 +56,8 @@ caee_status_t check_desc(const caee_layer_desc_t* d) {
     if (d->importance != CAEE_IMPORTANCE_MAX && d->importance != CAEE_IMPORTANCE_SUM &&
         d->importance != CAEE_IMPORTANCE_CIR)
         return fail(CAEE_ERR_INVALID_ARG, "unknown importance=%d", d->importance);
-    if (d->refill != CAEE_REFILL_SCORE && d->refill != CAEE_REFILL_NONE && d->refill != CAEE_REFILL_RANDOM)
+    if (d->refill != CAEE_REFILL_SCORE && d->refill != CAEE_REFILL_NONE && d->refill != CAEE_REFILL_RANDOM &&
+        d->refill != CAEE_REFILL_LITERAL)
         return fail(CAEE_ERR_INVALID_ARG, "unknown refill=%d", d->refill);
     if (d->w_dtype != CAEE_F32 && d->w_dtype != CAEE_BF16 && d->w_dtype != CAEE_FP8_E4M3)
         return fail(CAEE_ERR_INVALID_ARG, "unknown w_dtype=%d", d->w_dtype);

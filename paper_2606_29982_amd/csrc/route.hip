@@ -272,7 +272,10 @@ __device__ void compensate_token(const RouteParams& p, int t, int lane, const in
         const uint64_t ctr = ((uint64_t)p.seed << 32) | (uint64_t)(t * p.E + lane * EPL + i);
         rv[i] = p.refill == CAEE_REFILL_RANDOM ? (double)(splitmix64(ctr) >> 11) : key[i];
     }
-    const int to_fill = p.refill == CAEE_REFILL_NONE ? 0 : p.k - n_keep;
+    // LITERAL: K_final is the top-k of all of A_trans by key (the ordering
+    // pass below), no keep-first refill.
+    const bool literal = p.refill == CAEE_REFILL_LITERAL;
+    const int to_fill = p.refill == CAEE_REFILL_NONE || literal ? 0 : p.k - n_keep;
     int got = 0;
     for (int r = 0; r < to_fill; ++r) {
         double v = -INFINITY;
@@ -292,9 +295,15 @@ __device__ void compensate_token(const RouteParams& p, int t, int lane, const in
         ++got;
     }
 #pragma unroll
-    for (int i = 0; i < EPL; ++i) fin_f[i] = (in_k[i] && tr[i]) || take[i];
+    for (int i = 0; i < EPL; ++i) fin_f[i] = literal ? tr[i] : (in_k[i] && tr[i]) || take[i];
 
-    const int m = n_keep + got;
+    int m = n_keep + got;
+    if (literal) {
+        int n_tr = 0;
+#pragma unroll
+        for (int i = 0; i < EPL; ++i) n_tr += __popcll(__ballot(tr[i]));
+        m = n_tr < p.k ? n_tr : p.k;
+    }
     for (int r = 0; r < m; ++r) {
         double v = -INFINITY;
         int ei = kNoIdx;
@@ -314,6 +323,11 @@ __device__ void compensate_token(const RouteParams& p, int t, int lane, const in
             fin[r] = ei;
             sbuf[r] = sv;
         }
+    }
+    if (literal) {   // slots that hold an expert from outside K_t
+        got = 0;
+#pragma unroll
+        for (int i = 0; i < EPL; ++i) got += __popcll(__ballot(out_f[i] && !in_k[i]));
     }
     if (lane == 0) {
         double total = 0.0;

@@ -113,7 +113,7 @@ def test_r1_offload_sequence(r1_weights, r1_tiled, rule, tau):
 
 
 @pytest.mark.parametrize("T", [1, 8, 32, 128])
-@pytest.mark.parametrize("refill", ["none", "random"])
+@pytest.mark.parametrize("refill", ["none", "random", "literal"])
 def test_r1_refill_variants(T, refill, r1_weights):
     """Compensation ablation variants at the R1 shape: the offloading rule
     (CIR) with one bin, where every non-mandatory candidate with a cost is

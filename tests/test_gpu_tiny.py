@@ -196,12 +196,13 @@ def test_tiled_weights(shape, T):
     _run(shape, seed=T, tau=0.2, n_bins=4, T=T, tiled=True)
 
 
-@pytest.mark.parametrize("refill", ["none", "random"])
+@pytest.mark.parametrize("refill", ["none", "random", "literal"])
 @pytest.mark.parametrize("T", [5, 16, 40])
 @pytest.mark.parametrize("seed", [0, 3])
 def test_tiny_refill_variants(refill, T, seed):
-    """Compensation ablation variants (no refill; random refill by
-    SplitMix64 keys) against the oracle, through both routing paths."""
+    """Compensation variants (no refill; random refill by SplitMix64 keys;
+    the literal top-k of the masked keys) against the oracle, through both
+    routing paths."""
     got, ref = _run(TINY_F32, seed=seed, tau=0.7, n_bins=1, T=T, zipf=1.2, cost_kind="zipf", rule="cir",
                     refill=refill, rseed=11 + seed)
     if refill == "none":
