@@ -111,6 +111,35 @@ def time_steps(case, steps, warmup):
     return a.elapsed_time(b) / steps
 
 
+def graph_protocol(case, warmup=10, iters=50, flush_mb=512):
+    """The layer call captured once in a HIP graph and replayed: `warmup`
+    replays, then `iters` replays each timed on its own with events, with a
+    `flush_mb` MB buffer written between them (outside the timed region) so
+    that the 256 MB memory-side cache holds nothing of the previous call.
+    Returns the median, 10th and 90th percentile in microseconds."""
+    import torch
+    case.step()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        case.step()
+    for _ in range(warmup):
+        g.replay()
+    flush = torch.empty(flush_mb << 20, dtype=torch.uint8, device=case.y.device)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(iters)]
+    for a, b in ev:
+        flush.fill_(1)
+        a.record()
+        g.replay()
+        b.record()
+    torch.cuda.synchronize()
+    us = np.array([a.elapsed_time(b) * 1e3 for a, b in ev])
+    del g, flush
+    return {"us_p50": round(float(np.median(us)), 1), "us_p10": round(float(np.percentile(us, 10)), 1),
+            "us_p90": round(float(np.percentile(us, 90)), 1), "iters": iters, "warmup": warmup,
+            "flush_mb": flush_mb}
+
+
 def layer_bytes(shape, T, n_trans):
     """Algorithmic HBM bytes of one layer call: weights of every executed
     expert (A_trans plus the shared one), x read, y written, router logits,
@@ -431,6 +460,10 @@ def main():
         "kernel_us_per_step": {k: round(v * 1e3, 2) for k, v in kern.items()},
         "roofline": roofline,
     }
+    # The same call captured in a HIP graph, memory-side cache flushed before
+    # every timed replay (median and spread of single calls).
+    result["graph_protocol"] = graph_protocol(head)
+    log(f"graph protocol {result['graph_protocol']}")
 
     if not args.no_sweep:
         # Zipf-skewed popularity and cost table, experts placed on 8 bins
@@ -440,6 +473,7 @@ def main():
             for rule, tau, n_bins in (("max", 0.0, 8), ("max", 0.1, 8), ("sum", 0.6, 8), ("cir", 0.8, 8)):
                 c = Case(shape, T, tau, n_bins, Wt, dev, args.seed, skewed=True, rule=rule)
                 m = time_steps(c, max(10, args.steps // 2), 3)
+                gp = graph_protocol(c, warmup=5, iters=20)
                 s = c.stats()
                 b = layer_bytes(shape, T, s[5])
                 sweep.append({"T": T, "rule": rule, "tau": tau, "n_bins": n_bins, "inputs": "zipf-skewed",
@@ -447,7 +481,9 @@ def main():
                               "us_per_step": round(m * 1e3, 1), "tokens_per_s": round(T / (m * 1e-3), 1),
                               "hbm_gbps": round(b / (m * 1e-3) / 1e9, 1),
                               "hbm_frac": round(b / (m * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
-                              "act": s[0], "pruned": s[4], "executed": s[5] + shape.n_shared})
+                              "act": s[0], "pruned": s[4], "executed": s[5] + shape.n_shared,
+                              "graph_flushed_us_p50": gp["us_p50"], "graph_flushed_us_p10": gp["us_p10"],
+                              "graph_flushed_us_p90": gp["us_p90"]})
                 log(f"sweep {sweep[-1]}")
                 del c
         result["sweep"] = sweep
