@@ -30,14 +30,6 @@ constexpr int kTokThreads = kTokWaves * kWave;
 constexpr int kFusedT = CAEE_FUSED_T;
 constexpr int kNoIdx = 0x7fffffff;
 
-// Larger value wins; equal values go to the lower index.
-__device__ inline void argmax_merge(double& v, int& i, double ov, int oi) {
-    if (ov > v || (ov == v && oi < i)) {
-        v = ov;
-        i = oi;
-    }
-}
-
 // Cross-lane moves within a 16-lane row through DPP (no LDS round trip).
 template <int C>
 __device__ inline int dpp_i(int v) {
@@ -61,26 +53,52 @@ __device__ inline double readlane_d(double v, int lane) {
 // quad_perm [1,0,3,2], quad_perm [2,3,0,1], row_half_mirror, row_mirror.
 constexpr int kDppXor1 = 0xB1, kDppXor2 = 0x4E, kDppHalfMirror = 0x141, kDppMirror = 0x140;
 
-template <int C>
-__device__ inline void argmax_step(double& v, int& i) {
-    const double ov = dpp_d<C>(v);
-    const int oi = dpp_i<C>(i);
-    argmax_merge(v, i, ov, oi);
+
+// Row broadcasts of gfx9 DPP: lane 15 of each row to the next row, lane 31
+// to rows 2 and 3.  Rows outside `RM` keep their own value (update_dpp's
+// old operand), so a max or min with it changes nothing there.
+constexpr int kDppRowBcast15 = 0x142, kDppRowBcast31 = 0x143;
+template <int C, int RM>
+__device__ inline int dpp_upd_i(int v) {
+    return __builtin_amdgcn_update_dpp(v, v, C, RM, 0xF, false);
+}
+template <int C, int RM>
+__device__ inline double dpp_upd_d(double v) {
+    const long long b = __double_as_longlong(v);
+    const int lo = dpp_upd_i<C, RM>((int)b);
+    const int hi = dpp_upd_i<C, RM>((int)(b >> 32));
+    return __longlong_as_double(((long long)hi << 32) | (unsigned int)lo);
 }
 
-// Wave-wide argmax: butterfly inside each 16-lane row, then the four row
-// results are combined from scalar reads.  Every lane gets the result.
+// Wave-wide max and min, all in VALU: butterfly inside each 16-lane row,
+// then row 1 takes row 0's result and row 3 row 2's, then row 3 takes row
+// 1's; lane 63 ends with the wave's result, which every lane reads.
+__device__ inline double wave_max_d(double v) {
+    v = fmax(v, dpp_d<kDppXor1>(v));
+    v = fmax(v, dpp_d<kDppXor2>(v));
+    v = fmax(v, dpp_d<kDppHalfMirror>(v));
+    v = fmax(v, dpp_d<kDppMirror>(v));
+    v = fmax(v, dpp_upd_d<kDppRowBcast15, 0xA>(v));
+    v = fmax(v, dpp_upd_d<kDppRowBcast31, 0xC>(v));
+    return readlane_d(v, 63);
+}
+__device__ inline int wave_min_i(int v) {
+    v = min(v, dpp_i<kDppXor1>(v));
+    v = min(v, dpp_i<kDppXor2>(v));
+    v = min(v, dpp_i<kDppHalfMirror>(v));
+    v = min(v, dpp_i<kDppMirror>(v));
+    v = min(v, dpp_upd_i<kDppRowBcast15, 0xA>(v));
+    v = min(v, dpp_upd_i<kDppRowBcast31, 0xC>(v));
+    return __builtin_amdgcn_readlane(v, 63);
+}
+
+// Wave-wide argmax of (v, i): the largest v, and among the lanes holding it
+// the lowest i (the same result as merging pairs in any order).  Values are
+// never NaN.  Every lane gets the result.
 __device__ inline void wave_argmax(double& v, int& i) {
-    argmax_step<kDppXor1>(v, i);
-    argmax_step<kDppXor2>(v, i);
-    argmax_step<kDppHalfMirror>(v, i);
-    argmax_step<kDppMirror>(v, i);
-    double bv = readlane_d(v, 0);
-    int bi = __builtin_amdgcn_readlane(i, 0);
-#pragma unroll
-    for (int r = 1; r < 4; ++r) argmax_merge(bv, bi, readlane_d(v, 16 * r), __builtin_amdgcn_readlane(i, 16 * r));
-    v = bv;
-    i = bi;
+    const double m = wave_max_d(v);
+    i = wave_min_i(v == m ? i : kNoIdx);
+    v = m;
 }
 
 // Merge two (largest, second largest) pairs.
@@ -114,15 +132,26 @@ __device__ inline void load_scores(const RouteParams& p, int t, int lane, double
     }
 }
 
-// Broadcast s of expert `e` from the lane that holds it.
+// Each lane's score s of expert `e` (its own, or 0 when `valid` is false),
+// fetched from the lane that holds it: one shuffle per element slot, for all
+// lanes at once.
 template <int EPL>
-__device__ inline double score_of(const double (&s)[EPL], int lane, int e) {
-    double mine = 0.0;
+__device__ inline double fetch_score(const double (&s)[EPL], int e, bool valid, int E) {
+    const bool ok = valid && e >= 0 && e < E;
+    const int src = ok ? e / EPL : 0;
+    const int which = ok ? e % EPL : 0;
+    double got = 0.0;
 #pragma unroll
-    for (int i = 0; i < EPL; ++i)
-        if (lane * EPL + i == e) mine = s[i];
-    return __shfl(mine, e / EPL);
+    for (int i = 0; i < EPL; ++i) {
+        const double c = __shfl(s[i], src);
+        if (which == i) got = c;
+    }
+    return ok ? got : 0.0;
 }
+
+// Groups ranked in one pass (each lane reads every group's score) when
+// there are at most this many; more groups take one wave argmax per pick.
+constexpr int kRankGroups = 16;
 
 // Phase A for token t: writes K_t (rank order), G(t) and the token's top expert.
 template <int EPL>
@@ -153,16 +182,30 @@ __device__ void route_token(const RouteParams& p, int t, int lane, int* ids, dou
     const int my_group = lane_valid ? (lane * EPL) / p.gsize : kNoIdx;
 
     bool gsel = false;
-    for (int r = 0; r < p.topk_group; ++r) {
-        double v = (lane_valid && !gsel) ? gscore : -INFINITY;
-        int gi = (lane_valid && !gsel) ? my_group : kNoIdx;
-        wave_argmax(v, gi);
-        if (my_group == gi) gsel = true;
+    if (p.n_group <= kRankGroups) {
+        // The group's rank: groups with a larger score, or the same score and
+        // a lower index, come first; the first topk_group are selected.
+        int rank = 0;
+        for (int g2 = 0; g2 < p.n_group; ++g2) {
+            const double o = readlane_d(gscore, g2 * p.lpg);   // the group's first lane
+            rank += (o > gscore) | ((o == gscore) & (g2 < my_group));
+        }
+        gsel = lane_valid && rank < p.topk_group;
+    } else {
+        for (int r = 0; r < p.topk_group; ++r) {
+            double v = (lane_valid && !gsel) ? gscore : -INFINITY;
+            int gi = (lane_valid && !gsel) ? my_group : kNoIdx;
+            wave_argmax(v, gi);
+            if (my_group == gi) gsel = true;
+        }
     }
 
+    // Top-k keys of the selected groups; lane r keeps the r-th pick.
     bool chosen[EPL];
 #pragma unroll
     for (int i = 0; i < EPL; ++i) chosen[i] = false;
+    int my_id = kNoIdx;
+    double my_s = 0.0;
     for (int r = 0; r < p.k; ++r) {
         double v = -INFINITY;
         int ei = kNoIdx;
@@ -177,36 +220,30 @@ __device__ void route_token(const RouteParams& p, int t, int lane, int* ids, dou
 #pragma unroll
         for (int i = 0; i < EPL; ++i)
             if (lane * EPL + i == ei) chosen[i] = true;
-        const double sv = score_of<EPL>(s, lane, ei);
-        if (lane == 0) {
-            sids[r] = ei;
-            sbuf[r] = sv;
-        }
+        if (lane == r) my_id = ei;
     }
-    if (lane == 0) {
-        double total = 0.0;
-        for (int r = 0; r < p.k; ++r) total += sbuf[r];
-        int best = kNoIdx;
-        double bg = -1.0;
-        for (int r = 0; r < p.k; ++r) {
-            const double g = sbuf[r] / total;
-            const int e = sids[r];
-            ids[r] = e;
-            gout[r] = g;
-            if (g > bg || (g == bg && e < best)) {
-                bg = g;
-                best = e;
-            }
-        }
-        *top1 = best;
-        // Pairs that are mandatory on their own: the token's top expert, plus
-        // the threshold (MAX) or the cumulative-ratio prefix (CIR).
-        uint32_t flags = 0;
-        for (int r = 0; r < p.k; ++r) {
-            const bool f = sids[r] == best || (p.rule == CAEE_IMPORTANCE_MAX && sbuf[r] / total >= p.tau);
-            flags |= (uint32_t)f << r;
-        }
-        if (p.rule == CAEE_IMPORTANCE_CIR) {
+    my_s = fetch_score<EPL>(s, my_id, lane < p.k, p.E);
+    // G(t): each score over the token's k scores summed in rank order (the
+    // same additions on every lane), one slot per lane.
+    double total = 0.0;
+    for (int r = 0; r < p.k; ++r) total += readlane_d(my_s, r);
+    const bool mine = lane < p.k;
+    const double g = my_s / total;
+    double bg = mine ? g : -INFINITY;
+    int best = mine ? my_id : kNoIdx;
+    wave_argmax(bg, best);   // the token's top expert by G, ties to the lower index
+    // Pairs that are mandatory on their own: the token's top expert, plus
+    // the threshold (MAX) or the cumulative-ratio prefix (CIR).
+    uint32_t flags = (uint32_t)__ballot(mine && (my_id == best || (p.rule == CAEE_IMPORTANCE_MAX && g >= p.tau)));
+    if (mine) {
+        ids[lane] = my_id;
+        gout[lane] = g;
+        sids[lane] = my_id;
+        sbuf[lane] = my_s;
+    }
+    if (lane == 0) *top1 = best;
+    if (p.rule == CAEE_IMPORTANCE_CIR) {
+        if (lane == 0) {
             // Slots in gate order: score descending, lower expert first on ties.
             int ord[kMaxK];
             for (int r = 0; r < p.k; ++r) {
@@ -227,8 +264,9 @@ __device__ void route_token(const RouteParams& p, int t, int lane, int* ids, dou
                 if (cum / sum >= p.tau) break;
             }
         }
-        for (int r = 0; r < p.k; ++r) mflag[r] = (uint8_t)((flags >> r) & 1u);
+        flags = (uint32_t)__builtin_amdgcn_readfirstlane((int)flags);
     }
+    if (mine) mflag[lane] = (uint8_t)((flags >> lane) & 1u);
 }
 
 // SplitMix64 output for `state` (Steele, Lea and Flood 2014): golden-gamma
@@ -245,8 +283,6 @@ template <int EPL>
 __device__ void compensate_token(const RouteParams& p, int t, int lane, const int* orig,
                                  const uint8_t* trans, int* fin, double* sbuf, int* n_refill,
                                  int* n_pad) {
-    double s[EPL], key[EPL];
-    load_scores<EPL>(p, t, lane, s, key);
     bool in_k[EPL], tr[EPL], take[EPL], fin_f[EPL], out_f[EPL];
     // K_t: lane r < k holds its r-th expert; the list is broadcast lane by lane.
     const int my_orig = lane < p.k ? orig[lane] : -1;
@@ -262,7 +298,39 @@ __device__ void compensate_token(const RouteParams& p, int t, int lane, const in
 #pragma unroll
         for (int i = 0; i < EPL; ++i) in_k[i] |= (o == lane * EPL + i);
     }
-    const int n_keep = __popcll(__ballot(my_orig >= 0 && trans[my_orig]));
+    const bool kept = my_orig >= 0 && trans[my_orig];
+    const uint64_t kept_mask = __ballot(kept);
+    const int n_keep = __popcll(kept_mask);
+    int avail = 0;   // experts of A_trans outside K_t
+#pragma unroll
+    for (int i = 0; i < EPL; ++i) avail += __popcll(__ballot(tr[i] && !in_k[i]));
+    if (p.refill != CAEE_REFILL_LITERAL && (p.refill == CAEE_REFILL_NONE || n_keep == p.k || avail == 0)) {
+        // Nothing to refill: K_final = K_t ∩ A_trans in K_t's own (rank)
+        // order.  Each kept slot's score is recomputed by its lane with the
+        // same expression as the full pass, and summed in the same order.
+        double my_s = 0.0;
+        if (kept) my_s = 1.0 / (1.0 + exp(-(double)p.logits[(size_t)t * p.E + my_orig]));
+        double total = 0.0;
+        for (int r = 0; r < p.k; ++r)
+            if ((kept_mask >> r) & 1ull) total += readlane_d(my_s, r);
+        const int pos = __popcll(kept_mask & ((1ull << lane) - 1ull));
+        if (kept) {
+            const size_t o = (size_t)t * p.k + pos;
+            fin[pos] = my_orig;
+            p.topk_ids[o] = my_orig;
+            p.topk_w[o] = (float)(p.rs * (my_s / total));
+        }
+        if (lane >= n_keep && lane < p.k) {
+            const size_t o = (size_t)t * p.k + lane;
+            fin[lane] = -1;
+            p.topk_ids[o] = -1;
+            p.topk_w[o] = 0.0f;
+        }
+        if (lane == 0 && n_keep < p.k) atomicAdd(n_pad, p.k - n_keep);
+        return;
+    }
+    double s[EPL], key[EPL];
+    load_scores<EPL>(p, t, lane, s, key);
 
     // Refill order: router key (the paper's compensation) or, for the
     // ablation, a 53-bit random key (exact in a double) per (token, expert).
@@ -298,6 +366,8 @@ __device__ void compensate_token(const RouteParams& p, int t, int lane, const in
     for (int i = 0; i < EPL; ++i) fin_f[i] = literal ? tr[i] : (in_k[i] && tr[i]) || take[i];
 
     int m = n_keep + got;
+    int my_id = -1;   // lane r: the r-th expert of K_final and its score
+    double my_s = 0.0;
     if (literal) {
         int n_tr = 0;
 #pragma unroll
@@ -318,31 +388,26 @@ __device__ void compensate_token(const RouteParams& p, int t, int lane, const in
 #pragma unroll
         for (int i = 0; i < EPL; ++i)
             if (lane * EPL + i == ei) out_f[i] = true;
-        const double sv = score_of<EPL>(s, lane, ei);
-        if (lane == 0) {
-            fin[r] = ei;
-            sbuf[r] = sv;
-        }
+        if (lane == r) my_id = ei;
     }
+    my_s = fetch_score<EPL>(s, my_id, lane < m, p.E);
     if (literal) {   // slots that hold an expert from outside K_t
         got = 0;
 #pragma unroll
         for (int i = 0; i < EPL; ++i) got += __popcll(__ballot(out_f[i] && !in_k[i]));
     }
+    // Weights: scores over their sum in rank order (the same additions on
+    // every lane), one slot per lane; slots past m are padding.
+    double total = 0.0;
+    for (int r = 0; r < m; ++r) total += readlane_d(my_s, r);
+    if (lane < p.k) {
+        const size_t o = (size_t)t * p.k + lane;
+        const bool have = lane < m;
+        fin[lane] = have ? my_id : -1;
+        p.topk_ids[o] = have ? my_id : -1;
+        p.topk_w[o] = have ? (float)(p.rs * (my_s / total)) : 0.0f;
+    }
     if (lane == 0) {
-        double total = 0.0;
-        for (int r = 0; r < m; ++r) total += sbuf[r];
-        for (int r = 0; r < p.k; ++r) {
-            const size_t o = (size_t)t * p.k + r;
-            if (r < m) {
-                p.topk_ids[o] = fin[r];
-                p.topk_w[o] = (float)(p.rs * (sbuf[r] / total));
-            } else {
-                fin[r] = -1;
-                p.topk_ids[o] = -1;
-                p.topk_w[o] = 0.0f;
-            }
-        }
         atomicAdd(n_refill, got);
         atomicAdd(n_pad, p.k - m);
     }
