@@ -92,6 +92,19 @@ __device__ inline int wave_min_i(int v) {
     return __builtin_amdgcn_readlane(v, 63);
 }
 
+// Inclusive prefix sum over the 64 lanes, in VALU: shifts by 1, 2, 4, 8
+// within each row (lanes shifted in from outside the row read 0), then
+// rows 1 and 3 add the last lane of rows 0 and 2, rows 2 and 3 that of row 1.
+__device__ inline int wave_incl_scan(int v) {
+    v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xF, 0xF, true);   // row_shr:1
+    v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xF, 0xF, true);   // row_shr:2
+    v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xF, 0xF, true);   // row_shr:4
+    v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xF, 0xF, true);   // row_shr:8
+    v += __builtin_amdgcn_update_dpp(0, v, kDppRowBcast15, 0xA, 0xF, false);
+    v += __builtin_amdgcn_update_dpp(0, v, kDppRowBcast31, 0xC, 0xF, false);
+    return v;
+}
+
 // Wave-wide argmax of (v, i): the largest v, and among the lanes holding it
 // the lowest i (the same result as merging pairs in any order).  Values are
 // never NaN.  Every lane gets the result.
@@ -548,7 +561,7 @@ __device__ void prune_all(const RouteParams& p, int tid, int nthr, PruneShared& 
     if (wave == 0) {
         double fb = 0.0;
         for (int b = lane; b < nb; b += kWave) fb = fmax(fb, s_mload[b]);
-        for (int off = 32; off >= 1; off >>= 1) fb = fmax(fb, __shfl_xor(fb, off));
+        fb = wave_max_d(fb);
         if (lane == 0) s_fbase = fb;
     }
     for (int b = tid; b < nb && p.bin_loads; b += nthr) {
@@ -637,18 +650,8 @@ __device__ void build_lists(const RouteParams& p, const int* s_cnt, int* s_off, 
         ssum += (n > 0 && n <= cs) ? 1 : 0;
         bsum += n > cs ? (n + cb - 1) / cb : 0;
     }
-    int inc = sum, sinc = ssum, binc = bsum;
-    for (int off = 1; off < kWave; off <<= 1) {
-        const int o = __shfl_up(inc, off);
-        const int so = __shfl_up(sinc, off);
-        const int bo = __shfl_up(binc, off);
-        if (lane >= off) {
-            inc += o;
-            sinc += so;
-            binc += bo;
-        }
-    }
-    const int stotal = __shfl(sinc, kWave - 1);
+    const int inc = wave_incl_scan(sum), sinc = wave_incl_scan(ssum), binc = wave_incl_scan(bsum);
+    const int stotal = __builtin_amdgcn_readlane(sinc, kWave - 1);
     int run = inc - sum, srun = sinc - ssum, brun = stotal + binc - bsum;
     for (int x = lo; x < hi; ++x) {
         const int cnt = s_cnt[x];
@@ -674,8 +677,8 @@ __device__ void build_lists(const RouteParams& p, const int* s_cnt, int* s_off, 
         }
         run += cnt;
     }
-    const int total = __shfl(inc, kWave - 1);
-    const int btotal = __shfl(binc, kWave - 1);
+    const int total = __builtin_amdgcn_readlane(inc, kWave - 1);
+    const int btotal = __builtin_amdgcn_readlane(binc, kWave - 1);
     if (lane == 0) {
         s_off[nx] = total;
         p.perm_off[nx] = total;
@@ -880,45 +883,87 @@ __global__ __launch_bounds__(kTokThreads) void k_compensate(RouteParams p) {
 
 // Small batches: the whole routing step (phases A-C and the permutation)
 // in one workgroup of 16 wavefronts, one launch instead of four or five.
-// Phases are separated by workgroup barriers; their data passes through
-// global memory (visible across the workgroup's waves after a barrier) and
-// LDS, exactly as between the separate kernels.
+// Phases are separated by workgroup barriers.  Everything one phase hands to
+// the next (K_t, G, the mandatory flags, the cost and bin tables, A_trans,
+// K_final and its weights, the counters) stays in LDS: the phases run on a
+// copy of the parameters whose arrays point there, and the results the
+// caller and the FFN read are copied out at the end.
 constexpr int kFusedWaves = kRouteThreads / kWave;
 
 template <int EPL>
 __global__ __launch_bounds__(kRouteThreads) void k_route_fused(RouteParams p) {
     __shared__ double s_sbuf[kFusedWaves][kMaxK];
     __shared__ int s_ids[kFusedWaves][kMaxK];
-    __shared__ uint8_t s_trans[kMaxE];
     __shared__ PruneShared sp;
     __shared__ PermShared sq;
+    __shared__ int32_t l_orig[kFusedT * kMaxK], l_top1[kFusedT], l_fin[kFusedT * kMaxK], l_ctr[4];
+    __shared__ double l_g[kFusedT * kMaxK], l_isum[kMaxE];
+    __shared__ float l_w[kFusedT * kMaxK], l_cost[kMaxE];
+    __shared__ int32_t l_bin[kMaxE];
+    __shared__ uint8_t l_mflag[kFusedT * kMaxK], l_trans[kMaxE];
+    __shared__ uint32_t l_masks[4 * (kMaxE / 32)];
+    __shared__ int32_t l_stats[8];
+    __shared__ double l_bl[3 * kMaxE];
     const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
-    const int k = p.k;
-    if (tid < 4) p.counters[tid] = 0;
+    const int k = p.k, E = p.E;
+    RouteParams q = p;
+    q.orig_ids = l_orig;
+    q.gbuf = l_g;
+    q.top1 = l_top1;
+    q.mflag = l_mflag;
+    q.cost = l_cost;
+    q.bin = p.bin ? l_bin : nullptr;
+    q.trans = l_trans;
+    q.topk_ids = l_fin;
+    q.topk_w = l_w;
+    q.counters = l_ctr;
+    q.imp_sum = l_isum;
+    q.masks = p.masks ? l_masks : nullptr;
+    q.stats = p.stats ? l_stats : nullptr;
+    q.bin_loads = p.bin_loads && p.n_bins <= kMaxE ? l_bl : p.bin_loads;
+    // The tables, read by the waves that route no token while the others do.
+    for (int e = tid; e < E; e += kRouteThreads) {
+        l_cost[e] = p.cost[e];
+        if (p.bin) l_bin[e] = p.bin[e];
+    }
+    if (tid < 4) l_ctr[tid] = 0;
     for (int t = wave; t < p.T; t += kFusedWaves)
-        route_token<EPL>(p, t, lane, p.orig_ids + (size_t)t * k, p.gbuf + (size_t)t * k, p.top1 + t,
-                         p.mflag + (size_t)t * k, s_sbuf[wave], s_ids[wave]);
+        route_token<EPL>(q, t, lane, q.orig_ids + (size_t)t * k, q.gbuf + (size_t)t * k, q.top1 + t,
+                         q.mflag + (size_t)t * k, s_sbuf[wave], s_ids[wave]);
     __syncthreads();
     if (p.rule == CAEE_IMPORTANCE_SUM) {
-        for (int e = wave; e < p.E; e += kFusedWaves) importance_sum_expert(p, e, lane);
+        for (int e = wave; e < E; e += kFusedWaves) importance_sum_expert(q, e, lane);
         __syncthreads();
     }
-    prune_all(p, tid, kRouteThreads, sp);
+    prune_all(q, tid, kRouteThreads, sp);
     __syncthreads();
     __shared__ int s_cnt[2];
-    for (int e = tid; e < p.E; e += kRouteThreads) s_trans[e] = p.trans[e];
     if (tid < 2) s_cnt[tid] = 0;
     __syncthreads();
     for (int t = wave; t < p.T; t += kFusedWaves)
-        compensate_token<EPL>(p, t, lane, p.orig_ids + (size_t)t * k, s_trans, s_ids[wave], s_sbuf[wave],
+        compensate_token<EPL>(q, t, lane, q.orig_ids + (size_t)t * k, l_trans, s_ids[wave], s_sbuf[wave],
                               &s_cnt[0], &s_cnt[1]);
     __syncthreads();
     if (tid == 0) {   // the only workgroup: the call's totals
-        p.counters[1] = s_cnt[0];
-        p.counters[2] = s_cnt[1];
+        l_ctr[1] = s_cnt[0];
+        l_ctr[2] = s_cnt[1];
     }
     __syncthreads();
-    if (p.do_permute || p.stats) permute_small(p, tid, kRouteThreads, sq);
+    if (p.do_permute || p.stats) permute_small(q, tid, kRouteThreads, sq);
+    // Results read after this kernel: K_t, K_final and its weights, A_trans.
+    for (int i = tid; i < p.T * k; i += kRouteThreads) {
+        p.orig_ids[i] = l_orig[i];
+        p.topk_ids[i] = l_fin[i];
+        p.topk_w[i] = l_w[i];
+    }
+    for (int e = tid; e < E; e += kRouteThreads) p.trans[e] = l_trans[e];
+    if (tid < 4) p.counters[tid] = l_ctr[tid];
+    const int words = (E + 31) / 32;
+    if (p.masks)
+        for (int i = tid; i < 4 * words; i += kRouteThreads) p.masks[i] = l_masks[i];
+    if (p.stats && tid < 8) p.stats[tid] = l_stats[tid];
+    if (q.bin_loads == l_bl)
+        for (int i = tid; i < 3 * p.n_bins; i += kRouteThreads) p.bin_loads[i] = l_bl[i];
 }
 
 }  // namespace
