@@ -3,6 +3,7 @@
 // helpers (wave reductions, bf16 rounding, MFMA fragments).
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stddef.h>
 #include <stdint.h>
@@ -40,6 +41,38 @@ constexpr int kPrefillT = CAEE_PREFILL_T;
 #define CAEE_GEMM_T 256
 #endif
 constexpr int kGemmT = CAEE_GEMM_T;
+// Batches of kSharedEarlyMinT .. kSharedEarlyT tokens launch the shared
+// experts' gate/up next to routing: 0 never, 1 on the second stream, 2 on
+// the same stream without waiting for routing (an any-order launch; it ran
+// no concurrency here).  Below the minimum, routing is one short fused
+// kernel and the cross-queue hand-offs cost more than the overlap gains.
+#ifndef CAEE_SHARED_EARLY
+#define CAEE_SHARED_EARLY 1
+#endif
+#ifndef CAEE_SHARED_EARLY_MIN_T
+#define CAEE_SHARED_EARLY_MIN_T 17
+#endif
+#ifndef CAEE_SHARED_EARLY_T
+#define CAEE_SHARED_EARLY_T 128
+#endif
+constexpr int kSharedEarly = CAEE_SHARED_EARLY;
+constexpr int kSharedEarlyMinT = CAEE_SHARED_EARLY_MIN_T;
+constexpr int kSharedEarlyT = CAEE_SHARED_EARLY_T;
+
+// FFN launches; inside an AnyOrderLaunch scope the kernel may start before
+// the stream's earlier kernels have finished.
+extern thread_local bool g_launch_any_order;
+struct AnyOrderLaunch {
+    explicit AnyOrderLaunch(bool on) { g_launch_any_order = on; }
+    ~AnyOrderLaunch() { g_launch_any_order = false; }
+};
+template <typename K, typename... Args>
+inline void ffn_launch(K kernel, dim3 grid, dim3 block, hipStream_t s, Args... args) {
+    if (g_launch_any_order)
+        hipExtLaunchKernelGGL(kernel, grid, block, 0, s, nullptr, nullptr, hipExtAnyOrderLaunch, args...);
+    else
+        hipLaunchKernelGGL(kernel, grid, block, 0, s, args...);
+}
 constexpr int kFfnThreads = 256;    // 4 independent waves per FFN workgroup
 // Gate/up wave work items wanted per call before the contraction is split
 // (about 32 per SIMD: short items keep the tail of the launch short).
@@ -288,6 +321,11 @@ struct FfnParams {
     const void* const* wtab;
     const int32_t* pass_of;
     int pass_id;
+    // shared_only: the launch's list is one chunk of all T rows per shared
+    // expert (rows s*T .. s*T + T - 1, row s*T + t for token t), read from
+    // the parameters alone; skip_shared: chunks of shared slots are skipped.
+    int shared_only;
+    int skip_shared;
     // fp8 path: quantised activations and their per-token 128-channel scales
     uint8_t* xq;
     float* xs;
@@ -304,21 +342,27 @@ struct ChunkRef {
     int xs, row0, ntok;
 };
 
-__device__ inline int ffn_list_size(const FfnParams& p) { return p.n_chunks[p.list]; }
+__device__ inline int ffn_list_size(const FfnParams& p) {
+    return p.shared_only ? p.n_shared : p.n_chunks[p.list];
+}
 
 __device__ inline ChunkRef ffn_chunk(const FfnParams& p, int c) {
+    if (p.shared_only) return {p.E + c, c * p.T, p.T};
     const int32_t* ch = p.chunks + 4 * ((p.list ? p.n_chunks[0] : 0) + c);
     return {ch[0], ch[1], ch[2]};
 }
 
 // Token of permuted row `row` (of expert slot xs).
 __device__ inline int ffn_token(const FfnParams& p, int xs, int row) {
-    (void)xs;
+    if (p.shared_only) return row - (xs - p.E) * p.T;
     return p.perm_tok[row];
 }
 
-// Offload passes: only the chunks of experts in pass p.pass_id run.
-__device__ inline bool ffn_skip(const FfnParams& p, int xs) { return p.pass_of && p.pass_of[xs] != p.pass_id; }
+// Offload passes: only the chunks of experts in pass p.pass_id run; with
+// skip_shared, no chunk of a shared slot.
+__device__ inline bool ffn_skip(const FfnParams& p, int xs) {
+    return (p.skip_shared && xs >= p.E) || (p.pass_of && p.pass_of[xs] != p.pass_id);
+}
 
 // First byte of matrix w13 (w2 = false) or w2 of expert slot xs.
 __device__ inline const char* ffn_weights(const FfnParams& p, int xs, bool w2, size_t expert_bytes) {
@@ -379,11 +423,19 @@ void set_route_outputs(RouteParams& p, const caee_route_out_t* out, char* ws, co
 struct FfnCall {
     hipStream_t main = nullptr, side = nullptr;   // side == main until forked
     hipEvent_t ev_join = nullptr;
+    bool shared_early = false;       // the shared experts' gate/up is already launched
+    hipEvent_t ev_shared = nullptr;  // when on the side stream: its completion,
+    bool shared_wait = false;        // which the main stream waits for before a down product
 };
 caee_status_t ffn_begin(const caee_layer_desc_t* d, const FfnParams& p, const WsLayout& L, hipStream_t s,
                         FfnCall* call);
 caee_status_t ffn_routed(const caee_layer_desc_t* d, const FfnParams& p, const WsLayout& L, FfnCall* call,
                          bool big_on_side);
+// The shared experts' gate/up next to routing: their rows come first in the
+// permutation and hold every token, so they need nothing routing computes.
+// Called before routing is enqueued (second-stream mode) and after it
+// (same-stream mode, launched without waiting for routing to finish).
+caee_status_t ffn_shared_early(const caee_layer_desc_t* d, const FfnParams& p, FfnCall* call, bool after_route);
 caee_status_t ffn_end(const FfnParams& p, FfnCall* call);
 
 // Opt-in timing: events bracket each launch on the caller's stream.

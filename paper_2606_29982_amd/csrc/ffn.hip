@@ -485,10 +485,10 @@ int grid_for(long long waves_needed) {
 template <class M, template <class, int, int> class K, int U>
 hipError_t launch_nb(const FfnParams& p, int nb, dim3 grid, hipStream_t s) {
     switch (nb) {
-        case 1: hipLaunchKernelGGL((K<M, U, 1>::run), grid, dim3(kFfnThreads), 0, s, p); break;
-        case 2: hipLaunchKernelGGL((K<M, U, 2>::run), grid, dim3(kFfnThreads), 0, s, p); break;
-        case 4: hipLaunchKernelGGL((K<M, U, 4>::run), grid, dim3(kFfnThreads), 0, s, p); break;
-        case 8: hipLaunchKernelGGL((K<M, U, 8>::run), grid, dim3(kFfnThreads), 0, s, p); break;
+        case 1: ffn_launch(K<M, U, 1>::run, grid, dim3(kFfnThreads), s, p); break;
+        case 2: ffn_launch(K<M, U, 2>::run, grid, dim3(kFfnThreads), s, p); break;
+        case 4: ffn_launch(K<M, U, 4>::run, grid, dim3(kFfnThreads), s, p); break;
+        case 8: ffn_launch(K<M, U, 8>::run, grid, dim3(kFfnThreads), s, p); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();

@@ -571,8 +571,8 @@ hipError_t launch_gate_up_fp8(const FfnParams& p, int nb, int max_chunks, hipStr
     }
     const dim3 grid(grid_for_waves((long long)max_chunks * (p.f / 16) * p.ksplit));
     switch (nb) {
-        case 1: hipLaunchKernelGGL(k_gate_up_fp8<1>, grid, dim3(kFfnThreads), 0, s, p); break;
-        case 2: hipLaunchKernelGGL(k_gate_up_fp8<2>, grid, dim3(kFfnThreads), 0, s, p); break;
+        case 1: ffn_launch(k_gate_up_fp8<1>, grid, dim3(kFfnThreads), s, p); break;
+        case 2: ffn_launch(k_gate_up_fp8<2>, grid, dim3(kFfnThreads), s, p); break;
         case 4: hipLaunchKernelGGL(k_gate_up_fp8<4>, grid, dim3(kFfnThreads), 0, s, p); break;
         case 8: hipLaunchKernelGGL(k_gate_up_fp8<8>, grid, dim3(kFfnThreads), 0, s, p); break;
         default: return hipErrorInvalidValue;

@@ -634,18 +634,21 @@ __global__ __launch_bounds__(kRouteThreads) void k_prune(RouteParams p) {
 
 // Row offsets of every expert slot and the FFN work lists, from the slot
 // row counts in s_cnt (run by one wavefront).  Slot x (x < E routed, E+s
-// shared) owns rows [off[x], off[x] + count); then one small chunk per slot
-// with at most chunk_small rows, and ceil(rows / chunk_big) near-equal big
-// chunks per larger slot, the small chunks listed first.
+// shared) owns rows [off[x], off[x] + count); the shared slots come first
+// (shared expert s owns rows s*T .. s*T + T - 1, known before routing), then
+// the routed ones in expert order.  Then one small chunk per slot with at
+// most chunk_small rows, and ceil(rows / chunk_big) near-equal big chunks per
+// larger slot, the small chunks listed first.
 __device__ void build_lists(const RouteParams& p, const int* s_cnt, int* s_off, int lane) {
-    const int nx = p.E + p.n_shared;
+    const int nx = p.E + p.n_shared, ns = p.n_shared, E = p.E;
     const int cs = p.chunk_small, cb = p.chunk_big;
     const int per = (nx + kWave - 1) / kWave;
     const int lo = lane * per;
     const int hi = min(lo + per, nx);
+    auto slot_at = [&](int j) { return j < ns ? E + j : j - ns; };   // j-th slot in row order
     int sum = 0, ssum = 0, bsum = 0;
-    for (int x = lo; x < hi; ++x) {
-        const int n = s_cnt[x];
+    for (int j = lo; j < hi; ++j) {
+        const int n = s_cnt[slot_at(j)];
         sum += n;
         ssum += (n > 0 && n <= cs) ? 1 : 0;
         bsum += n > cs ? (n + cb - 1) / cb : 0;
@@ -653,7 +656,8 @@ __device__ void build_lists(const RouteParams& p, const int* s_cnt, int* s_off, 
     const int inc = wave_incl_scan(sum), sinc = wave_incl_scan(ssum), binc = wave_incl_scan(bsum);
     const int stotal = __builtin_amdgcn_readlane(sinc, kWave - 1);
     int run = inc - sum, srun = sinc - ssum, brun = stotal + binc - bsum;
-    for (int x = lo; x < hi; ++x) {
+    for (int j = lo; j < hi; ++j) {
+        const int x = slot_at(j);
         const int cnt = s_cnt[x];
         s_off[x] = run;
         p.perm_off[x] = run;
