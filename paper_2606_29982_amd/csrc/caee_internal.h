@@ -41,6 +41,12 @@ constexpr int kPrefillT = CAEE_PREFILL_T;
 #define CAEE_GEMM_T 256
 #endif
 constexpr int kGemmT = CAEE_GEMM_T;
+// bf16 big chunks (experts with more rows than a small chunk holds) run
+// the same LDS-pipelined GEMM, as wide as its token tile (0 disables).
+#ifndef CAEE_GEMM_BF16
+#define CAEE_GEMM_BF16 1
+#endif
+constexpr int kGemmBf16 = CAEE_GEMM_BF16;
 // Batches of kSharedEarlyMinT .. kSharedEarlyT tokens launch the shared
 // experts' gate/up next to routing: 0 never, 1 on the second stream, 2 on
 // the same stream without waiting for routing (an any-order launch; it ran
@@ -188,6 +194,7 @@ inline int big_token_blocks(const caee_layer_desc_t& d) {
 }
 
 bool gemm_fp8_applies(const caee_layer_desc_t& d, bool tiled);
+bool gemm_bf16_applies(const caee_layer_desc_t& d, bool tiled);
 int gemm_fp8_blocks();
 bool gemm_fp8_fuses_quant();   // the GEMM's gate/up writes the e4m3 H rows itself
 
@@ -198,7 +205,7 @@ bool gemm_fp8_fuses_quant();   // the GEMM's gate/up writes the e4m3 H rows itse
 // big_token_blocks, which never gives fewer chunks.
 inline int call_big_blocks(const caee_layer_desc_t& d, bool tiled) {
     const int nb = big_token_blocks(d);
-    return nb > 0 && gemm_fp8_applies(d, tiled) ? gemm_fp8_blocks() : nb;
+    return nb > 0 && (gemm_fp8_applies(d, tiled) || gemm_bf16_applies(d, tiled)) ? gemm_fp8_blocks() : nb;
 }
 
 // Rows per big chunk of a call (16 when there are no big chunks).
@@ -388,7 +395,8 @@ hipError_t launch_gate_up_fp8(const FfnParams& p, int nb, int max_chunks, hipStr
 hipError_t launch_quant_list(const FfnParams& p, int nb, int max_chunks, bool transposed, hipStream_t s);
 hipError_t launch_gather_xs(const FfnParams& p, int max_chunks, hipStream_t s);
 bool gemm_fp8_supports(const FfnParams& p, int nb);
-hipError_t launch_gemm_fp8(const FfnParams& p, bool gate_up, int max_chunks, hipStream_t s);
+bool gemm_bf16_supports(const FfnParams& p, int nb);
+hipError_t launch_gemm(const FfnParams& p, bool gate_up, bool fp8, int max_chunks, hipStream_t s);
 hipError_t launch_down_fp8(const FfnParams& p, int nb, int max_chunks, hipStream_t s);
 hipError_t launch_pack(const void* src, void* dst, long long rows, long long row_units, long long count,
                        hipStream_t s);

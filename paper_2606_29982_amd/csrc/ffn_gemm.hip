@@ -34,6 +34,7 @@ typedef int i32x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void lds_void_t;
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 
 constexpr int kScaleOne = 127;        // E8M0 1.0: the MFMA's own block scales are unused
 // Workgroup tile: kTiles 16-row weight tiles x kNT 16-token tiles, 8 waves
@@ -59,7 +60,10 @@ constexpr bool kFuseQuant = kTiles == 16;
 constexpr int kStages = 3;
 constexpr int kGemmWaves = 8;
 constexpr int kGemmThreads = kGemmWaves * kWave;
-constexpr int kLoadsPerStage = 7;     // per wave: 2 weight, 4 row, 1 scale loads
+// Loads per wave and stage: the weight and token-row pieces, plus (8-bit)
+// one load of the rows' block scales.
+template <bool kFp8>
+constexpr int loads_per_stage() { return kTiles / 4 + kNT / 4 + (kFp8 ? 1 : 0); }
 constexpr int kMaxKBlocks = 128;      // contraction up to 16384
 constexpr int kXcds = 8;              // accelerator complex dies, each with its own L2
 
@@ -74,6 +78,11 @@ __device__ inline i32x8_t join(const u32x4_t& lo, const u32x4_t& hi) {
 }
 
 __device__ inline float silu_mul(float g, float u) { return g / (1.0f + __expf(-g)) * u; }
+
+__device__ inline uint32_t bf16_bits(float v) {   // round to nearest even
+    const uint32_t u = __float_as_uint(v);
+    return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+}
 
 // Waits until at most n of this wave's vector memory loads are outstanding
 // (gfx9 s_waitcnt: vmcnt in bits 3:0 and 15:14, expcnt and lgkmcnt not waited).
@@ -91,8 +100,13 @@ __device__ inline void stage_barrier() {
     asm volatile("" ::: "memory");
 }
 
-template <bool kGateUp>
-__global__ __launch_bounds__(kGemmThreads) void k_gemm_fp8(FfnParams p) {
+// kFp8: e4m3 weights with fp32 block scales and quantised rows, one scaled
+// 16x16x128 MFMA per 128-element stage; otherwise bf16 weights and rows,
+// two 16x16x32 MFMAs per 64-element stage (the same 128 bytes per row).
+template <bool kGateUp, bool kFp8>
+__global__ __launch_bounds__(kGemmThreads) void k_gemm(FfnParams p) {
+    constexpr int kLoadsPerStage = loads_per_stage<kFp8>();
+    constexpr int kEb = kFp8 ? 1 : 2;                  // bytes per element
     // The ring's stages are separate LDS objects (and the code below names
     // each statically), so the compiler can tell a read of one stage from the
     // loads still filling the others and does not wait for those.
@@ -105,14 +119,14 @@ __global__ __launch_bounds__(kGemmThreads) void k_gemm_fp8(FfnParams p) {
     const int wq = wave % kRowWaves, wc = wave / kRowWaves;   // weight rows, token columns
     const int r = lane & 15, g = lane >> 4;
     const int K = kGateUp ? p.d : p.f;                 // contraction length
-    const int kblocks = K / 128;
-    const size_t ksteps = (size_t)K / 64;              // 64-byte steps per weight row
-    const size_t row_units = (size_t)K / 16;           // 16-byte pieces per token row
+    const int kblocks = K * kEb / 128;                 // pipeline stages (128 bytes of each row)
+    const size_t ksteps = (size_t)K * kEb / 64;        // 64-byte steps per weight row
+    const size_t row_units = (size_t)K * kEb / 16;     // 16-byte pieces per token row
     const int rows_out = kGateUp ? p.f : p.d;          // features (gate/up) or output rows (down)
     const int groups = kGateUp ? rows_out / (16 * kTiles / 2) : rows_out / (16 * kTiles);
     const int n_chunks = ffn_list_size(p);
     const int total = n_chunks * groups;
-    const size_t expert_bytes = kGateUp ? (size_t)2 * p.f * p.d : (size_t)p.d * p.f;
+    const size_t expert_bytes = (kGateUp ? (size_t)2 * p.f * p.d : (size_t)p.d * p.f) * kEb;
     const size_t scales_per_expert = (size_t)((kGateUp ? 2 * p.f : p.d) / 128) * kblocks;
     const f32x4_t zero = {0.f, 0.f, 0.f, 0.f};
     // Workgroups go to the XCDs round robin (workgroup b to XCD b % 8).  With
@@ -134,7 +148,7 @@ __global__ __launch_bounds__(kGemmThreads) void k_gemm_fp8(FfnParams p) {
         if (ffn_skip(p, xs)) continue;   // uniform over the workgroup
         const int nb = (ntok + 15) >> 4;
         const u32x4_t* wb = (const u32x4_t*)ffn_weights(p, xs, kGateUp ? false : true, expert_bytes);
-        const float* wsc = ffn_scales(p, xs, kGateUp ? false : true, scales_per_expert);
+        const float* wsc = kFp8 ? ffn_scales(p, xs, kGateUp ? false : true, scales_per_expert) : nullptr;
         // Expert-relative weight tile of workgroup tile slot i.
         auto tile_of = [&](int i) {
             if (kGateUp) return i < kTiles / 2 ? grp * (kTiles / 2) + i : p.f / 16 + grp * (kTiles / 2) + i - kTiles / 2;
@@ -157,13 +171,13 @@ __global__ __launch_bounds__(kGemmThreads) void k_gemm_fp8(FfnParams p) {
             int n = 16 * (j >> 1) + r;
             n = n < ntok ? n : 0;          // padded token columns read a valid row; results dropped
             const int row = kGateUp ? ffn_token(p, xs, row0 + n) : row0 + n;
-            bsrc[i] = (const u32x4_t*)(kGateUp ? (const void*)p.xq : (const void*)p.hq) + (size_t)row * row_units +
-                      (j & 1) * 4 + g;
+            const void* rows = kFp8 ? (kGateUp ? (const void*)p.xq : (const void*)p.hq) : (kGateUp ? p.x : p.h);
+            bsrc[i] = (const u32x4_t*)rows + (size_t)row * row_units + (j & 1) * 4 + g;
         }
         // Row scales, transposed and in permuted row order ([block][row]):
         // one 128-byte line per wave and block.
-        const float* xsrc;
-        {
+        const float* xsrc = nullptr;
+        if (kFp8) {
             int n = kXPer * wave + lane % kXPer;
             n = n < ntok ? n : 0;
             xsrc = (kGateUp ? p.xst : p.hst) + row0 + n;
@@ -181,7 +195,9 @@ __global__ __launch_bounds__(kGemmThreads) void k_gemm_fp8(FfnParams p) {
                 __builtin_amdgcn_global_load_lds((const void*)(bsrc[i] + (size_t)kb * 8),
                                                  (lds_void_t*)&s.b[j >> 1][j & 1][0], 16, 0, 0);
             }
-            __builtin_amdgcn_global_load_lds((const void*)(xsrc + (size_t)kb * p.P), (lds_void_t*)&s.x[wave][0], 4, 0, 0);
+            if (kFp8)
+                __builtin_amdgcn_global_load_lds((const void*)(xsrc + (size_t)kb * p.P), (lds_void_t*)&s.x[wave][0], 4,
+                                                 0, 0);
         };
         // Weight tiles this wave multiplies: gate/up -> slots 2q, 2q+1 (gate)
         // and 4+2q, 5+2q (up); down -> slots 4q..4q+3.
@@ -191,11 +207,12 @@ __global__ __launch_bounds__(kGemmThreads) void k_gemm_fp8(FfnParams p) {
             aslot[i] = kGateUp ? (i < 2 ? 2 * wq + i : kTiles / 2 + 2 * wq + i - 2) : 4 * wq + i;
             srow[i] = aslot[i] >= kTiles / 2;
         }
-        for (int q = tid; q < 2 * kblocks; q += kGemmThreads) {
-            const int h = q >= kblocks, kb = q - h * kblocks;
-            const int row = (tile_of(h * (kTiles / 2)) * 16) / 128;
-            wsl[h][kb] = wsc[(size_t)row * kblocks + kb];
-        }
+        if (kFp8)
+            for (int q = tid; q < 2 * kblocks; q += kGemmThreads) {
+                const int h = q >= kblocks, kb = q - h * kblocks;
+                const int row = (tile_of(h * (kTiles / 2)) * 16) / 128;
+                wsl[h][kb] = wsc[(size_t)row * kblocks + kb];
+            }
         __syncthreads();
 
         f32x4_t acc[4][kWaveNT];
@@ -206,6 +223,26 @@ __global__ __launch_bounds__(kGemmThreads) void k_gemm_fp8(FfnParams p) {
 
         // Multiplies block kb, held in stage s.
         auto compute = [&](int kb, const GemmStage& s) __attribute__((always_inline)) {
+            if (!kFp8) {
+                // bf16: the stage's two 64-byte steps are two MFMAs deep.
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    bf16x8_t af[4];
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) af[i] = __builtin_bit_cast(bf16x8_t, s.a[aslot[i]][h][lane]);
+#pragma unroll
+                    for (int j = 0; j < kWaveNT; ++j) {
+                        const int n = kWaveNT * wc + j;
+                        if (n < nb) {
+                            const bf16x8_t bf = __builtin_bit_cast(bf16x8_t, s.b[n][h][lane]);
+#pragma unroll
+                            for (int i = 0; i < 4; ++i)
+                                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bf, acc[i][j], 0, 0, 0);
+                        }
+                    }
+                }
+                return;
+            }
             i32x8_t af[4];
             float ws[4];
 #pragma unroll
@@ -278,7 +315,7 @@ __global__ __launch_bounds__(kGemmThreads) void k_gemm_fp8(FfnParams p) {
         }
         // All waves are done with the ring before the next item refills it.
         stage_barrier();
-        if constexpr (kGateUp && kFuseQuant) {
+        if constexpr (kGateUp && kFp8 && kFuseQuant) {
             // Per token row: amax over the item's 128 SwiGLU values (this
             // lane's 8, the 4 lanes of the column, the row waves through
             // LDS), scale = amax / 448 (1 if zero), codes of value / scale:
@@ -332,7 +369,15 @@ __global__ __launch_bounds__(kGemmThreads) void k_gemm_fp8(FfnParams p) {
                     float h[4];
 #pragma unroll
                     for (int v = 0; v < 4; ++v) h[v] = silu_mul(acc[i][j][v], acc[i + 2][j][v]);
-                    *(float4*)((float*)p.h + (size_t)(row0 + tn) * p.f + col) = make_float4(h[0], h[1], h[2], h[3]);
+                    const size_t o = (size_t)(row0 + tn) * p.f + col;
+                    if (kFp8) {
+                        *(float4*)((float*)p.h + o) = make_float4(h[0], h[1], h[2], h[3]);
+                    } else {   // bf16 SwiGLU rows, rounded to nearest even
+                        uint2 pk;
+                        pk.x = bf16_bits(h[0]) | (bf16_bits(h[1]) << 16);
+                        pk.y = bf16_bits(h[2]) | (bf16_bits(h[3]) << 16);
+                        *(uint2*)((uint16_t*)p.h + o) = pk;
+                    }
                 }
             } else {
 #pragma unroll
@@ -382,7 +427,19 @@ int gemm_fp8_blocks() { return kNT; }
 
 bool gemm_fp8_fuses_quant() { return kFuseQuant; }
 
-hipError_t launch_gemm_fp8(const FfnParams& p, bool gate_up, int max_chunks, hipStream_t s) {
+// bf16: 64-element stages; gate/up items of kTiles / 2 features, down items
+// of kTiles row tiles.
+bool gemm_bf16_supports(const FfnParams& p, int nb) {
+    return kGemmBf16 && nb == kNT && p.tiled && p.d % 64 == 0 && p.f % 64 == 0 && p.f % (8 * kTiles) == 0 &&
+           p.d % (16 * kTiles) == 0;
+}
+
+bool gemm_bf16_applies(const caee_layer_desc_t& d, bool tiled) {
+    return kGemmBf16 && d.w_dtype == CAEE_BF16 && tiled && d.d % 64 == 0 && d.f % 64 == 0 &&
+           d.f % (8 * kTiles) == 0 && d.d % (16 * kTiles) == 0;
+}
+
+hipError_t launch_gemm(const FfnParams& p, bool gate_up, bool fp8, int max_chunks, hipStream_t s) {
     const int groups = gate_up ? p.f / (16 * kTiles / 2) : p.d / (16 * kTiles);
     // One workgroup per CU at a time (the ring fills the LDS); with the plain
     // order, two per CU so that a CU whose items end early takes more.
@@ -390,8 +447,14 @@ hipError_t launch_gemm_fp8(const FfnParams& p, bool gate_up, int max_chunks, hip
     const long long cap = (long long)device_cu_count() * (CAEE_GEMM_XCD ? 1 : 2);
     if (items > cap) items = cap;
     if (items < 1) items = 1;
-    if (gate_up) hipLaunchKernelGGL(k_gemm_fp8<true>, dim3((unsigned)items), dim3(kGemmThreads), 0, s, p);
-    else hipLaunchKernelGGL(k_gemm_fp8<false>, dim3((unsigned)items), dim3(kGemmThreads), 0, s, p);
+    const dim3 grid((unsigned)items), block(kGemmThreads);
+    if (fp8) {
+        if (gate_up) ffn_launch(k_gemm<true, true>, grid, block, s, p);
+        else ffn_launch(k_gemm<false, true>, grid, block, s, p);
+    } else {
+        if (gate_up) ffn_launch(k_gemm<true, false>, grid, block, s, p);
+        else ffn_launch(k_gemm<false, false>, grid, block, s, p);
+    }
     return hipGetLastError();
 }
 
