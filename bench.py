@@ -31,7 +31,17 @@ W_EXPERT_BYTES_FP8 = 3 * 7168 * 2048 + 4 * (2 * 2048 // 128) * (7168 // 128) + 4
 PAIR_FLOPS = 6 * 7168 * 2048    # one (token, expert) pair through gate, up and down
 METRIC = "MoE-layer tokens/s + achieved HBM GB/s (% of peak) at T=1..128, with vs without pruning"
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gate_up_r1_t32_traffic.json")
-FFN_SOURCE = os.path.join(ROOT, "paper_2606_29982_amd", "csrc", "ffn.hip")
+# The gate/up kernel's source and the header holding its tuning constants:
+# a traffic figure holds only for the build they describe.
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2606_29982_amd", "csrc", n) for n in ("ffn.hip", "caee_internal.h")]
+
+
+def kernel_sources_sha256():
+    h = hashlib.sha256()
+    for path in KERNEL_SOURCES:
+        with open(path, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
 
 
 def parse():
@@ -148,11 +158,10 @@ def layer_bytes(shape, T, n_trans):
             + T * shape.E * 4 + 12 * shape.E)
 
 
-def gate_up_bytes(shape, T, n_trans, rows):
+def gate_up_bytes(shape, T, n_experts, rows):
     """Algorithmic bytes of one gate/up launch: the gate and up matrices of
-    every executed expert, x read once, the bf16 SwiGLU rows written."""
-    return ((n_trans + shape.n_shared) * 2 * shape.f * shape.d * 2 + T * shape.d * 2
-            + rows * shape.f * 2)
+    the experts it runs, x read once, the bf16 SwiGLU rows written."""
+    return n_experts * 2 * shape.f * shape.d * 2 + T * shape.d * 2 + rows * shape.f * 2
 
 
 def traffic_entry():
@@ -161,9 +170,7 @@ def traffic_entry():
     try:
         with open(TRAFFIC_FILE) as fh:
             rec = json.load(fh)
-        with open(FFN_SOURCE, "rb") as fh:
-            src = hashlib.sha256(fh.read()).hexdigest()
-        if rec.get("ffn_source_sha256") != src:
+        if rec.get("sources_sha256") != kernel_sources_sha256():
             return None
         return rec.get("bytes_per_launch")
     except (OSError, ValueError):
@@ -435,13 +442,17 @@ def main():
         + ", ".join(f"{k} {v * 1e3:.1f} ({launches[k]:.0f} launches)" for k, v in kern.items()))
 
     b_layer = layer_bytes(shape, args.T, n_trans)
-    # gate/up runs as two launches per step: the shared expert (next to
-    # routing) and the routed experts; each launch reads x once.
+    # The routed experts' gate/up launch.  When the shared experts' gate/up
+    # ran next to routing (its own launch and timing kind), this launch
+    # leaves them out.
+    shared_apart = launches["gate_up_shared"] > 0
     n_gu = max(int(round(launches["gate_up"])), 1)
-    gu_bytes = gate_up_bytes(shape, args.T, n_trans, rows) + (n_gu - 1) * args.T * shape.d * 2
+    gu_rows = args.T * shape.k + (0 if shared_apart else args.T * shape.n_shared)
+    gu_bytes = gate_up_bytes(shape, args.T, n_trans + (0 if shared_apart else shape.n_shared), gu_rows)
+    gu_bytes += (n_gu - 1) * args.T * shape.d * 2   # every launch reads x once
     gu_gbps = gu_bytes / (kern["gate_up"] * 1e-3) / 1e9
     traffic = traffic_entry()
-    roofline = {"kernel": "k_gate_up (expert gate/up + SwiGLU)", "bound": "hbm",
+    roofline = {"kernel": "k_gate_up (routed experts' gate/up + SwiGLU)", "bound": "hbm",
                 "achieved": round(gu_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                 "frac": round(gu_gbps / HBM_PEAK_GBPS, 4), "traffic": traffic,
                 "launches_per_step": n_gu, "bytes_per_launch": round(gu_bytes / n_gu),

@@ -274,12 +274,11 @@ caee_status_t order(hipEvent_t ev, hipStream_t from, hipStream_t to, const char*
 }
 
 caee_status_t gate_up_list(const caee_layer_desc_t* d, FfnParams p, int list, int nb, int max_chunks,
-                           hipStream_t s) {
+                           hipStream_t s, int kind = CAEE_KERNEL_GATE_UP) {
     p.list = list;
     if (d->w_dtype == CAEE_FP8_E4M3)
-        return timed_launch(CAEE_KERNEL_GATE_UP, s, "gate/up", [&] { return launch_gate_up_fp8(p, nb, max_chunks, s); });
-    return timed_launch(CAEE_KERNEL_GATE_UP, s, "gate/up",
-                        [&] { return launch_gate_up(p, d->w_dtype, nb, max_chunks, s); });
+        return timed_launch(kind, s, "gate/up", [&] { return launch_gate_up_fp8(p, nb, max_chunks, s); });
+    return timed_launch(kind, s, "gate/up", [&] { return launch_gate_up(p, d->w_dtype, nb, max_chunks, s); });
 }
 
 caee_status_t down_list(const caee_layer_desc_t* d, FfnParams p, int list, int nb, int max_chunks, hipStream_t s) {
@@ -323,7 +322,7 @@ caee_status_t ffn_shared_early(const caee_layer_desc_t* d, const FfnParams& p, F
     }
     {
         AnyOrderLaunch scope(kSharedEarly == 2);
-        CAEE_TRY(gate_up_list(d, q, 0, nb, d->n_shared, st));
+        CAEE_TRY(gate_up_list(d, q, 0, nb, d->n_shared, st, CAEE_KERNEL_GATE_UP_SHARED));
     }
     if (ss) {
         const hipError_t e = hipEventRecord(ss->shared, ss->stream);

@@ -53,37 +53,44 @@ __device__ inline float silu_mul(float g, float u) { return g / (1.0f + __expf(-
 // Contraction of one 16-row weight tile against up to NB 16-token blocks,
 // over `nsteps` k-steps starting at the given pointers.  Weights are loaded
 // U steps ahead of the MFMAs that consume them (register double buffer).
-template <class M, int U, int NA, int NB>
-__device__ inline void tile_contract(const u32x4_t* const (&a)[NA], int astep, const u32x4_t* const (&b)[NB],
-                                     int nb, int nsteps, f32x4_t (&acc)[NA][NB]) {
+// kTail: nsteps need not be a multiple of U; steps past the end are neither
+// multiplied nor read (their weight loads repeat the last step, inside the
+// row).  Without it every batch of U steps is whole.
+template <class M, int U, int NA, int NB, bool kTail>
+__device__ inline void tile_contract_steps(const u32x4_t* const (&a)[NA], int astep, const u32x4_t* const (&b)[NB],
+                                           int nb, int nsteps, f32x4_t (&acc)[NA][NB]) {
+    auto in_row = [&](int st) { return !kTail || st < nsteps ? st : nsteps - 1; };
     u32x4_t cur[NA][U], nxt[NA][U];
 #pragma unroll
     for (int m = 0; m < NA; ++m)
 #pragma unroll
-        for (int u = 0; u < U; ++u) cur[m][u] = __builtin_nontemporal_load(a[m] + (size_t)astep * u);
+        for (int u = 0; u < U; ++u) cur[m][u] = __builtin_nontemporal_load(a[m] + (size_t)astep * in_row(u));
     for (int ks = 0; ks < nsteps; ks += U) {
         const bool more = CAEE_FFN_PIPELINE && ks + U < nsteps;
         if (!CAEE_FFN_PIPELINE && ks > 0) {
 #pragma unroll
             for (int m = 0; m < NA; ++m)
 #pragma unroll
-                for (int u = 0; u < U; ++u) cur[m][u] = __builtin_nontemporal_load(a[m] + (size_t)astep * (ks + u));
+                for (int u = 0; u < U; ++u)
+                    cur[m][u] = __builtin_nontemporal_load(a[m] + (size_t)astep * in_row(ks + u));
         }
         if (more) {
 #pragma unroll
             for (int m = 0; m < NA; ++m)
 #pragma unroll
                 for (int u = 0; u < U; ++u)
-                    nxt[m][u] = __builtin_nontemporal_load(a[m] + (size_t)astep * (ks + U + u));
+                    nxt[m][u] = __builtin_nontemporal_load(a[m] + (size_t)astep * in_row(ks + U + u));
         }
 #pragma unroll
         for (int tb = 0; tb < NB; ++tb) {
             if (tb < nb) {
 #pragma unroll
                 for (int u = 0; u < U; ++u) {
-                    const u32x4_t bv = b[tb][4 * (ks + u)];
+                    if (!kTail || ks + u < nsteps) {
+                        const u32x4_t bv = b[tb][4 * (ks + u)];
 #pragma unroll
-                    for (int m = 0; m < NA; ++m) M::mma(acc[m][tb], cur[m][u], bv);
+                        for (int m = 0; m < NA; ++m) M::mma(acc[m][tb], cur[m][u], bv);
+                    }
                 }
             }
         }
@@ -94,6 +101,13 @@ __device__ inline void tile_contract(const u32x4_t* const (&a)[NA], int astep, c
                 for (int u = 0; u < U; ++u) cur[m][u] = nxt[m][u];
         }
     }
+}
+
+template <class M, int U, int NA, int NB>
+__device__ inline void tile_contract(const u32x4_t* const (&a)[NA], int astep, const u32x4_t* const (&b)[NB],
+                                     int nb, int nsteps, f32x4_t (&acc)[NA][NB]) {
+    if (nsteps % U == 0) tile_contract_steps<M, U, NA, NB, false>(a, astep, b, nb, nsteps, acc);
+    else tile_contract_steps<M, U, NA, NB, true>(a, astep, b, nb, nsteps, acc);
 }
 
 template <class M>
