@@ -442,17 +442,14 @@ def main():
         + ", ".join(f"{k} {v * 1e3:.1f} ({launches[k]:.0f} launches)" for k, v in kern.items()))
 
     b_layer = layer_bytes(shape, args.T, n_trans)
-    # The routed experts' gate/up launch.  When the shared experts' gate/up
-    # ran next to routing (its own launch and timing kind), this launch
-    # leaves them out.
-    shared_apart = launches["gate_up_shared"] > 0
+    # The gate/up launch of the routed and shared experts.
     n_gu = max(int(round(launches["gate_up"])), 1)
-    gu_rows = args.T * shape.k + (0 if shared_apart else args.T * shape.n_shared)
-    gu_bytes = gate_up_bytes(shape, args.T, n_trans + (0 if shared_apart else shape.n_shared), gu_rows)
+    gu_rows = args.T * (shape.k + shape.n_shared)
+    gu_bytes = gate_up_bytes(shape, args.T, n_trans + shape.n_shared, gu_rows)
     gu_bytes += (n_gu - 1) * args.T * shape.d * 2   # every launch reads x once
     gu_gbps = gu_bytes / (kern["gate_up"] * 1e-3) / 1e9
     traffic = traffic_entry()
-    roofline = {"kernel": "k_gate_up (routed experts' gate/up + SwiGLU)", "bound": "hbm",
+    roofline = {"kernel": "k_gate_up (expert gate/up + SwiGLU)", "bound": "hbm",
                 "achieved": round(gu_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                 "frac": round(gu_gbps / HBM_PEAK_GBPS, 4), "traffic": traffic,
                 "launches_per_step": n_gu, "bytes_per_launch": round(gu_bytes / n_gu),

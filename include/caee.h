@@ -49,7 +49,7 @@
 extern "C" {
 #endif
 
-#define CAEE_ABI_VERSION 6
+#define CAEE_ABI_VERSION 7
 
 typedef enum caee_status {
     CAEE_OK = 0,
@@ -356,8 +356,7 @@ typedef enum caee_kernel_kind {
     CAEE_KERNEL_DOWN = 2,     /* expert down products */
     CAEE_KERNEL_COMBINE = 3,  /* weighted combine into y */
     CAEE_KERNEL_QUANT = 4,    /* fp8 activation quantisation (x and the SwiGLU rows) */
-    CAEE_KERNEL_GATE_UP_SHARED = 5,   /* the shared experts' gate/up when launched next to routing */
-    CAEE_KERNEL_KINDS = 6
+    CAEE_KERNEL_KINDS = 5
 } caee_kernel_kind_t;
 caee_status_t caee_timing_enable(int on);
 caee_status_t caee_timing_reset(void);

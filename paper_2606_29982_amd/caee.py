@@ -17,7 +17,7 @@ LIB_PATH = os.path.join(HERE, "libcaee.so")
 
 CAEE_OK, CAEE_ERR_INVALID_ARG, CAEE_ERR_UNSUPPORTED, CAEE_ERR_WORKSPACE, CAEE_ERR_HIP, CAEE_ERR_CAPACITY = range(6)
 CAEE_F32, CAEE_BF16, CAEE_FP8_E4M3 = 0, 1, 2
-KERNEL_KINDS = {"route": 0, "gate_up": 1, "down": 2, "combine": 3, "quant": 4, "gate_up_shared": 5}
+KERNEL_KINDS = {"route": 0, "gate_up": 1, "down": 2, "combine": 3, "quant": 4}
 DTYPE_CODE = {"f32": CAEE_F32, "bf16": CAEE_BF16, "fp8": CAEE_FP8_E4M3}
 IMPORTANCE_CODE = {"max": 0, "sum": 1, "cir": 2}
 REFILL_CODE = {"score": 0, "none": 1, "random": 2, "literal": 3}

@@ -12,7 +12,6 @@
 
 namespace caee {
 
-thread_local bool g_launch_any_order = false;
 
 namespace {
 thread_local std::string g_last_error;
@@ -244,7 +243,7 @@ namespace {
 // kept until the process ends; default priority.
 struct SideStream {
     hipStream_t stream = nullptr;
-    hipEvent_t fork = nullptr, join = nullptr, shared = nullptr;
+    hipEvent_t fork = nullptr, join = nullptr;
 };
 
 caee_status_t side_stream(SideStream** out) {
@@ -256,7 +255,6 @@ caee_status_t side_stream(SideStream** out) {
         hipError_t e = hipStreamCreateWithFlags(&ss.stream, hipStreamNonBlocking);
         if (e == hipSuccess) e = hipEventCreateWithFlags(&ss.fork, hipEventDisableTiming);
         if (e == hipSuccess) e = hipEventCreateWithFlags(&ss.join, hipEventDisableTiming);
-        if (e == hipSuccess) e = hipEventCreateWithFlags(&ss.shared, hipEventDisableTiming);
         if (e != hipSuccess) {
             ss = SideStream{};
             return fail(CAEE_ERR_HIP, "side stream creation failed: %s", hipGetErrorString(e));
@@ -274,7 +272,8 @@ caee_status_t order(hipEvent_t ev, hipStream_t from, hipStream_t to, const char*
 }
 
 caee_status_t gate_up_list(const caee_layer_desc_t* d, FfnParams p, int list, int nb, int max_chunks,
-                           hipStream_t s, int kind = CAEE_KERNEL_GATE_UP) {
+                           hipStream_t s) {
+    const int kind = CAEE_KERNEL_GATE_UP;
     p.list = list;
     if (d->w_dtype == CAEE_FP8_E4M3)
         return timed_launch(kind, s, "gate/up", [&] { return launch_gate_up_fp8(p, nb, max_chunks, s); });
@@ -302,38 +301,6 @@ caee_status_t ffn_begin(const caee_layer_desc_t* d, const FfnParams& p, const Ws
     return CAEE_OK;
 }
 
-caee_status_t ffn_shared_early(const caee_layer_desc_t* d, const FfnParams& p, FfnCall* call, bool after_route) {
-    if (kSharedEarly == 0 || d->n_shared == 0 || d->T < kSharedEarlyMinT || d->T > kSharedEarlyT) return CAEE_OK;
-    if (after_route != (kSharedEarly == 2)) return CAEE_OK;
-    FfnParams q = p;
-    q.shared_only = 1;
-    // One chunk of T rows per shared expert, in a kernel compiled for 1, 2,
-    // 4 or 8 token blocks.
-    const int blocks = (d->T + 15) / 16;
-    const int nb = blocks <= 1 ? 1 : blocks <= 2 ? 2 : blocks <= 4 ? 4 : 8;
-    hipStream_t st = call->main;
-    SideStream* ss = nullptr;
-    if (kSharedEarly == 1) {
-        CAEE_TRY(side_stream(&ss));
-        CAEE_TRY(order(ss->fork, call->main, ss->stream, "fork to the side stream"));
-        call->side = ss->stream;
-        call->ev_join = ss->join;
-        st = ss->stream;
-    }
-    {
-        AnyOrderLaunch scope(kSharedEarly == 2);
-        CAEE_TRY(gate_up_list(d, q, 0, nb, d->n_shared, st, CAEE_KERNEL_GATE_UP_SHARED));
-    }
-    if (ss) {
-        const hipError_t e = hipEventRecord(ss->shared, ss->stream);
-        if (e != hipSuccess) return fail(CAEE_ERR_HIP, "hipEventRecord failed: %s", hipGetErrorString(e));
-        call->ev_shared = ss->shared;
-        call->shared_wait = true;
-    }
-    call->shared_early = true;
-    return CAEE_OK;
-}
-
 caee_status_t ffn_routed(const caee_layer_desc_t* d, const FfnParams& p, const WsLayout& L, FfnCall* call,
                          bool big_on_side) {
     const int nb_small = small_token_blocks(*d), nb_big = call_big_blocks(*d, p.tiled);
@@ -350,9 +317,6 @@ caee_status_t ffn_routed(const caee_layer_desc_t* d, const FfnParams& p, const W
         CAEE_TRY(order(ss->fork, s, ss->stream, "fork to the side stream"));
         sb = call->side;
     }
-    // Gate/up skips the shared experts when they already ran next to routing.
-    FfnParams pg = p;
-    pg.skip_shared = call->shared_early ? 1 : 0;
     // One list's chain: gate/up, (fp8) quantisation of its SwiGLU rows, down.
     // The 8-bit GEMM reads its rows' block scales transposed and in permuted
     // row order: gathered once for x, written so by the quantiser for H.
@@ -363,16 +327,10 @@ caee_status_t ffn_routed(const caee_layer_desc_t* d, const FfnParams& p, const W
         if (gemm)
             CAEE_TRY(timed_launch(CAEE_KERNEL_QUANT, st, "gather x scales",
                                   [&] { return launch_gather_xs(q, L.max_chunks, st); }));
-        CAEE_TRY(gate_up_list(d, pg, list, nb, L.max_chunks, st));
+        CAEE_TRY(gate_up_list(d, p, list, nb, L.max_chunks, st));
         if (d->w_dtype == CAEE_FP8_E4M3 && !(gemm && gemm_fp8_fuses_quant()))
             CAEE_TRY(timed_launch(CAEE_KERNEL_QUANT, st, "quantise H",
                                   [&] { return launch_quant_list(q, nb, L.max_chunks, gemm, st); }));
-        // The shared experts' SwiGLU rows, when the second stream made them.
-        if (call->shared_wait && st == call->main) {
-            const hipError_t e = hipStreamWaitEvent(st, call->ev_shared, 0);
-            if (e != hipSuccess) return fail(CAEE_ERR_HIP, "hipStreamWaitEvent failed: %s", hipGetErrorString(e));
-            call->shared_wait = false;
-        }
         return down_list(d, p, list, nb, L.max_chunks, st);
     };
     if (nb_big) CAEE_TRY(chain(1, nb_big, sb));
@@ -470,9 +428,7 @@ caee_status_t caee_expert_ffn(const caee_layer_desc_t* desc, const void* x, cons
     const FfnParams fp = make_ffn_params(desc, x, topk_ids, topk_w, weights, y, (char*)ws, L);
     FfnCall call;
     CAEE_TRY(ffn_begin(desc, fp, L, s, &call));
-    CAEE_TRY(ffn_shared_early(desc, fp, &call, false));
     CAEE_TRY(timed_launch(CAEE_KERNEL_ROUTE, s, "permute", [&] { return launch_permute(p, s); }));
-    CAEE_TRY(ffn_shared_early(desc, fp, &call, true));
     CAEE_TRY(ffn_routed(desc, fp, L, &call, true));
     return ffn_end(fp, &call);
 }
@@ -498,9 +454,7 @@ caee_status_t caee_moe_layer(const caee_layer_desc_t* desc, const void* x, const
     const FfnParams fp = make_ffn_params(desc, x, p.topk_ids, p.topk_w, weights, y, wsb, L);
     FfnCall call;
     CAEE_TRY(ffn_begin(desc, fp, L, s, &call));
-    CAEE_TRY(ffn_shared_early(desc, fp, &call, false));
     CAEE_TRY(run_route_layer(desc, p, out, wsb, L, s));
-    CAEE_TRY(ffn_shared_early(desc, fp, &call, true));
     CAEE_TRY(ffn_routed(desc, fp, L, &call, true));
     return ffn_end(fp, &call);
 }

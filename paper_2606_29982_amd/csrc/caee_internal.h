@@ -3,7 +3,6 @@
 // helpers (wave reductions, bf16 rounding, MFMA fragments).
 #pragma once
 
-#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stddef.h>
 #include <stdint.h>
@@ -47,39 +46,13 @@ constexpr int kGemmT = CAEE_GEMM_T;
 #define CAEE_GEMM_BF16 1
 #endif
 constexpr int kGemmBf16 = CAEE_GEMM_BF16;
-// Batches of kSharedEarlyMinT .. kSharedEarlyT tokens launch the shared
-// experts' gate/up next to routing: 0 never, 1 on the second stream, 2 on
-// the same stream without waiting for routing (an any-order launch; it ran
-// no concurrency here).  Below the minimum, routing is one short fused
-// kernel and the cross-queue hand-offs cost more than the overlap gains.
-#ifndef CAEE_SHARED_EARLY
-#define CAEE_SHARED_EARLY 1
-#endif
-#ifndef CAEE_SHARED_EARLY_MIN_T
-#define CAEE_SHARED_EARLY_MIN_T 17
-#endif
-#ifndef CAEE_SHARED_EARLY_T
-#define CAEE_SHARED_EARLY_T 128
-#endif
-constexpr int kSharedEarly = CAEE_SHARED_EARLY;
-constexpr int kSharedEarlyMinT = CAEE_SHARED_EARLY_MIN_T;
-constexpr int kSharedEarlyT = CAEE_SHARED_EARLY_T;
-
-// FFN launches; inside an AnyOrderLaunch scope the kernel may start before
-// the stream's earlier kernels have finished.
-extern thread_local bool g_launch_any_order;
-struct AnyOrderLaunch {
-    explicit AnyOrderLaunch(bool on) { g_launch_any_order = on; }
-    ~AnyOrderLaunch() { g_launch_any_order = false; }
-};
+// FFN kernel launch (one place to change how the FFN kernels are enqueued).
 template <typename K, typename... Args>
 inline void ffn_launch(K kernel, dim3 grid, dim3 block, hipStream_t s, Args... args) {
-    if (g_launch_any_order)
-        hipExtLaunchKernelGGL(kernel, grid, block, 0, s, nullptr, nullptr, hipExtAnyOrderLaunch, args...);
-    else
-        hipLaunchKernelGGL(kernel, grid, block, 0, s, args...);
+    hipLaunchKernelGGL(kernel, grid, block, 0, s, args...);
 }
 constexpr int kFfnThreads = 256;    // 4 independent waves per FFN workgroup
+
 // Gate/up wave work items wanted per call before the contraction is split
 // (about 64 per SIMD: short items keep the tail of the launch short; 64
 // measured faster than 32 and 16 at 32 tokens, equal elsewhere).
@@ -111,10 +84,6 @@ constexpr int kFp8U = 2;            // 128-wide fp8 MFMA blocks per step (4 x 16
 // Minimum resident waves per SIMD the FFN kernels are compiled for (0: no bound).
 #ifndef CAEE_FFN_WAVES_PER_EU
 #define CAEE_FFN_WAVES_PER_EU 0
-#endif
-// Load weights one step block ahead of the MFMAs that use them.
-#ifndef CAEE_FFN_PIPELINE
-#define CAEE_FFN_PIPELINE 1
 #endif
 
 // ---------------------------------------------------------------------------
@@ -151,6 +120,9 @@ inline int elem_bytes(int dtype) {
     return dtype == CAEE_F32 ? 4 : dtype == CAEE_BF16 ? 2 : 1;
 }
 
+#ifndef CAEE_SPLIT_MAX
+#define CAEE_SPLIT_MAX 4
+#endif
 // Split of the gate/up contraction: when a call has few chunks, the d
 // dimension is cut into up to 4 ranges (the waves of one workgroup) so that
 // every SIMD gets several work items.  The host fixes the largest split the
@@ -163,7 +135,7 @@ inline int gate_up_split(const caee_layer_desc_t& d) {
     const int ksteps = fp8 ? d.d / 128 : d.d * elem_bytes(d.w_dtype) / 64;
     const int U = fp8 ? kFp8U : kGateUpU;
     int S = 1;
-    while (S < 4 && ksteps % (2 * S * U) == 0) S *= 2;
+    while (S < CAEE_SPLIT_MAX && ksteps % (2 * S * U) == 0) S *= 2;
     return S;
 }
 
@@ -329,11 +301,6 @@ struct FfnParams {
     const void* const* wtab;
     const int32_t* pass_of;
     int pass_id;
-    // shared_only: the launch's list is one chunk of all T rows per shared
-    // expert (rows s*T .. s*T + T - 1, row s*T + t for token t), read from
-    // the parameters alone; skip_shared: chunks of shared slots are skipped.
-    int shared_only;
-    int skip_shared;
     // fp8 path: quantised activations and their per-token 128-channel scales
     uint8_t* xq;
     float* xs;
@@ -350,27 +317,21 @@ struct ChunkRef {
     int xs, row0, ntok;
 };
 
-__device__ inline int ffn_list_size(const FfnParams& p) {
-    return p.shared_only ? p.n_shared : p.n_chunks[p.list];
-}
+__device__ inline int ffn_list_size(const FfnParams& p) { return p.n_chunks[p.list]; }
 
 __device__ inline ChunkRef ffn_chunk(const FfnParams& p, int c) {
-    if (p.shared_only) return {p.E + c, c * p.T, p.T};
     const int32_t* ch = p.chunks + 4 * ((p.list ? p.n_chunks[0] : 0) + c);
     return {ch[0], ch[1], ch[2]};
 }
 
 // Token of permuted row `row` (of expert slot xs).
 __device__ inline int ffn_token(const FfnParams& p, int xs, int row) {
-    if (p.shared_only) return row - (xs - p.E) * p.T;
+    (void)xs;
     return p.perm_tok[row];
 }
 
-// Offload passes: only the chunks of experts in pass p.pass_id run; with
-// skip_shared, no chunk of a shared slot.
-__device__ inline bool ffn_skip(const FfnParams& p, int xs) {
-    return (p.skip_shared && xs >= p.E) || (p.pass_of && p.pass_of[xs] != p.pass_id);
-}
+// Offload passes: only the chunks of experts in pass p.pass_id run.
+__device__ inline bool ffn_skip(const FfnParams& p, int xs) { return p.pass_of && p.pass_of[xs] != p.pass_id; }
 
 // First byte of matrix w13 (w2 = false) or w2 of expert slot xs.
 __device__ inline const char* ffn_weights(const FfnParams& p, int xs, bool w2, size_t expert_bytes) {
@@ -432,19 +393,11 @@ void set_route_outputs(RouteParams& p, const caee_route_out_t* out, char* ws, co
 struct FfnCall {
     hipStream_t main = nullptr, side = nullptr;   // side == main until forked
     hipEvent_t ev_join = nullptr;
-    bool shared_early = false;       // the shared experts' gate/up is already launched
-    hipEvent_t ev_shared = nullptr;  // when on the side stream: its completion,
-    bool shared_wait = false;        // which the main stream waits for before a down product
 };
 caee_status_t ffn_begin(const caee_layer_desc_t* d, const FfnParams& p, const WsLayout& L, hipStream_t s,
                         FfnCall* call);
 caee_status_t ffn_routed(const caee_layer_desc_t* d, const FfnParams& p, const WsLayout& L, FfnCall* call,
                          bool big_on_side);
-// The shared experts' gate/up next to routing: their rows come first in the
-// permutation and hold every token, so they need nothing routing computes.
-// Called before routing is enqueued (second-stream mode) and after it
-// (same-stream mode, launched without waiting for routing to finish).
-caee_status_t ffn_shared_early(const caee_layer_desc_t* d, const FfnParams& p, FfnCall* call, bool after_route);
 caee_status_t ffn_end(const FfnParams& p, FfnCall* call);
 
 // Opt-in timing: events bracket each launch on the caller's stream.

@@ -26,7 +26,7 @@ def test_exports_every_declared_symbol():
     for n in names:
         assert hasattr(lib, n), n
     assert set(names) == set(caee.EXPORTED)
-    assert caee.abi_version() == 6
+    assert caee.abi_version() == 7
 
 
 def _layer(**kw):

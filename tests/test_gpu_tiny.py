@@ -121,6 +121,21 @@ def test_expert_ffn_with_given_ids_and_empty_slots():
     check_y(y.cpu().numpy().astype(np.float64), ref, 1e-5)
 
 
+def test_expert_ffn_without_rows_writes_zeros():
+    # every slot empty and no shared expert: no expert rows, y = 0
+    shape = TINY_F32.with_(n_shared=0, T=5)
+    layer = caee.Layer.from_shape(shape)
+    ws = caee.alloc_workspace(layer, DEV)
+    W = w_to_dev(make_expert_weights_np(shape, seed=0), DEV)
+    x = torch.randn((shape.T, shape.d), device=DEV)
+    ids = torch.full((shape.T, shape.k), -1, dtype=torch.int32, device=DEV)
+    w = torch.zeros((shape.T, shape.k), device=DEV)
+    y = torch.full((shape.T, shape.d), 7.0, device=DEV)
+    caee.expert_ffn(layer, x, ids, w, W, y, ws)
+    torch.cuda.synchronize()
+    assert torch.all(y == 0.0)
+
+
 def test_empty_batch_leaves_output_untouched():
     shape = TINY_F32.with_(T=0, n_bins=1)
     layer = caee.Layer.from_shape(shape)
