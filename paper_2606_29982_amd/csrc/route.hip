@@ -169,7 +169,7 @@ constexpr int kRankGroups = 16;
 // Phase A for token t: writes K_t (rank order), G(t) and the token's top expert.
 template <int EPL>
 __device__ void route_token(const RouteParams& p, int t, int lane, int* ids, double* gout,
-                            int* top1, uint8_t* mflag, double* sbuf, int* sids) {
+                            int* top1, uint8_t* mflag) {
     double s[EPL], key[EPL];
     load_scores<EPL>(p, t, lane, s, key);
     const bool lane_valid = lane * EPL < p.E;
@@ -251,33 +251,28 @@ __device__ void route_token(const RouteParams& p, int t, int lane, int* ids, dou
     if (mine) {
         ids[lane] = my_id;
         gout[lane] = g;
-        sids[lane] = my_id;
-        sbuf[lane] = my_s;
     }
     if (lane == 0) *top1 = best;
     if (p.rule == CAEE_IMPORTANCE_CIR) {
-        if (lane == 0) {
-            // Slots in gate order: score descending, lower expert first on ties.
-            int ord[kMaxK];
-            for (int r = 0; r < p.k; ++r) {
-                int j = r;
-                while (j > 0 && (sbuf[ord[j - 1]] < sbuf[r] ||
-                                 (sbuf[ord[j - 1]] == sbuf[r] && sids[ord[j - 1]] > sids[r]))) {
-                    ord[j] = ord[j - 1];
-                    --j;
-                }
-                ord[j] = r;
-            }
-            double sum = 0.0;
-            for (int j = 0; j < p.k; ++j) sum += sbuf[ord[j]];
-            double cum = 0.0;
-            for (int j = 0; j < p.k; ++j) {
-                cum += sbuf[ord[j]];
-                flags |= 1u << ord[j];
-                if (cum / sum >= p.tau) break;
-            }
+        // Slots in gate order (score descending, lower expert first on ties):
+        // each slot's lane counts the slots ahead of it; the prefix then
+        // walks the positions in order, the same additions on every lane.
+        int ahead = 0;
+        for (int j = 0; j < p.k; ++j) {
+            const double sj = readlane_d(my_s, j);
+            const int ij = __builtin_amdgcn_readlane(my_id, j);
+            ahead += (sj > my_s || (sj == my_s && ij < my_id)) ? 1 : 0;
         }
-        flags = (uint32_t)__builtin_amdgcn_readfirstlane((int)flags);
+        auto lane_at = [&](int q) { return __ffsll((long long)__ballot(mine && ahead == q)) - 1; };
+        double sum = 0.0;
+        for (int q = 0; q < p.k; ++q) sum += readlane_d(my_s, lane_at(q));
+        double cum = 0.0;
+        for (int q = 0; q < p.k; ++q) {
+            const int l = lane_at(q);
+            cum += readlane_d(my_s, l);
+            flags |= 1u << l;
+            if (cum / sum >= p.tau) break;
+        }
     }
     if (mine) mflag[lane] = (uint8_t)((flags >> lane) & 1u);
 }
@@ -430,15 +425,13 @@ __device__ void compensate_token(const RouteParams& p, int t, int lane, const in
 // the counters the later kernels of this call accumulate into.
 template <int EPL>
 __global__ __launch_bounds__(kTokThreads) void k_route_tokens(RouteParams p) {
-    __shared__ double s_sbuf[kTokWaves][kMaxK];
-    __shared__ int s_ids[kTokWaves][kMaxK];
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = threadIdx.x / kWave;
     const int t = blockIdx.x * kTokWaves + wave;
     if (blockIdx.x == 0 && threadIdx.x < 4) p.counters[threadIdx.x] = 0;
     if (t < p.T)
         route_token<EPL>(p, t, lane, p.orig_ids + (size_t)t * p.k, p.gbuf + (size_t)t * p.k, p.top1 + t,
-                         p.mflag + (size_t)t * p.k, s_sbuf[wave], s_ids[wave]);
+                         p.mflag + (size_t)t * p.k);
 }
 
 // Batch-summed importance (SUM rule): one wavefront per expert adds the
@@ -467,6 +460,18 @@ __device__ void importance_sum_expert(const RouteParams& p, int e, int lane) {
     if (lane == 0) p.imp_sum[e] = sum;
 }
 
+// The same sums for small batches, one thread per expert walking the
+// (token, slot) pairs in order (reads of one LDS word by every thread).
+__device__ void importance_sum_small(const RouteParams& p, int tid, int nthr) {
+    const int n = p.T * p.k;
+    for (int e = tid; e < p.E; e += nthr) {
+        double sum = 0.0;
+        for (int i = 0; i < n; ++i)
+            if (p.orig_ids[i] == e) sum += p.gbuf[i];
+        p.imp_sum[e] = sum;
+    }
+}
+
 __global__ __launch_bounds__(kTokThreads) void k_importance_sum(RouteParams p) {
     const int e = blockIdx.x * kTokWaves + threadIdx.x / kWave;
     if (e < p.E) importance_sum_expert(p, e, threadIdx.x & (kWave - 1));
@@ -481,6 +486,8 @@ struct PruneShared {
     uint8_t act[kMaxE], must[kMaxE], prom[kMaxE];
     float cost[kMaxE];
     int bin[kMaxE];
+    int cand[kMaxE];        // candidates as gathered
+    unsigned long long cimp[kMaxE];   // their importance bits
     int sorted[kMaxE];      // candidates in visiting order
     int cbin[kMaxE];        // their bins
     float ccost[kMaxE];     // their costs
@@ -496,6 +503,8 @@ __device__ void prune_all(const RouteParams& p, int tid, int nthr, PruneShared& 
     float* s_cost = sh.cost;
     int* s_bin = sh.bin;
     int* s_sorted = sh.sorted;
+    int* s_cand = sh.cand;
+    unsigned long long* s_cimp = sh.cimp;
     int* s_cbin = sh.cbin;
     float* s_ccost = sh.ccost;
     double *s_aload = sh.aload, *s_mload = sh.mload;
@@ -535,26 +544,35 @@ __device__ void prune_all(const RouteParams& p, int tid, int nthr, PruneShared& 
         __syncthreads();
     }
 
-    // Step 2: per-bin loads of A_act and A_must; candidate visiting order
-    // (importance descending, index ascending).
+    // Step 2: per-bin loads of A_act and A_must; the candidates (active, not
+    // mandatory) gathered in any order, then each placed at its rank in the
+    // visiting order (importance descending, index ascending).
     for (int e = tid; e < E; e += nthr) {
         const double c = (double)s_cost[e];
         const int b = s_bin[e];
         if (s_act[e] && b >= 0) atomicAdd(&s_aload[b], c);
         if (s_must[e] && b >= 0) atomicAdd(&s_mload[b], c);
         if (s_act[e] && !s_must[e]) {
-            const unsigned long long ie = s_imp[e];
+            const int i = atomicAdd(&s_ncand, 1);
+            s_cand[i] = e;
+            s_cimp[i] = s_imp[e];
+        }
+    }
+    __syncthreads();
+    {
+        const int n_cand = s_ncand;
+        for (int i = tid; i < n_cand; i += nthr) {
+            const int e = s_cand[i];
+            const unsigned long long ie = s_cimp[i];
             int rank = 0;
-#pragma unroll 8
-            for (int o = 0; o < E; ++o) {
-                const unsigned long long io = s_imp[o];
-                const bool cand = s_act[o] && !s_must[o];
-                rank += (cand && (io > ie || (io == ie && o < e))) ? 1 : 0;
+            for (int j = 0; j < n_cand; ++j) {
+                const unsigned long long io = s_cimp[j];
+                const int o = s_cand[j];
+                rank += (io > ie || (io == ie && o < e)) ? 1 : 0;
             }
             s_sorted[rank] = e;
-            s_cbin[rank] = b;
+            s_cbin[rank] = s_bin[e];
             s_ccost[rank] = s_cost[e];
-            atomicAdd(&s_ncand, 1);
         }
     }
     __syncthreads();
@@ -933,10 +951,10 @@ __global__ __launch_bounds__(kRouteThreads) void k_route_fused(RouteParams p) {
     if (tid < 4) l_ctr[tid] = 0;
     for (int t = wave; t < p.T; t += kFusedWaves)
         route_token<EPL>(q, t, lane, q.orig_ids + (size_t)t * k, q.gbuf + (size_t)t * k, q.top1 + t,
-                         q.mflag + (size_t)t * k, s_sbuf[wave], s_ids[wave]);
+                         q.mflag + (size_t)t * k);
     __syncthreads();
     if (p.rule == CAEE_IMPORTANCE_SUM) {
-        for (int e = wave; e < E; e += kFusedWaves) importance_sum_expert(q, e, lane);
+        importance_sum_small(q, tid, kRouteThreads);
         __syncthreads();
     }
     prune_all(q, tid, kRouteThreads, sp);
