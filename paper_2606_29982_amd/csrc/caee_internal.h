@@ -68,8 +68,18 @@ constexpr long long kTargetItems = CAEE_TARGET_ITEMS;
 #ifndef CAEE_DOWN_U
 #define CAEE_DOWN_U 8   // 8 loads in flight per lane measured 2 % faster at 32 tokens than 4; 16 slower
 #endif
+// The same for the decode kernels (one token block), whose contraction
+// double-buffers both operands.
+#ifndef CAEE_GATE_UP_U1
+#define CAEE_GATE_UP_U1 4
+#endif
+#ifndef CAEE_DOWN_U1
+#define CAEE_DOWN_U1 8
+#endif
 constexpr int kGateUpU = CAEE_GATE_UP_U;
 constexpr int kDownU = CAEE_DOWN_U;
+constexpr int kGateUpU1 = CAEE_GATE_UP_U1;
+constexpr int kDownU1 = CAEE_DOWN_U1;
 // Whether the LDS-staged kernels run the big chunks (0: the direct kernels).
 #ifndef CAEE_BIG_STAGED
 #define CAEE_BIG_STAGED 1

@@ -537,10 +537,10 @@ int grid_for(long long waves_needed) {
     return (int)(wgs < 1 ? 1 : (wgs < cap ? wgs : cap));
 }
 
-template <class M, template <class, int, int> class K, int U>
+template <class M, template <class, int, int> class K, int U1, int U>
 hipError_t launch_nb(const FfnParams& p, int nb, dim3 grid, hipStream_t s) {
     switch (nb) {
-        case 1: ffn_launch(K<M, U, 1>::run, grid, dim3(kFfnThreads), s, p); break;
+        case 1: ffn_launch(K<M, U1, 1>::run, grid, dim3(kFfnThreads), s, p); break;
         case 2: ffn_launch(K<M, U, 2>::run, grid, dim3(kFfnThreads), s, p); break;
         case 4: ffn_launch(K<M, U, 4>::run, grid, dim3(kFfnThreads), s, p); break;
         case 8: ffn_launch(K<M, U, 8>::run, grid, dim3(kFfnThreads), s, p); break;
@@ -585,8 +585,8 @@ hipError_t launch_gate_up(const FfnParams& p, int w_dtype, int nb, int max_chunk
         return hipErrorInvalidValue;
     }
     const dim3 grid(grid_for((long long)max_chunks * (p.f / 16) * p.ksplit));   // waves wanted
-    if (w_dtype == CAEE_BF16) return launch_nb<Bf16Math, GateUpK, kGateUpU>(p, nb, grid, s);
-    if (w_dtype == CAEE_F32) return launch_nb<F32Math, GateUpK, kGateUpU>(p, nb, grid, s);
+    if (w_dtype == CAEE_BF16) return launch_nb<Bf16Math, GateUpK, kGateUpU1, kGateUpU>(p, nb, grid, s);
+    if (w_dtype == CAEE_F32) return launch_nb<F32Math, GateUpK, kGateUpU1, kGateUpU>(p, nb, grid, s);
     return hipErrorInvalidValue;
 }
 
@@ -599,8 +599,8 @@ hipError_t launch_down(const FfnParams& p, int w_dtype, int nb, int max_chunks, 
         return hipErrorInvalidValue;
     }
     const dim3 grid(grid_for((long long)max_chunks * (p.d / 16)));
-    if (w_dtype == CAEE_BF16) return launch_nb<Bf16Math, DownK, kDownU>(p, nb, grid, s);
-    if (w_dtype == CAEE_F32) return launch_nb<F32Math, DownK, kDownU>(p, nb, grid, s);
+    if (w_dtype == CAEE_BF16) return launch_nb<Bf16Math, DownK, kDownU1, kDownU>(p, nb, grid, s);
+    if (w_dtype == CAEE_F32) return launch_nb<F32Math, DownK, kDownU1, kDownU>(p, nb, grid, s);
     return hipErrorInvalidValue;
 }
 
