@@ -33,7 +33,8 @@ METRIC = "MoE-layer tokens/s + achieved HBM GB/s (% of peak) at T=1..128, with v
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gate_up_r1_t32_traffic.json")
 # The gate/up kernel's source and the header holding its tuning constants:
 # a traffic figure holds only for the build they describe.
-KERNEL_SOURCES = [os.path.join(ROOT, "paper_2606_29982_amd", "csrc", n) for n in ("ffn.hip", "caee_internal.h")]
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2606_29982_amd", "csrc", n)
+                  for n in ("ffn.hip", "ffn_tile.h", "caee_internal.h")]
 
 
 def kernel_sources_sha256():

@@ -317,6 +317,9 @@ caee_status_t ffn_routed(const caee_layer_desc_t* d, const FfnParams& p, const W
         CAEE_TRY(order(ss->fork, s, ss->stream, "fork to the side stream"));
         sb = call->side;
     }
+    // Gate/up skips the shared experts when the routing launch ran them.
+    FfnParams pg = p;
+    pg.skip_shared = call->shared_done ? 1 : 0;
     // One list's chain: gate/up, (fp8) quantisation of its SwiGLU rows, down.
     // The 8-bit GEMM reads its rows' block scales transposed and in permuted
     // row order: gathered once for x, written so by the quantiser for H.
@@ -327,7 +330,7 @@ caee_status_t ffn_routed(const caee_layer_desc_t* d, const FfnParams& p, const W
         if (gemm)
             CAEE_TRY(timed_launch(CAEE_KERNEL_QUANT, st, "gather x scales",
                                   [&] { return launch_gather_xs(q, L.max_chunks, st); }));
-        CAEE_TRY(gate_up_list(d, p, list, nb, L.max_chunks, st));
+        CAEE_TRY(gate_up_list(d, pg, list, nb, L.max_chunks, st));
         if (d->w_dtype == CAEE_FP8_E4M3 && !(gemm && gemm_fp8_fuses_quant()))
             CAEE_TRY(timed_launch(CAEE_KERNEL_QUANT, st, "quantise H",
                                   [&] { return launch_quant_list(q, nb, L.max_chunks, gemm, st); }));
@@ -352,10 +355,12 @@ void set_route_outputs(RouteParams& p, const caee_route_out_t* out, char* ws, co
 }
 
 caee_status_t run_route_layer(const caee_layer_desc_t* d, RouteParams& p, const caee_route_out_t* out, char* ws,
-                              const WsLayout& L, hipStream_t s) {
+                              const WsLayout& L, hipStream_t s, const FfnParams* shared_fp) {
     set_route_outputs(p, out, ws, L);
     p.do_permute = 1;
-    (void)d;
+    if (shared_fp)
+        return timed_launch(CAEE_KERNEL_ROUTE, s, "route",
+                            [&] { return launch_route_shared(p, *shared_fp, d->w_dtype, s); });
     return timed_launch(CAEE_KERNEL_ROUTE, s, "route", [&] { return launch_route(p, s); });
 }
 
@@ -454,7 +459,8 @@ caee_status_t caee_moe_layer(const caee_layer_desc_t* desc, const void* x, const
     const FfnParams fp = make_ffn_params(desc, x, p.topk_ids, p.topk_w, weights, y, wsb, L);
     FfnCall call;
     CAEE_TRY(ffn_begin(desc, fp, L, s, &call));
-    CAEE_TRY(run_route_layer(desc, p, out, wsb, L, s));
+    call.shared_done = route_runs_shared(*desc);
+    CAEE_TRY(run_route_layer(desc, p, out, wsb, L, s, call.shared_done ? &fp : nullptr));
     CAEE_TRY(ffn_routed(desc, fp, L, &call, true));
     return ffn_end(fp, &call);
 }

@@ -52,6 +52,10 @@ inline void ffn_launch(K kernel, dim3 grid, dim3 block, hipStream_t s, Args... a
     hipLaunchKernelGGL(kernel, grid, block, 0, s, args...);
 }
 constexpr int kFfnThreads = 256;    // 4 independent waves per FFN workgroup
+#ifndef CAEE_ROUTE_SHARED
+#define CAEE_ROUTE_SHARED 1   // batches of up to 16 tokens run the shared experts' gate/up in the routing launch
+#endif
+constexpr bool kRouteShared = CAEE_ROUTE_SHARED != 0;
 
 // Gate/up wave work items wanted per call before the contraction is split
 // (about 64 per SIMD: short items keep the tail of the launch short; 64
@@ -318,6 +322,7 @@ struct FfnParams {
     float* hs;
     float* xst;       // 8-bit GEMM: block scales transposed, [block][permuted row]
     float* hst;
+    int skip_shared;  // chunks of shared slots are skipped (their gate/up already ran)
 };
 
 // ---------------------------------------------------------------------------
@@ -340,8 +345,11 @@ __device__ inline int ffn_token(const FfnParams& p, int xs, int row) {
     return p.perm_tok[row];
 }
 
-// Offload passes: only the chunks of experts in pass p.pass_id run.
-__device__ inline bool ffn_skip(const FfnParams& p, int xs) { return p.pass_of && p.pass_of[xs] != p.pass_id; }
+// Offload passes: only the chunks of experts in pass p.pass_id run; with
+// skip_shared, no chunk of a shared slot.
+__device__ inline bool ffn_skip(const FfnParams& p, int xs) {
+    return (p.skip_shared && xs >= p.E) || (p.pass_of && p.pass_of[xs] != p.pass_id);
+}
 
 // First byte of matrix w13 (w2 = false) or w2 of expert slot xs.
 __device__ inline const char* ffn_weights(const FfnParams& p, int xs, bool w2, size_t expert_bytes) {
@@ -357,6 +365,11 @@ __device__ inline const float* ffn_scales(const FfnParams& p, int xs, bool w2, s
 
 // Host-side launchers (defined next to their kernels).
 hipError_t launch_route(const RouteParams& p, hipStream_t s);
+// Small batches: the single-workgroup routing launch also runs the shared
+// experts' gate/up (their rows hold every token and come first, so they
+// need nothing routing computes) in workgroups of its own.
+bool route_runs_shared(const caee_layer_desc_t& d);
+hipError_t launch_route_shared(const RouteParams& p, const FfnParams& fp, int w_dtype, hipStream_t s);
 hipError_t launch_permute(const RouteParams& p, hipStream_t s);
 hipError_t launch_gate_up(const FfnParams& p, int w_dtype, int nb, int max_chunks, hipStream_t s);
 hipError_t launch_down(const FfnParams& p, int w_dtype, int nb, int max_chunks, hipStream_t s);
@@ -391,7 +404,7 @@ FfnParams make_ffn_params(const caee_layer_desc_t* d, const void* x, const int32
 // Routing, pruning, compensation and permutation of a whole-layer call; the
 // routing results go to `out` when given, else to the workspace.
 caee_status_t run_route_layer(const caee_layer_desc_t* d, RouteParams& p, const caee_route_out_t* out, char* ws,
-                              const WsLayout& L, hipStream_t s);
+                              const WsLayout& L, hipStream_t s, const FfnParams* shared_fp = nullptr);
 void set_route_outputs(RouteParams& p, const caee_route_out_t* out, char* ws, const WsLayout& L);
 
 // The FFN of one layer call, in three parts:
@@ -403,6 +416,7 @@ void set_route_outputs(RouteParams& p, const caee_route_out_t* out, char* ws, co
 struct FfnCall {
     hipStream_t main = nullptr, side = nullptr;   // side == main until forked
     hipEvent_t ev_join = nullptr;
+    bool shared_done = false;   // the routing launch already ran the shared experts' gate/up
 };
 caee_status_t ffn_begin(const caee_layer_desc_t* d, const FfnParams& p, const WsLayout& L, hipStream_t s,
                         FfnCall* call);

@@ -327,7 +327,8 @@ caee_status_t caee_offload_layer(caee_offload_t* h, const caee_layer_desc_t* des
             (void)hipStreamWaitEvent(fc.main, fc.ev_join, 0);
         return st;
     };
-    caee_status_t st = run_route_layer(desc, rp, out, wsb, L, s);
+    fc.shared_done = route_runs_shared(d);   // as caee_moe_layer, so both give the same bits
+    caee_status_t st = run_route_layer(desc, rp, out, wsb, L, s, fc.shared_done ? &fp : nullptr);
     if (st != CAEE_OK) return joined(st);
     // 2. read A_trans back.
     hipError_t he = hipMemcpyAsync(h->host_trans, wsb + L.trans, E, hipMemcpyDeviceToHost, s);

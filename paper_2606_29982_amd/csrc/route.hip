@@ -21,6 +21,8 @@
 namespace caee {
 namespace {
 
+#include "ffn_tile.h"
+
 constexpr int kTokWaves = 4;                       // tokens (wavefronts) per workgroup
 constexpr int kTokThreads = kTokWaves * kWave;
 // Batches up to this many tokens are routed by one fused single-workgroup kernel.
@@ -913,7 +915,7 @@ __global__ __launch_bounds__(kTokThreads) void k_compensate(RouteParams p) {
 constexpr int kFusedWaves = kRouteThreads / kWave;
 
 template <int EPL>
-__global__ __launch_bounds__(kRouteThreads) void k_route_fused(RouteParams p) {
+__device__ void route_fused_body(const RouteParams& p) {
     __shared__ double s_sbuf[kFusedWaves][kMaxK];
     __shared__ int s_ids[kFusedWaves][kMaxK];
     __shared__ PruneShared sp;
@@ -988,7 +990,90 @@ __global__ __launch_bounds__(kRouteThreads) void k_route_fused(RouteParams p) {
         for (int i = tid; i < 3 * p.n_bins; i += kRouteThreads) p.bin_loads[i] = l_bl[i];
 }
 
+template <int EPL>
+__global__ __launch_bounds__(kRouteThreads) void k_route_fused(RouteParams p) {
+    route_fused_body<EPL>(p);
+}
+
+// The shared experts' gate/up for a batch of at most 16 tokens, run by the
+// workgroups after the first in the routing launch.  Item = one 16-column
+// tile (gate and up rows) of one shared expert; the 16 waves of the
+// workgroup take consecutive ranges of the contraction, and wave 0 adds the
+// 16 partial sums in wave order (deterministic) and stores the SwiGLU rows.
+// Shared expert s owns rows s*T .. s*T + T - 1 (row s*T + t for token t).
+template <class M>
+__device__ void shared_gate_up(const FfnParams& p, int wg, int n_wg) {
+    constexpr int kWaves = kRouteThreads / kWave;
+    __shared__ f32x4_t s_part[kWaves][2][kWave];
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    const int r = lane & 15, g = lane >> 4;
+    const int tiles = p.f / 16;
+    const size_t row_units = (size_t)p.d * M::kElemBytes / 16;
+    const int ksteps = (int)(row_units / 4);
+    const int kper = (ksteps + kWaves - 1) / kWaves;
+    const int k0 = min(ksteps, wave * kper), k1 = min(ksteps, k0 + kper);
+    const size_t expert_bytes = (size_t)2 * p.f * p.d * M::kElemBytes;
+    const int astep = p.tiled ? 64 : 4;
+    for (int item = wg; item < p.n_shared * tiles; item += n_wg) {
+        const int sh = item / tiles, jt = item - sh * tiles;
+        const u32x4_t* wb = (const u32x4_t*)((const char*)p.sh_w13 + (size_t)sh * expert_bytes);
+        const u32x4_t* const a[2] = {
+            p.tiled ? wb + ((size_t)jt * ksteps + k0) * 64 + lane
+                    : wb + (size_t)(jt * 16 + r) * row_units + g + 4 * (size_t)k0,
+            p.tiled ? wb + ((size_t)(tiles + jt) * ksteps + k0) * 64 + lane
+                    : wb + (size_t)(p.f + jt * 16 + r) * row_units + g + 4 * (size_t)k0};
+        const int t = r < p.T ? r : 0;   // padded token columns read a valid row; results dropped
+        const u32x4_t* const xb[1] = {(const u32x4_t*)p.x + (size_t)t * row_units + g + 4 * (size_t)k0};
+        f32x4_t acc[2][1] = {{f32x4_t{0.f, 0.f, 0.f, 0.f}}, {f32x4_t{0.f, 0.f, 0.f, 0.f}}};
+        if (k1 > k0) tile_contract<M, 2, 2, 1>(a, astep, xb, 1, k1 - k0, acc);   // short rows leave waves idle
+        s_part[wave][0][lane] = acc[0][0];
+        s_part[wave][1][lane] = acc[1][0];
+        __syncthreads();
+        if (wave == 0 && r < p.T) {
+            f32x4_t gs = s_part[0][0][lane], us = s_part[0][1][lane];
+            for (int w = 1; w < kWaves; ++w) {
+                gs += s_part[w][0][lane];
+                us += s_part[w][1][lane];
+            }
+            float h[4];
+#pragma unroll
+            for (int v = 0; v < 4; ++v) h[v] = silu_mul(gs[v], us[v]);
+            store_h<M>(p, (size_t)(sh * p.T + r) * p.f + jt * 16 + 4 * g, h);
+        }
+        __syncthreads();
+    }
+}
+
+template <int EPL, class M>
+__global__ __launch_bounds__(kRouteThreads) void k_route_fused_shared(RouteParams p, FfnParams fp) {
+    if (blockIdx.x == 0) route_fused_body<EPL>(p);
+    else shared_gate_up<M>(fp, blockIdx.x - 1, gridDim.x - 1);
+}
+
 }  // namespace
+
+bool route_runs_shared(const caee_layer_desc_t& d) {
+    return kRouteShared && d.T <= kFusedT && d.n_shared > 0 && d.w_dtype != CAEE_FP8_E4M3;
+}
+
+hipError_t launch_route_shared(const RouteParams& p, const FfnParams& fp, int w_dtype, hipStream_t s) {
+    const int items = fp.n_shared * (fp.f / 16);
+    const int cap = device_cu_count() - 1;
+    const dim3 grid(1 + (items < cap ? items : cap));
+    auto go = [&](auto k) -> hipError_t {
+        hipLaunchKernelGGL(k, grid, dim3(kRouteThreads), 0, s, p, fp);
+        return hipGetLastError();
+    };
+    const bool bf16 = w_dtype == CAEE_BF16;
+    if (w_dtype != CAEE_BF16 && w_dtype != CAEE_F32) return hipErrorInvalidValue;
+    switch (p.epl) {
+        case 1: return bf16 ? go(k_route_fused_shared<1, Bf16Math>) : go(k_route_fused_shared<1, F32Math>);
+        case 2: return bf16 ? go(k_route_fused_shared<2, Bf16Math>) : go(k_route_fused_shared<2, F32Math>);
+        case 4: return bf16 ? go(k_route_fused_shared<4, Bf16Math>) : go(k_route_fused_shared<4, F32Math>);
+        default: return hipErrorInvalidValue;
+    }
+}
 
 hipError_t launch_route(const RouteParams& p, hipStream_t s) {
     const dim3 tok_grid((p.T + kTokWaves - 1) / kTokWaves);
