@@ -533,7 +533,8 @@ def main():
         link_model = cres["link"]
         result["calibration"] = {
             "hbm": {**cres["hbm"].as_dict(), "expert_cost_us": round(float(cres["hbm"].cost_us(W_EXPERT_BYTES)), 2)},
-            "h2d": {**cres["link"].as_dict(), "expert_cost_us": round(float(cres["link"].cost_us(W_EXPERT_BYTES)), 1)}}
+            "h2d": {**cres["link"].as_dict(), "expert_cost_us": round(float(cres["link"].cost_us(W_EXPERT_BYTES)), 1)},
+            "samples": cres["samples"]}
         log(f"calibration {result['calibration']}")
 
     if not args.no_offload:
