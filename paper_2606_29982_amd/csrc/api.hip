@@ -223,7 +223,8 @@ FfnParams make_ffn_params(const caee_layer_desc_t* d, const void* x, const int32
     p.topk_ids = ids;
     p.topk_w = w;
     p.h = ws + L.h;
-    p.yperm = (float*)(ws + L.y);
+    p.yperm = ws + L.y;
+    p.y_half = y_row_bytes(*d) == 2;
     p.y = y;
     p.y_bf16 = d->y_dtype == CAEE_BF16;
     p.P = L.P;

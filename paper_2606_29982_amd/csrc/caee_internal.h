@@ -82,6 +82,9 @@ constexpr long long kTargetItems = CAEE_TARGET_ITEMS;
 #endif
 constexpr int kGateUpU = CAEE_GATE_UP_U;
 constexpr int kDownU = CAEE_DOWN_U;
+#ifndef CAEE_DOWN_AHEAD_NB
+#define CAEE_DOWN_AHEAD_NB 1   // down kernels up to this many token blocks double-buffer the H rows too
+#endif
 constexpr int kGateUpU1 = CAEE_GATE_UP_U1;
 constexpr int kDownU1 = CAEE_DOWN_U1;
 // Whether the LDS-staged kernels run the big chunks (0: the direct kernels).
@@ -129,6 +132,17 @@ struct WsLayout {
 };
 
 inline size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
+
+// Bytes per element of the expert output rows Y: bf16 on the 8-bit path,
+// where they are the largest intermediate at prefill sizes, else fp32.
+inline int y_row_bytes(const caee_layer_desc_t& d) { return d.w_dtype == CAEE_FP8_E4M3 ? 2 : 4; }
+
+// bf16 bits of v, rounded to nearest even (finite values).
+__host__ __device__ inline uint32_t bf16_rne(float v) {
+    union { float f; uint32_t u; } c;
+    c.f = v;
+    return (c.u + 0x7FFFu + ((c.u >> 16) & 1u)) >> 16;
+}
 
 inline int elem_bytes(int dtype) {
     return dtype == CAEE_F32 ? 4 : dtype == CAEE_BF16 ? 2 : 1;
@@ -230,7 +244,7 @@ inline WsLayout ws_layout(const caee_layer_desc_t& d) {
     L.n_chunks = take(16);
     const int h_bytes = d.w_dtype == CAEE_FP8_E4M3 ? 4 : elem_bytes(d.w_dtype);
     L.h = take(size_t(L.P) * d.f * h_bytes);
-    L.y = take(size_t(L.P) * d.d * 4);
+    L.y = take(size_t(L.P) * d.d * y_row_bytes(d));
     const bool fp8 = d.w_dtype == CAEE_FP8_E4M3;
     L.xq = take(fp8 ? T * d.d : 0);
     L.xs = take(fp8 ? T * (d.d / 128) * 4 : 0);
@@ -303,7 +317,7 @@ struct FfnParams {
     const int32_t* topk_ids;
     const float* topk_w;
     void* h;
-    float* yperm;
+    void* yperm;      // [P][d] expert output rows, fp32 (bf16 when y_half)
     void* y;
     int y_bf16;
     int P;
@@ -323,6 +337,7 @@ struct FfnParams {
     float* xst;       // 8-bit GEMM: block scales transposed, [block][permuted row]
     float* hst;
     int skip_shared;  // chunks of shared slots are skipped (their gate/up already ran)
+    int y_half;       // the expert output rows are bf16 (8-bit path): half the traffic of the combine
 };
 
 // ---------------------------------------------------------------------------
@@ -356,6 +371,29 @@ __device__ inline const char* ffn_weights(const FfnParams& p, int xs, bool w2, s
     if (xs >= p.E) return (const char*)(w2 ? p.sh_w2 : p.sh_w13) + (size_t)(xs - p.E) * expert_bytes;
     if (p.wtab) return (const char*)p.wtab[2 * xs + (w2 ? 1 : 0)];
     return (const char*)(w2 ? p.w2 : p.w13) + (size_t)xs * expert_bytes;
+}
+
+// Four consecutive outputs of expert output row `row`, column `col`.
+__device__ inline void store_y4(const FfnParams& p, size_t row, int col, float a, float b, float c, float e) {
+    const size_t o = row * p.d + col;
+    if (p.y_half) {
+        uint2 pk;
+        pk.x = bf16_rne(a) | (bf16_rne(b) << 16);
+        pk.y = bf16_rne(c) | (bf16_rne(e) << 16);
+        *(uint2*)((uint16_t*)p.yperm + o) = pk;
+    } else {
+        *(float4*)((float*)p.yperm + o) = make_float4(a, b, c, e);
+    }
+}
+
+__device__ inline float4 load_y4(const FfnParams& p, size_t row, int col) {
+    const size_t o = row * p.d + col;
+    if (p.y_half) {
+        const uint2 pk = *(const uint2*)((const uint16_t*)p.yperm + o);
+        return make_float4(__uint_as_float(pk.x << 16), __uint_as_float(pk.x & 0xFFFF0000u),
+                           __uint_as_float(pk.y << 16), __uint_as_float(pk.y & 0xFFFF0000u));
+    }
+    return *(const float4*)((const float*)p.yperm + o);
 }
 
 __device__ inline const float* ffn_scales(const FfnParams& p, int xs, bool w2, size_t per_expert) {

@@ -151,12 +151,12 @@ __global__ CAEE_FFN_BOUNDS void k_down(FfnParams p) {
         f32x4_t acc[1][NB];
 #pragma unroll
         for (int tb = 0; tb < NB; ++tb) acc[0][tb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-        tile_contract<M, U, 1, NB>(a, astep, hb, nb, ksteps, acc);
+        tile_contract<M, U, 1, NB, (NB <= CAEE_DOWN_AHEAD_NB)>(a, astep, hb, nb, ksteps, acc);
 #pragma unroll
         for (int tb = 0; tb < NB; ++tb) {
             const int n = tb * 16 + r;
             if (tb < nb && n < ntok) {
-                float* o = p.yperm + (size_t)(row0 + n) * p.d + it * 16 + 4 * g;
+                float* o = (float*)p.yperm + (size_t)(row0 + n) * p.d + it * 16 + 4 * g;
                 *(float4*)o = make_float4(acc[0][tb][0], acc[0][tb][1], acc[0][tb][2], acc[0][tb][3]);
             }
         }
@@ -331,7 +331,7 @@ __global__ __launch_bounds__(kFfnThreads) void k_down_big(FfnParams p) {
             for (int tb = 0; tb < NB; ++tb) {
                 const int n = tb * 16 + r;
                 if (tb < nb && n < ntok) {
-                    float* o = p.yperm + (size_t)(row0 + n) * p.d + (it0 + m) * 16 + 4 * g;
+                    float* o = (float*)p.yperm + (size_t)(row0 + n) * p.d + (it0 + m) * 16 + 4 * g;
                     *(float4*)o = make_float4(acc[m][tb][0], acc[m][tb][1], acc[m][tb][2], acc[m][tb][3]);
                 }
             }
@@ -366,7 +366,7 @@ __global__ __launch_bounds__(256) void k_combine(FfnParams p) {
         const int pos = p.perm_pos[t * slots + j];
         if (pos < 0) continue;
         const float w = p.topk_w[t * p.k + j];
-        const float4 v = *(const float4*)(p.yperm + (size_t)pos * p.d + c);
+        const float4 v = load_y4(p, (size_t)pos, c);
         acc.x = fmaf(w, v.x, acc.x);
         acc.y = fmaf(w, v.y, acc.y);
         acc.z = fmaf(w, v.z, acc.z);
@@ -374,7 +374,7 @@ __global__ __launch_bounds__(256) void k_combine(FfnParams p) {
     }
     for (int s = 0; s < p.n_shared; ++s) {
         const int pos = p.perm_pos[t * slots + p.k + s];
-        const float4 v = *(const float4*)(p.yperm + (size_t)pos * p.d + c);
+        const float4 v = load_y4(p, (size_t)pos, c);
         acc.x += v.x;
         acc.y += v.y;
         acc.z += v.z;

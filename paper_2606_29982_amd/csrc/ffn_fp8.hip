@@ -285,8 +285,8 @@ __global__ __launch_bounds__(kFfnThreads) void k_down_fp8(FfnParams p) {
         for (int tb = 0; tb < NB; ++tb) {
             const int n = tb * 16 + r;
             if (tb < nb && n < ntok) {
-                float* o = p.yperm + (size_t)(row0 + n) * p.d + it * 16 + 4 * g;
-                *(float4*)o = make_float4(acc[0][tb][0], acc[0][tb][1], acc[0][tb][2], acc[0][tb][3]);
+                store_y4(p, (size_t)(row0 + n), it * 16 + 4 * g, acc[0][tb][0], acc[0][tb][1], acc[0][tb][2],
+                         acc[0][tb][3]);
             }
         }
     }
@@ -526,8 +526,8 @@ __global__ __launch_bounds__(kFfnThreads) void k_down_fp8_big(FfnParams p) {
             for (int tb = 0; tb < NB; ++tb) {
                 const int n = tb * 16 + r;
                 if (tb < nb && n < ntok) {
-                    float* o = p.yperm + (size_t)(row0 + n) * p.d + (it0 + m) * 16 + 4 * g;
-                    *(float4*)o = make_float4(acc[m][tb][0], acc[m][tb][1], acc[m][tb][2], acc[m][tb][3]);
+                    store_y4(p, (size_t)(row0 + n), (it0 + m) * 16 + 4 * g, acc[m][tb][0], acc[m][tb][1],
+                             acc[m][tb][2], acc[m][tb][3]);
                 }
             }
     }

@@ -79,10 +79,6 @@ __device__ inline i32x8_t join(const u32x4_t& lo, const u32x4_t& hi) {
 
 __device__ inline float silu_mul(float g, float u) { return g / (1.0f + __expf(-g)) * u; }
 
-__device__ inline uint32_t bf16_bits(float v) {   // round to nearest even
-    const uint32_t u = __float_as_uint(v);
-    return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
-}
 
 // Waits until at most n of this wave's vector memory loads are outstanding
 // (gfx9 s_waitcnt: vmcnt in bits 3:0 and 15:14, expcnt and lgkmcnt not waited).
@@ -374,16 +370,16 @@ __global__ __launch_bounds__(kGemmThreads) void k_gemm(FfnParams p) {
                         *(float4*)((float*)p.h + o) = make_float4(h[0], h[1], h[2], h[3]);
                     } else {   // bf16 SwiGLU rows, rounded to nearest even
                         uint2 pk;
-                        pk.x = bf16_bits(h[0]) | (bf16_bits(h[1]) << 16);
-                        pk.y = bf16_bits(h[2]) | (bf16_bits(h[3]) << 16);
+                        pk.x = bf16_rne(h[0]) | (bf16_rne(h[1]) << 16);
+                        pk.y = bf16_rne(h[2]) | (bf16_rne(h[3]) << 16);
                         *(uint2*)((uint16_t*)p.h + o) = pk;
                     }
                 }
             } else {
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    float* o = p.yperm + (size_t)(row0 + tn) * p.d + (grp * kTiles + 4 * wq + i) * 16 + 4 * g;
-                    *(float4*)o = make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
+                    store_y4(p, (size_t)(row0 + tn), (grp * kTiles + 4 * wq + i) * 16 + 4 * g, acc[i][j][0],
+                             acc[i][j][1], acc[i][j][2], acc[i][j][3]);
                 }
             }
         }

@@ -27,10 +27,6 @@ struct F32Math {
     }
 };
 
-__device__ inline uint32_t bf16_rne(float v) {
-    const uint32_t u = __float_as_uint(v);
-    return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
-}
 
 __device__ inline float silu_mul(float g, float u) { return g / (1.0f + __expf(-g)) * u; }
 
@@ -56,10 +52,10 @@ __device__ inline u32x4_t load_cached(const u32x4_t* p) { return *(g_u32x4_t*)p;
 //
 // More token blocks: the activation pieces are loaded next to the MFMAs
 // (double-buffering them too costs the kernel a resident wave per SIMD).
-template <class M, int U, int NA, int NB, bool kTail>
+template <class M, int U, int NA, int NB, bool kTail, bool kAhead>
 __device__ inline void tile_contract_steps(const u32x4_t* const (&a)[NA], int astep, const u32x4_t* const (&b)[NB],
                                            int nb, int nsteps, f32x4_t (&acc)[NA][NB]) {
-    if constexpr (NB == 1) {
+    if constexpr (kAhead) {
         auto load = [&](u32x4_t (&w)[NA][U], u32x4_t (&x)[NB][U], int s) __attribute__((always_inline)) {
 #pragma unroll
             for (int u = 0; u < U; ++u) {
@@ -67,16 +63,20 @@ __device__ inline void tile_contract_steps(const u32x4_t* const (&a)[NA], int as
                 const bool in = st < nsteps;
 #pragma unroll
                 for (int m = 0; m < NA; ++m) w[m][u] = load_stream(in ? a[m] + (size_t)astep * st : b[0]);
-                x[0][u] = load_cached(in ? b[0] + 4 * st : b[0]);
+#pragma unroll
+                for (int tb = 0; tb < NB; ++tb) x[tb][u] = load_cached(in ? b[tb] + 4 * st : b[0]);
             }
         };
         auto mul = [&](const u32x4_t (&w)[NA][U], const u32x4_t (&x)[NB][U], int s) __attribute__((always_inline)) {
-            if (nb > 0) {
 #pragma unroll
-                for (int u = 0; u < U; ++u) {
-                    if (!kTail || s + u < nsteps) {
+            for (int tb = 0; tb < NB; ++tb) {
+                if (tb < nb) {
 #pragma unroll
-                        for (int m = 0; m < NA; ++m) M::mma(acc[m][0], w[m][u], x[0][u]);
+                    for (int u = 0; u < U; ++u) {
+                        if (!kTail || s + u < nsteps) {
+#pragma unroll
+                            for (int m = 0; m < NA; ++m) M::mma(acc[m][tb], w[m][u], x[tb][u]);
+                        }
                     }
                 }
             }
@@ -128,11 +128,11 @@ __device__ inline void tile_contract_steps(const u32x4_t* const (&a)[NA], int as
     }
 }
 
-template <class M, int U, int NA, int NB>
+template <class M, int U, int NA, int NB, bool kAhead = (NB == 1)>
 __device__ inline void tile_contract(const u32x4_t* const (&a)[NA], int astep, const u32x4_t* const (&b)[NB],
                                      int nb, int nsteps, f32x4_t (&acc)[NA][NB]) {
-    if (nsteps % U == 0) tile_contract_steps<M, U, NA, NB, false>(a, astep, b, nb, nsteps, acc);
-    else tile_contract_steps<M, U, NA, NB, true>(a, astep, b, nb, nsteps, acc);
+    if (nsteps % U == 0) tile_contract_steps<M, U, NA, NB, false, kAhead>(a, astep, b, nb, nsteps, acc);
+    else tile_contract_steps<M, U, NA, NB, true, kAhead>(a, astep, b, nb, nsteps, acc);
 }
 
 template <class M>
