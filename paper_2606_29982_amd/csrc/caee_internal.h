@@ -149,7 +149,7 @@ inline int elem_bytes(int dtype) {
 }
 
 #ifndef CAEE_SPLIT_MAX
-#define CAEE_SPLIT_MAX 4
+#define CAEE_SPLIT_MAX 4   // largest contraction split (the 4 waves of a workgroup); 2 and 1 measured slower at T <= 32
 #endif
 // Split of the gate/up contraction: when a call has few chunks, the d
 // dimension is cut into up to 4 ranges (the waves of one workgroup) so that
