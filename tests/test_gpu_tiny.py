@@ -86,6 +86,14 @@ def test_expert_counts_and_lane_layouts(E, G, tg, k):
     _run(shape, seed=E, tau=0.05, n_bins=4)
 
 
+@pytest.mark.parametrize("shape", [TINY_F32, TINY_BF16], ids=["f32", "bf16"])
+@pytest.mark.parametrize("T", [1, 7, 16, 40])
+def test_two_shared_experts(shape, T):
+    # up to 16 tokens the routing launch runs the shared experts' gate/up
+    # (rows s*T + t of shared expert s); 40 tokens take the FFN launches
+    _run(shape.with_(n_shared=2), seed=30 + T, tau=0.2, n_bins=4, T=T, tiled=T % 2 == 0)
+
+
 def test_no_shared_expert_and_k1():
     _run(TINY_F32.with_(n_shared=0), seed=5, tau=0.1, n_bins=4)
     _run(TINY_F32.with_(k=1, topk_group=1), seed=6, tau=0.1, n_bins=2)
