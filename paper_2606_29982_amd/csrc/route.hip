@@ -1054,7 +1054,8 @@ __global__ __launch_bounds__(kRouteThreads) void k_route_fused_shared(RouteParam
 }  // namespace
 
 bool route_runs_shared(const caee_layer_desc_t& d) {
-    return kRouteShared && d.T <= kFusedT && d.n_shared > 0 && d.w_dtype != CAEE_FP8_E4M3;
+    // one 16-token block: the workgroups' tiles hold every token of the batch
+    return kRouteShared && d.T <= 16 && d.T <= kFusedT && d.n_shared > 0 && d.w_dtype != CAEE_FP8_E4M3;
 }
 
 hipError_t launch_route_shared(const RouteParams& p, const FfnParams& fp, int w_dtype, hipStream_t s) {
