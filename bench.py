@@ -474,6 +474,20 @@ def main():
     result["graph_protocol"] = graph_protocol(head)
     log(f"graph protocol {result['graph_protocol']}")
 
+    link_model = None
+    if not args.no_calibrate:
+        # Offline cost calibration (alpha, beta of both data paths), before the
+        # sweeps: run after them (and the 8-bit rows and the ablation), this
+        # process's 42 MB host copies took twice their time.
+        from paper_2606_29982_amd import calibrate as cal
+        cres = cal.calibrate(dev)
+        link_model = cres["link"]
+        result["calibration"] = {
+            "hbm": {**cres["hbm"].as_dict(), "expert_cost_us": round(float(cres["hbm"].cost_us(W_EXPERT_BYTES)), 2)},
+            "h2d": {**cres["link"].as_dict(), "expert_cost_us": round(float(cres["link"].cost_us(W_EXPERT_BYTES)), 1)},
+            "samples": cres["samples"]}
+        log(f"calibration {result['calibration']}")
+
     if not args.no_sweep:
         # Zipf-skewed popularity and cost table, experts placed on 8 bins
         # (EP8-style), with and without pruning under each importance rule.
@@ -524,18 +538,6 @@ def main():
 
     if not args.no_sweep:
         result["compensation_ablation"] = ablation_rows(args, shape, Wt, dev)
-
-    link_model = None
-    if not args.no_calibrate:
-        # Offline cost calibration (alpha, beta of both data paths).
-        from paper_2606_29982_amd import calibrate as cal
-        cres = cal.calibrate(dev)
-        link_model = cres["link"]
-        result["calibration"] = {
-            "hbm": {**cres["hbm"].as_dict(), "expert_cost_us": round(float(cres["hbm"].cost_us(W_EXPERT_BYTES)), 2)},
-            "h2d": {**cres["link"].as_dict(), "expert_cost_us": round(float(cres["link"].cost_us(W_EXPERT_BYTES)), 1)},
-            "samples": cres["samples"]}
-        log(f"calibration {result['calibration']}")
 
     if not args.no_offload:
         result["offload"] = offload_rows(args, shape, Wt, dev, link_model)
