@@ -56,6 +56,12 @@ constexpr int kFfnThreads = 256;    // 4 independent waves per FFN workgroup
 #define CAEE_ROUTE_SHARED 1   // batches of up to 16 tokens run the shared experts' gate/up in the routing launch
 #endif
 constexpr bool kRouteShared = CAEE_ROUTE_SHARED != 0;
+// Contraction steps loaded ahead by those workgroups (1024 threads: at most
+// 128 registers per lane; 4 spills).
+#ifndef CAEE_ROUTE_SHARED_U
+#define CAEE_ROUTE_SHARED_U 2
+#endif
+constexpr int kRouteSharedU = CAEE_ROUTE_SHARED_U;
 
 // Gate/up wave work items wanted per call before the contraction is split
 // (about 64 per SIMD: short items keep the tail of the launch short; 64
@@ -295,6 +301,7 @@ struct RouteParams {
     int32_t* perm_blk;
     int32_t* chunks;
     int32_t* n_chunks;
+    double* sslot;      // scores s of each token's K_t slots [T][k] when kept by routing (else recomputed)
     int do_permute;     // 0: the permutation kernel only reports the refill/empty-slot counts
 };
 

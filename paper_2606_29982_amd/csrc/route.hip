@@ -253,6 +253,7 @@ __device__ void route_token(const RouteParams& p, int t, int lane, int* ids, dou
     if (mine) {
         ids[lane] = my_id;
         gout[lane] = g;
+        if (p.sslot) p.sslot[(size_t)t * p.k + lane] = my_s;
     }
     if (lane == 0) *top1 = best;
     if (p.rule == CAEE_IMPORTANCE_CIR) {
@@ -319,7 +320,9 @@ __device__ void compensate_token(const RouteParams& p, int t, int lane, const in
         // order.  Each kept slot's score is recomputed by its lane with the
         // same expression as the full pass, and summed in the same order.
         double my_s = 0.0;
-        if (kept) my_s = 1.0 / (1.0 + exp(-(double)p.logits[(size_t)t * p.E + my_orig]));
+        if (kept)
+            my_s = p.sslot ? p.sslot[(size_t)t * p.k + lane]
+                           : 1.0 / (1.0 + exp(-(double)p.logits[(size_t)t * p.E + my_orig]));
         double total = 0.0;
         for (int r = 0; r < p.k; ++r)
             if ((kept_mask >> r) & 1ull) total += readlane_d(my_s, r);
@@ -496,6 +499,7 @@ struct PruneShared {
     double aload[kMaxBins], mload[kMaxBins];
     double fbase;
     int ncand;
+    int stat[5];            // step-4 counts: active, mandatory, promoted, pruned, kept
 };
 
 // Run by one workgroup of `nthr` threads (a multiple of the wave size).
@@ -525,6 +529,7 @@ __device__ void prune_all(const RouteParams& p, int tid, int nthr, PruneShared& 
     }
     for (int b = tid; b < nb; b += nthr) s_aload[b] = s_mload[b] = 0.0;
     if (tid == 0) s_ncand = 0;
+    if (tid < 5) sh.stat[tid] = 0;
     __syncthreads();
 
     // Step 1: A_act, importance, A_must (pairs mandatory on their own, and
@@ -608,42 +613,43 @@ __device__ void prune_all(const RouteParams& p, int tid, int nthr, PruneShared& 
     }
     __syncthreads();
 
-    // Step 4: A_trans = A_must + promoted; masks and counters by ballot.
+    // Step 4: A_trans = A_must + promoted; masks and counters by ballot,
+    // one 64-expert block per wave, counts added in LDS.
     for (int e = tid; e < E; e += nthr) p.trans[e] = s_must[e] | s_prom[e];
-    if (wave == 0) {
-        const int words = (E + 31) / 32;
-        int n_act = 0, n_must = 0, n_prom = 0, n_pruned = 0, n_trans = 0;
-        for (int base = 0; base < E; base += kWave) {
-            const int e = base + lane;
-            const bool v = e < E;
-            const bool act = v && s_act[e], must = v && s_must[e], prom = v && s_prom[e];
-            const bool trans = must || prom;
-            const unsigned long long ba = __ballot(act), bm = __ballot(must), bt = __ballot(trans),
-                                     bp = __ballot(act && !trans), bpr = __ballot(prom);
-            n_act += __popcll(ba);
-            n_must += __popcll(bm);
-            n_prom += __popcll(bpr);
-            n_pruned += __popcll(bp);
-            n_trans += __popcll(bt);
-            if (p.masks && lane < 2) {
-                const int w = base / 32 + lane;
-                if (w < words) {
-                    const int sh = 32 * lane;
-                    p.masks[w] = (uint32_t)(ba >> sh);
-                    p.masks[words + w] = (uint32_t)(bm >> sh);
-                    p.masks[2 * words + w] = (uint32_t)(bt >> sh);
-                    p.masks[3 * words + w] = (uint32_t)(bp >> sh);
-                }
+    const int words = (E + 31) / 32;
+    for (int base = wave * kWave; base < E; base += nthr) {
+        const int e = base + lane;
+        const bool v = e < E;
+        const bool act = v && s_act[e], must = v && s_must[e], prom = v && s_prom[e];
+        const bool trans = must || prom;
+        const unsigned long long ba = __ballot(act), bm = __ballot(must), bt = __ballot(trans),
+                                 bp = __ballot(act && !trans), bpr = __ballot(prom);
+        if (lane == 0) {
+            atomicAdd(&sh.stat[0], __popcll(ba));
+            atomicAdd(&sh.stat[1], __popcll(bm));
+            atomicAdd(&sh.stat[2], __popcll(bpr));
+            atomicAdd(&sh.stat[3], __popcll(bp));
+            atomicAdd(&sh.stat[4], __popcll(bt));
+        }
+        if (p.masks && lane < 2) {
+            const int w = base / 32 + lane;
+            if (w < words) {
+                const int sh_ = 32 * lane;
+                p.masks[w] = (uint32_t)(ba >> sh_);
+                p.masks[words + w] = (uint32_t)(bm >> sh_);
+                p.masks[2 * words + w] = (uint32_t)(bt >> sh_);
+                p.masks[3 * words + w] = (uint32_t)(bp >> sh_);
             }
         }
-        if (p.stats && lane == 0) {
-            p.stats[0] = n_act;
-            p.stats[1] = n_must;
-            p.stats[2] = n_cand;
-            p.stats[3] = n_prom;
-            p.stats[4] = n_pruned;
-            p.stats[5] = n_trans;
-        }
+    }
+    __syncthreads();
+    if (p.stats && tid == 0) {
+        p.stats[0] = sh.stat[0];   // |A_act|
+        p.stats[1] = sh.stat[1];   // |A_must|
+        p.stats[2] = n_cand;
+        p.stats[3] = sh.stat[2];   // promoted
+        p.stats[4] = sh.stat[3];   // pruned
+        p.stats[5] = sh.stat[4];   // |A_trans|
     }
 }
 
@@ -659,23 +665,52 @@ __global__ __launch_bounds__(kRouteThreads) void k_prune(RouteParams p) {
 // the routed ones in expert order.  Then one small chunk per slot with at
 // most chunk_small rows, and ceil(rows / chunk_big) near-equal big chunks per
 // larger slot, the small chunks listed first.
-__device__ void build_lists(const RouteParams& p, const int* s_cnt, int* s_off, int lane) {
+__device__ void build_lists(const RouteParams& p, const int* s_cnt, int* s_off, int tid) {
+    // Run by the first four waves of the workgroup (every thread calls it:
+    // it holds a barrier).  Lane gl of the 256 takes slots [gl*per, gl*per+per)
+    // in row order, so the scans below follow the slots' row order.
+    constexpr int kW = 4;
+    __shared__ int s_tot[kW][3];
     const int nx = p.E + p.n_shared, ns = p.n_shared, E = p.E;
     const int cs = p.chunk_small, cb = p.chunk_big;
-    const int per = (nx + kWave - 1) / kWave;
-    const int lo = lane * per;
+    const int lane = tid & (kWave - 1), wave = tid / kWave;
+    const bool active = wave < kW;   // uniform per wave
+    const int per = (nx + kW * kWave - 1) / (kW * kWave);
+    const int gl = wave * kWave + lane;
+    const int lo = gl * per;
     const int hi = min(lo + per, nx);
     auto slot_at = [&](int j) { return j < ns ? E + j : j - ns; };   // j-th slot in row order
-    int sum = 0, ssum = 0, bsum = 0;
-    for (int j = lo; j < hi; ++j) {
-        const int n = s_cnt[slot_at(j)];
-        sum += n;
-        ssum += (n > 0 && n <= cs) ? 1 : 0;
-        bsum += n > cs ? (n + cb - 1) / cb : 0;
+    int sum = 0, ssum = 0, bsum = 0, inc = 0, sinc = 0, binc = 0;
+    if (active) {
+        for (int j = lo; j < hi; ++j) {
+            const int n = s_cnt[slot_at(j)];
+            sum += n;
+            ssum += (n > 0 && n <= cs) ? 1 : 0;
+            bsum += n > cs ? (n + cb - 1) / cb : 0;
+        }
+        inc = wave_incl_scan(sum);
+        sinc = wave_incl_scan(ssum);
+        binc = wave_incl_scan(bsum);
+        if (lane == kWave - 1) {
+            s_tot[wave][0] = inc;
+            s_tot[wave][1] = sinc;
+            s_tot[wave][2] = binc;
+        }
     }
-    const int inc = wave_incl_scan(sum), sinc = wave_incl_scan(ssum), binc = wave_incl_scan(bsum);
-    const int stotal = __builtin_amdgcn_readlane(sinc, kWave - 1);
-    int run = inc - sum, srun = sinc - ssum, brun = stotal + binc - bsum;
+    __syncthreads();
+    if (!active) return;
+    int base = 0, sbase = 0, bbase = 0, total = 0, stotal = 0, btotal = 0;
+    for (int w = 0; w < kW; ++w) {
+        if (w < wave) {
+            base += s_tot[w][0];
+            sbase += s_tot[w][1];
+            bbase += s_tot[w][2];
+        }
+        total += s_tot[w][0];
+        stotal += s_tot[w][1];
+        btotal += s_tot[w][2];
+    }
+    int run = base + inc - sum, srun = sbase + sinc - ssum, brun = stotal + bbase + binc - bsum;
     for (int j = lo; j < hi; ++j) {
         const int x = slot_at(j);
         const int cnt = s_cnt[x];
@@ -701,9 +736,7 @@ __device__ void build_lists(const RouteParams& p, const int* s_cnt, int* s_off, 
         }
         run += cnt;
     }
-    const int total = __builtin_amdgcn_readlane(inc, kWave - 1);
-    const int btotal = __builtin_amdgcn_readlane(binc, kWave - 1);
-    if (lane == 0) {
+    if (gl == 0) {
         s_off[nx] = total;
         p.perm_off[nx] = total;
         p.n_chunks[0] = stotal;
@@ -794,7 +827,7 @@ __device__ void permute_small(const RouteParams& p, int tid, int nthr, PermShare
         s_cnt[x] = c;
     }
     __syncthreads();
-    if (tid < kWave) build_lists(p, s_cnt, s_off, tid);
+    build_lists(p, s_cnt, s_off, tid);
     __syncthreads();
     place_shared(p, s_off, tid, nthr);
     place_entries(p, 0, T, W, s_off, tid, nthr, s_mask);
@@ -841,7 +874,7 @@ __global__ __launch_bounds__(kRouteThreads) void k_permute_scan(RouteParams p) {
         s_cnt[x] = c;
     }
     __syncthreads();
-    if (tid < kWave) build_lists(p, s_cnt, s_off, tid);
+    build_lists(p, s_cnt, s_off, tid);
     __syncthreads();
     for (int x = tid; x < E; x += kRouteThreads) {
         int run = s_off[x];
@@ -928,6 +961,7 @@ __device__ void route_fused_body(const RouteParams& p) {
     __shared__ uint32_t l_masks[4 * (kMaxE / 32)];
     __shared__ int32_t l_stats[8];
     __shared__ double l_bl[3 * kMaxE];
+    __shared__ double l_s[kFusedT * kMaxK];
     const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
     const int k = p.k, E = p.E;
     RouteParams q = p;
@@ -945,6 +979,7 @@ __device__ void route_fused_body(const RouteParams& p) {
     q.masks = p.masks ? l_masks : nullptr;
     q.stats = p.stats ? l_stats : nullptr;
     q.bin_loads = p.bin_loads && p.n_bins <= kMaxE ? l_bl : p.bin_loads;
+    q.sslot = l_s;
     // The tables, read by the waves that route no token while the others do.
     for (int e = tid; e < E; e += kRouteThreads) {
         l_cost[e] = p.cost[e];
@@ -1026,7 +1061,7 @@ __device__ void shared_gate_up(const FfnParams& p, int wg, int n_wg) {
         const int t = r < p.T ? r : 0;   // padded token columns read a valid row; results dropped
         const u32x4_t* const xb[1] = {(const u32x4_t*)p.x + (size_t)t * row_units + g + 4 * (size_t)k0};
         f32x4_t acc[2][1] = {{f32x4_t{0.f, 0.f, 0.f, 0.f}}, {f32x4_t{0.f, 0.f, 0.f, 0.f}}};
-        if (k1 > k0) tile_contract<M, 2, 2, 1>(a, astep, xb, 1, k1 - k0, acc);   // short rows leave waves idle
+        if (k1 > k0) tile_contract<M, kRouteSharedU, 2, 1>(a, astep, xb, 1, k1 - k0, acc);   // short rows leave waves idle
         s_part[wave][0][lane] = acc[0][0];
         s_part[wave][1][lane] = acc[1][0];
         __syncthreads();
