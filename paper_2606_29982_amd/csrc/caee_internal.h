@@ -127,7 +127,7 @@ struct WsLayout {
     size_t chunks;              // [max_chunks][4] (expert slot, first row, rows, 0): small chunks, then big
     size_t n_chunks;            // [2] small and big chunk counts
     size_t h;                   // [P][f] SwiGLU activations (weight dtype; fp32 for fp8)
-    size_t y;                   // [P][d] fp32 expert outputs
+    size_t y;                   // [P][d] expert outputs (fp32; bf16 on the 8-bit path)
     size_t xq, xs;              // fp8 path: [T][d] e4m3 codes of x and [T][d/128] fp32 scales
     size_t hq, hs;              // fp8 path: [P][f] e4m3 codes of H and [P][f/128] fp32 scales
     size_t xst, hst;            // fp8 GEMM: [d/128][P] and [f/128][P] block scales of the permuted rows

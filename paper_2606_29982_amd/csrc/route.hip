@@ -1,5 +1,6 @@
 // Routing, cost-aware pruning, compensation and token permutation for one
-// MoE layer call, in a single 1024-thread workgroup (decode batches).
+// MoE layer call: token-parallel kernels, and for batches of up to 16 tokens
+// one 1024-thread workgroup that runs every phase.
 //
 //   phase A (one wavefront per token): sigmoid scores, group-limited top-k
 //            K_t and normalised gate weights G(t)_e (Sec. II-A);
@@ -9,8 +10,8 @@
 //   phase C (one wavefront per token): masking of pruned experts and
 //            top-k refill from A_trans (Sec. IV-C), weight renormalisation;
 //   permute: stable counting sort of the (token, expert) pairs by expert,
-//            shared experts last, and the FFN work list (expert chunks of
-//            at most kChunkTokens rows).
+//            the shared experts' rows first, and the FFN work lists (small
+//            and big expert chunks).
 //
 // Every decision is taken in float64 with ties to the lower index, so the
 // result does not depend on the order in which lanes or waves finish.

@@ -38,10 +38,9 @@ def test_tiny_fp8(seed, tiled):
     print(f"  max|err|/max|ref| = {rel:.3e}")
 
 
-# 20 and 70 tokens: the shared expert's gate/up runs next to routing (its rows
-# in the small and in the big list).  T=600 takes the prefill GEMM (128-row
-# chunks): ragged chunk tails, a one-block contraction in the down product
-# (f=128) and two in gate/up.
+# 20 and 70 tokens: the shared expert's rows in the small and in the big
+# list.  T=600 takes the prefill GEMM (128-row chunks): ragged chunk tails, a
+# one-block contraction in the down product (f=128) and two in gate/up.
 @pytest.mark.parametrize("T", [1, 5, 20, 40, 70, 130, 600])
 def test_tiny_fp8_batches(T):
     _tiny(7, 0.2, 4, T=T, tiled=True, zipf=1.1 if T > 100 else None)

@@ -213,8 +213,9 @@ def test_tiled_layout_order(dtype):
     assert np.array_equal(ddst.cpu().numpy().view(np.uint32).reshape(want.shape), want)
 
 
-# 40 and 130 tokens: big chunks (the bf16 GEMM) and the shared experts'
-# gate/up next to routing; the down contraction (f = 128) is 4 or 8 steps.
+# 1, 3 and 16 tokens: the routing launch runs the shared expert's gate/up;
+# 40, 70 and 130 tokens: big chunks (the bf16 GEMM); the down contraction
+# (f = 128) is 4 or 8 steps.
 @pytest.mark.parametrize("shape", [TINY_F32, TINY_BF16], ids=["f32", "bf16"])
 @pytest.mark.parametrize("T", [1, 3, 16, 40, 70, 130])
 def test_tiled_weights(shape, T):
