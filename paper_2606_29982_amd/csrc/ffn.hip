@@ -354,40 +354,60 @@ __global__ __launch_bounds__(256) void k_pack(const u32x4_t* __restrict__ src, u
     }
 }
 
-// One thread per 4 output features of one token.
+// One thread per W output features of one token: 4, or 8 when the expert
+// output rows are bf16 (one 16-byte load per row).  Slots are added in
+// order with fp32 fused multiply-adds, then the shared experts.
+template <int W>
 __global__ __launch_bounds__(256) void k_combine(FfnParams p) {
-    const int per_tok = (p.d / 4 + 255) / 256;
+    const int per_tok = (p.d / W + 255) / 256;
     const int t = blockIdx.x / per_tok;
-    const int c = ((blockIdx.x - t * per_tok) * 256 + threadIdx.x) * 4;
+    const int c = ((blockIdx.x - t * per_tok) * 256 + threadIdx.x) * W;
     if (c >= p.d) return;
     const int slots = p.k + p.n_shared;
-    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    auto load = [&](int pos, float (&v)[W]) {
+        if constexpr (W == 8) {
+            const uint4 pk = *(const uint4*)((const uint16_t*)p.yperm + (size_t)pos * p.d + c);
+            const uint32_t u[4] = {pk.x, pk.y, pk.z, pk.w};
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                v[2 * i] = __uint_as_float(u[i] << 16);
+                v[2 * i + 1] = __uint_as_float(u[i] & 0xFFFF0000u);
+            }
+        } else {
+            const float4 f = load_y4(p, (size_t)pos, c);
+            v[0] = f.x;
+            v[1] = f.y;
+            v[2] = f.z;
+            v[3] = f.w;
+        }
+    };
+    float acc[W], v[W];
+#pragma unroll
+    for (int i = 0; i < W; ++i) acc[i] = 0.f;
     for (int j = 0; j < p.k; ++j) {
         const int pos = p.perm_pos[t * slots + j];
         if (pos < 0) continue;
         const float w = p.topk_w[t * p.k + j];
-        const float4 v = load_y4(p, (size_t)pos, c);
-        acc.x = fmaf(w, v.x, acc.x);
-        acc.y = fmaf(w, v.y, acc.y);
-        acc.z = fmaf(w, v.z, acc.z);
-        acc.w = fmaf(w, v.w, acc.w);
+        load(pos, v);
+#pragma unroll
+        for (int i = 0; i < W; ++i) acc[i] = fmaf(w, v[i], acc[i]);
     }
     for (int s = 0; s < p.n_shared; ++s) {
-        const int pos = p.perm_pos[t * slots + p.k + s];
-        const float4 v = load_y4(p, (size_t)pos, c);
-        acc.x += v.x;
-        acc.y += v.y;
-        acc.z += v.z;
-        acc.w += v.w;
+        load(p.perm_pos[t * slots + p.k + s], v);
+#pragma unroll
+        for (int i = 0; i < W; ++i) acc[i] += v[i];
     }
     const size_t o = (size_t)t * p.d + c;
-    if (p.y_bf16) {
-        uint2 pk;
-        pk.x = bf16_rne(acc.x) | (bf16_rne(acc.y) << 16);
-        pk.y = bf16_rne(acc.z) | (bf16_rne(acc.w) << 16);
-        *(uint2*)((uint16_t*)p.y + o) = pk;
-    } else {
-        *(float4*)((float*)p.y + o) = acc;
+#pragma unroll
+    for (int i = 0; i < W; i += 4) {
+        if (p.y_bf16) {
+            uint2 pk;
+            pk.x = bf16_rne(acc[i]) | (bf16_rne(acc[i + 1]) << 16);
+            pk.y = bf16_rne(acc[i + 2]) | (bf16_rne(acc[i + 3]) << 16);
+            *(uint2*)((uint16_t*)p.y + o + i) = pk;
+        } else {
+            *(float4*)((float*)p.y + o + i) = make_float4(acc[i], acc[i + 1], acc[i + 2], acc[i + 3]);
+        }
     }
 }
 
@@ -477,8 +497,8 @@ hipError_t launch_pack(const void* src, void* dst, long long rows, long long row
 }
 
 hipError_t launch_combine(const FfnParams& p, hipStream_t s) {
-    const dim3 grid(((p.d / 4 + 255) / 256) * p.T);
-    hipLaunchKernelGGL(k_combine, grid, dim3(256), 0, s, p);
+    if (p.y_half) hipLaunchKernelGGL(k_combine<8>, dim3(((p.d / 8 + 255) / 256) * p.T), dim3(256), 0, s, p);
+    else hipLaunchKernelGGL(k_combine<4>, dim3(((p.d / 4 + 255) / 256) * p.T), dim3(256), 0, s, p);
     return hipGetLastError();
 }
 
