@@ -535,11 +535,27 @@ __device__ void prune_all(const RouteParams& p, int tid, int nthr, PruneShared& 
 
     // Step 1: A_act, importance, A_must (pairs mandatory on their own, and
     // for the SUM rule every expert whose summed weight reaches tau).
-    for (int i = tid; i < T * k; i += nthr) {
-        const int e = p.orig_ids[i];
-        atomicMax(&s_imp[e], (unsigned long long)__double_as_longlong(p.gbuf[i]));
-        s_act[e] = 1;
-        if (p.mflag[i]) s_must[e] = 1;
+    // Batches of 8 pairs per thread: their loads are issued together.
+    constexpr int kB = 8;
+    for (int i0 = tid; i0 < T * k; i0 += kB * nthr) {
+        int ev[kB];
+        double gv[kB];
+        uint8_t mv[kB];
+#pragma unroll
+        for (int b = 0; b < kB; ++b) {
+            const int i = i0 + b * nthr;
+            const bool in = i < T * k;
+            ev[b] = in ? p.orig_ids[i] : -1;
+            gv[b] = in ? p.gbuf[i] : 0.0;
+            mv[b] = in ? p.mflag[i] : 0;
+        }
+#pragma unroll
+        for (int b = 0; b < kB; ++b) {
+            if (ev[b] < 0) continue;
+            atomicMax(&s_imp[ev[b]], (unsigned long long)__double_as_longlong(gv[b]));
+            s_act[ev[b]] = 1;
+            if (mv[b]) s_must[ev[b]] = 1;
+        }
     }
     __syncthreads();
     if (p.rule == CAEE_IMPORTANCE_SUM) {
@@ -748,7 +764,7 @@ __device__ void build_lists(const RouteParams& p, const int* s_cnt, int* s_off, 
 // Token-block bitmasks: bit (t - t0) of word (x, (t - t0) / 64) is set when
 // token t of [t0, t0 + tn) chose routed expert x.  W words per expert.
 __device__ void fill_masks(const RouteParams& p, int t0, int tn, int W, int tid, int nthr,
-                           unsigned long long* s_mask) {
+                           unsigned long long* s_mask, int* s_pre) {
     const int E = p.E, k = p.k;
     for (int i = tid; i < E * W; i += nthr) s_mask[i] = 0ull;
     __syncthreads();
@@ -760,13 +776,21 @@ __device__ void fill_masks(const RouteParams& p, int t0, int tn, int W, int tid,
         }
     }
     __syncthreads();
+    // s_pre[e*W + w]: tokens of words 0..w-1 that chose expert e.
+    for (int i = tid; i < E * W; i += nthr) {
+        const int w = i % W;
+        int c = 0;
+        for (int v = i - w; v < i; ++v) c += __popcll(s_mask[v]);
+        s_pre[i] = c;
+    }
+    __syncthreads();
 }
 
 // Rows of the (token, slot) entries of tokens [t0, t0 + tn): routed entry
 // of expert e goes to row base[e] + (number of earlier tokens of the block
 // that chose e); caller-supplied ids outside [0, E) are empty slots.
 __device__ void place_entries(const RouteParams& p, int t0, int tn, int W, const int* base, int tid, int nthr,
-                              const unsigned long long* s_mask) {
+                              const unsigned long long* s_mask, const int* s_pre) {
     const int E = p.E, k = p.k, slots = k + p.n_shared;
     for (int i = tid; i < tn * k; i += nthr) {
         const int tl = i / k, j = i - tl * k;
@@ -776,9 +800,8 @@ __device__ void place_entries(const RouteParams& p, int t0, int tn, int W, const
             p.perm_pos[(size_t)t * slots + j] = -1;
             continue;
         }
-        const unsigned long long* m = s_mask + e * W;
-        int rank = __popcll(m[tl >> 6] & ((1ull << (tl & 63)) - 1ull));
-        for (int w = 0; w < (tl >> 6); ++w) rank += __popcll(m[w]);
+        const int w = e * W + (tl >> 6);
+        const int rank = s_pre[w] + __popcll(s_mask[w] & ((1ull << (tl & 63)) - 1ull));
         const int pos = base[e] + rank;
         p.perm_tok[pos] = t;
         p.perm_pos[(size_t)t * slots + j] = pos;
@@ -805,6 +828,7 @@ struct PermShared {
     int cnt[kMaxE + kMaxShared];
     int off[kMaxE + kMaxShared + 1];
     unsigned long long mask[kMaxE * (kMaskT / 64)];
+    int pre[kMaxE * (kMaskT / 64)];
 };
 
 __device__ void permute_small(const RouteParams& p, int tid, int nthr, PermShared& sh) {
@@ -818,7 +842,7 @@ __device__ void permute_small(const RouteParams& p, int tid, int nthr, PermShare
     if (!p.do_permute) return;
     const int T = p.T, E = p.E;
     const int W = (T + 63) / 64;
-    fill_masks(p, 0, T, W, tid, nthr, s_mask);
+    fill_masks(p, 0, T, W, tid, nthr, s_mask, sh.pre);
     for (int x = tid; x < E + p.n_shared; x += nthr) {
         int c = T;
         if (x < E) {
@@ -831,7 +855,7 @@ __device__ void permute_small(const RouteParams& p, int tid, int nthr, PermShare
     build_lists(p, s_cnt, s_off, tid);
     __syncthreads();
     place_shared(p, s_off, tid, nthr);
-    place_entries(p, 0, T, W, s_off, tid, nthr, s_mask);
+    place_entries(p, 0, T, W, s_off, tid, nthr, s_mask, sh.pre);
 }
 
 __global__ __launch_bounds__(kRouteThreads) void k_permute(RouteParams p) {
@@ -891,11 +915,12 @@ __global__ __launch_bounds__(kRouteThreads) void k_permute_scan(RouteParams p) {
 // (3) per block, the rows of its (token, slot) entries.
 __global__ __launch_bounds__(kRouteThreads) void k_permute_place(RouteParams p) {
     __shared__ unsigned long long s_mask[kMaxE * (kMaskT / 64)];
+    __shared__ int s_pre[kMaxE * (kMaskT / 64)];
     const int tid = threadIdx.x, b = blockIdx.x;
     const int t0 = b * kMaskT, tn = min(kMaskT, p.T - t0);
     const int W = (tn + 63) / 64;
-    fill_masks(p, t0, tn, W, tid, kRouteThreads, s_mask);
-    place_entries(p, t0, tn, W, p.perm_blk + (size_t)b * p.E, tid, kRouteThreads, s_mask);
+    fill_masks(p, t0, tn, W, tid, kRouteThreads, s_mask, s_pre);
+    place_entries(p, t0, tn, W, p.perm_blk + (size_t)b * p.E, tid, kRouteThreads, s_mask, s_pre);
 }
 
 hipError_t launch_permutation(const RouteParams& p, hipStream_t s) {
