@@ -124,7 +124,7 @@ struct WsLayout {
     size_t perm_tok;            // [P] token of each permuted row
     size_t perm_pos;            // [T][k + n_shared] permuted row of each (token, slot), -1 unused
     size_t perm_blk;            // [ceil(T / kMaskT)][E] per token block: expert counts, then first rows
-    size_t chunks;              // [max_chunks][4] (expert slot, first row, rows, 0): small chunks, then big
+    size_t chunks;              // [max_chunks][4] (expert slot, first row, rows, pair): small chunks, then big
     size_t n_chunks;            // [2] small and big chunk counts
     size_t h;                   // [P][f] SwiGLU activations (weight dtype; fp32 for fp8)
     size_t y;                   // [P][d] expert outputs (fp32; bf16 on the 8-bit path)
@@ -352,13 +352,14 @@ struct FfnParams {
 // listed first, then the big ones).
 struct ChunkRef {
     int xs, row0, ntok;
+    int pair;   // list offset (+1 / -1) of the other piece of a pair, 0 if unpaired
 };
 
 __device__ inline int ffn_list_size(const FfnParams& p) { return p.n_chunks[p.list]; }
 
 __device__ inline ChunkRef ffn_chunk(const FfnParams& p, int c) {
     const int32_t* ch = p.chunks + 4 * ((p.list ? p.n_chunks[0] : 0) + c);
-    return {ch[0], ch[1], ch[2]};
+    return {ch[0], ch[1], ch[2], ch[3]};
 }
 
 // Token of permuted row `row` (of expert slot xs).

@@ -24,6 +24,15 @@
 // 128-byte line per wave and block.  Measured at the 4096-token prefill, the
 // 256 x 128 tile is faster than 128 x 256 (which reads each weight byte once
 // for experts with up to 256 rows, but issues twice the token-row loads).
+//
+// The 8-bit down product runs a pair of chunks of one expert (adjacent
+// pieces of a slot cut into several, at most 256 rows together) in the
+// 128 x 256 shape of the same stage: half the weight tiles, twice the token
+// tiles, the same six loads per wave.  Each chunk of the pair keeps its
+// groups' worth of items, which take the pair's first and second half of
+// the weight-row groups, so the item list stays dense, and the pair's
+// weights stream once instead of once per chunk.  Gate/up stays in the
+// 256 x 128 shape: its epilogue quantises whole 128-feature blocks.
 #include "caee_internal.h"
 #include "fp8_codec.h"
 
@@ -46,7 +55,6 @@ constexpr int kTiles = CAEE_GEMM_TILES;
 constexpr int kNT = 128 / kTiles;
 constexpr int kWaveNT = 4;            // token tiles per wave
 constexpr int kRowWaves = kTiles / 4; // waves across the weight rows
-constexpr int kXPer = 2 * kNT;        // tokens whose scales one wave loads
 static_assert(kTiles == 8 || kTiles == 16, "tile shape");
 // With 256-row tiles a gate/up item holds 128 features, one quantisation
 // block of each of its token rows: the epilogue quantises the SwiGLU rows
@@ -60,17 +68,23 @@ constexpr bool kFuseQuant = kTiles == 16;
 constexpr int kStages = 3;
 constexpr int kGemmWaves = 8;
 constexpr int kGemmThreads = kGemmWaves * kWave;
+// 8-bit down items of paired chunks take the other shape of the same stage.
+constexpr bool kWideDown = kTiles == 16;
+// Fragments of one stage: 2 halves of every weight tile, then of every token
+// tile (either shape: 2 * (16 + 8) = 2 * (8 + 16)).
+constexpr int kFrags = 2 * (kTiles + kNT);
+constexpr int kLoads = kTiles / 4 + kNT / 4;   // fragment loads per wave and stage, either shape
+
 // Loads per wave and stage: the weight and token-row pieces, plus (8-bit)
 // one load of the rows' block scales.
 template <bool kFp8>
-constexpr int loads_per_stage() { return kTiles / 4 + kNT / 4 + (kFp8 ? 1 : 0); }
+constexpr int loads_per_stage() { return kLoads + (kFp8 ? 1 : 0); }
 constexpr int kMaxKBlocks = 128;      // contraction up to 16384
 constexpr int kXcds = 8;              // accelerator complex dies, each with its own L2
 
 struct GemmStage {
-    u32x4_t a[kTiles][2][kWave];      // weight fragments: [tile][half of the block][lane]
-    u32x4_t b[kNT][2][kWave];         // token-row fragments: [token tile][half][lane]
-    float x[kGemmWaves][kWave];       // row scales: token n at [n / kXPer][n % kXPer]
+    u32x4_t f[kFrags][kWave];         // [2 * tile + half] weights, then [2 * tiles + 2 * token tile + half] rows
+    float x[kGemmWaves][kWave];       // row scales: token n at [n / per][n % per], per = 2 * token tiles
 };
 
 __device__ inline i32x8_t join(const u32x4_t& lo, const u32x4_t& hi) {
@@ -111,9 +125,12 @@ __global__ __launch_bounds__(kGemmThreads) void k_gemm(FfnParams p) {
     // weight rows each fall in one 128-row scale row.  Read from LDS in the
     // pipeline, as a global load there would make the wave drain its loads.
     __shared__ float wsl[2][kMaxKBlocks];
-    const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
-    const int wq = wave % kRowWaves, wc = wave / kRowWaves;   // weight rows, token columns
+    const int tid = threadIdx.x, lane = tid & (kWave - 1);
+    // Wave index as a scalar: the tile and fragment indices derived from it
+    // stay in scalar registers.
+    const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
     const int r = lane & 15, g = lane >> 4;
+    constexpr bool kWide = kWideDown && kFp8 && !kGateUp;
     const int K = kGateUp ? p.d : p.f;                 // contraction length
     const int kblocks = K * kEb / 128;                 // pipeline stages (128 bytes of each row)
     const size_t ksteps = (size_t)K * kEb / 64;        // 64-byte steps per weight row
@@ -138,59 +155,75 @@ __global__ __launch_bounds__(kGemmThreads) void k_gemm(FfnParams p) {
         item_step = per;
     }
     for (; item < item_end; item += item_step) {
-        const int c = item / groups, grp = item - c * groups;
+        const int c = item / groups;
         const ChunkRef ck = ffn_chunk(p, c);
-        const int xs = ck.xs, row0 = ck.row0, ntok = ck.ntok;
+        const int xs = ck.xs;
         if (ffn_skip(p, xs)) continue;   // uniform over the workgroup
+        int row0 = ck.row0, ntok = ck.ntok, grp = item - c * groups;
+        // Paired chunk: the pair's rows, and half-group grp (first chunk of
+        // the pair) or groups + grp (second).
+        const bool wide = kWide && ck.pair != 0;
+        if (wide) {
+            const ChunkRef o = ffn_chunk(p, c + ck.pair);
+            if (ck.pair < 0) {
+                row0 = o.row0;
+                grp += groups;
+            }
+            ntok += o.ntok;
+        }
+        // Item shape: tiles weight tiles x nts token tiles; waves rw across
+        // the weight rows (4 x 4 output tiles per wave in both shapes).
+        const int tiles = wide ? kTiles / 2 : kTiles, nts = wide ? 2 * kNT : kNT;
+        const int rw = tiles / 4, wq = wave % rw, wc = wave / rw;   // weight rows, token columns
+        const int na = tiles / 4;                          // weight fragment loads per wave (the rest: rows)
+        const int bbase = 2 * tiles;                       // first token-row fragment of a stage
+        const int xsh = wide ? 5 : 4;                      // log2 of the tokens per wave whose scales it loads
         const int nb = (ntok + 15) >> 4;
         const u32x4_t* wb = (const u32x4_t*)ffn_weights(p, xs, kGateUp ? false : true, expert_bytes);
         const float* wsc = kFp8 ? ffn_scales(p, xs, kGateUp ? false : true, scales_per_expert) : nullptr;
         // Expert-relative weight tile of workgroup tile slot i.
         auto tile_of = [&](int i) {
             if (kGateUp) return i < kTiles / 2 ? grp * (kTiles / 2) + i : p.f / 16 + grp * (kTiles / 2) + i - kTiles / 2;
-            return grp * kTiles + i;
+            return grp * tiles + i;
         };
-        // This wave's loads per stage: (tile, half) pairs j = kTiles/4 * w + i
-        // of the weights, (token tile, half) pairs j = kNT/4 * w + i of the
-        // rows, and the scales of tokens kXPer * w .. + kXPer - 1 (the other
-        // lanes repeat them into padding).
-        const u32x4_t* asrc[kTiles / 4];
+        // This wave's kLoads fragment loads per stage: (tile, half) pairs
+        // j = na * w + i of the weights, then (token tile, half) pairs
+        // j = (kLoads - na) * w + i of the rows; and the scales of tokens
+        // per * w .. + per - 1 (the other lanes repeat them into padding).
+        const u32x4_t* src[kLoads];
+        int frag[kLoads], stride[kLoads];
 #pragma unroll
-        for (int i = 0; i < kTiles / 4; ++i) {
-            const int j = kTiles / 4 * wave + i;
-            asrc[i] = wb + (size_t)tile_of(j >> 1) * ksteps * 64 + (j & 1) * 64 + lane;
-        }
-        const u32x4_t* bsrc[kNT / 4];
-#pragma unroll
-        for (int i = 0; i < kNT / 4; ++i) {
-            const int j = kNT / 4 * wave + i;
-            int n = 16 * (j >> 1) + r;
-            n = n < ntok ? n : 0;          // padded token columns read a valid row; results dropped
-            const int row = kGateUp ? ffn_token(p, xs, row0 + n) : row0 + n;
-            const void* rows = kFp8 ? (kGateUp ? (const void*)p.xq : (const void*)p.hq) : (kGateUp ? p.x : p.h);
-            bsrc[i] = (const u32x4_t*)rows + (size_t)row * row_units + (j & 1) * 4 + g;
+        for (int i = 0; i < kLoads; ++i) {
+            if (i < na) {
+                const int j = na * wave + i;
+                src[i] = wb + (size_t)tile_of(j >> 1) * ksteps * 64 + (j & 1) * 64 + lane;
+                frag[i] = j;
+                stride[i] = 128;
+            } else {
+                const int j = (kLoads - na) * wave + i - na;
+                int n = 16 * (j >> 1) + r;
+                n = n < ntok ? n : 0;          // padded token columns read a valid row; results dropped
+                const int row = kGateUp ? ffn_token(p, xs, row0 + n) : row0 + n;
+                const void* rows = kFp8 ? (kGateUp ? (const void*)p.xq : (const void*)p.hq) : (kGateUp ? p.x : p.h);
+                src[i] = (const u32x4_t*)rows + (size_t)row * row_units + (j & 1) * 4 + g;
+                frag[i] = bbase + j;
+                stride[i] = 8;
+            }
         }
         // Row scales, transposed and in permuted row order ([block][row]):
         // one 128-byte line per wave and block.
         const float* xsrc = nullptr;
         if (kFp8) {
-            int n = kXPer * wave + lane % kXPer;
+            const int per = 1 << xsh;
+            int n = per * wave + (lane & (per - 1));
             n = n < ntok ? n : 0;
             xsrc = (kGateUp ? p.xst : p.hst) + row0 + n;
         }
         auto issue = [&](int kb, GemmStage& s) __attribute__((always_inline)) {
 #pragma unroll
-            for (int i = 0; i < kTiles / 4; ++i) {
-                const int j = kTiles / 4 * wave + i;
-                __builtin_amdgcn_global_load_lds((const void*)(asrc[i] + (size_t)kb * 128),
-                                                 (lds_void_t*)&s.a[j >> 1][j & 1][0], 16, 0, 0);
-            }
-#pragma unroll
-            for (int i = 0; i < kNT / 4; ++i) {
-                const int j = kNT / 4 * wave + i;
-                __builtin_amdgcn_global_load_lds((const void*)(bsrc[i] + (size_t)kb * 8),
-                                                 (lds_void_t*)&s.b[j >> 1][j & 1][0], 16, 0, 0);
-            }
+            for (int i = 0; i < kLoads; ++i)
+                __builtin_amdgcn_global_load_lds((const void*)(src[i] + (size_t)kb * stride[i]),
+                                                 (lds_void_t*)&s.f[frag[i]][0], 16, 0, 0);
             if (kFp8)
                 __builtin_amdgcn_global_load_lds((const void*)(xsrc + (size_t)kb * p.P), (lds_void_t*)&s.x[wave][0], 4,
                                                  0, 0);
@@ -201,12 +234,12 @@ __global__ __launch_bounds__(kGemmThreads) void k_gemm(FfnParams p) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             aslot[i] = kGateUp ? (i < 2 ? 2 * wq + i : kTiles / 2 + 2 * wq + i - 2) : 4 * wq + i;
-            srow[i] = aslot[i] >= kTiles / 2;
+            srow[i] = aslot[i] >= tiles / 2;
         }
         if (kFp8)
             for (int q = tid; q < 2 * kblocks; q += kGemmThreads) {
                 const int h = q >= kblocks, kb = q - h * kblocks;
-                const int row = (tile_of(h * (kTiles / 2)) * 16) / 128;
+                const int row = (tile_of(h * (tiles / 2)) * 16) / 128;
                 wsl[h][kb] = wsc[(size_t)row * kblocks + kb];
             }
         __syncthreads();
@@ -225,12 +258,12 @@ __global__ __launch_bounds__(kGemmThreads) void k_gemm(FfnParams p) {
                 for (int h = 0; h < 2; ++h) {
                     bf16x8_t af[4];
 #pragma unroll
-                    for (int i = 0; i < 4; ++i) af[i] = __builtin_bit_cast(bf16x8_t, s.a[aslot[i]][h][lane]);
+                    for (int i = 0; i < 4; ++i) af[i] = __builtin_bit_cast(bf16x8_t, s.f[2 * aslot[i] + h][lane]);
 #pragma unroll
                     for (int j = 0; j < kWaveNT; ++j) {
                         const int n = kWaveNT * wc + j;
                         if (n < nb) {
-                            const bf16x8_t bf = __builtin_bit_cast(bf16x8_t, s.b[n][h][lane]);
+                            const bf16x8_t bf = __builtin_bit_cast(bf16x8_t, s.f[bbase + 2 * n + h][lane]);
 #pragma unroll
                             for (int i = 0; i < 4; ++i)
                                 acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bf, acc[i][j], 0, 0, 0);
@@ -243,16 +276,16 @@ __global__ __launch_bounds__(kGemmThreads) void k_gemm(FfnParams p) {
             float ws[4];
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                af[i] = join(s.a[aslot[i]][0][lane], s.a[aslot[i]][1][lane]);
+                af[i] = join(s.f[2 * aslot[i]][lane], s.f[2 * aslot[i] + 1][lane]);
                 ws[i] = wsl[srow[i]][kb];
             }
 #pragma unroll
             for (int j = 0; j < kWaveNT; ++j) {
                 const int n = kWaveNT * wc + j;
                 if (n < nb) {
-                    const i32x8_t bf = join(s.b[n][0][lane], s.b[n][1][lane]);
+                    const i32x8_t bf = join(s.f[bbase + 2 * n][lane], s.f[bbase + 2 * n + 1][lane]);
                     const int tok = 16 * n + r;
-                    const float xsv = s.x[tok / kXPer][tok % kXPer];
+                    const float xsv = s.x[tok >> xsh][tok & ((1 << xsh) - 1)];
                     f32x4_t part[4];
 #pragma unroll
                     for (int i = 0; i < 4; ++i)
@@ -378,7 +411,7 @@ __global__ __launch_bounds__(kGemmThreads) void k_gemm(FfnParams p) {
             } else {
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    store_y4(p, (size_t)(row0 + tn), (grp * kTiles + 4 * wq + i) * 16 + 4 * g, acc[i][j][0],
+                    store_y4(p, (size_t)(row0 + tn), (grp * tiles + 4 * wq + i) * 16 + 4 * g, acc[i][j][0],
                              acc[i][j][1], acc[i][j][2], acc[i][j][3]);
                 }
             }

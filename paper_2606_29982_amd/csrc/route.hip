@@ -747,7 +747,9 @@ __device__ void build_lists(const RouteParams& p, const int* s_cnt, int* s_off, 
                 chk[0] = x;
                 chk[1] = run + c * size;
                 chk[2] = min(size, cnt - c * size);
-                chk[3] = 0;
+                // Pieces 2i and 2i + 1 form a pair (rows adjacent, at most
+                // 2 * chunk_big together); a last odd piece has none.
+                chk[3] = (c & 1) ? -1 : (c + 1 < pieces ? 1 : 0);
             }
             brun += pieces;
         }

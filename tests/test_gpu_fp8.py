@@ -39,9 +39,11 @@ def test_tiny_fp8(seed, tiled):
 
 
 # 20 and 70 tokens: the shared expert's rows in the small and in the big
-# list.  T=600 takes the prefill GEMM (128-row chunks): ragged chunk tails, a
-# one-block contraction in the down product (f=128) and two in gate/up.
-@pytest.mark.parametrize("T", [1, 5, 20, 40, 70, 130, 600])
+# list.  T=600 and 1100 take the prefill GEMM (128-row chunks; down runs the
+# pairs of chunks of an expert cut into several in its 128 x 256 shape, and a
+# last odd chunk alone): ragged chunk tails, a one-block contraction in the
+# down product (f=128) and two in gate/up.
+@pytest.mark.parametrize("T", [1, 5, 20, 40, 70, 130, 600, 1100])
 def test_tiny_fp8_batches(T):
     _tiny(7, 0.2, 4, T=T, tiled=True, zipf=1.1 if T > 100 else None)
 
