@@ -30,7 +30,7 @@ W_EXPERT_BYTES = 3 * 7168 * 2048 * 2
 W_EXPERT_BYTES_FP8 = 3 * 7168 * 2048 + 4 * (2 * 2048 // 128) * (7168 // 128) + 4 * (7168 // 128) * (2048 // 128)
 PAIR_FLOPS = 6 * 7168 * 2048    # one (token, expert) pair through gate, up and down
 METRIC = "MoE-layer tokens/s + achieved HBM GB/s (% of peak) at T=1..128, with vs without pruning"
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gate_up_r1_t32_traffic.json")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gate_up_deepseek_r1_t32_traffic.json")
 # The gate/up kernel's source and the header holding its tuning constants:
 # a traffic figure holds only for the build they describe.
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2606_29982_amd", "csrc", n)
