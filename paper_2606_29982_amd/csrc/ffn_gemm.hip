@@ -1,4 +1,5 @@
-// Prefill-class 8-bit expert products for big chunks.
+// LDS-pipelined expert products for big chunks: 8-bit at prefill sizes,
+// bf16 for the hot experts of decode batches.
 //
 // A workgroup of 8 waves computes a 256-weight-row x 128-token tile (or,
 // built with CAEE_GEMM_TILES=8, 128 x 256) of one chunk over the whole
@@ -18,8 +19,10 @@
 // instructions.  With R = kTiles / 4 waves across the rows, wave
 // w = R * c + q takes token tiles 4c .. 4c + 3 and
 //   gate/up: features 2q, 2q + 1 of the tile's kTiles / 2 (gate and up rows
-//            of each) -> fp32 SwiGLU rows;
-//   down:    row tiles 4q .. 4q + 3 -> fp32 Y rows.
+//            of each) -> SwiGLU rows (8-bit: e4m3 codes + block scales;
+//            bf16: bf16);
+//   down:    row tiles 4q .. 4q + 3 -> Y rows (bf16 on the 8-bit path,
+//            fp32 otherwise).
 // The rows' block scales are read transposed ([block][permuted row]), one
 // 128-byte line per wave and block.  Measured at the 4096-token prefill, the
 // 256 x 128 tile is faster than 128 x 256 (which reads each weight byte once
