@@ -275,7 +275,7 @@ def offload_rows(args, shape, Wt, dev, link_model=None):
         ws = caee.alloc_workspace(layer, dev)
         out = caee.alloc_route_out(layer, dev)
         y = torch.empty((T, shape.d), dtype=torch.bfloat16, device=dev)
-        acc = torch.zeros(8, dtype=torch.int64, device=dev)
+        acc = torch.zeros(caee.STATS, dtype=torch.int64, device=dev)
         for x, logits, bias in dev_calls[:4]:        # warm-up, then a cold cache
             h(layer, x, logits, bias, y, ws, out)
         torch.cuda.synchronize()
@@ -472,6 +472,7 @@ def main():
     # The same call captured in a HIP graph, memory-side cache flushed before
     # every timed replay (median and spread of single calls).
     result["graph_protocol"] = graph_protocol(head)
+    result["hbm_frac_flushed"] = round(b_layer / (result["graph_protocol"]["us_p50"] * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4)
     log(f"graph protocol {result['graph_protocol']}")
 
     link_model = None
@@ -499,14 +500,21 @@ def main():
                 gp = graph_protocol(c, warmup=5, iters=20)
                 s = c.stats()
                 b = layer_bytes(shape, T, s[5])
+                loads = c.out["bin_loads"].cpu().numpy() / 1e9   # cost units (weight bytes x multiplier), in G
                 sweep.append({"T": T, "rule": rule, "tau": tau, "n_bins": n_bins, "inputs": "zipf-skewed",
                               "pruning": "off" if tau == 0.0 else "on",
                               "us_per_step": round(m * 1e3, 1), "tokens_per_s": round(T / (m * 1e-3), 1),
                               "hbm_gbps": round(b / (m * 1e-3) / 1e9, 1),
                               "hbm_frac": round(b / (m * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
-                              "act": s[0], "pruned": s[4], "executed": s[5] + shape.n_shared,
+                              "act": s[0], "must": s[1], "pruned": s[4], "executed": s[5] + shape.n_shared,
+                              "fallback": s[8],
                               "graph_flushed_us_p50": gp["us_p50"], "graph_flushed_us_p10": gp["us_p10"],
-                              "graph_flushed_us_p90": gp["us_p90"]})
+                              "graph_flushed_us_p90": gp["us_p90"],
+                              "hbm_frac_flushed": round(b / (gp["us_p50"] * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),
+                              "bin_loads_g": {"act": [round(v, 3) for v in loads[0]],
+                                              "must": [round(v, 3) for v in loads[1]],
+                                              "trans": [round(v, 3) for v in loads[2]]},
+                              "f_base_g": round(float(loads[1].max()), 3)})
                 log(f"sweep {sweep[-1]}")
                 del c
         result["sweep"] = sweep
@@ -538,6 +546,16 @@ def main():
 
     if not args.no_sweep:
         result["compensation_ablation"] = ablation_rows(args, shape, Wt, dev)
+
+    if link_model is not None and not args.no_sweep:
+        # The host link measured again after the sweeps, the 8-bit rows and the
+        # ablation: the same copies, to compare with the samples above.
+        from paper_2606_29982_amd import calibrate as cal
+        ls, lt = cal.measure_link(dev)
+        again = cal.fit_link(ls, lt, cal.LINK_GBPS)
+        result["calibration"]["h2d_after_sweeps"] = {**again.as_dict(),
+                                                     "samples": [(n, round(t, 2)) for n, t in zip(ls, lt)]}
+        log(f"host link after the sweeps {result['calibration']['h2d_after_sweeps']}")
 
     if not args.no_offload:
         result["offload"] = offload_rows(args, shape, Wt, dev, link_model)

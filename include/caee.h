@@ -49,7 +49,7 @@
 extern "C" {
 #endif
 
-#define CAEE_ABI_VERSION 7
+#define CAEE_ABI_VERSION 8
 
 typedef enum caee_status {
     CAEE_OK = 0,
@@ -66,8 +66,13 @@ typedef enum caee_dtype {
     CAEE_FP8_E4M3 = 2   /* OCP FP8 E4M3 (max 448), used with fp32 block scales */
 } caee_dtype_t;
 
-/* Mandatory-set rule of the pruning step (Sec. IV-B step 1).  Every rule
- * also keeps each token's own top expert, so no token loses all experts. */
+/* Mandatory-set rule of the pruning step (Sec. IV-B step 1).  A_must holds
+ * exactly the experts the rule makes mandatory.  The paper's steps leave one
+ * case undefined: when steps 1-4 leave A_trans empty (no mandatory expert and
+ * no candidate the expansion keeps), the final top-k of Sec. IV-C has nothing
+ * to choose from.  Only then are steps 2-4 run again with every token's own
+ * top expert (largest G, lower index on ties) added to A_must; stats[8]
+ * reports it.  desc.keep_top1 = 1 adds those experts in every call. */
 typedef enum caee_importance {
     /* I(e) = largest normalised gate weight any token of the batch gives e;
      * A_must = {e : I(e) >= tau}.  Sec. IV-B leaves I(e) open; with this
@@ -123,6 +128,8 @@ typedef struct caee_layer_desc {
     int32_t y_dtype;      /* output dtype: CAEE_F32 or CAEE_BF16 */
     int32_t refill;       /* a caee_refill_t; CAEE_REFILL_SCORE is the paper's method */
     uint32_t seed;        /* CAEE_REFILL_RANDOM: seed of the random keys; ignored otherwise */
+    int32_t keep_top1;    /* 0: A_must as Sec. IV-B step 1 defines it (the paper's method);
+                             1: each token's own top expert is also mandatory in every call */
 } caee_layer_desc_t;
 
 /* Storage order of the expert matrices. */
@@ -166,8 +173,9 @@ typedef struct caee_route_out {
     float* topk_w;       /* [T][k] routed_scaling * s_e / sum_{K_final} s; 0 in unused slots (required) */
     int32_t* orig_ids;   /* [T][k] K_t before pruning (optional, may be NULL) */
     uint32_t* masks;     /* [4][ceil(E/32)] bitmaps A_act, A_must, A_trans, pruned; bit e%32 of word e/32 (optional) */
-    int32_t* stats;      /* [8] |A_act|, |A_must|, |A_cand|, promoted, pruned, |A_trans|,
-                            refilled slots, empty slots (optional) */
+    int32_t* stats;      /* [9] |A_act|, |A_must|, |A_cand|, promoted, pruned, |A_trans|,
+                            refilled slots, empty slots, and 1 if A_trans came out empty and
+                            each token's top expert was made mandatory, else 0 (optional) */
     double* bin_loads;   /* [3][n_bins] per-bin summed cost of A_act, of A_must (max = F_base)
                             and of A_trans (optional) */
 } caee_route_out_t;
@@ -191,7 +199,9 @@ caee_status_t caee_route_prune(const caee_layer_desc_t* desc, const float* logit
  * equation): y_t = sum_j topk_w[t][j] * E_{topk_ids[t][j]}(x_t) + sum_s E^sh_s(x_t).
  *   x [T][d] (x_dtype); topk_ids/topk_w [T][k] as written by
  *   caee_route_prune (an id outside [0,E) marks an empty slot and its
- *   weight is ignored); y [T][d] (y_dtype), fully overwritten. */
+ *   weight is ignored; an expert named in several slots of one token adds
+ *   its output once per slot, with that slot's weight); y [T][d] (y_dtype),
+ *   fully overwritten. */
 caee_status_t caee_expert_ffn(const caee_layer_desc_t* desc, const void* x,
                               const int32_t* topk_ids, const float* topk_w,
                               const caee_expert_weights_t* weights, void* y,

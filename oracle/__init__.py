@@ -23,6 +23,8 @@ the paper (Cost-Aware Expert Execution, arxiv 2606.29982):
   offload.py       residency cost table and the LRU device cache (Sec. IV-A, V-B)
   calibration.py   the least-squares fit of the cost model's alpha and beta
                    (Sec. IV-A, offline calibration)
+  margins.py       the gap of every routing / pruning decision to its flip
+                   (near-ties between two correct implementations)
 
 Where the paper is silent or ambiguous the reading taken is stated in the
 docstring of the function that takes it.  Routing and pruning decisions are
@@ -37,3 +39,4 @@ from .ffn import (bf16_bits_to_f64, e4m3_decode, e4m3_encode_rne,  # noqa: F401
                   quantize_e4m3_blocks, swiglu_expert, expert_weights_f64)
 from .layer import moe_layer_ref  # noqa: F401
 from .calibration import fit_alpha_beta, fit_grouped, cost_of  # noqa: F401
+from .margins import decision_margins  # noqa: F401

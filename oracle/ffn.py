@@ -42,14 +42,14 @@ def _e4m3_table() -> np.ndarray:
 
 
 _E4M3_POS = _e4m3_table()
+# Every byte: codes 0..127 are the positive half (127 = NaN), bit 7 the sign.
+_E4M3_ALL = np.concatenate([_E4M3_POS, [np.nan], -_E4M3_POS, [np.nan]])
 
 
 def e4m3_decode(codes: np.ndarray) -> np.ndarray:
     """e4m3 codes (uint8) -> float64.  NaN codes decode to NaN."""
-    c = np.asarray(codes, dtype=np.uint8).astype(np.int64)
-    mag = c & 0x7F
-    out = np.where(mag == 127, np.nan, _E4M3_POS[np.minimum(mag, 126)])
-    return np.where(c & 0x80, -out, out)
+    c = np.ascontiguousarray(codes, dtype=np.uint8)
+    return _E4M3_ALL[c.ravel()].reshape(c.shape)
 
 
 def e4m3_encode_rne(v: np.ndarray) -> np.ndarray:
@@ -96,8 +96,10 @@ def expert_weights_f64(w13, w2, dtype: str, w13_scale=None, w2_scale=None, block
         for codes, sc in ((w13, w13_scale), (w2, w2_scale)):
             v = e4m3_decode(codes)
             r, c = v.shape
-            s = np.repeat(np.repeat(np.asarray(sc, np.float64), block, axis=0), block, axis=1)
-            out.append(v * s[:r, :c])
+            # element (i, j) times the scale of block (i // block, j // block)
+            sc = np.asarray(sc, np.float64)
+            blocks = v.reshape(r // block, block, c // block, block)
+            out.append((blocks * sc[:, None, :, None]).reshape(r, c))
         return out[0], out[1]
     raise ValueError(dtype)
 

@@ -25,7 +25,7 @@ def moe_layer_ref(*, E, n_group, topk_group, k, routed_scaling, tau, n_bins,
                   logits, bias=None, cost, bins=None,
                   x=None, x_dtype="f32", w_dtype="f32", n_shared=0,
                   get_expert=None, get_shared=None, tokens=None, rule="max", refill="score",
-                  seed=0) -> dict:
+                  seed=0, keep_top1=False) -> dict:
     """Run the layer.  Routing/pruning/compensation always run on the whole
     batch (pruning is a batch-level decision).  When ``x`` and the weight
     getters are given, the output rows y_t are computed for ``tokens``
@@ -37,14 +37,14 @@ def moe_layer_ref(*, E, n_group, topk_group, k, routed_scaling, tau, n_bins,
     logits = np.asarray(logits, np.float32)
     T = logits.shape[0]
     s, keys, orig_ids, g = route_batch(logits, bias, n_group, topk_group, k)
-    pr = prune_batch(orig_ids, g, E, tau, cost, bins, n_bins, rule=rule, s=s)
+    pr = prune_batch(orig_ids, g, E, tau, cost, bins, n_bins, rule=rule, s=s, keep_top1=keep_top1)
     ids, w, n_refill = compensate_batch(keys, s, orig_ids, pr["trans"], k, routed_scaling, refill, seed)
     out = dict(s=s, keys=keys, orig_ids=orig_ids, g=g, topk_ids=ids, topk_w=w, **pr)
     out["stats"] = dict(
         n_act=int(pr["act"].sum()), n_must=int(pr["must"].sum()),
         n_cand=int(pr["cand"].sum()), n_promoted=int(pr["promoted"].sum()),
         n_pruned=int(pr["pruned"].sum()), n_trans=int(pr["trans"].sum()),
-        n_refill=int(n_refill), n_pad=int((ids < 0).sum()))
+        n_refill=int(n_refill), n_pad=int((ids < 0).sum()), fallback=int(pr["fallback"]))
     if x is None or get_expert is None:
         return out
     tokens = list(range(T)) if tokens is None else list(tokens)

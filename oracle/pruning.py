@@ -28,8 +28,14 @@ Readings taken where the paper is silent or inconsistent:
   * the candidate set is the activated experts that are not mandatory (the
     text writes the complement in all experts, but the final set must lie in
     the activated set);
-  * every token's own top expert is mandatory, so no token loses all its
-    experts;
+  * step 1 is taken as written: A_must holds only the experts the rule makes
+    mandatory.  The one case the paper leaves undefined is an empty A_trans
+    (no mandatory expert and no candidate the expansion can keep for free):
+    the final top-k of Sec. IV-C would then have nothing to choose from.
+    Only then, steps 1-4 run again with every token's own top expert (largest
+    G, lower index on ties) made mandatory.  ``keep_top1=True`` makes those
+    top experts mandatory in every call (a stricter variant, not the paper's
+    step 1);
   * expansion visits candidates by importance, highest first, ties to the
     lower index, and keeps F_base fixed at its step-2 value while bin loads
     grow; "does not increase above F_base" is tested as load + cost <= F_base.
@@ -87,12 +93,12 @@ def cir_mandatory(orig_ids: np.ndarray, s: np.ndarray, theta_imp: float, E: int)
     return must
 
 
-def mandatory_split(act: np.ndarray, imp: np.ndarray, tau: float, top1, extra=None):
-    """Step 1: A_must = {e in A_act : I(e) >= tau} plus each token's top
-    expert (plus ``extra`` mandatory experts); A_cand = A_act minus A_must.
+def mandatory_split(act: np.ndarray, imp: np.ndarray, tau: float, forced=(), extra=None):
+    """Step 1: A_must = {e in A_act : I(e) >= tau}, plus the experts listed
+    in ``forced`` and the mask ``extra``; A_cand = A_act minus A_must.
     Pass tau = inf to skip the threshold."""
     must = act & (imp >= float(tau))
-    for e in top1:
+    for e in forced:
         must[e] = True
     if extra is not None:
         must |= extra
@@ -132,24 +138,33 @@ def cost_aware_greedy(must: np.ndarray, cand: np.ndarray, imp: np.ndarray,
 
 
 def prune_batch(orig_ids: np.ndarray, g: np.ndarray, E: int, tau: float,
-                cost: np.ndarray, bins, n_bins: int, rule: str = "max", s=None) -> dict:
+                cost: np.ndarray, bins, n_bins: int, rule: str = "max", s=None,
+                keep_top1: bool = False) -> dict:
     """Steps 1-4 for a routed batch under mandatory ``rule`` ("max", "sum"
     or "cir"; "cir" needs the router scores ``s`` [T][E]).  Returns every set
-    as a bool[E] mask plus the loads and F_base."""
+    as a bool[E] mask plus the loads, F_base and ``fallback`` (True when
+    A_trans came out empty and the steps were rerun with each token's top
+    expert mandatory)."""
     act, imp, top1 = importance_max(orig_ids, g, E)
     if rule == "max":
-        must, cand = mandatory_split(act, imp, tau, top1)
+        thr, extra = tau, None
     elif rule == "sum":
         imp = importance_sum(orig_ids, g, E)
-        must, cand = mandatory_split(act, imp, tau, top1)
+        thr, extra = tau, None
     elif rule == "cir":
-        must, cand = mandatory_split(act, imp, float("inf"), top1, cir_mandatory(orig_ids, s, tau, E))
+        thr, extra = float("inf"), cir_mandatory(orig_ids, s, tau, E)
     else:
         raise ValueError(rule)
+    must, cand = mandatory_split(act, imp, thr, top1 if keep_top1 else (), extra)
     trans, promoted, must_loads, final_loads, f_base, order = cost_aware_greedy(
         must, cand, imp, cost, bins, n_bins)
+    fallback = bool(act.any() and not trans.any())
+    if fallback:
+        must, cand = mandatory_split(act, imp, thr, top1, extra)
+        trans, promoted, must_loads, final_loads, f_base, order = cost_aware_greedy(
+            must, cand, imp, cost, bins, n_bins)
     return dict(act=act, imp=imp, top1=top1, must=must, cand=cand,
                 promoted=promoted, trans=trans, pruned=act & ~trans,
                 act_loads=bin_loads(act, cost, bins, n_bins),
                 must_loads=must_loads, trans_loads=final_loads,
-                f_base=f_base, cand_order=order)
+                f_base=f_base, cand_order=order, fallback=fallback)

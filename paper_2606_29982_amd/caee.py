@@ -35,7 +35,7 @@ class LayerDesc(ctypes.Structure):
         ("routed_scaling", ctypes.c_float), ("tau", ctypes.c_float),
         ("n_bins", ctypes.c_int32), ("importance", ctypes.c_int32),
         ("x_dtype", ctypes.c_int32), ("w_dtype", ctypes.c_int32), ("y_dtype", ctypes.c_int32),
-        ("refill", ctypes.c_int32), ("seed", ctypes.c_uint32)]
+        ("refill", ctypes.c_int32), ("seed", ctypes.c_uint32), ("keep_top1", ctypes.c_int32)]
 
 
 class ExpertWeights(ctypes.Structure):
@@ -45,6 +45,7 @@ class ExpertWeights(ctypes.Structure):
 
 
 LAYOUT_ROWMAJOR, LAYOUT_TILED = 0, 1
+STATS = 9   # entries of caee_route_out_t.stats
 
 
 class OffloadDesc(ctypes.Structure):
@@ -155,13 +156,14 @@ class Layer:
     importance: str = "max"     # "max" | "sum" | "cir" (caee_importance_t)
     refill: str = "score"       # "score" | "none" | "random" | "literal" (caee_refill_t)
     seed: int = 0               # random refill keys
+    keep_top1: bool = False     # each token's top expert mandatory in every call (not the paper's step 1)
 
     def desc(self) -> LayerDesc:
         return LayerDesc(self.T, self.d, self.f, self.E, self.n_group, self.topk_group, self.k,
                          self.n_shared, self.routed_scaling, self.tau, self.n_bins,
                          IMPORTANCE_CODE[self.importance],
                          DTYPE_CODE[self.x_dtype], DTYPE_CODE[self.w_dtype], DTYPE_CODE[self.y_dtype],
-                         REFILL_CODE[self.refill], self.seed & 0xFFFFFFFF)
+                         REFILL_CODE[self.refill], self.seed & 0xFFFFFFFF, 1 if self.keep_top1 else 0)
 
     @classmethod
     def from_shape(cls, shape, **over) -> "Layer":
@@ -273,7 +275,7 @@ def alloc_route_out(layer: Layer, device, full: bool = True) -> dict:
         words = (layer.E + 31) // 32
         out["orig_ids"] = torch.empty((T, k), dtype=torch.int32, device=device)
         out["masks"] = torch.empty((4, words), dtype=torch.int32, device=device)
-        out["stats"] = torch.empty(8, dtype=torch.int32, device=device)
+        out["stats"] = torch.empty(STATS, dtype=torch.int32, device=device)
         out["bin_loads"] = torch.empty((3, layer.n_bins), dtype=torch.float64, device=device)
     return out
 

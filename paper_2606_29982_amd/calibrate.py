@@ -147,7 +147,8 @@ def calibrate(device) -> dict:
     hbm = fit_grouped([s[0] for s in hs], [s[1] for s in hs], [s[2] for s in hs], HBM_GBPS)
     return {"hbm": hbm, "link": link,
             "samples": {"hbm": [(m, n, round(t, 2)) for m, n, t in hs],
-                        "link": [(n, round(t, 2)) for n, t in zip(ls, lt)]}}
+                        "link": [(n, round(t, 2)) for n, t in zip(ls, lt)]},
+            "raw": {"hbm": hs, "link": list(zip(ls, lt))}}
 
 
 def cost_table(model: CostModel, expert_bytes, E: int, resident=None) -> np.ndarray:

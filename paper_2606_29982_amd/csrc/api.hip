@@ -60,6 +60,8 @@ caee_status_t check_desc(const caee_layer_desc_t* d) {
     if (d->refill != CAEE_REFILL_SCORE && d->refill != CAEE_REFILL_NONE && d->refill != CAEE_REFILL_RANDOM &&
         d->refill != CAEE_REFILL_LITERAL)
         return fail(CAEE_ERR_INVALID_ARG, "unknown refill=%d", d->refill);
+    if (d->keep_top1 != 0 && d->keep_top1 != 1)
+        return fail(CAEE_ERR_INVALID_ARG, "keep_top1=%d must be 0 or 1", d->keep_top1);
     if (d->w_dtype != CAEE_F32 && d->w_dtype != CAEE_BF16 && d->w_dtype != CAEE_FP8_E4M3)
         return fail(CAEE_ERR_INVALID_ARG, "unknown w_dtype=%d", d->w_dtype);
     const int want_x = d->w_dtype == CAEE_F32 ? CAEE_F32 : CAEE_BF16;
@@ -188,6 +190,7 @@ RouteParams make_route_params(const caee_layer_desc_t* d, const float* logits, c
     p.rule = d->importance;
     p.refill = d->refill;
     p.seed = d->seed;
+    p.keep_top1 = d->keep_top1;
     p.counters = (int32_t*)(ws + L.counters);
     p.chunk_small = L.chunk_small;
     p.chunk_big = L.chunk_big;

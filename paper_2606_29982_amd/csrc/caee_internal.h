@@ -21,6 +21,7 @@ constexpr int kMaxBins = 256;
 constexpr int kMaxT = 65536;        // tokens per call
 constexpr int kMaskT = 1024;        // token block of the permutation (one LDS bitmask per expert)
 constexpr int kRouteThreads = 1024;
+constexpr int kStats = 9;          // entries of caee_route_out_t.stats
 // 16-token MFMA column blocks one FFN work item can hold (1, 2, 4 or 8).
 #ifndef CAEE_MAX_TOKEN_BLOCKS
 #define CAEE_MAX_TOKEN_BLOCKS 8
@@ -275,6 +276,7 @@ struct RouteParams {
     int rule;       // caee_importance_t
     int refill;     // caee_refill_t
     uint32_t seed;  // random refill keys
+    int keep_top1;  // each token's top expert mandatory in every call (else only when A_trans comes out empty)
     const float* logits;
     const float* bias;
     const float* cost;

@@ -248,9 +248,10 @@ __device__ void route_token(const RouteParams& p, int t, int lane, int* ids, dou
     double bg = mine ? g : -INFINITY;
     int best = mine ? my_id : kNoIdx;
     wave_argmax(bg, best);   // the token's top expert by G, ties to the lower index
-    // Pairs that are mandatory on their own: the token's top expert, plus
-    // the threshold (MAX) or the cumulative-ratio prefix (CIR).
-    uint32_t flags = (uint32_t)__ballot(mine && (my_id == best || (p.rule == CAEE_IMPORTANCE_MAX && g >= p.tau)));
+    // Pairs that are mandatory on their own: the threshold (MAX) or the
+    // cumulative-ratio prefix (CIR), and with keep_top1 the token's top expert.
+    uint32_t flags = (uint32_t)__ballot(
+        mine && ((p.keep_top1 && my_id == best) || (p.rule == CAEE_IMPORTANCE_MAX && g >= p.tau)));
     if (mine) {
         ids[lane] = my_id;
         gout[lane] = g;
@@ -501,7 +502,74 @@ struct PruneShared {
     double fbase;
     int ncand;
     int stat[5];            // step-4 counts: active, mandatory, promoted, pruned, kept
+    int fallback;           // A_trans came out empty: steps 2-3 rerun with each token's top expert mandatory
 };
+
+// Steps 2-3 of Sec. IV-B from the membership in sh.act / sh.must: per-bin
+// loads of A_act and A_must, F_base, the candidates (active, not mandatory)
+// in visiting order (importance descending, index ascending), and the
+// cost-invariant expansion into sh.prom, one bin per thread (bins are
+// independent).  Expects sh.prom, the loads and the candidate count zeroed.
+// Ends with a barrier.
+__device__ void prune_expand(const RouteParams& p, int tid, int nthr, PruneShared& sh) {
+    const int lane = tid & (kWave - 1);
+    const int wave = tid / kWave;
+    const int E = p.E, nb = p.n_bins;
+    for (int e = tid; e < E; e += nthr) {
+        const double c = (double)sh.cost[e];
+        const int b = sh.bin[e];
+        if (sh.act[e] && b >= 0) atomicAdd(&sh.aload[b], c);
+        if (sh.must[e] && b >= 0) atomicAdd(&sh.mload[b], c);
+        if (sh.act[e] && !sh.must[e]) {
+            const int i = atomicAdd(&sh.ncand, 1);
+            sh.cand[i] = e;
+            sh.cimp[i] = sh.imp[e];
+        }
+    }
+    __syncthreads();
+    const int n_cand = sh.ncand;
+    for (int i = tid; i < n_cand; i += nthr) {
+        const int e = sh.cand[i];
+        const unsigned long long ie = sh.cimp[i];
+        int rank = 0;
+        for (int j = 0; j < n_cand; ++j) {
+            const unsigned long long io = sh.cimp[j];
+            const int o = sh.cand[j];
+            rank += (io > ie || (io == ie && o < e)) ? 1 : 0;
+        }
+        sh.sorted[rank] = e;
+        sh.cbin[rank] = sh.bin[e];
+        sh.ccost[rank] = sh.cost[e];
+    }
+    __syncthreads();
+    if (wave == 0) {
+        double fb = 0.0;
+        for (int b = lane; b < nb; b += kWave) fb = fmax(fb, sh.mload[b]);
+        fb = wave_max_d(fb);
+        if (lane == 0) sh.fbase = fb;
+    }
+    for (int b = tid; b < nb && p.bin_loads; b += nthr) {
+        p.bin_loads[b] = sh.aload[b];
+        p.bin_loads[nb + b] = sh.mload[b];
+    }
+    __syncthreads();
+
+    // Step 3: expansion, walking the candidates in visiting order.
+    const double fbase = sh.fbase;
+    for (int b = tid; b < nb; b += nthr) {
+        double load = sh.mload[b];
+        for (int r = 0; r < n_cand; ++r) {
+            if (sh.cbin[r] != b) continue;
+            const double c = (double)sh.ccost[r];
+            if (load + c <= fbase) {
+                sh.prom[sh.sorted[r]] = 1;
+                load += c;
+            }
+        }
+        if (p.bin_loads) p.bin_loads[2 * nb + b] = load;
+    }
+    __syncthreads();
+}
 
 // Run by one workgroup of `nthr` threads (a multiple of the wave size).
 __device__ void prune_all(const RouteParams& p, int tid, int nthr, PruneShared& sh) {
@@ -509,13 +577,7 @@ __device__ void prune_all(const RouteParams& p, int tid, int nthr, PruneShared& 
     uint8_t *s_act = sh.act, *s_must = sh.must, *s_prom = sh.prom;
     float* s_cost = sh.cost;
     int* s_bin = sh.bin;
-    int* s_sorted = sh.sorted;
-    int* s_cand = sh.cand;
-    unsigned long long* s_cimp = sh.cimp;
-    int* s_cbin = sh.cbin;
-    float* s_ccost = sh.ccost;
     double *s_aload = sh.aload, *s_mload = sh.mload;
-    double& s_fbase = sh.fbase;
     int& s_ncand = sh.ncand;
     const int lane = tid & (kWave - 1);
     const int wave = tid / kWave;
@@ -529,7 +591,10 @@ __device__ void prune_all(const RouteParams& p, int tid, int nthr, PruneShared& 
         s_bin[e] = (b >= 0 && b < nb) ? b : -1;   // out-of-range bins (a precondition violation) count nowhere
     }
     for (int b = tid; b < nb; b += nthr) s_aload[b] = s_mload[b] = 0.0;
-    if (tid == 0) s_ncand = 0;
+    if (tid == 0) {
+        s_ncand = 0;
+        sh.fallback = 0;
+    }
     if (tid < 5) sh.stat[tid] = 0;
     __syncthreads();
 
@@ -568,67 +633,24 @@ __device__ void prune_all(const RouteParams& p, int tid, int nthr, PruneShared& 
         __syncthreads();
     }
 
-    // Step 2: per-bin loads of A_act and A_must; the candidates (active, not
-    // mandatory) gathered in any order, then each placed at its rank in the
-    // visiting order (importance descending, index ascending).
-    for (int e = tid; e < E; e += nthr) {
-        const double c = (double)s_cost[e];
-        const int b = s_bin[e];
-        if (s_act[e] && b >= 0) atomicAdd(&s_aload[b], c);
-        if (s_must[e] && b >= 0) atomicAdd(&s_mload[b], c);
-        if (s_act[e] && !s_must[e]) {
-            const int i = atomicAdd(&s_ncand, 1);
-            s_cand[i] = e;
-            s_cimp[i] = s_imp[e];
+    prune_expand(p, tid, nthr, sh);
+    // A_trans = A_must + promoted is empty only when no thread sees a member.
+    // Then Sec. IV-C's final top-k would have nothing to choose from: steps
+    // 2-3 run again with every token's own top expert mandatory (the only
+    // departure from step 1 as written).
+    bool member = false;
+    for (int e = tid; e < E; e += nthr) member |= (s_must[e] | s_prom[e]) != 0;
+    if (!__syncthreads_or(member)) {   // (nothing was promoted either: s_prom stays zero)
+        for (int t = tid; t < T; t += nthr) s_must[p.top1[t]] = 1;
+        for (int b = tid; b < nb; b += nthr) s_aload[b] = s_mload[b] = 0.0;
+        if (tid == 0) {
+            s_ncand = 0;
+            sh.fallback = 1;
         }
+        __syncthreads();
+        prune_expand(p, tid, nthr, sh);
     }
-    __syncthreads();
-    {
-        const int n_cand = s_ncand;
-        for (int i = tid; i < n_cand; i += nthr) {
-            const int e = s_cand[i];
-            const unsigned long long ie = s_cimp[i];
-            int rank = 0;
-            for (int j = 0; j < n_cand; ++j) {
-                const unsigned long long io = s_cimp[j];
-                const int o = s_cand[j];
-                rank += (io > ie || (io == ie && o < e)) ? 1 : 0;
-            }
-            s_sorted[rank] = e;
-            s_cbin[rank] = s_bin[e];
-            s_ccost[rank] = s_cost[e];
-        }
-    }
-    __syncthreads();
-    if (wave == 0) {
-        double fb = 0.0;
-        for (int b = lane; b < nb; b += kWave) fb = fmax(fb, s_mload[b]);
-        fb = wave_max_d(fb);
-        if (lane == 0) s_fbase = fb;
-    }
-    for (int b = tid; b < nb && p.bin_loads; b += nthr) {
-        p.bin_loads[b] = s_aload[b];
-        p.bin_loads[nb + b] = s_mload[b];
-    }
-    __syncthreads();
-
-    // Step 3: cost-invariant expansion, one bin per thread (bins are
-    // independent), walking the candidates in visiting order.
     const int n_cand = s_ncand;
-    const double fbase = s_fbase;
-    for (int b = tid; b < nb; b += nthr) {
-        double load = s_mload[b];
-        for (int r = 0; r < n_cand; ++r) {
-            if (s_cbin[r] != b) continue;
-            const double c = (double)s_ccost[r];
-            if (load + c <= fbase) {
-                s_prom[s_sorted[r]] = 1;
-                load += c;
-            }
-        }
-        if (p.bin_loads) p.bin_loads[2 * nb + b] = load;
-    }
-    __syncthreads();
 
     // Step 4: A_trans = A_must + promoted; masks and counters by ballot,
     // one 64-expert block per wave, counts added in LDS.
@@ -667,6 +689,7 @@ __device__ void prune_all(const RouteParams& p, int tid, int nthr, PruneShared& 
         p.stats[3] = sh.stat[2];   // promoted
         p.stats[4] = sh.stat[3];   // pruned
         p.stats[5] = sh.stat[4];   // |A_trans|
+        p.stats[8] = sh.fallback;
     }
 }
 
@@ -764,9 +787,11 @@ __device__ void build_lists(const RouteParams& p, const int* s_cnt, int* s_off, 
 }
 
 // Token-block bitmasks: bit (t - t0) of word (x, (t - t0) / 64) is set when
-// token t of [t0, t0 + tn) chose routed expert x.  W words per expert.
-__device__ void fill_masks(const RouteParams& p, int t0, int tn, int W, int tid, int nthr,
-                           unsigned long long* s_mask, int* s_pre) {
+// token t of [t0, t0 + tn) chose routed expert x.  W words per expert.  An
+// expert named twice in one token's list sets one bit: it gets one row, which
+// both slots read.
+__device__ void token_masks(const RouteParams& p, int t0, int tn, int W, int tid, int nthr,
+                            unsigned long long* s_mask) {
     const int E = p.E, k = p.k;
     for (int i = tid; i < E * W; i += nthr) s_mask[i] = 0ull;
     __syncthreads();
@@ -778,6 +803,13 @@ __device__ void fill_masks(const RouteParams& p, int t0, int tn, int W, int tid,
         }
     }
     __syncthreads();
+}
+
+// The bitmasks, and per word the number of set bits in the words before it.
+__device__ void fill_masks(const RouteParams& p, int t0, int tn, int W, int tid, int nthr,
+                           unsigned long long* s_mask, int* s_pre) {
+    const int E = p.E;
+    token_masks(p, t0, tn, W, tid, nthr, s_mask);
     // s_pre[e*W + w]: tokens of words 0..w-1 that chose expert e.
     for (int i = tid; i < E * W; i += nthr) {
         const int w = i % W;
@@ -867,18 +899,19 @@ __global__ __launch_bounds__(kRouteThreads) void k_permute(RouteParams p) {
 
 // Larger batches: the tokens are cut into blocks of kMaskT.
 // (1) per block, each routed expert's token count;
+// counted from the same bitmasks (k_permute_place) as the rows are placed,
+// so a repeated expert in one token's list counts once;
 __global__ __launch_bounds__(kRouteThreads) void k_permute_count(RouteParams p) {
-    __shared__ int s_c[kMaxE];
+    __shared__ unsigned long long s_mask[kMaxE * (kMaskT / 64)];
     const int tid = threadIdx.x, b = blockIdx.x;
     const int t0 = b * kMaskT, tn = min(kMaskT, p.T - t0);
-    for (int e = tid; e < p.E; e += kRouteThreads) s_c[e] = 0;
-    __syncthreads();
-    for (int i = tid; i < tn * p.k; i += kRouteThreads) {
-        const int e = p.topk_ids[(size_t)t0 * p.k + i];
-        if (e >= 0 && e < p.E) atomicAdd(&s_c[e], 1);
+    const int W = (tn + 63) / 64;
+    token_masks(p, t0, tn, W, tid, kRouteThreads, s_mask);
+    for (int e = tid; e < p.E; e += kRouteThreads) {
+        int c = 0;
+        for (int w = 0; w < W; ++w) c += __popcll(s_mask[e * W + w]);
+        p.perm_blk[(size_t)b * p.E + e] = c;
     }
-    __syncthreads();
-    for (int e = tid; e < p.E; e += kRouteThreads) p.perm_blk[(size_t)b * p.E + e] = s_c[e];
 }
 
 // (2) one workgroup: slot totals, offsets and work lists, each block's first
@@ -987,7 +1020,7 @@ __device__ void route_fused_body(const RouteParams& p) {
     __shared__ int32_t l_bin[kMaxE];
     __shared__ uint8_t l_mflag[kFusedT * kMaxK], l_trans[kMaxE];
     __shared__ uint32_t l_masks[4 * (kMaxE / 32)];
-    __shared__ int32_t l_stats[8];
+    __shared__ int32_t l_stats[kStats];
     __shared__ double l_bl[3 * kMaxE];
     __shared__ double l_s[kFusedT * kMaxK];
     const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
@@ -1048,7 +1081,7 @@ __device__ void route_fused_body(const RouteParams& p) {
     const int words = (E + 31) / 32;
     if (p.masks)
         for (int i = tid; i < 4 * words; i += kRouteThreads) p.masks[i] = l_masks[i];
-    if (p.stats && tid < 8) p.stats[tid] = l_stats[tid];
+    if (p.stats && tid < kStats) p.stats[tid] = l_stats[tid];
     if (q.bin_loads == l_bl)
         for (int i = tid; i < 3 * p.n_bins; i += kRouteThreads) p.bin_loads[i] = l_bl[i];
 }

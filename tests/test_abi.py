@@ -26,7 +26,7 @@ def test_exports_every_declared_symbol():
     for n in names:
         assert hasattr(lib, n), n
     assert set(names) == set(caee.EXPORTED)
-    assert caee.abi_version() == 7
+    assert caee.abi_version() == 8
 
 
 def _layer(**kw):
@@ -69,6 +69,15 @@ def test_descriptor_validation(kw, status):
     assert st == status, caee.lib.caee_last_error().decode()
     if st != caee.CAEE_OK:
         assert caee.lib.caee_last_error().decode()
+
+
+def test_keep_top1_must_be_a_flag():
+    d = _layer().desc()
+    n = ctypes.c_size_t(0)
+    for v, status in ((0, caee.CAEE_OK), (1, caee.CAEE_OK), (2, caee.CAEE_ERR_INVALID_ARG),
+                      (-1, caee.CAEE_ERR_INVALID_ARG)):
+        d.keep_top1 = v
+        assert caee.lib.caee_workspace_size(ctypes.byref(d), ctypes.byref(n)) == status
 
 
 def test_workspace_size_monotone_in_T():

@@ -1,7 +1,12 @@
-"""Offline cost calibration on the device: both data paths measured, and
-the fitted cost model explains the measurements."""
+"""Offline cost calibration on the device: both data paths measured, the
+fitted cost model explains the measurements, and the fit and the cost table
+it emits equal the oracle's (closed-form and normal-equation least squares
+of Sec. IV-A's cost model) on the same measured samples."""
+import numpy as np
 import pytest
 import torch
+
+import oracle
 
 from paper_2606_29982_amd import calibrate as cal
 
@@ -18,3 +23,19 @@ def test_calibration_on_device():
     assert 1.0 <= link.alpha < 3.0 and link.r2 > 0.98
     # a whole R1 expert (88 MB) costs far more over the host link than from HBM
     assert link.cost_us(88080384) > 20 * hbm.cost_us(88080384)
+
+    # the library's fit against the oracle's on the same (unrounded) samples
+    ls = [n for n, _ in res["raw"]["link"]]
+    lt = [t for _, t in res["raw"]["link"]]
+    a, b = oracle.fit_alpha_beta(ls, lt, cal.LINK_GBPS * 1e3)
+    np.testing.assert_allclose([link.alpha, link.beta], [a, b], rtol=1e-9, atol=1e-9)
+    hs = res["raw"]["hbm"]
+    a2, b2, c0 = oracle.fit_grouped([s[0] for s in hs], [s[1] for s in hs], [s[2] for s in hs], cal.HBM_GBPS * 1e3)
+    np.testing.assert_allclose([hbm.alpha, hbm.beta, hbm.c0_us], [a2, b2, c0], rtol=1e-9, atol=1e-9)
+    # the offloading cost table: the calibrated miss cost for every expert not
+    # resident, 0 for the resident ones (Sec. IV-A residency factor)
+    resident = np.zeros(256, bool)
+    resident[::5] = True
+    table = cal.cost_table(link, 88080384, 256, resident)
+    want = np.where(resident, 0.0, oracle.cost_of([88080384], a, b, cal.LINK_GBPS * 1e3)[0]).astype(np.float32)
+    np.testing.assert_array_equal(table, want)

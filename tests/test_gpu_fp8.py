@@ -91,9 +91,10 @@ def r1_fp8():
     torch.cuda.empty_cache()
 
 
-@pytest.mark.parametrize("T,tokens,rule,tau", [(64, [0, 31, 63], "max", 0.05), (64, [5, 60], "sum", 1.2),
-                                               (1, [0], "max", 0.0)])
+@pytest.mark.parametrize("T,tokens,rule,tau", [(64, None, "max", 0.05), (64, [5, 60], "sum", 1.2),
+                                               (1, None, "max", 0.0)])
 def test_r1_fp8_decode(T, tokens, rule, tau, r1_fp8):
+    # tokens None: every token of the batch
     W, Wt = r1_fp8
     inp = make_routing_inputs(R1_FP8, seed=3, T=T, zipf_logit_s=1.1, cost_kind="zipf", n_bins=8)
     print(f"fp8 R1 T={T} rule={rule} tau={tau}", flush=True)
@@ -101,17 +102,50 @@ def test_r1_fp8_decode(T, tokens, rule, tau, r1_fp8):
     get, get_sh = getters_dev(W, "fp8")
     ref = oracle_layer(R1_FP8, inp, tau, 8, get, get_sh, tokens=tokens, rule=rule)
     check_route(got, ref, R1_FP8.E)
-    rel = check_y(got["y"][tokens], ref["y"], 6e-2)
-    print(f"  max|err|/max|ref| = {rel:.3e}", flush=True)
+    toks = list(range(T)) if tokens is None else tokens
+    rel = check_y(got["y"][toks], ref["y"], 6e-2)
+    print(f"  {len(toks)} tokens: max|err|/max|ref| = {rel:.3e}", flush=True)
+
+
+def prefill_subset(topk_ids, T, n_shared, n=256, chunk=128, seed=0):
+    """A fixed subset of ``n`` tokens of a prefill batch that covers the
+    edges of the FFN's work items: an expert slot with r rows is cut into
+    ceil(r / chunk) near-equal pieces of consecutive rows (tokens in
+    ascending order), so the first and last token of every piece of the
+    shared experts (which hold every token) and of every routed expert cut
+    into two or three pieces are included; the rest is drawn at random."""
+    pick = set()
+    def edges(rows):
+        r = len(rows)
+        pieces = -(-r // chunk)
+        size = -(-r // pieces)
+        for c in range(pieces):
+            pick.add(int(rows[c * size]))
+            pick.add(int(rows[min(r, (c + 1) * size) - 1]))
+    if n_shared:
+        edges(np.arange(T))
+    multi = []
+    for e in range(int(topk_ids.max()) + 1):
+        rows = np.flatnonzero((topk_ids == e).any(axis=1))
+        if chunk < len(rows) <= 3 * chunk:
+            multi.append((e, rows))
+    for e, rows in multi[:24]:
+        edges(rows)
+    rng = np.random.default_rng(seed)
+    rest = [t for t in rng.permutation(T).tolist() if t not in pick]
+    out = sorted(pick) + rest[:max(0, n - len(pick))]
+    return sorted(out)[:max(n, len(pick))], len(multi)
 
 
 def test_r1_fp8_prefill(r1_fp8):
     W, Wt = r1_fp8
     T = 4096
     inp = make_routing_inputs(R1_FP8, seed=4, T=T, cost_kind="zipf", n_bins=8)
-    tokens = [0, 1234, 4095]
     print("fp8 R1 prefill T=4096", flush=True)
     got = gpu_layer(R1_FP8, inp, 0.05, 8, Wt, DEV)
+    tokens, n_multi = prefill_subset(got["topk_ids"], T, R1_FP8.n_shared)
+    assert n_multi >= 2, "the batch has fewer than two experts cut into two or three pieces"
+    print(f"  {len(tokens)} tokens ({n_multi} routed experts of two or three pieces)", flush=True)
     get, get_sh = getters_dev(W, "fp8")
     ref = oracle_layer(R1_FP8, inp, 0.05, 8, get, get_sh, tokens=tokens)
     check_route(got, ref, R1_FP8.E)

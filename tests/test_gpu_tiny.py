@@ -18,20 +18,21 @@ TOL = {"f32": 1e-5, "bf16": 2e-2}
 
 
 def _run(shape, seed=0, tau=0.1, n_bins=4, T=None, zipf=None, cost_kind="uniform", mutate=None, rule="max",
-         tiled=False, refill="score", rseed=0):
+         tiled=False, refill="score", rseed=0, keep_top1=False):
     inp = make_routing_inputs(shape, seed=seed, T=T, zipf_logit_s=zipf, cost_kind=cost_kind,
                               n_bins=n_bins)
     if mutate:
         mutate(inp)
     W = make_expert_weights_np(shape, seed=seed)
     print(f"case {shape.name} seed={seed} tau={tau} n_bins={n_bins} T={inp.logits.shape[0]} rule={rule} "
-          f"refill={refill}", flush=True)
+          f"refill={refill} keep_top1={keep_top1}", flush=True)
     Wd = w_to_dev(W, DEV)
     if tiled:
         Wd = caee.pack_weights(Wd, shape.w_dtype)
-    got = gpu_layer(shape, inp, tau, n_bins, Wd, DEV, rule=rule, refill=refill, seed=rseed)
+    got = gpu_layer(shape, inp, tau, n_bins, Wd, DEV, rule=rule, refill=refill, seed=rseed, keep_top1=keep_top1)
     get, get_sh = getters_np(W, shape.w_dtype)
-    ref = oracle_layer(shape, inp, tau, n_bins, get, get_sh, rule=rule, refill=refill, seed=rseed)
+    ref = oracle_layer(shape, inp, tau, n_bins, get, get_sh, rule=rule, refill=refill, seed=rseed,
+                       keep_top1=keep_top1)
     check_route(got, ref, shape.E)
     check_y(got["y"], ref["y"], TOL[shape.w_dtype])
     return got, ref
@@ -70,33 +71,30 @@ def test_equal_logits_and_resident_experts():
     # every token's top expert (lowest index), 1..3 share its bin and are pruned
     assert ref["orig_ids"][0].tolist() == [0, 1, 2, 3]
     assert ref["topk_ids"][0].tolist() == [0, -1, -1, -1]
+    # (no weight reaches tau and every cost is positive: A_trans would be
+    # empty, so expert 0, every token's top expert, was made mandatory)
+    assert ref["stats"]["fallback"] == 1 and got["stats"][8] == 1
     got, ref = _run(TINY_F32, seed=1, tau=0.3, n_bins=4, cost_kind="zero")
     assert not ref["pruned"].any()
 
 
 def test_threshold_above_every_weight():
-    # only each token's top expert is mandatory; freed slots refill from A_trans
+    # no expert is mandatory and every cost is positive: A_trans would be
+    # empty, so each token's top expert is made mandatory; freed slots refill
+    # from A_trans
     got, ref = _run(TINY_F32, seed=2, tau=0.9, n_bins=1, T=3)
-    assert ref["stats"]["n_pad"] > 0
+    assert ref["stats"]["n_pad"] > 0 and ref["stats"]["fallback"] == 1
 
 
-@pytest.mark.parametrize("E,G,tg,k", [(64, 8, 4, 6), (128, 8, 2, 8), (256, 8, 4, 8), (32, 1, 1, 16)])
-def test_expert_counts_and_lane_layouts(E, G, tg, k):
-    shape = TINY_F32.with_(E=E, n_group=G, topk_group=tg, k=k, d=128, f=128, T=24)
-    _run(shape, seed=E, tau=0.05, n_bins=4)
-
-
-@pytest.mark.parametrize("shape", [TINY_F32, TINY_BF16], ids=["f32", "bf16"])
-@pytest.mark.parametrize("T", [1, 7, 16, 40])
-def test_two_shared_experts(shape, T):
-    # up to 16 tokens the routing launch runs the shared experts' gate/up
-    # (rows s*T + t of shared expert s); 40 tokens take the FFN launches
-    _run(shape.with_(n_shared=2), seed=30 + T, tau=0.2, n_bins=4, T=T, tiled=T % 2 == 0)
-
-
-def test_no_shared_expert_and_k1():
-    _run(TINY_F32.with_(n_shared=0), seed=5, tau=0.1, n_bins=4)
-    _run(TINY_F32.with_(k=1, topk_group=1), seed=6, tau=0.1, n_bins=2)
+@pytest.mark.parametrize("keep_top1", [False, True])
+@pytest.mark.parametrize("T", [1, 5, 16, 40, 300])
+@pytest.mark.parametrize("rule,tau", [("sum", 1.2), ("sum", 2.5), ("max", 0.3)])
+def test_step1_literal_and_keep_top1(keep_top1, T, rule, tau):
+    # Sec. IV-B step 1 as written (default) and the variant that also keeps
+    # every token's top expert, through the single-workgroup (T <= 16) and
+    # the multi-kernel routing paths; Zipf costs on 4 bins
+    _run(TINY_F32, seed=60 + T, tau=tau, n_bins=4, T=T, zipf=1.1, cost_kind="zipf", rule=rule,
+         keep_top1=keep_top1)
 
 
 def test_expert_ffn_with_given_ids_and_empty_slots():
@@ -127,6 +125,44 @@ def test_expert_ffn_with_given_ids_and_empty_slots():
     w13, w2 = get_sh(0)
     ref += swiglu_expert(x, w13, w2)
     check_y(y.cpu().numpy().astype(np.float64), ref, 1e-5)
+
+
+@pytest.mark.parametrize("T", [40, 1100])
+def test_expert_ffn_repeated_ids(T):
+    # caller-given ids may name one expert twice in a token's list: each
+    # occurrence adds its own weight.  40 tokens take the single-workgroup
+    # permutation, 1100 the per-1024-token-block one.
+    shape = TINY_F32.with_(T=T)
+    inp = make_routing_inputs(shape, seed=12)
+    W = make_expert_weights_np(shape, seed=12)
+    rng = np.random.default_rng(12)
+    ids = np.stack([rng.choice(shape.E, shape.k, replace=False) for _ in range(T)]).astype(np.int32)
+    rep = rng.random(T) < 0.3
+    ids[rep, 1] = ids[rep, 0]                     # a repeated expert
+    ids[rng.random(T) < 0.1, 2] = -1              # some empty slots
+    w = rng.random((T, shape.k)).astype(np.float32)
+    layer = caee.Layer.from_shape(shape)
+    ws = caee.alloc_workspace(layer, DEV)
+    yfull = torch.full((T + 2, shape.d), 7.0, dtype=torch.float32, device=DEV)
+    print(f"expert_ffn repeated ids T={T}", flush=True)
+    caee.expert_ffn(layer, to_dev(inp.x, DEV), to_dev(ids, DEV), to_dev(w, DEV), w_to_dev(W, DEV),
+                    yfull[1:T + 1], ws)
+    torch.cuda.synchronize()
+    assert torch.all(yfull[0] == 7.0) and torch.all(yfull[T + 1] == 7.0), "write outside y"
+    get, get_sh = getters_np(W, "f32")
+    from oracle import swiglu_expert
+    x = inp.x.astype(np.float64)
+    ref = np.zeros((T, shape.d))
+    for e in range(shape.E):
+        rows, cols = np.nonzero(ids == e)
+        if rows.size:
+            w13, w2 = get(e)
+            ye = swiglu_expert(x[rows], w13, w2)
+            for r, c, v in zip(rows, cols, ye):
+                ref[r] += float(w[r, c]) * v
+    w13, w2 = get_sh(0)
+    ref += swiglu_expert(x, w13, w2)
+    check_y(yfull[1:T + 1].cpu().numpy().astype(np.float64), ref, 1e-5)
 
 
 def test_expert_ffn_without_rows_writes_zeros():

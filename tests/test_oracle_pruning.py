@@ -113,14 +113,77 @@ def test_special_cases():
         assert np.array_equal(sc["trans"], base["trans"])
 
 
-def test_top1_always_kept():
+def test_empty_trans_fallback():
+    # tau above any gate weight: A_must is empty; with every cost positive the
+    # expansion keeps nothing, so A_trans would be empty and the steps rerun
+    # with each token's top expert mandatory
     rng = np.random.default_rng(8)
     E = 16
     s, keys, ids, g = _random_batch(rng, 6, E, 4, 2, 4)
-    pr = prune_batch(ids, g, E, 2.0, np.ones(E, np.float32), None, 1)   # tau above any weight
+    pr = prune_batch(ids, g, E, 2.0, np.ones(E, np.float32), None, 1)
+    assert pr["fallback"]
     for t in range(6):
         assert pr["trans"][ids[t][int(np.argmax(g[t]))]]
     assert np.array_equal(pr["must"], _mask(E, pr["top1"]))
+    # one free (zero-cost) activated expert: A_trans = {it}, no fallback
+    c = np.ones(E, np.float32)
+    free = int(ids[3][2])
+    c[free] = 0.0
+    pr = prune_batch(ids, g, E, 2.0, c, None, 1)
+    assert not pr["fallback"] and not pr["must"].any()
+    assert np.flatnonzero(pr["trans"]).tolist() == [free]
+
+
+def test_step1_literal_vs_keep_top1(golden):
+    # Sec. IV-B step 1 as written against the stricter variant that also
+    # keeps each token's top expert, on a hand example where they differ
+    g_ = golden("mandatory_step1_hand_example.json")
+    E = g_["E"]
+    ids = np.array(g_["orig_ids"])
+    g = np.array(g_["g"])
+    bins = np.array(g_["bins"], dtype=np.int32)
+    for key, keep in (("literal", False), ("keep_top1", True)):
+        want = g_[key]
+        pr = prune_batch(ids, g, E, g_["theta"], np.array(g_["cost"], np.float32), bins, g_["n_bins"],
+                         rule="sum", keep_top1=keep)
+        assert pr["imp"].tolist() == g_["expected_importance"]
+        assert np.flatnonzero(pr["must"]).tolist() == want["must"], want["note"]
+        assert pr["must_loads"].tolist() == want["must_loads"]
+        assert pr["f_base"] == want["f_base"]
+        assert pr["cand_order"] == want["cand_order"]
+        assert np.flatnonzero(pr["promoted"]).tolist() == want["promoted"]
+        assert np.flatnonzero(pr["trans"]).tolist() == want["trans"]
+        assert np.flatnonzero(pr["pruned"]).tolist() == want["pruned"]
+        assert pr["trans_loads"].tolist() == want["trans_loads"]
+        assert pr["fallback"] == want["fallback"]
+    for case in g_["empty_cases"]:
+        pr = prune_batch(ids, g, E, case["theta"], np.array(case["cost"], np.float32), bins, g_["n_bins"],
+                         rule="sum")
+        assert np.flatnonzero(pr["must"]).tolist() == case["must"], case["note"]
+        assert np.flatnonzero(pr["trans"]).tolist() == case["trans"], case["note"]
+        assert np.flatnonzero(pr["pruned"]).tolist() == case["pruned"], case["note"]
+        assert pr["fallback"] == case["fallback"], case["note"]
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_keep_top1_contains_literal(seed):
+    # the variant only adds mandatory experts: its A_must holds the literal
+    # one and every token's top expert, and it prunes a subset of what the
+    # literal set prunes whenever both keep at least one expert
+    rng = np.random.default_rng(50 + seed)
+    E = 16
+    s, keys, ids, g = _random_batch(rng, 8, E, 4, 2, 4)
+    cost = rng.uniform(1, 4, E).astype(np.float32)
+    bins = (np.arange(E) // 4).astype(np.int32)
+    for rule, th in (("max", 0.3), ("sum", 0.6), ("sum", 1.5)):
+        lit = prune_batch(ids, g, E, th, cost, bins, 4, rule=rule)
+        top = prune_batch(ids, g, E, th, cost, bins, 4, rule=rule, keep_top1=True)
+        assert not top["fallback"]
+        assert np.all(top["must"] >= _mask(E, top["top1"]))
+        if not lit["fallback"]:
+            assert np.all(top["must"] >= lit["must"])
+        else:
+            assert np.array_equal(lit["must"], top["must"]) and np.array_equal(lit["trans"], top["trans"])
 
 
 def test_loads_exact_under_dynamic_range():
@@ -180,14 +243,40 @@ def test_importance_rule_invariants(seed):
     assert np.array_equal(full["must"], full["act"]) and not full["pruned"].any()
     tiny = prune_batch(ids, g, E, 1e-9, cost, bins, 4, rule="cir", s=s)
     assert np.array_equal(tiny["must"], np.isin(np.arange(E), tiny["top1"]))
-    # SUM with a threshold above the batch total keeps only the top experts
+    # SUM with a threshold above the batch total: A_must empty, every cost
+    # positive, so A_trans would be empty and the fallback keeps the top experts
     top = prune_batch(ids, g, E, T + 1.0, cost, bins, 4, rule="sum")
+    assert top["fallback"]
     assert np.array_equal(top["must"], np.isin(np.arange(E), top["top1"]))
-    # larger thresholds never grow the mandatory set
+    # larger thresholds never grow the step-1 set (SUM) and larger ratios
+    # never shrink it (CIR), among calls that need no fallback
     for rule in ("sum", "cir"):
         prev = None
         for th in ((0.2, 0.5, 1.0, 2.0) if rule == "sum" else (0.3, 0.6, 0.9)):
-            m = prune_batch(ids, g, E, th, cost, bins, 4, rule=rule, s=s)["must"]
+            pr = prune_batch(ids, g, E, th, cost, bins, 4, rule=rule, s=s)
+            if pr["fallback"]:
+                continue
+            m = pr["must"]
             if prev is not None:
                 assert np.all(m <= prev) if rule == "sum" else np.all(prev <= m)
             prev = m
+
+
+def test_step1_readings_differ_on_tiny_layers():
+    # the GPU parity cases of both readings (tiny layer, Zipf costs on 4 bins)
+    # include calls where the two prune different sets and calls that need
+    # the fallback
+    from oracle import moe_layer_ref
+    from synth_inputs import TINY_F32, make_routing_inputs
+    sh = TINY_F32
+    differ = fallback = 0
+    for T in (1, 5, 16, 40, 300):
+        for rule, tau in (("sum", 1.2), ("sum", 2.5), ("max", 0.3)):
+            inp = make_routing_inputs(sh, seed=60 + T, T=T, zipf_logit_s=1.1, cost_kind="zipf", n_bins=4)
+            kw = dict(E=sh.E, n_group=sh.n_group, topk_group=sh.topk_group, k=sh.k, routed_scaling=1.0,
+                      tau=tau, n_bins=4, logits=inp.logits, cost=inp.cost, bins=inp.bins, rule=rule)
+            a = moe_layer_ref(**kw)
+            b = moe_layer_ref(**kw, keep_top1=True)
+            differ += int(not np.array_equal(a["trans"], b["trans"]))
+            fallback += a["stats"]["fallback"]
+    assert differ > 0 and fallback > 0
