@@ -216,6 +216,30 @@ caee_status_t caee_moe_layer(const caee_layer_desc_t* desc, const void* x,
                              void* y, const caee_route_out_t* out, void* ws,
                              size_t ws_bytes, void* stream);
 
+/* Bytes of the library's own scratch array (per GPU) behind
+ * caee_moe_layer_noalloc: enough for a DeepSeek-R1-shaped layer (d 7168,
+ * f 2048, 256 experts, top-8, one shared expert) up to 128 tokens. */
+#define CAEE_SCRATCH_BYTES (48u << 20)
+
+/* caee_moe_layer without a caller workspace, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc).  Same arguments, results and
+ * kernels as caee_moe_layer, minus ws/ws_bytes: the scratch space is a
+ * file-scope device array of CAEE_SCRATCH_BYTES in the library, one per GPU,
+ * whose address is looked up once per device on the first call there (with
+ * that device current) and held until the process ends.  All kernels run on
+ * `stream` (no second stream is created).  The call allocates nothing and
+ * needs nothing in the array cleared: every byte the kernels read is written
+ * earlier in the same call.
+ * Returns CAEE_ERR_UNSUPPORTED, launching nothing, when the call needs more
+ * than CAEE_SCRATCH_BYTES (caee_workspace_size tells).  Every call on one GPU
+ * uses the same array: calls that overlap on one GPU (different streams or
+ * threads without ordering between them) race and give undefined results. */
+caee_status_t caee_moe_layer_noalloc(const caee_layer_desc_t* desc, const void* x,
+                                     const float* logits, const float* bias, const float* cost,
+                                     const int32_t* bin, const caee_expert_weights_t* weights,
+                                     void* y, const caee_route_out_t* out, void* stream);
+
 /* Repack `count` consecutive row-major matrices [rows][cols] of dtype
  * `w_dtype` from `src` into CAEE_LAYOUT_TILED order at `dst` (same size,
  * must not overlap).  rows must be a multiple of 16 and a row a multiple of

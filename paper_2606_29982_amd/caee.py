@@ -85,6 +85,8 @@ def _load(path: str = LIB_PATH):
         "caee_expert_ffn": (st, [desc_p, P, P, P, ctypes.POINTER(ExpertWeights), P, P, ctypes.c_size_t, P]),
         "caee_moe_layer": (st, [desc_p, P, P, P, P, P, ctypes.POINTER(ExpertWeights), P,
                                 ctypes.POINTER(RouteOut), P, ctypes.c_size_t, P]),
+        "caee_moe_layer_noalloc": (st, [desc_p, P, P, P, P, P, ctypes.POINTER(ExpertWeights), P,
+                                        ctypes.POINTER(RouteOut), P]),
         "caee_pack_matrix": (st, [ctypes.c_int32, P, P, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, P]),
         "caee_quantize_rows": (st, [ctypes.c_int32, P, ctypes.c_int64, ctypes.c_int64, P, P, P]),
         "caee_offload_create": (st, [desc_p, ctypes.POINTER(OffloadDesc), ctypes.POINTER(P)]),
@@ -119,7 +121,7 @@ def load_library(path: str) -> None:
     lib = _load(path)
 
 
-EXPORTED = ("caee_workspace_size", "caee_route_prune", "caee_expert_ffn", "caee_moe_layer",
+EXPORTED = ("caee_workspace_size", "caee_route_prune", "caee_expert_ffn", "caee_moe_layer", "caee_moe_layer_noalloc",
             "caee_pack_matrix", "caee_quantize_rows", "caee_offload_create", "caee_offload_destroy",
             "caee_offload_layer", "caee_offload_stats", "caee_offload_residency", "caee_offload_reset",
             "caee_lru_step", "caee_status_str", "caee_last_error", "caee_abi_version",
@@ -303,6 +305,21 @@ def moe_layer(layer: Layer, x, logits, bias, cost, bins, weights: dict, y, ws, o
     _check(lib.caee_moe_layer(ctypes.byref(d), _ptr(x), _ptr(logits), _ptr(bias), _ptr(cost), _ptr(bins),
                               ctypes.byref(w), _ptr(y), None if ro is None else ctypes.byref(ro),
                               _ptr(ws), ws.numel(), _stream(x)))
+    return y
+
+
+SCRATCH_BYTES = 48 << 20   # CAEE_SCRATCH_BYTES: the library's own scratch array per GPU
+
+
+def moe_layer_noalloc(layer: Layer, x, logits, bias, cost, bins, weights: dict, y, out: Optional[dict] = None):
+    """caee_moe_layer_noalloc: the whole layer in the library's scratch array
+    (no workspace argument; allocates nothing)."""
+    d = layer.desc()
+    w = _weights(weights)
+    ro = _route_out(out)
+    _check(lib.caee_moe_layer_noalloc(ctypes.byref(d), _ptr(x), _ptr(logits), _ptr(bias), _ptr(cost), _ptr(bins),
+                                      ctypes.byref(w), _ptr(y), None if ro is None else ctypes.byref(ro),
+                                      _stream(x)))
     return y
 
 

@@ -5,6 +5,7 @@
 
 #include <cstdarg>
 #include <cstdio>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -15,6 +16,9 @@ namespace caee {
 
 namespace {
 thread_local std::string g_last_error;
+// Set while the no-allocation entry point runs: opt-in timing (which
+// creates HIP events) stays off for its launches.
+thread_local bool g_no_timing = false;
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
@@ -140,6 +144,8 @@ Timing& timing() {
     static Timing t;
     return t;
 }
+
+bool timing_suppressed() { return g_no_timing; }
 
 hipEvent_t take_event() {
     Timing& tm = timing();
@@ -382,6 +388,70 @@ int device_cu_count() {
 
 }  // namespace caee
 
+namespace caee {
+namespace {
+caee_status_t check_layer_args(const caee_layer_desc_t* desc, const void* x, const float* logits, const float* bias,
+                               const float* cost, const int32_t* bin, const caee_expert_weights_t* weights,
+                               const void* y, const caee_route_out_t* out) {
+    CAEE_TRY(check_desc(desc));
+    CAEE_TRY(check_ptr(x, "x", true));
+    CAEE_TRY(check_route_inputs(desc, logits, bias, cost, bin));
+    if (out) CAEE_TRY(check_route_out(out));
+    CAEE_TRY(check_weights(desc, weights));
+    CAEE_TRY(check_ptr(y, "y", true));
+    return CAEE_OK;
+}
+
+// The whole layer on validated arguments and a checked workspace; the big
+// chunks run on a second stream when `side` is set.
+caee_status_t moe_layer_run(const caee_layer_desc_t* desc, const void* x, const float* logits, const float* bias,
+                            const float* cost, const int32_t* bin, const caee_expert_weights_t* weights, void* y,
+                            const caee_route_out_t* out, char* wsb, const WsLayout& L, hipStream_t s, bool side) {
+    RouteParams p = make_route_params(desc, logits, bias, cost, bin, wsb, L);
+    p.chunk_big = call_chunk_big(*desc, weights->layout == CAEE_LAYOUT_TILED);
+    set_route_outputs(p, out, wsb, L);
+    const FfnParams fp = make_ffn_params(desc, x, p.topk_ids, p.topk_w, weights, y, wsb, L);
+    FfnCall call;
+    CAEE_TRY(ffn_begin(desc, fp, L, s, &call));
+    call.shared_done = route_runs_shared(*desc);
+    CAEE_TRY(run_route_layer(desc, p, out, wsb, L, s, call.shared_done ? &fp : nullptr));
+    CAEE_TRY(ffn_routed(desc, fp, L, &call, side));
+    return ffn_end(fp, &call);
+}
+
+// Scratch space of caee_moe_layer_noalloc: one array per GPU (each device
+// holds its own copy at its own address), never freed.  In host code the
+// array's name is not a device address; every host use goes through the
+// address hipGetSymbolAddress returns for the current device.
+__device__ __align__(256) unsigned char scratch[CAEE_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_at[kMaxDevices] = {};
+
+caee_status_t scratch_address(void** at) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices)
+        return fail(CAEE_ERR_HIP, "hipGetDevice failed or device index out of range");
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_at[dev]) {
+        void* p = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p)
+            return fail(CAEE_ERR_HIP, "hipGetSymbolAddress of the scratch array failed: %s", hipGetErrorString(e));
+        g_scratch_at[dev] = p;
+    }
+    *at = g_scratch_at[dev];
+    return CAEE_OK;
+}
+
+struct NoTimingScope {
+    NoTimingScope() { g_no_timing = true; }
+    ~NoTimingScope() { g_no_timing = false; }
+};
+}  // namespace
+}  // namespace caee
+
 using namespace caee;
 
 extern "C" {
@@ -446,27 +516,28 @@ caee_status_t caee_moe_layer(const caee_layer_desc_t* desc, const void* x, const
                              const float* cost, const int32_t* bin, const caee_expert_weights_t* weights, void* y,
                              const caee_route_out_t* out, void* ws, size_t ws_bytes, void* stream) {
     g_last_error.clear();
-    CAEE_TRY(check_desc(desc));
-    CAEE_TRY(check_ptr(x, "x", true));
-    CAEE_TRY(check_route_inputs(desc, logits, bias, cost, bin));
-    if (out) CAEE_TRY(check_route_out(out));
-    CAEE_TRY(check_weights(desc, weights));
-    CAEE_TRY(check_ptr(y, "y", true));
+    CAEE_TRY(check_layer_args(desc, x, logits, bias, cost, bin, weights, y, out));
     WsLayout L;
     CAEE_TRY(check_ws(desc, ws, ws_bytes, &L));
     if (desc->T == 0) return CAEE_OK;
-    char* wsb = (char*)ws;
-    RouteParams p = make_route_params(desc, logits, bias, cost, bin, wsb, L);
-    p.chunk_big = call_chunk_big(*desc, weights->layout == CAEE_LAYOUT_TILED);
-    hipStream_t s = as_stream(stream);
-    set_route_outputs(p, out, wsb, L);
-    const FfnParams fp = make_ffn_params(desc, x, p.topk_ids, p.topk_w, weights, y, wsb, L);
-    FfnCall call;
-    CAEE_TRY(ffn_begin(desc, fp, L, s, &call));
-    call.shared_done = route_runs_shared(*desc);
-    CAEE_TRY(run_route_layer(desc, p, out, wsb, L, s, call.shared_done ? &fp : nullptr));
-    CAEE_TRY(ffn_routed(desc, fp, L, &call, true));
-    return ffn_end(fp, &call);
+    return moe_layer_run(desc, x, logits, bias, cost, bin, weights, y, out, (char*)ws, L, as_stream(stream), true);
+}
+
+caee_status_t caee_moe_layer_noalloc(const caee_layer_desc_t* desc, const void* x, const float* logits,
+                                     const float* bias, const float* cost, const int32_t* bin,
+                                     const caee_expert_weights_t* weights, void* y, const caee_route_out_t* out,
+                                     void* stream) {
+    g_last_error.clear();
+    CAEE_TRY(check_layer_args(desc, x, logits, bias, cost, bin, weights, y, out));
+    const WsLayout L = ws_layout(*desc);
+    if (L.total > (size_t)CAEE_SCRATCH_BYTES)
+        return fail(CAEE_ERR_UNSUPPORTED, "the call needs %zu bytes of scratch; the library's array holds %zu "
+                    "(use caee_moe_layer with a workspace)", L.total, (size_t)CAEE_SCRATCH_BYTES);
+    if (desc->T == 0) return CAEE_OK;
+    void* at = nullptr;
+    CAEE_TRY(scratch_address(&at));
+    NoTimingScope no_timing;
+    return moe_layer_run(desc, x, logits, bias, cost, bin, weights, y, out, (char*)at, L, as_stream(stream), false);
 }
 
 caee_status_t caee_pack_matrix(int32_t w_dtype, const void* src, void* dst, int64_t rows, int64_t cols,

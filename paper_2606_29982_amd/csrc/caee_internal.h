@@ -486,6 +486,7 @@ struct Timing {
 };
 Timing& timing();
 hipEvent_t take_event();
+bool timing_suppressed();   // the calling thread runs a call that must create no events
 
 // Runs one launch, bracketed by timing events when timing is on.
 template <class F>
@@ -493,7 +494,7 @@ caee_status_t timed_launch(int kind, hipStream_t s, const char* what, F&& launch
     Timing& tm = timing();
     hipEvent_t a = nullptr, b = nullptr;
     bool timed = false;
-    if (tm.on) {
+    if (tm.on && !timing_suppressed()) {
         a = take_event();
         b = take_event();
         timed = a && b && hipEventRecord(a, s) == hipSuccess;

@@ -199,3 +199,20 @@ def test_offload_null_handle():
     assert st == caee.CAEE_ERR_INVALID_ARG
     caee.lib.caee_offload_destroy(None)
     assert caee.lib.caee_offload_reset(None) == caee.CAEE_ERR_INVALID_ARG
+
+
+def test_noalloc_refuses_oversize_and_empty_calls_on_the_host():
+    # a batch whose workspace exceeds the library's scratch array is refused
+    # before any launch; an empty batch does nothing (no GPU needed for either)
+    w = caee.ExpertWeights(FAKE, FAKE, None, None, FAKE, FAKE, None, None, 1)
+    for T, status in ((256, caee.CAEE_ERR_UNSUPPORTED), (0, caee.CAEE_OK)):
+        layer = _layer(T=T)
+        d = layer.desc()
+        st = caee.lib.caee_moe_layer_noalloc(ctypes.byref(d), FAKE, FAKE, None, FAKE, FAKE, ctypes.byref(w),
+                                             FAKE, None, None)
+        assert st == status, caee.lib.caee_last_error().decode()
+    assert caee.workspace_size(_layer(T=128)) <= caee.SCRATCH_BYTES < caee.workspace_size(_layer(T=256))
+    # invalid arguments are rejected as by caee_moe_layer
+    d = _layer(k=17).desc()
+    assert caee.lib.caee_moe_layer_noalloc(ctypes.byref(d), FAKE, FAKE, None, FAKE, FAKE, ctypes.byref(w), FAKE,
+                                           None, None) == caee.CAEE_ERR_INVALID_ARG
