@@ -124,10 +124,17 @@ def time_steps(case, steps, warmup):
 
 def graph_protocol(case, warmup=10, iters=50, flush_mb=512):
     """The layer call captured once in a HIP graph and replayed: `warmup`
-    replays, then `iters` replays each timed on its own with events, with a
-    `flush_mb` MB buffer written between them (outside the timed region) so
-    that the 256 MB memory-side cache holds nothing of the previous call.
-    Returns the median, 10th and 90th percentile in microseconds."""
+    replays, then `iters` replays each timed on its own with events, with the
+    caches flushed before each one (outside the timed region) in two ways:
+      * "write": a `flush_mb` MB buffer is written, so that the 256 MB
+        memory-side cache holds nothing of the previous call -- but it then
+        holds the flush's own dirty lines, which the timed call has to write
+        back to HBM as it streams its weights;
+      * "clean": the same write, then a second `flush_mb` MB buffer is read,
+        which evicts those dirty lines (written back before the timed call):
+        the call starts from caches that hold neither its data nor dirty
+        lines.
+    Returns the median and the 10th / 90th percentiles of both, in us."""
     import torch
     case.step()
     torch.cuda.synchronize()
@@ -137,18 +144,25 @@ def graph_protocol(case, warmup=10, iters=50, flush_mb=512):
     for _ in range(warmup):
         g.replay()
     flush = torch.empty(flush_mb << 20, dtype=torch.uint8, device=case.y.device)
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(iters)]
-    for a, b in ev:
-        flush.fill_(1)
-        a.record()
-        g.replay()
-        b.record()
-    torch.cuda.synchronize()
-    us = np.array([a.elapsed_time(b) * 1e3 for a, b in ev])
-    del g, flush
-    return {"us_p50": round(float(np.median(us)), 1), "us_p10": round(float(np.percentile(us, 10)), 1),
-            "us_p90": round(float(np.percentile(us, 90)), 1), "iters": iters, "warmup": warmup,
-            "flush_mb": flush_mb}
+    rd = torch.ones(flush_mb << 17, dtype=torch.int64, device=case.y.device)
+    res = {"iters": iters, "warmup": warmup, "flush_mb": flush_mb}
+    for mode in ("write", "clean"):
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(iters)]
+        for a, b in ev:
+            flush.fill_(1)
+            if mode == "clean":
+                rd.sum()
+            a.record()
+            g.replay()
+            b.record()
+        torch.cuda.synchronize()
+        us = np.array([a.elapsed_time(b) * 1e3 for a, b in ev])
+        key = "" if mode == "clean" else "_write_flush"
+        res["us_p50" + key] = round(float(np.median(us)), 1)
+        res["us_p10" + key] = round(float(np.percentile(us, 10)), 1)
+        res["us_p90" + key] = round(float(np.percentile(us, 90)), 1)
+    del g, flush, rd
+    return res
 
 
 def layer_bytes(shape, T, n_trans):
@@ -219,25 +233,29 @@ def cpu_baseline(shape, case, W, sample_tokens):
             "seconds": round(dt, 2)}
 
 
-def pinned_h2d_gbps(dev, nbytes, reps=8):
+def pinned_h2d_gbps(dev, nbytes, reps=8, n_streams=3):
     """Peak host-to-device bandwidth of page-locked memory: one expert-sized
-    copy repeated on its own stream, timed with events."""
+    copy repeated on a stream, timed with events, best of `n_streams`
+    streams (the copy runtime can put one stream's copies of a given size on
+    a half-rate path)."""
     import torch
     src = torch.empty(nbytes, dtype=torch.uint8, pin_memory=True)
     src.fill_(1)
     dst = torch.empty(nbytes, dtype=torch.uint8, device=dev)
-    s = torch.cuda.Stream(device=dev)
-    with torch.cuda.stream(s):
-        dst.copy_(src, non_blocking=True)
-        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        a.record(s)
-        for _ in range(reps):
+    best = 0.0
+    for _ in range(n_streams):
+        s = torch.cuda.Stream(device=dev)
+        with torch.cuda.stream(s):
             dst.copy_(src, non_blocking=True)
-        b.record(s)
-    b.synchronize()
-    gbps = reps * nbytes / (a.elapsed_time(b) * 1e-3) / 1e9
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(s)
+            for _ in range(reps):
+                dst.copy_(src, non_blocking=True)
+            b.record(s)
+        b.synchronize()
+        best = max(best, reps * nbytes / (a.elapsed_time(b) * 1e-3) / 1e9)
     del src, dst
-    return gbps
+    return best
 
 
 def offload_rows(args, shape, Wt, dev, link_model=None):
@@ -472,7 +490,9 @@ def main():
     # The same call captured in a HIP graph, memory-side cache flushed before
     # every timed replay (median and spread of single calls).
     result["graph_protocol"] = graph_protocol(head)
-    result["hbm_frac_flushed"] = round(b_layer / (result["graph_protocol"]["us_p50"] * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4)
+    gp = result["graph_protocol"]
+    result["hbm_frac_flushed"] = round(b_layer / (gp["us_p50"] * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4)
+    result["hbm_frac_flushed_write"] = round(b_layer / (gp["us_p50_write_flush"] * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4)
     log(f"graph protocol {result['graph_protocol']}")
 
     link_model = None
@@ -511,6 +531,9 @@ def main():
                               "graph_flushed_us_p50": gp["us_p50"], "graph_flushed_us_p10": gp["us_p10"],
                               "graph_flushed_us_p90": gp["us_p90"],
                               "hbm_frac_flushed": round(b / (gp["us_p50"] * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),
+                              "graph_write_flush_us_p50": gp["us_p50_write_flush"],
+                              "hbm_frac_flushed_write": round(b / (gp["us_p50_write_flush"] * 1e-6) / 1e9
+                                                              / HBM_PEAK_GBPS, 4),
                               "bin_loads_g": {"act": [round(v, 3) for v in loads[0]],
                                               "must": [round(v, 3) for v in loads[1]],
                                               "trans": [round(v, 3) for v in loads[2]]},

@@ -18,6 +18,23 @@ HIP_FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
              "-Wno-unused-command-line-argument"]
 
 
+# Host-side AddressSanitizer and UndefinedBehaviorSanitizer for a checking
+# build of the host code (argument validation, workspace layout, the
+# residency plan); each flag is scoped to the host pass, the device code is
+# built as usual.
+SANITIZE_HOST = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+                 "-Xarch_host", "-fno-omit-frame-pointer", "-Xarch_host", "-fno-sanitize-recover=all"]
+
+
+def asan_runtime() -> str:
+    """The ASan runtime a process must preload to load the sanitized build."""
+    clang = os.path.join(os.path.dirname(os.path.realpath(hipcc())), "..", "lib", "llvm", "bin", "clang")
+    if not os.path.exists(clang):
+        clang = "/opt/rocm/llvm/bin/clang"
+    out = subprocess.run([clang, "-print-file-name=libclang_rt.asan-x86_64.so"], capture_output=True, text=True)
+    return out.stdout.strip()
+
+
 def hipcc() -> str:
     for cand in (os.environ.get("HIPCC"), "/opt/rocm/bin/hipcc", shutil.which("hipcc")):
         if cand and os.path.exists(cand):
@@ -25,15 +42,19 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found")
 
 
-def build(verbose: bool = False, out: str = LIB, defines=()) -> str:
+def build(verbose: bool = False, out: str = LIB, defines=(), sanitize_host: bool = False) -> str:
     """Compile every HIP source into one shared library; returns its path.
-    ``defines`` are extra -D options (tuning knobs of the kernels)."""
+    ``defines`` are extra -D options (tuning knobs of the kernels);
+    ``sanitize_host`` builds the host code with ASan and UBSan (load it with
+    the runtime of ``asan_runtime()`` preloaded)."""
     objs = []
     t0 = time.time()
     procs = []
+    flags = HIP_FLAGS + (["-g", *SANITIZE_HOST] if sanitize_host else [])
+    os.makedirs(os.path.dirname(out), exist_ok=True)
     for src in SOURCES:
         obj = out + "." + src.replace(".hip", ".o")
-        cmd = [hipcc(), *HIP_FLAGS, *[f"-D{d}" for d in defines], "-c", os.path.join(CSRC, src), "-o", obj]
+        cmd = [hipcc(), *flags, *[f"-D{d}" for d in defines], "-c", os.path.join(CSRC, src), "-o", obj]
         if verbose:
             print(" ".join(cmd), flush=True)
         procs.append((src, subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT)))
@@ -46,7 +67,8 @@ def build(verbose: bool = False, out: str = LIB, defines=()) -> str:
         if verbose and log:
             sys.stderr.write(log.decode(errors="replace"))
     tmp = out + ".tmp"
-    cmd = [hipcc(), "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", tmp]
+    link = [*SANITIZE_HOST, "-shared-libasan"] if sanitize_host else []
+    cmd = [hipcc(), "--offload-arch=gfx950", "-shared", "-fPIC", *link, *objs, "-o", tmp]
     subprocess.run(cmd, check=True)
     os.replace(tmp, out)
     for o in objs:

@@ -13,7 +13,8 @@ from dataclasses import dataclass
 from typing import Optional
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libcaee.so")
+# CAEE_LIBRARY names another build of the library (e.g. the host-sanitized one).
+LIB_PATH = os.environ.get("CAEE_LIBRARY") or os.path.join(HERE, "libcaee.so")
 
 CAEE_OK, CAEE_ERR_INVALID_ARG, CAEE_ERR_UNSUPPORTED, CAEE_ERR_WORKSPACE, CAEE_ERR_HIP, CAEE_ERR_CAPACITY = range(6)
 CAEE_F32, CAEE_BF16, CAEE_FP8_E4M3 = 0, 1, 2

@@ -86,22 +86,30 @@ def _time_us(fn, reps: int, stream) -> float:
     return float(np.median([a.elapsed_time(b) * 1e3 for a, b in ev]))
 
 
-def measure_link(device, sizes_bytes=(1 << 20, 4 << 20, 16 << 20, 44040192, 88080384), reps: int = 7):
-    """Times (us) of page-locked host-to-device copies of each size."""
+def measure_link(device, sizes_bytes=(1 << 20, 4 << 20, 16 << 20, 44040192, 88080384), reps: int = 7,
+                 n_streams: int = 3):
+    """Times (us) of page-locked host-to-device copies of each size: the
+    fastest, over `n_streams` streams, of the median of `reps` copies on one
+    stream.  The copy runtime picks the copy path per stream and size: on
+    one stream a given size can run at half the link rate (about 30 against
+    56 GB/s) on every repetition while other sizes run at full rate, and a
+    different stream slows a different set of sizes; the calibration wants
+    the link, not that choice."""
     import torch
     top = max(sizes_bytes)
     src = torch.empty(top, dtype=torch.uint8, pin_memory=True)
     src.fill_(1)
     dst = torch.empty(top, dtype=torch.uint8, device=device)
-    s = torch.cuda.Stream(device=device)
-    times = []
-    with torch.cuda.stream(s):
-        for n in sizes_bytes:                 # warm every size once
-            dst[:n].copy_(src[:n], non_blocking=True)
-        s.synchronize()
-        for n in sizes_bytes:
-            times.append(_time_us(lambda: dst[:n].copy_(src[:n], non_blocking=True), reps, s))
-    return list(sizes_bytes), times
+    best = [float("inf")] * len(sizes_bytes)
+    for _ in range(n_streams):
+        s = torch.cuda.Stream(device=device)
+        with torch.cuda.stream(s):
+            for n in sizes_bytes:                 # warm every size once
+                dst[:n].copy_(src[:n], non_blocking=True)
+            s.synchronize()
+            for i, n in enumerate(sizes_bytes):
+                best[i] = min(best[i], _time_us(lambda: dst[:n].copy_(src[:n], non_blocking=True), reps, s))
+    return list(sizes_bytes), best
 
 
 def measure_hbm(device, d: int = 7168, fs=(512, 1024, 2048), counts=(8, 16, 32, 64), reps: int = 7, seed: int = 0):

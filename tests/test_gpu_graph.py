@@ -70,3 +70,15 @@ def test_graph_replays_match_eager(shape, T, tiled):
             assert torch.equal(graph.out[name], eager.out[name]), name
     # the two input sets route differently, so the replays did not reuse a result
     assert not torch.equal(to_dev(inps[0].logits, DEV), to_dev(inps[1].logits, DEV))
+
+
+def test_first_call_of_a_process_under_capture():
+    # A fresh process whose first layer call is captured: the library's
+    # second stream and its fork/join events are created during capture.
+    import subprocess
+    import sys
+    script = __file__.replace("test_gpu_graph.py", "graph_first_call.py")
+    print("running the first call of a new process under graph capture", flush=True)
+    r = subprocess.run([sys.executable, "-u", script], capture_output=True, text=True, timeout=240)
+    print(r.stdout[-2000:], r.stderr[-2000:], flush=True)
+    assert r.returncode == 0 and "first call under capture ok" in r.stdout
