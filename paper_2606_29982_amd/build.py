@@ -10,7 +10,7 @@ import time
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libcaee.so")
-SOURCES = ["api.hip", "route.hip", "ffn.hip", "ffn_fp8.hip", "ffn_gemm.hip", "offload.hip"]
+SOURCES = ["api.hip", "route.hip", "ffn.hip", "ffn_fp8.hip", "ffn_gemm.hip", "ffn_prefill8.hip", "offload.hip"]
 
 # Packed-fp32 VALU ops are disabled on every HIP translation unit.
 HIP_FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",

@@ -34,9 +34,9 @@ constexpr int kMaxTokenBlocks = CAEE_MAX_TOKEN_BLOCKS;
 #define CAEE_PREFILL_T 65536
 #endif
 constexpr int kPrefillT = CAEE_PREFILL_T;
-// 8-bit batches above this many tokens run their big chunks (as wide as the
-// GEMM's token tile) with the LDS-pipelined GEMM kernels, when the weights
-// are tiled and the sizes fit (0 disables them).
+// 8-bit batches above this many tokens run their big chunks (as wide as its
+// token tile: 256 rows) with the prefill kernel of ffn_prefill8.hip, when the
+// weights are tiled and the sizes fit (0 disables it).
 #ifndef CAEE_GEMM_T
 #define CAEE_GEMM_T 256
 #endif
@@ -203,7 +203,8 @@ inline int big_token_blocks(const caee_layer_desc_t& d) {
 
 bool gemm_fp8_applies(const caee_layer_desc_t& d, bool tiled);
 bool gemm_bf16_applies(const caee_layer_desc_t& d, bool tiled);
-int gemm_fp8_blocks();
+int gemm_fp8_blocks();         // 16-token blocks of an 8-bit big chunk
+int gemm_bf16_blocks();        // 16-token blocks of a bf16 big chunk
 bool gemm_fp8_fuses_quant();   // the GEMM's gate/up writes the e4m3 H rows itself
 
 // 16-token column blocks of a call's big chunks: the width of the 8-bit
@@ -213,7 +214,9 @@ bool gemm_fp8_fuses_quant();   // the GEMM's gate/up writes the e4m3 H rows itse
 // big_token_blocks, which never gives fewer chunks.
 inline int call_big_blocks(const caee_layer_desc_t& d, bool tiled) {
     const int nb = big_token_blocks(d);
-    return nb > 0 && (gemm_fp8_applies(d, tiled) || gemm_bf16_applies(d, tiled)) ? gemm_fp8_blocks() : nb;
+    if (nb > 0 && gemm_fp8_applies(d, tiled)) return gemm_fp8_blocks();
+    if (nb > 0 && gemm_bf16_applies(d, tiled)) return gemm_bf16_blocks();
+    return nb;
 }
 
 // Rows per big chunk of a call (16 when there are no big chunks).
@@ -429,7 +432,8 @@ hipError_t launch_quant_list(const FfnParams& p, int nb, int max_chunks, bool tr
 hipError_t launch_gather_xs(const FfnParams& p, int max_chunks, hipStream_t s);
 bool gemm_fp8_supports(const FfnParams& p, int nb);
 bool gemm_bf16_supports(const FfnParams& p, int nb);
-hipError_t launch_gemm(const FfnParams& p, bool gate_up, bool fp8, int max_chunks, hipStream_t s);
+hipError_t launch_gemm(const FfnParams& p, bool gate_up, int max_chunks, hipStream_t s);   // bf16 big chunks
+hipError_t launch_prefill8(const FfnParams& p, bool gate_up, int max_chunks, hipStream_t s);
 hipError_t launch_down_fp8(const FfnParams& p, int nb, int max_chunks, hipStream_t s);
 hipError_t launch_pack(const void* src, void* dst, long long rows, long long row_units, long long count,
                        hipStream_t s);

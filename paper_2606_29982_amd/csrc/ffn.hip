@@ -457,7 +457,7 @@ hipError_t launch_big(const FfnParams& p, bool gate_up, int nb, dim3 grid, hipSt
 }  // namespace
 
 hipError_t launch_gate_up(const FfnParams& p, int w_dtype, int nb, int max_chunks, hipStream_t s) {
-    if (w_dtype == CAEE_BF16 && gemm_bf16_supports(p, nb)) return launch_gemm(p, true, false, max_chunks, s);
+    if (w_dtype == CAEE_BF16 && gemm_bf16_supports(p, nb)) return launch_gemm(p, true, max_chunks, s);
     if (nb >= 4 && kBigStaged) {
         const dim3 grid(grid_for((long long)max_chunks * (p.f / 16)));
         if (w_dtype == CAEE_BF16) return launch_big<Bf16Math>(p, true, nb, grid, s);
@@ -471,7 +471,7 @@ hipError_t launch_gate_up(const FfnParams& p, int w_dtype, int nb, int max_chunk
 }
 
 hipError_t launch_down(const FfnParams& p, int w_dtype, int nb, int max_chunks, hipStream_t s) {
-    if (w_dtype == CAEE_BF16 && gemm_bf16_supports(p, nb)) return launch_gemm(p, false, false, max_chunks, s);
+    if (w_dtype == CAEE_BF16 && gemm_bf16_supports(p, nb)) return launch_gemm(p, false, max_chunks, s);
     if (nb >= 4 && kBigStaged) {
         const dim3 grid(grid_for((long long)max_chunks * (p.d / 16) / 2));
         if (w_dtype == CAEE_BF16) return launch_big<Bf16Math>(p, false, nb, grid, s);

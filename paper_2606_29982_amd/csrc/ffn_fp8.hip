@@ -561,7 +561,7 @@ hipError_t launch_quant_list(const FfnParams& p, int nb, int max_chunks, bool tr
 }
 
 hipError_t launch_gate_up_fp8(const FfnParams& p, int nb, int max_chunks, hipStream_t s) {
-    if (gemm_fp8_supports(p, nb)) return launch_gemm(p, true, true, max_chunks, s);
+    if (gemm_fp8_supports(p, nb)) return launch_prefill8(p, true, max_chunks, s);
     if (nb >= 4 && kBigStaged) {
         const dim3 grid(grid_for_waves((long long)max_chunks * (p.f / 16) / CAEE_FP8_BIG_TW_GU));
         if (nb == 4) hipLaunchKernelGGL(k_gate_up_fp8_big<4>, grid, dim3(kFfnThreads), 0, s, p);
@@ -581,7 +581,7 @@ hipError_t launch_gate_up_fp8(const FfnParams& p, int nb, int max_chunks, hipStr
 }
 
 hipError_t launch_down_fp8(const FfnParams& p, int nb, int max_chunks, hipStream_t s) {
-    if (gemm_fp8_supports(p, nb)) return launch_gemm(p, false, true, max_chunks, s);
+    if (gemm_fp8_supports(p, nb)) return launch_prefill8(p, false, max_chunks, s);
     if (nb >= 4 && kBigStaged) {
         const dim3 grid(grid_for_waves((long long)max_chunks * (p.d / 16) / CAEE_FP8_BIG_TW_DN));
         if (nb == 4) hipLaunchKernelGGL(k_down_fp8_big<4>, grid, dim3(kFfnThreads), 0, s, p);

@@ -1,0 +1,350 @@
+// 8-bit expert products of prefill batches: e4m3 weights (fp32 128x128
+// block scales) against e4m3 token rows (fp32 scale per row and 128-wide
+// block), for the big chunks of an 8-bit layer (experts with more rows than
+// a small chunk, cut into near-equal chunks of at most 256 rows).
+//
+// A workgroup of 8 waves computes 256 weight rows x (up to) 256 tokens of
+// one chunk over the whole contraction, one 128-deep block per pipeline
+// stage:
+//   * the chunk's token rows (and their block scales) go global -> LDS with
+//     the direct-to-LDS loads, in MFMA B-fragment order, three stages in a
+//     ring; every wave reads every token fragment of a stage from LDS;
+//   * each wave owns two 16-row weight tiles (32 rows), which nobody else
+//     reads: they go global -> registers, two stages ahead of their MFMAs,
+//     and never pass through LDS.
+// So a chunk of up to 256 rows (every routed expert of a 4096-token batch of
+// the DeepSeek-R1 layer) streams each of its weight bytes once, and the
+// bytes in flight per CU are the token ring's plus every wave's register
+// stages.  Per stage a wave issues the same nine loads (four token
+// fragments, one row-scale load, four weight pieces), so it waits for its
+// oldest stage with a constant vmcnt, and one barrier per stage publishes
+// the ring's stage to all waves.
+//
+// Work items: (chunk, weight group); gate/up groups are 128 features (the
+// gate and up rows of each; wave w takes feature tile w of both), down
+// groups 256 output rows (wave w takes tiles 2w, 2w + 1).  Gate/up ends in
+// SwiGLU and quantises its 128 features per token (amax across the waves
+// through LDS) into e4m3 codes and a transposed block scale, the input of
+// the down product; down writes bf16 expert output rows.
+//
+// Per block: one scaled 16x16x128 MFMA (unit E8M0 scales) per (weight tile,
+// token tile), its partial sums times weight block scale x row block scale
+// added in fp32.
+#include "caee_internal.h"
+#include "fp8_codec.h"
+
+namespace caee {
+namespace {
+
+typedef int i32x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef const __attribute__((address_space(1))) u32x4_t g_u32x4_t;
+
+constexpr int kP8Waves = 8;
+constexpr int kP8Threads = kP8Waves * kWave;
+// Token tiles of an item (16 tokens each) and stages of the load ring.
+#ifndef CAEE_P8_NT
+#define CAEE_P8_NT 16
+#endif
+#ifndef CAEE_P8_RING
+#define CAEE_P8_RING 3
+#endif
+constexpr int kP8NT = CAEE_P8_NT;
+constexpr int kRing = CAEE_P8_RING;
+static_assert(kP8NT % 4 == 0 && kP8NT <= 16, "token tiles: a multiple of 4, at most 16");
+static_assert(kRing == 3 || kRing == 4, "ring of 3 or 4 stages");
+constexpr int kP8TokLoads = 2 * kP8NT / kP8Waves;  // token fragment loads per wave and stage
+constexpr int kP8Loads = kP8TokLoads + 1 + 4;      // + row scales + two tiles x two halves of weights
+constexpr int kP8MaxKBlocks = 128;        // contraction up to 16384
+constexpr int kScaleOne = 127;            // E8M0 1.0: the MFMA's own block scales are unused
+constexpr int kXcds = 8;                  // accelerator complex dies, each with its own L2
+// Items grouped by XCD: all weight groups of a chunk run on one XCD, so its
+// token rows are fetched into one L2 once (workgroups go to the XCDs round
+// robin, workgroup b to XCD b % 8).
+#ifndef CAEE_P8_XCD
+#define CAEE_P8_XCD 1
+#endif
+
+struct P8Stage {
+    u32x4_t f[2 * kP8NT][kWave];          // token tile n, half h at [2n + h]: the B fragment of lane l
+    float x[kP8Waves][kWave];             // row block scales: token n at [n / 32][n % 32]
+};
+
+__device__ inline i32x8_t join(const u32x4_t& lo, const u32x4_t& hi) {
+    return i32x8_t{(int)lo[0], (int)lo[1], (int)lo[2], (int)lo[3], (int)hi[0], (int)hi[1], (int)hi[2], (int)hi[3]};
+}
+
+__device__ inline float silu_mul(float g, float u) { return g / (1.0f + __expf(-g)) * u; }
+
+// Waits until at most N of this wave's vector memory loads are outstanding
+// (gfx9 s_waitcnt: vmcnt in bits 3:0 and 15:14, expcnt and lgkmcnt not waited).
+template <int N>
+__device__ inline void wait_vm() {
+    __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | (((N >> 4) & 3) << 14));
+}
+
+// Workgroup barrier without the memory fence of __syncthreads (which would
+// wait for every load in flight); the empty asm keeps the compiler from
+// moving memory accesses across it.
+__device__ inline void stage_barrier() {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
+// Weight pieces of one stage in registers: [tile][half].
+struct WReg {
+    u32x4_t v[2][2];
+};
+
+template <bool kGateUp>
+__global__ __launch_bounds__(kP8Threads) void k_prefill8(FfnParams p) {
+    // Separate LDS objects, each named statically below, so that the
+    // compiler can tell a read of one stage from the loads filling another.
+    __shared__ P8Stage st0, st1, st2, st3;
+    __shared__ float wsl[2][kP8MaxKBlocks];   // weight block scales of the item's two 128-row scale rows
+    const int tid = threadIdx.x, lane = tid & (kWave - 1);
+    const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
+    const int r = lane & 15, g = lane >> 4;
+    const int K = kGateUp ? p.d : p.f;
+    const int kblocks = K / 128;
+    const size_t ksteps = (size_t)K / 64;          // 64-byte steps of a weight row (tiled layout)
+    const size_t row_units = (size_t)K / 16;       // 16-byte pieces of a token row
+    const int groups = kGateUp ? p.f / 128 : p.d / 256;
+    const int total = ffn_list_size(p) * groups;
+    const size_t expert_bytes = kGateUp ? (size_t)2 * p.f * p.d : (size_t)p.d * p.f;
+    const size_t scales_per_expert = (size_t)((kGateUp ? 2 * p.f : p.d) / 128) * kblocks;
+    const f32x4_t zero = {0.f, 0.f, 0.f, 0.f};
+
+    // Item order: plain (workgroup b takes items b, b + grid, ...), or by
+    // XCD (XCD x takes the chunks x, x + 8, ..., all groups of each, its
+    // workgroups striding through that list).
+    const bool by_xcd = CAEE_P8_XCD && gridDim.x % kXcds == 0;
+    const int xcd = blockIdx.x % kXcds;
+    const int n_local = by_xcd ? (ffn_list_size(p) - xcd + kXcds - 1) / kXcds * groups : total;
+    for (int it = by_xcd ? blockIdx.x / kXcds : blockIdx.x; it < n_local;
+         it += by_xcd ? gridDim.x / kXcds : gridDim.x) {
+        const int c = by_xcd ? xcd + kXcds * (it / groups) : it / groups;
+        const int grp = it % groups;
+        const ChunkRef ck = ffn_chunk(p, c);
+        const int xs = ck.xs;
+        if (ffn_skip(p, xs)) continue;   // uniform over the workgroup
+        const int row0 = ck.row0, ntok = ck.ntok;
+        const int nb = (ntok + 15) >> 4;
+        const u32x4_t* wb = (const u32x4_t*)ffn_weights(p, xs, !kGateUp, expert_bytes);
+        const float* wsc = ffn_scales(p, xs, !kGateUp, scales_per_expert);
+        // This wave's weight tiles and the scale rows they fall in.
+        const int t0 = kGateUp ? grp * 8 + wave : grp * 16 + 2 * wave;
+        const int t1 = kGateUp ? p.f / 16 + grp * 8 + wave : t0 + 1;
+        const int srow0 = kGateUp ? grp : 2 * grp;                 // wsl[0]
+        const int srow1 = kGateUp ? p.f / 128 + grp : 2 * grp + 1; // wsl[1]
+        const int ws0 = kGateUp ? 0 : (wave >= 4 ? 1 : 0), ws1 = kGateUp ? 1 : ws0;
+        const u32x4_t* wsrc[2] = {wb + (size_t)t0 * ksteps * 64 + lane, wb + (size_t)t1 * ksteps * 64 + lane};
+        // Token fragments j = 4 * wave + i: token tile j / 2, half j % 2.
+        const u32x4_t* tsrc[kP8TokLoads];
+#pragma unroll
+        for (int i = 0; i < kP8TokLoads; ++i) {
+            const int j = kP8TokLoads * wave + i;
+            int n = 16 * (j >> 1) + r;
+            n = n < ntok ? n : 0;          // padded token columns read a valid row; results dropped
+            const size_t row = kGateUp ? (size_t)ffn_token(p, xs, row0 + n) : (size_t)(row0 + n);
+            tsrc[i] = (const u32x4_t*)(kGateUp ? p.xq : p.hq) + row * row_units + (j & 1) * 4 + g;
+        }
+        // Row scales, transposed and in permuted row order ([block][row]):
+        // wave w loads tokens 32w .. 32w + 31 (lanes 32..63 repeat them).
+        int xn = 32 * wave + (lane & 31);
+        xn = xn < ntok ? xn : 0;
+        const float* xsrc = (kGateUp ? p.xst : p.hst) + row0 + xn;
+
+        for (int q = tid; q < 2 * kblocks; q += kP8Threads) {
+            const int h = q >= kblocks, kb = q - h * kblocks;
+            wsl[h][kb] = wsc[(size_t)(h ? srow1 : srow0) * kblocks + kb];
+        }
+        __syncthreads();
+
+        auto issue = [&](int kb, P8Stage& s, WReg& w) __attribute__((always_inline)) {
+#pragma unroll
+            for (int i = 0; i < kP8TokLoads; ++i)
+                __builtin_amdgcn_global_load_lds((const void*)(tsrc[i] + (size_t)kb * 8),
+                                                 (lds_void_t*)&s.f[kP8TokLoads * wave + i][0], 16, 0, 0);
+            __builtin_amdgcn_global_load_lds((const void*)(xsrc + (size_t)kb * p.P), (lds_void_t*)&s.x[wave][0], 4,
+                                             0, 0);
+#pragma unroll
+            for (int t = 0; t < 2; ++t)
+#pragma unroll
+                for (int h = 0; h < 2; ++h)
+                    w.v[t][h] = __builtin_nontemporal_load((g_u32x4_t*)(wsrc[t] + (size_t)(2 * kb + h) * 64));
+        };
+
+        f32x4_t acc[2][kP8NT];
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+            for (int n = 0; n < kP8NT; ++n) acc[t][n] = zero;
+
+        auto compute = [&](int kb, const P8Stage& s, const WReg& w) __attribute__((always_inline)) {
+            const i32x8_t a0 = join(w.v[0][0], w.v[0][1]), a1 = join(w.v[1][0], w.v[1][1]);
+            const float wa = wsl[ws0][kb], wc = wsl[ws1][kb];
+#pragma unroll
+            for (int n = 0; n < kP8NT; ++n) {
+                if (n < nb) {
+                    const i32x8_t bf = join(s.f[2 * n][lane], s.f[2 * n + 1][lane]);
+                    const int tok = 16 * n + r;
+                    const float xv = s.x[tok >> 5][tok & 31];
+                    const f32x4_t p0 =
+                        __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a0, bf, zero, 0, 0, 0, kScaleOne, 0, kScaleOne);
+                    const f32x4_t p1 =
+                        __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a1, bf, zero, 0, 0, 0, kScaleOne, 0, kScaleOne);
+                    acc[0][n] += p0 * (wa * xv);
+                    acc[1][n] += p1 * (wc * xv);
+                }
+                // One token tile's fragment and partial sums live at a time
+                // (hoisting all sixteen would spill the accumulators); the
+                // other wave of the SIMD covers the MFMA latency.
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        };
+
+        // Step v waits for this wave's loads of block v - (kRing - 1) (those
+        // of the later blocks may stay in flight), passes a barrier that
+        // publishes every wave's token loads of that block and guarantees
+        // that all waves are done with block v - kRing, refills that stage
+        // and register set with block v, and multiplies block v - (kRing - 1).
+        // The steps run in whole groups of kRing, so every step issues its
+        // loads unconditionally (steps past the last block re-read it, from
+        // L2, into a stage nobody multiplies) and the compiler's wait analysis
+        // sees the same loads per step on every path: the only waits in the
+        // loop are the kernel's own.  One code path for every step, so the
+        // accumulators live in one set of registers throughout.
+        constexpr int kAhead = kRing - 1;
+        WReg w0, w1, w2, w3;
+        const int nsteps = (kblocks + kAhead + kRing - 1) / kRing * kRing;
+        auto step = [&](int v, P8Stage& fill, WReg& wf, const P8Stage& use, const WReg& wu)
+                        __attribute__((always_inline)) {
+            wait_vm<(kAhead - 1) * kP8Loads>();
+            stage_barrier();
+            issue(v < kblocks ? v : kblocks - 1, fill, wf);
+            if (v >= kAhead && v - kAhead < kblocks) compute(v - kAhead, use, wu);
+        };
+#pragma clang loop unroll(disable)
+        for (int v = 0; v < nsteps; v += kRing) {
+            if constexpr (kRing == 3) {
+                step(v, st0, w0, st1, w1);
+                step(v + 1, st1, w1, st2, w2);
+                step(v + 2, st2, w2, st0, w0);
+            } else {
+                step(v, st0, w0, st1, w1);
+                step(v + 1, st1, w1, st2, w2);
+                step(v + 2, st2, w2, st3, w3);
+                step(v + 3, st3, w3, st0, w0);
+            }
+        }
+        wait_vm<0>();   // the re-reads past the last block have landed
+        // Every wave is done with the ring before the epilogue reuses st0 and
+        // the next item refills it.
+        stage_barrier();
+
+        if constexpr (kGateUp) {
+            // Lane (r, g) holds features 16 * wave + 4g .. + 3 of the group
+            // for token 16n + r.  Per token: amax over the group's 128 SwiGLU
+            // values (this lane's 4, the 4 lanes of the column, the 8 waves
+            // through LDS), scale = amax / 448 (1 if zero), codes of value /
+            // scale: the activation quantiser's arithmetic.
+            float* red = reinterpret_cast<float*>(&st0);   // [wave][256 tokens]; the ring is idle
+            static_assert(sizeof(P8Stage) >= kP8Waves * 256 * sizeof(float), "epilogue buffer");
+            float hv[kP8NT][4];
+#pragma unroll
+            for (int n = 0; n < kP8NT; ++n) {
+                float m = 0.0f;
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    hv[n][v] = silu_mul(acc[0][n][v], acc[1][n][v]);
+                    m = fmaxf(m, fabsf(hv[n][v]));
+                }
+                m = fmaxf(m, __shfl_xor(m, 16));
+                m = fmaxf(m, __shfl_xor(m, 32));
+                if (g == 0) red[wave * 256 + 16 * n + r] = m;
+            }
+            __syncthreads();
+#pragma unroll
+            for (int n = 0; n < kP8NT; ++n) {
+                const int tn = 16 * n + r;
+                if (n >= nb || tn >= ntok) continue;
+                float m = 0.0f;
+#pragma unroll
+                for (int q = 0; q < kP8Waves; ++q) m = fmaxf(m, red[q * 256 + tn]);
+                const float sc = m > 0.0f ? m / kE4M3Max : 1.0f;
+                const size_t row = (size_t)(row0 + tn);
+                uint32_t word = 0;
+#pragma unroll
+                for (int v = 0; v < 4; ++v) word |= e4m3_code(hv[n][v] / sc) << (8 * v);
+                *(uint32_t*)(p.hq + row * p.f + grp * 128 + 16 * wave + 4 * g) = word;
+                if (wave == 0 && g == 0) p.hst[(size_t)grp * p.P + row] = sc;
+            }
+        } else {
+#pragma unroll
+            for (int n = 0; n < kP8NT; ++n) {
+                const int tn = 16 * n + r;
+                if (n >= nb || tn >= ntok) continue;
+#pragma unroll
+                for (int t = 0; t < 2; ++t)
+                    store_y4(p, (size_t)(row0 + tn), (t ? t1 : t0) * 16 + 4 * g, acc[t][n][0], acc[t][n][1],
+                             acc[t][n][2], acc[t][n][3]);
+            }
+        }
+    }
+}
+
+// Block scales of x for the rows of the big chunks, transposed and in
+// permuted row order: xst[b][row] = xs[token of row][b].  One workgroup per
+// chunk, one thread per row (coalesced stores).
+__global__ __launch_bounds__(256) void k_gather_xs(FfnParams p) {
+    const int nblk = p.d / 128;
+    for (int c = blockIdx.x; c < ffn_list_size(p); c += gridDim.x) {
+        const ChunkRef ck = ffn_chunk(p, c);
+        for (int n = threadIdx.x; n < ck.ntok; n += blockDim.x) {
+            const int row = ck.row0 + n;
+            const float* src = p.xs + (size_t)ffn_token(p, ck.xs, row) * nblk;
+            for (int b = 0; b < nblk; ++b) p.xst[(size_t)b * p.P + row] = src[b];
+        }
+    }
+}
+
+}  // namespace
+
+hipError_t launch_gather_xs(const FfnParams& p, int max_chunks, hipStream_t s) {
+    const int blocks = max_chunks > 0 ? max_chunks : 1;
+    hipLaunchKernelGGL(k_gather_xs, dim3((unsigned)blocks), dim3(256), 0, s, p);
+    return hipGetLastError();
+}
+
+bool gemm_fp8_supports(const FfnParams& p, int nb) {
+    return nb == kP8NT && p.tiled && p.f % 128 == 0 && p.d % 256 == 0 && p.d / 128 <= kP8MaxKBlocks &&
+           p.f / 128 <= kP8MaxKBlocks;
+}
+
+bool gemm_fp8_applies(const caee_layer_desc_t& d, bool tiled) {
+    return kGemmT > 0 && d.w_dtype == CAEE_FP8_E4M3 && d.T > kGemmT && tiled && d.f % 128 == 0 &&
+           d.d % 256 == 0 && d.d / 128 <= kP8MaxKBlocks && d.f / 128 <= kP8MaxKBlocks;
+}
+
+int gemm_fp8_blocks() { return kP8NT; }
+
+bool gemm_fp8_fuses_quant() { return true; }
+
+hipError_t launch_prefill8(const FfnParams& p, bool gate_up, int max_chunks, hipStream_t s) {
+    const int groups = gate_up ? p.f / 128 : p.d / 256;
+    // One workgroup per CU at a time (the ring takes most of the LDS); two
+    // per CU in the grid, so that a CU whose items end early takes more.
+    long long items = (long long)max_chunks * groups;
+    const long long cap = (long long)device_cu_count() * 2;
+    if (items > cap) items = cap;
+    if (items < 1) items = 1;
+    if (gate_up) ffn_launch(k_prefill8<true>, dim3((unsigned)items), dim3(kP8Threads), s, p);
+    else ffn_launch(k_prefill8<false>, dim3((unsigned)items), dim3(kP8Threads), s, p);
+    return hipGetLastError();
+}
+
+}  // namespace caee
