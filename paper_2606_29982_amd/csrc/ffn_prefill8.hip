@@ -7,18 +7,22 @@
 // one chunk over the whole contraction, one 128-deep block per pipeline
 // stage:
 //   * the chunk's token rows (and their block scales) go global -> LDS with
-//     the direct-to-LDS loads, in MFMA B-fragment order, three stages in a
-//     ring; every wave reads every token fragment of a stage from LDS;
+//     direct-to-LDS buffer loads, in MFMA B-fragment order, three stages
+//     ahead of their multiply in a ring of four; every wave reads every
+//     token fragment of a stage from LDS;
 //   * each wave owns two 16-row weight tiles (32 rows), which nobody else
 //     reads: they go global -> registers, two stages ahead of their MFMAs,
 //     and never pass through LDS.
 // So a chunk of up to 256 rows (every routed expert of a 4096-token batch of
 // the DeepSeek-R1 layer) streams each of its weight bytes once, and the
 // bytes in flight per CU are the token ring's plus every wave's register
-// stages.  Per stage a wave issues the same nine loads (four token
-// fragments, one row-scale load, four weight pieces), so it waits for its
-// oldest stage with a constant vmcnt, and one barrier per stage publishes
-// the ring's stage to all waves.
+// stages.  An item is compiled for its chunk's token-tile count rounded up
+// to an even number (2, 4, ..., 16), so every stage is straight-line code:
+// per stage a wave issues the same loads (its share of the token fragments,
+// one row-scale load, four weight pieces) and waits for its oldest stage
+// with a constant vmcnt, one barrier per stage publishes the ring's stage to
+// all waves, and the multiplies of a stage are software-pipelined over the
+// token tiles (fragment reads two tiles ahead, scaling one tile behind).
 //
 // Work items: (chunk, weight group); gate/up groups are 128 features (the
 // gate and up rows of each; wave w takes feature tile w of both), down
@@ -33,6 +37,8 @@
 #include "caee_internal.h"
 #include "fp8_codec.h"
 
+#include <type_traits>
+
 namespace caee {
 namespace {
 
@@ -44,20 +50,10 @@ typedef const __attribute__((address_space(1))) u32x4_t g_u32x4_t;
 
 constexpr int kP8Waves = 8;
 constexpr int kP8Threads = kP8Waves * kWave;
-// Token tiles of an item (16 tokens each) and stages of the load ring.
-#ifndef CAEE_P8_NT
-#define CAEE_P8_NT 16
-#endif
-#ifndef CAEE_P8_RING
-#define CAEE_P8_RING 3
-#endif
-constexpr int kP8NT = CAEE_P8_NT;
-constexpr int kRing = CAEE_P8_RING;
-static_assert(kP8NT % 4 == 0 && kP8NT <= 16, "token tiles: a multiple of 4, at most 16");
-static_assert(kRing == 3 || kRing == 4, "ring of 3 or 4 stages");
-constexpr int kP8TokLoads = 2 * kP8NT / kP8Waves;  // token fragment loads per wave and stage
-constexpr int kP8Loads = kP8TokLoads + 1 + 4;      // + row scales + two tiles x two halves of weights
+// Token tiles of an item at most (16 tokens each: chunks of up to 256 rows).
+constexpr int kP8NT = 16;
 constexpr int kP8MaxKBlocks = 128;        // contraction up to 16384
+constexpr int kBufWord3 = 0x00020000;      // buffer descriptor word 3: 32-bit data format, raw access
 constexpr int kScaleOne = 127;            // E8M0 1.0: the MFMA's own block scales are unused
 constexpr int kXcds = 8;                  // accelerator complex dies, each with its own L2
 // Items grouped by XCD: all weight groups of a chunk run on one XCD, so its
@@ -99,10 +95,23 @@ struct WReg {
     u32x4_t v[2][2];
 };
 
+template <int N>
+using IntC = std::integral_constant<int, N>;
+
+// Token tiles whose fragments a stage's multiply reads from LDS ahead of
+// their MFMAs: two, or one for the widest items (whose accumulators leave no
+// registers for a third fragment).
+#ifndef CAEE_P8_AHEAD_MAX_NB
+#define CAEE_P8_AHEAD_MAX_NB 12
+#endif
+constexpr int kP8Ahead(int nb) { return nb <= CAEE_P8_AHEAD_MAX_NB ? 2 : 1; }
+
 template <bool kGateUp>
 __global__ __launch_bounds__(kP8Threads) void k_prefill8(FfnParams p) {
-    // Separate LDS objects, each named statically below, so that the
-    // compiler can tell a read of one stage from the loads filling another.
+#if defined(__HIP_DEVICE_COMPILE__)   // the buffer-descriptor type exists for the GPU target only
+    // Token ring: block v's token fragments and row scales in slot v % 4.
+    // Four LDS objects, each named statically below, so that the compiler
+    // can tell a read of one slot from the loads filling another.
     __shared__ P8Stage st0, st1, st2, st3;
     __shared__ float wsl[2][kP8MaxKBlocks];   // weight block scales of the item's two 128-row scale rows
     const int tid = threadIdx.x, lane = tid & (kWave - 1);
@@ -117,6 +126,14 @@ __global__ __launch_bounds__(kP8Threads) void k_prefill8(FfnParams p) {
     const size_t expert_bytes = kGateUp ? (size_t)2 * p.f * p.d : (size_t)p.d * p.f;
     const size_t scales_per_expert = (size_t)((kGateUp ? 2 * p.f : p.d) / 128) * kblocks;
     const f32x4_t zero = {0.f, 0.f, 0.f, 0.f};
+    // Token rows (e4m3 codes) and their transposed block scales; loads past
+    // the end of a buffer return zero.
+    const uint32_t tbytes = kGateUp ? (uint32_t)((size_t)p.T * p.d) : (uint32_t)((size_t)p.P * p.f);
+    const uint32_t sbytes = (uint32_t)((size_t)kblocks * p.P * 4);
+    const __amdgpu_buffer_rsrc_t tbuf =
+        __builtin_amdgcn_make_buffer_rsrc((void*)(kGateUp ? p.xq : p.hq), 0, (int)tbytes, kBufWord3);
+    const __amdgpu_buffer_rsrc_t sbuf =
+        __builtin_amdgcn_make_buffer_rsrc((void*)(kGateUp ? p.xst : p.hst), 0, (int)sbytes, kBufWord3);
 
     // Item order: plain (workgroup b takes items b, b + grid, ...), or by
     // XCD (XCD x takes the chunks x, x + 8, ..., all groups of each, its
@@ -142,21 +159,14 @@ __global__ __launch_bounds__(kP8Threads) void k_prefill8(FfnParams p) {
         const int srow1 = kGateUp ? p.f / 128 + grp : 2 * grp + 1; // wsl[1]
         const int ws0 = kGateUp ? 0 : (wave >= 4 ? 1 : 0), ws1 = kGateUp ? 1 : ws0;
         const u32x4_t* wsrc[2] = {wb + (size_t)t0 * ksteps * 64 + lane, wb + (size_t)t1 * ksteps * 64 + lane};
-        // Token fragments j = 4 * wave + i: token tile j / 2, half j % 2.
-        const u32x4_t* tsrc[kP8TokLoads];
-#pragma unroll
-        for (int i = 0; i < kP8TokLoads; ++i) {
-            const int j = kP8TokLoads * wave + i;
-            int n = 16 * (j >> 1) + r;
-            n = n < ntok ? n : 0;          // padded token columns read a valid row; results dropped
-            const size_t row = kGateUp ? (size_t)ffn_token(p, xs, row0 + n) : (size_t)(row0 + n);
-            tsrc[i] = (const u32x4_t*)(kGateUp ? p.xq : p.hq) + row * row_units + (j & 1) * 4 + g;
-        }
         // Row scales, transposed and in permuted row order ([block][row]):
         // wave w loads tokens 32w .. 32w + 31 (lanes 32..63 repeat them).
         int xn = 32 * wave + (lane & 31);
         xn = xn < ntok ? xn : 0;
-        const float* xsrc = (kGateUp ? p.xst : p.hst) + row0 + xn;
+        // Byte offsets within the buffers the direct-to-LDS loads read (the
+        // host keeps every buffer below 4 GiB): buffer loads, whose waits the
+        // compiler counts apart from the LDS reads of the multiply.
+        const uint32_t xoff = (uint32_t)(row0 + xn) * 4u;
 
         for (int q = tid; q < 2 * kblocks; q += kP8Threads) {
             const int h = q >= kblocks, kb = q - h * kblocks;
@@ -164,137 +174,237 @@ __global__ __launch_bounds__(kP8Threads) void k_prefill8(FfnParams p) {
         }
         __syncthreads();
 
-        auto issue = [&](int kb, P8Stage& s, WReg& w) __attribute__((always_inline)) {
+        // The item for NB token tiles (the chunk's tile count rounded up to
+        // an even number): loads, multiplies and waits are all fixed by NB,
+        // so each stage is straight-line code whose waits the compiler can
+        // count exactly.
+        auto run = [&](auto nbc) __attribute__((always_inline)) {
+            constexpr int NB = decltype(nbc)::value;
+            // Token fragments of a stage: 2 NB (tile n, half h at 2n + h),
+            // kTok per wave; fragments past 2 NB (when 8 kTok > 2 NB) read
+            // row 0 into stage slots nobody multiplies.
+            constexpr int kTok = (2 * NB + kP8Waves - 1) / kP8Waves;
+            constexpr int kLoads = kTok + 1 + 4;   // + row scales + two tiles x two halves of weights
+            static_assert(kTok * kP8Waves <= 2 * kP8NT, "stage slots");
+            uint32_t toff[kTok];
 #pragma unroll
-            for (int i = 0; i < kP8TokLoads; ++i)
-                __builtin_amdgcn_global_load_lds((const void*)(tsrc[i] + (size_t)kb * 8),
-                                                 (lds_void_t*)&s.f[kP8TokLoads * wave + i][0], 16, 0, 0);
-            __builtin_amdgcn_global_load_lds((const void*)(xsrc + (size_t)kb * p.P), (lds_void_t*)&s.x[wave][0], 4,
-                                             0, 0);
+            for (int i = 0; i < kTok; ++i) {
+                const int j = kTok * wave + i;
+                int n = 16 * (j >> 1) + r;
+                n = n < ntok ? n : 0;          // padded token columns read a valid row; results dropped
+                const uint32_t row = kGateUp ? (uint32_t)ffn_token(p, xs, row0 + n) : (uint32_t)(row0 + n);
+                toff[i] = (row * (uint32_t)row_units + (uint32_t)((j & 1) * 4 + g)) * 16u;
+            }
+
+            auto issue_tok = [&](int kb, P8Stage& s) __attribute__((always_inline)) {
+#pragma unroll
+                for (int i = 0; i < kTok; ++i)
+                    __builtin_amdgcn_raw_ptr_buffer_load_lds(tbuf, (lds_void_t*)&s.f[kTok * wave + i][0], 16, toff[i],
+                                                             kb * 128, 0, 0);
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(sbuf, (lds_void_t*)&s.x[wave][0], 4, xoff, kb * p.P * 4, 0, 0);
+            };
+            auto issue_w = [&](int kb, WReg& w) __attribute__((always_inline)) {
+#pragma unroll
+                for (int t = 0; t < 2; ++t)
+#pragma unroll
+                    for (int h = 0; h < 2; ++h)
+                        w.v[t][h] = __builtin_nontemporal_load((g_u32x4_t*)(wsrc[t] + (size_t)(2 * kb + h) * 64));
+            };
+
+            f32x4_t acc[2][NB];
 #pragma unroll
             for (int t = 0; t < 2; ++t)
 #pragma unroll
-                for (int h = 0; h < 2; ++h)
-                    w.v[t][h] = __builtin_nontemporal_load((g_u32x4_t*)(wsrc[t] + (size_t)(2 * kb + h) * 64));
-        };
+                for (int n = 0; n < NB; ++n) acc[t][n] = zero;
 
-        f32x4_t acc[2][kP8NT];
-#pragma unroll
-        for (int t = 0; t < 2; ++t)
-#pragma unroll
-            for (int n = 0; n < kP8NT; ++n) acc[t][n] = zero;
-
-        auto compute = [&](int kb, const P8Stage& s, const WReg& w) __attribute__((always_inline)) {
-            const i32x8_t a0 = join(w.v[0][0], w.v[0][1]), a1 = join(w.v[1][0], w.v[1][1]);
-            const float wa = wsl[ws0][kb], wc = wsl[ws1][kb];
-#pragma unroll
-            for (int n = 0; n < kP8NT; ++n) {
-                if (n < nb) {
-                    const i32x8_t bf = join(s.f[2 * n][lane], s.f[2 * n + 1][lane]);
+            // One stage: per token tile two MFMAs (one per weight tile) on its
+            // fragment.  Software-pipelined over the tiles: while tile n's
+            // MFMAs run, the fragment and row scale of tile n + 2 are read
+            // from LDS and tile n - 1's partial sums (its MFMAs are done) are
+            // scaled into their accumulators, so neither the LDS latency nor
+            // the MFMA latency is waited for in line.
+            auto compute = [&](int kb, const P8Stage& s, const WReg& w) __attribute__((always_inline)) {
+                const i32x8_t a0 = join(w.v[0][0], w.v[0][1]), a1 = join(w.v[1][0], w.v[1][1]);
+                const float wa = wsl[ws0][kb], wc = wsl[ws1][kb];
+                auto frag = [&](int n) __attribute__((always_inline)) {
+                    return join(s.f[2 * n][lane], s.f[2 * n + 1][lane]);
+                };
+                auto xsc = [&](int n) __attribute__((always_inline)) {
                     const int tok = 16 * n + r;
-                    const float xv = s.x[tok >> 5][tok & 31];
-                    const f32x4_t p0 =
-                        __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a0, bf, zero, 0, 0, 0, kScaleOne, 0, kScaleOne);
-                    const f32x4_t p1 =
-                        __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a1, bf, zero, 0, 0, 0, kScaleOne, 0, kScaleOne);
-                    acc[0][n] += p0 * (wa * xv);
-                    acc[1][n] += p1 * (wc * xv);
+                    return s.x[tok >> 5][tok & 31];
+                };
+                constexpr int D = kP8Ahead(NB);   // fragment reads ahead of their MFMAs
+                i32x8_t bq[D + 1];
+                float xq[D + 1];
+#pragma unroll
+                for (int n = 0; n < D && n < NB; ++n) {
+                    bq[n] = frag(n);
+                    xq[n] = xsc(n);
                 }
-                // One token tile's fragment and partial sums live at a time
-                // (hoisting all sixteen would spill the accumulators); the
-                // other wave of the SIMD covers the MFMA latency.
-                __builtin_amdgcn_sched_barrier(0);
-            }
-        };
+                f32x4_t pp0 = zero, pp1 = zero;
+                float ps0 = 0.0f, ps1 = 0.0f;
+#pragma unroll
+                for (int n = 0; n < NB; ++n) {
+                    if (n + D < NB) {
+                        bq[(n + D) % (D + 1)] = frag(n + D);
+                        xq[(n + D) % (D + 1)] = xsc(n + D);
+                    }
+                    const i32x8_t& b = bq[n % (D + 1)];
+                    const f32x4_t q0 =
+                        __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a0, b, zero, 0, 0, 0, kScaleOne, 0, kScaleOne);
+                    const f32x4_t q1 =
+                        __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a1, b, zero, 0, 0, 0, kScaleOne, 0, kScaleOne);
+                    if (n > 0) {
+                        acc[0][n - 1] += pp0 * ps0;
+                        acc[1][n - 1] += pp1 * ps1;
+                    }
+                    pp0 = q0;
+                    pp1 = q1;
+                    ps0 = wa * xq[n % (D + 1)];
+                    ps1 = wc * xq[n % (D + 1)];
+                    // Issue order within the tile: its two MFMAs, the LDS
+                    // reads of tile n + D, then the VALU work (tile n - 1's
+                    // scaling, whose MFMAs are done by now, and tile n's
+                    // scale factors).
+                    __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+                    if (n + D < NB) __builtin_amdgcn_sched_group_barrier(0x100, 3, 0);
+                    if (n > 0) __builtin_amdgcn_sched_group_barrier(0x002, 10, 0);
+                    else __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
+                    __builtin_amdgcn_sched_barrier(0);
+                }
+                acc[0][NB - 1] += pp0 * ps0;
+                acc[1][NB - 1] += pp1 * ps1;
+            };
 
-        // Step v waits for this wave's loads of block v - (kRing - 1) (those
-        // of the later blocks may stay in flight), passes a barrier that
-        // publishes every wave's token loads of that block and guarantees
-        // that all waves are done with block v - kRing, refills that stage
-        // and register set with block v, and multiplies block v - (kRing - 1).
-        // The steps run in whole groups of kRing, so every step issues its
-        // loads unconditionally (steps past the last block re-read it, from
-        // L2, into a stage nobody multiplies) and the compiler's wait analysis
-        // sees the same loads per step on every path: the only waits in the
-        // loop are the kernel's own.  One code path for every step, so the
-        // accumulators live in one set of registers throughout.
-        constexpr int kAhead = kRing - 1;
-        WReg w0, w1, w2, w3;
-        const int nsteps = (kblocks + kAhead + kRing - 1) / kRing * kRing;
-        auto step = [&](int v, P8Stage& fill, WReg& wf, const P8Stage& use, const WReg& wu)
-                        __attribute__((always_inline)) {
-            wait_vm<(kAhead - 1) * kP8Loads>();
-            stage_barrier();
-            issue(v < kblocks ? v : kblocks - 1, fill, wf);
-            if (v >= kAhead && v - kAhead < kblocks) compute(v - kAhead, use, wu);
-        };
+            // Token rows go three blocks ahead of their multiply (ring of
+            // four), weights two (three register sets): step v issues the
+            // tokens of block v + 1 and the weights of block v, and
+            // multiplies block v - 2.  It first waits until at most the loads
+            // of the previous step are outstanding (so this wave's tokens and
+            // weights of block v - 2 have landed: loads complete in order)
+            // and passes a barrier that publishes every wave's token loads of
+            // block v - 2 and guarantees that all waves are done with block
+            // v - 3, whose ring slot the tokens of v + 1 refill.  The steps run
+            // in whole groups of three, so every step issues its loads
+            // unconditionally (steps past the last block re-read it, from L2,
+            // into a slot nobody multiplies) and the compiler's wait analysis
+            // sees the same loads per step on every path: the only waits in
+            // the loop are the kernel's own.  One code path for every step, so
+            // the accumulators live in one set of registers throughout.
+            WReg w0, w1, w2;
+            auto slot = [&](auto jc) -> P8Stage& {
+                constexpr int J = decltype(jc)::value & 3;
+                if constexpr (J == 0) return st0;
+                else if constexpr (J == 1) return st1;
+                else if constexpr (J == 2) return st2;
+                else return st3;
+            };
+            auto wset = [&](auto jc) -> WReg& {
+                constexpr int J = decltype(jc)::value % 3;
+                if constexpr (J == 0) return w0;
+                else if constexpr (J == 1) return w1;
+                else return w2;
+            };
+            issue_tok(0, st0);
+            // Step v = 12 m + J (J static: slot and register set are named).
+            auto step = [&](int v, auto jc) __attribute__((always_inline)) {
+                constexpr int J = decltype(jc)::value;
+                wait_vm<kLoads>();
+                stage_barrier();
+                const int vt = v + 1 < kblocks ? v + 1 : kblocks - 1;
+                issue_tok(vt, slot(IntC<J + 1>{}));
+                issue_w(v < kblocks ? v : kblocks - 1, wset(IntC<J>{}));
+                if (v >= 2 && v - 2 < kblocks) compute(v - 2, slot(IntC<J + 2>{}), wset(IntC<J + 1>{}));
+            };
+            // Whole groups of three steps; the twelve-step body (lcm of the
+            // ring and the register sets) is entered at the group the
+            // remaining step count needs, so at most two steps past the
+            // first one without a multiply are run.
+            const int nsteps = (kblocks + 2 + 2) / 3 * 3;
 #pragma clang loop unroll(disable)
-        for (int v = 0; v < nsteps; v += kRing) {
-            if constexpr (kRing == 3) {
-                step(v, st0, w0, st1, w1);
-                step(v + 1, st1, w1, st2, w2);
-                step(v + 2, st2, w2, st0, w0);
-            } else {
-                step(v, st0, w0, st1, w1);
-                step(v + 1, st1, w1, st2, w2);
-                step(v + 2, st2, w2, st3, w3);
-                step(v + 3, st3, w3, st0, w0);
+            for (int v = 0; v < nsteps; v += 12) {
+                step(v, IntC<0>{});
+                step(v + 1, IntC<1>{});
+                step(v + 2, IntC<2>{});
+                if (v + 3 >= nsteps) break;
+                step(v + 3, IntC<3>{});
+                step(v + 4, IntC<4>{});
+                step(v + 5, IntC<5>{});
+                if (v + 6 >= nsteps) break;
+                step(v + 6, IntC<6>{});
+                step(v + 7, IntC<7>{});
+                step(v + 8, IntC<8>{});
+                if (v + 9 >= nsteps) break;
+                step(v + 9, IntC<9>{});
+                step(v + 10, IntC<10>{});
+                step(v + 11, IntC<11>{});
             }
-        }
-        wait_vm<0>();   // the re-reads past the last block have landed
-        // Every wave is done with the ring before the epilogue reuses st0 and
-        // the next item refills it.
-        stage_barrier();
+            wait_vm<0>();   // the re-reads past the last block have landed
+            // Every wave is done with the ring before the epilogue reuses
+            // st0 and the next item refills it.
+            stage_barrier();
 
-        if constexpr (kGateUp) {
-            // Lane (r, g) holds features 16 * wave + 4g .. + 3 of the group
-            // for token 16n + r.  Per token: amax over the group's 128 SwiGLU
-            // values (this lane's 4, the 4 lanes of the column, the 8 waves
-            // through LDS), scale = amax / 448 (1 if zero), codes of value /
-            // scale: the activation quantiser's arithmetic.
-            float* red = reinterpret_cast<float*>(&st0);   // [wave][256 tokens]; the ring is idle
-            static_assert(sizeof(P8Stage) >= kP8Waves * 256 * sizeof(float), "epilogue buffer");
-            float hv[kP8NT][4];
+            if constexpr (kGateUp) {
+                // Lane (r, g) holds features 16 * wave + 4g .. + 3 of the group
+                // for token 16n + r.  Per token: amax over the group's 128
+                // SwiGLU values (this lane's 4, the 4 lanes of the column, the
+                // 8 waves through LDS), scale = amax / 448 (1 if zero), codes
+                // of value / scale: the activation quantiser's arithmetic.
+                float* red = reinterpret_cast<float*>(&st0);   // [wave][256 tokens]; the ring is idle
+                static_assert(sizeof(P8Stage) >= kP8Waves * 256 * sizeof(float), "epilogue buffer");
+                float hv[NB][4];
 #pragma unroll
-            for (int n = 0; n < kP8NT; ++n) {
-                float m = 0.0f;
+                for (int n = 0; n < NB; ++n) {
+                    float m = 0.0f;
 #pragma unroll
-                for (int v = 0; v < 4; ++v) {
-                    hv[n][v] = silu_mul(acc[0][n][v], acc[1][n][v]);
-                    m = fmaxf(m, fabsf(hv[n][v]));
+                    for (int v = 0; v < 4; ++v) {
+                        hv[n][v] = silu_mul(acc[0][n][v], acc[1][n][v]);
+                        m = fmaxf(m, fabsf(hv[n][v]));
+                    }
+                    m = fmaxf(m, __shfl_xor(m, 16));
+                    m = fmaxf(m, __shfl_xor(m, 32));
+                    if (g == 0) red[wave * 256 + 16 * n + r] = m;
                 }
-                m = fmaxf(m, __shfl_xor(m, 16));
-                m = fmaxf(m, __shfl_xor(m, 32));
-                if (g == 0) red[wave * 256 + 16 * n + r] = m;
+                __syncthreads();
+#pragma unroll
+                for (int n = 0; n < NB; ++n) {
+                    const int tn = 16 * n + r;
+                    if (n >= nb || tn >= ntok) continue;
+                    float m = 0.0f;
+#pragma unroll
+                    for (int q = 0; q < kP8Waves; ++q) m = fmaxf(m, red[q * 256 + tn]);
+                    const float sc = m > 0.0f ? m / kE4M3Max : 1.0f;
+                    const size_t row = (size_t)(row0 + tn);
+                    uint32_t word = 0;
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) word |= e4m3_code(hv[n][v] / sc) << (8 * v);
+                    *(uint32_t*)(p.hq + row * p.f + grp * 128 + 16 * wave + 4 * g) = word;
+                    if (wave == 0 && g == 0) p.hst[(size_t)grp * p.P + row] = sc;
+                }
+            } else {
+#pragma unroll
+                for (int n = 0; n < NB; ++n) {
+                    const int tn = 16 * n + r;
+                    if (n >= nb || tn >= ntok) continue;
+#pragma unroll
+                    for (int t = 0; t < 2; ++t)
+                        store_y4(p, (size_t)(row0 + tn), (t ? t1 : t0) * 16 + 4 * g, acc[t][n][0], acc[t][n][1],
+                                 acc[t][n][2], acc[t][n][3]);
+                }
             }
-            __syncthreads();
-#pragma unroll
-            for (int n = 0; n < kP8NT; ++n) {
-                const int tn = 16 * n + r;
-                if (n >= nb || tn >= ntok) continue;
-                float m = 0.0f;
-#pragma unroll
-                for (int q = 0; q < kP8Waves; ++q) m = fmaxf(m, red[q * 256 + tn]);
-                const float sc = m > 0.0f ? m / kE4M3Max : 1.0f;
-                const size_t row = (size_t)(row0 + tn);
-                uint32_t word = 0;
-#pragma unroll
-                for (int v = 0; v < 4; ++v) word |= e4m3_code(hv[n][v] / sc) << (8 * v);
-                *(uint32_t*)(p.hq + row * p.f + grp * 128 + 16 * wave + 4 * g) = word;
-                if (wave == 0 && g == 0) p.hst[(size_t)grp * p.P + row] = sc;
-            }
-        } else {
-#pragma unroll
-            for (int n = 0; n < kP8NT; ++n) {
-                const int tn = 16 * n + r;
-                if (n >= nb || tn >= ntok) continue;
-#pragma unroll
-                for (int t = 0; t < 2; ++t)
-                    store_y4(p, (size_t)(row0 + tn), (t ? t1 : t0) * 16 + 4 * g, acc[t][n][0], acc[t][n][1],
-                             acc[t][n][2], acc[t][n][3]);
-            }
+        };
+        switch ((nb + 1) >> 1) {
+            case 1: run(IntC<2>{}); break;
+            case 2: run(IntC<4>{}); break;
+            case 3: run(IntC<6>{}); break;
+            case 4: run(IntC<8>{}); break;
+            case 5: run(IntC<10>{}); break;
+            case 6: run(IntC<12>{}); break;
+            case 7: run(IntC<14>{}); break;
+            default: run(IntC<16>{}); break;
         }
     }
+#endif
 }
 
 // Block scales of x for the rows of the big chunks, transposed and in
@@ -320,14 +430,22 @@ hipError_t launch_gather_xs(const FfnParams& p, int max_chunks, hipStream_t s) {
     return hipGetLastError();
 }
 
+// The buffers the kernel reads through buffer descriptors (token codes and
+// block scales of x and of the SwiGLU rows) must hold fewer than 2^31 bytes.
+static bool p8_buffers_fit(long long T, long long P, long long d, long long f) {
+    const long long lim = 1LL << 31;
+    return T * d < lim && P * f < lim && (d / 128) * P * 4 < lim && (f / 128) * P * 4 < lim;
+}
+
 bool gemm_fp8_supports(const FfnParams& p, int nb) {
     return nb == kP8NT && p.tiled && p.f % 128 == 0 && p.d % 256 == 0 && p.d / 128 <= kP8MaxKBlocks &&
-           p.f / 128 <= kP8MaxKBlocks;
+           p.f / 128 <= kP8MaxKBlocks && p8_buffers_fit(p.T, p.P, p.d, p.f);
 }
 
 bool gemm_fp8_applies(const caee_layer_desc_t& d, bool tiled) {
     return kGemmT > 0 && d.w_dtype == CAEE_FP8_E4M3 && d.T > kGemmT && tiled && d.f % 128 == 0 &&
-           d.d % 256 == 0 && d.d / 128 <= kP8MaxKBlocks && d.f / 128 <= kP8MaxKBlocks;
+           d.d % 256 == 0 && d.d / 128 <= kP8MaxKBlocks && d.f / 128 <= kP8MaxKBlocks &&
+           p8_buffers_fit(d.T, (long long)d.T * (d.k + d.n_shared), d.d, d.f);
 }
 
 int gemm_fp8_blocks() { return kP8NT; }
