@@ -61,6 +61,8 @@ def parse():
     ap.add_argument("--case", default=None,
                     help="time one configuration only, DTYPE:T[:skewed] (e.g. bf16:128:skewed, fp8:4096), "
                          "and print its line instead of the headline")
+    ap.add_argument("--graph", action="store_true",
+                    help="with --case: also time single flushed graph replays (the survey's protocol) and print them")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="finish with one device-to-device copy of this many bytes (a known-size "
                          "reference for HBM traffic counters)")
@@ -356,9 +358,14 @@ def run_case(args, dev):
     ms = time_steps(c, args.steps, args.warmup)
     s = c.stats()
     b = (s[5] + shape.n_shared) * (W_EXPERT_BYTES if dtype == "bf16" else W_EXPERT_BYTES_FP8)
-    print(json.dumps({"case": args.case, "us_per_step": round(ms * 1e3, 1), "tokens_per_s": round(T / (ms * 1e-3), 1),
-                      "weight_gbps": round(b / (ms * 1e-3) / 1e9, 1), "executed": s[5] + shape.n_shared,
-                      "steps": args.steps, "warmup": args.warmup}), flush=True)
+    line = {"case": args.case, "us_per_step": round(ms * 1e3, 1), "tokens_per_s": round(T / (ms * 1e-3), 1),
+            "weight_gbps": round(b / (ms * 1e-3) / 1e9, 1), "executed": s[5] + shape.n_shared,
+            "steps": args.steps, "warmup": args.warmup}
+    if args.graph:
+        gp = graph_protocol(c)
+        line["graph_protocol"] = gp
+        line["weight_frac_flushed"] = round(b / (gp["us_p50"] * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4)
+    print(json.dumps(line), flush=True)
 
 
 def ablation_rows(args, shape, Wt, dev):
