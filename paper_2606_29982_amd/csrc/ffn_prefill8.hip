@@ -8,16 +8,18 @@
 // stage:
 //   * the chunk's token rows (and their block scales) go global -> LDS with
 //     direct-to-LDS buffer loads, in MFMA B-fragment order, three stages
-//     ahead of their multiply in a ring of four; every wave reads every
-//     token fragment of a stage from LDS;
+//     ahead of their multiply in a ring of four, issued among the multiplies
+//     of the stage before; every wave reads every token fragment of a stage
+//     from LDS;
 //   * each wave owns two 16-row weight tiles (32 rows), which nobody else
-//     reads: they go global -> registers, two stages ahead of their MFMAs,
-//     and never pass through LDS.
+//     reads: they go global -> registers, three stages ahead of their MFMAs
+//     (two for items of more than 12 token tiles, whose accumulators leave
+//     room for three register sets only), and never pass through LDS.
 // So a chunk of up to 256 rows (every routed expert of a 4096-token batch of
 // the DeepSeek-R1 layer) streams each of its weight bytes once, and the
 // bytes in flight per CU are the token ring's plus every wave's register
-// stages.  An item is compiled for its chunk's token-tile count rounded up
-// to an even number (2, 4, ..., 16), so every stage is straight-line code:
+// stages.  An item is compiled for its chunk's token-tile count (1 .. 16),
+// so every stage is straight-line code:
 // per stage a wave issues the same loads (its share of the token fragments,
 // one row-scale load, four weight pieces) and waits for its oldest stage
 // with a constant vmcnt, one barrier per stage publishes the ring's stage to
@@ -98,6 +100,16 @@ struct WReg {
 template <int N>
 using IntC = std::integral_constant<int, N>;
 
+// f(IntC<B>{}), ..., f(IntC<E - 1>{}): a loop whose index is a constant in
+// every copy of the body.
+template <int B, int E, class F>
+__device__ __attribute__((always_inline)) inline void static_for(F&& f) {
+    if constexpr (B < E) {
+        f(IntC<B>{});
+        static_for<B + 1, E>(f);
+    }
+}
+
 // Token tiles whose fragments a stage's multiply reads from LDS ahead of
 // their MFMAs: two, or one for the widest items (whose accumulators leave no
 // registers for a third fragment).
@@ -105,6 +117,27 @@ using IntC = std::integral_constant<int, N>;
 #define CAEE_P8_AHEAD_MAX_NB 12
 #endif
 constexpr int kP8Ahead(int nb) { return nb <= CAEE_P8_AHEAD_MAX_NB ? 2 : 1; }
+
+// Weight register sets of a stage loop: four (weights loaded three blocks
+// ahead of their multiply) up to this many token tiles, three (two blocks
+// ahead) above, where the accumulators leave no room for a fourth set.
+#ifndef CAEE_P8_W4_MAX_NB
+#define CAEE_P8_W4_MAX_NB 12
+#endif
+constexpr int kP8WSets(int nb) { return nb <= CAEE_P8_W4_MAX_NB ? 4 : 3; }
+
+// Token-row loads of a step issued among the multiplies of its tiles (1), or
+// all at once before them (0).  (Spreading the weight loads the same way
+// measured slower.)
+#ifndef CAEE_P8_SPREAD
+#define CAEE_P8_SPREAD 1
+#endif
+
+// Token tiles an item is compiled for: its chunk's count rounded up to an
+// even number (1), or the count itself (0).
+#ifndef CAEE_P8_EVEN
+#define CAEE_P8_EVEN 0
+#endif
 
 template <bool kGateUp>
 __global__ __launch_bounds__(kP8Threads) void k_prefill8(FfnParams p) {
@@ -223,7 +256,24 @@ __global__ __launch_bounds__(kP8Threads) void k_prefill8(FfnParams p) {
             // from LDS and tile n - 1's partial sums (its MFMAs are done) are
             // scaled into their accumulators, so neither the LDS latency nor
             // the MFMA latency is waited for in line.
-            auto compute = [&](int kb, const P8Stage& s, const WReg& w) __attribute__((always_inline)) {
+            // Load k of a step (kTok token fragments, the row scales, then the
+            // four weight pieces): compute() can spread the token loads over
+            // its tiles.
+            auto issue_one = [&](auto kc, int vt, P8Stage& st, int vw, WReg& w) __attribute__((always_inline)) {
+                constexpr int k = decltype(kc)::value;
+                if constexpr (k < kTok) {
+                    __builtin_amdgcn_raw_ptr_buffer_load_lds(tbuf, (lds_void_t*)&st.f[kTok * wave + k][0], 16, toff[k],
+                                                             vt * 128, 0, 0);
+                } else if constexpr (k == kTok) {
+                    __builtin_amdgcn_raw_ptr_buffer_load_lds(sbuf, (lds_void_t*)&st.x[wave][0], 4, xoff, vt * p.P * 4, 0,
+                                                             0);
+                } else {
+                    constexpr int q = k - kTok - 1, t = q >> 1, h = q & 1;
+                    w.v[t][h] = __builtin_nontemporal_load((g_u32x4_t*)(wsrc[t] + (size_t)(2 * vw + h) * 64));
+                }
+            };
+            auto compute = [&](int kb, const P8Stage& s, const WReg& w, int vt, P8Stage& st, int vw,
+                               WReg& wn) __attribute__((always_inline)) {
                 const i32x8_t a0 = join(w.v[0][0], w.v[0][1]), a1 = join(w.v[1][0], w.v[1][1]);
                 const float wa = wsl[ws0][kb], wc = wsl[ws1][kb];
                 auto frag = [&](int n) __attribute__((always_inline)) {
@@ -243,9 +293,9 @@ __global__ __launch_bounds__(kP8Threads) void k_prefill8(FfnParams p) {
                 }
                 f32x4_t pp0 = zero, pp1 = zero;
                 float ps0 = 0.0f, ps1 = 0.0f;
-#pragma unroll
-                for (int n = 0; n < NB; ++n) {
-                    if (n + D < NB) {
+                static_for<0, NB>([&](auto nc) __attribute__((always_inline)) {
+                    constexpr int n = decltype(nc)::value;
+                    if constexpr (n + D < NB) {
                         bq[(n + D) % (D + 1)] = frag(n + D);
                         xq[(n + D) % (D + 1)] = xsc(n + D);
                     }
@@ -254,7 +304,7 @@ __global__ __launch_bounds__(kP8Threads) void k_prefill8(FfnParams p) {
                         __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a0, b, zero, 0, 0, 0, kScaleOne, 0, kScaleOne);
                     const f32x4_t q1 =
                         __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a1, b, zero, 0, 0, 0, kScaleOne, 0, kScaleOne);
-                    if (n > 0) {
+                    if constexpr (n > 0) {
                         acc[0][n - 1] += pp0 * ps0;
                         acc[1][n - 1] += pp1 * ps1;
                     }
@@ -266,32 +316,42 @@ __global__ __launch_bounds__(kP8Threads) void k_prefill8(FfnParams p) {
                     // reads of tile n + D, then the VALU work (tile n - 1's
                     // scaling, whose MFMAs are done by now, and tile n's
                     // scale factors).
+                    // Token-row loads of this tile: [n L / NB, (n + 1) L / NB) of the
+                    // step's L = kTok + 1.
+                    constexpr int lo = CAEE_P8_SPREAD ? n * (kTok + 1) / NB : 0;
+                    constexpr int hi = CAEE_P8_SPREAD ? (n + 1) * (kTok + 1) / NB : 0;
+                    static_for<lo, hi>([&](auto kc) __attribute__((always_inline)) { issue_one(kc, vt, st, vw, wn); });
                     __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
-                    if (n + D < NB) __builtin_amdgcn_sched_group_barrier(0x100, 3, 0);
-                    if (n > 0) __builtin_amdgcn_sched_group_barrier(0x002, 10, 0);
+                    static_for<lo, hi>([&](auto) __attribute__((always_inline)) {
+                        __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+                    });
+                    if constexpr (n + D < NB) __builtin_amdgcn_sched_group_barrier(0x100, 3, 0);
+                    if constexpr (n > 0) __builtin_amdgcn_sched_group_barrier(0x002, 10, 0);
                     else __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
                     __builtin_amdgcn_sched_barrier(0);
-                }
+                });
                 acc[0][NB - 1] += pp0 * ps0;
                 acc[1][NB - 1] += pp1 * ps1;
             };
 
             // Token rows go three blocks ahead of their multiply (ring of
-            // four), weights two (three register sets): step v issues the
-            // tokens of block v + 1 and the weights of block v, and
-            // multiplies block v - 2.  It first waits until at most the loads
-            // of the previous step are outstanding (so this wave's tokens and
-            // weights of block v - 2 have landed: loads complete in order)
+            // four), weights three (four register sets) or two (three sets):
+            // step v issues the tokens of block v + 1 and the weights of
+            // block v + 1 (or v), and multiplies block v - 2.  It first waits
+            // until at most the loads of the previous two steps (one step)
+            // are outstanding (so this wave's tokens and weights of block
+            // v - 2 have landed: loads complete in order)
             // and passes a barrier that publishes every wave's token loads of
             // block v - 2 and guarantees that all waves are done with block
             // v - 3, whose ring slot the tokens of v + 1 refill.  The steps run
-            // in whole groups of three, so every step issues its loads
+            // in whole groups (of two, or of three), so every step issues its loads
             // unconditionally (steps past the last block re-read it, from L2,
             // into a slot nobody multiplies) and the compiler's wait analysis
             // sees the same loads per step on every path: the only waits in
             // the loop are the kernel's own.  One code path for every step, so
             // the accumulators live in one set of registers throughout.
-            WReg w0, w1, w2;
+            constexpr int NW = kP8WSets(NB);
+            WReg w0, w1, w2, w3;
             auto slot = [&](auto jc) -> P8Stage& {
                 constexpr int J = decltype(jc)::value & 3;
                 if constexpr (J == 0) return st0;
@@ -300,26 +360,51 @@ __global__ __launch_bounds__(kP8Threads) void k_prefill8(FfnParams p) {
                 else return st3;
             };
             auto wset = [&](auto jc) -> WReg& {
-                constexpr int J = decltype(jc)::value % 3;
+                constexpr int J = decltype(jc)::value % NW;
                 if constexpr (J == 0) return w0;
                 else if constexpr (J == 1) return w1;
-                else return w2;
+                else if constexpr (J == 2) return w2;
+                else return w3;
             };
             issue_tok(0, st0);
-            // Step v = 12 m + J (J static: slot and register set are named).
+            if constexpr (NW == 4) issue_w(0, w0);
+            // Step v = 12 m + J, or 4 m + J with four weight sets (J static:
+            // slot and register set are named).  With four sets step v
+            // loads the weights of block v + 1 and waits for the loads of
+            // step v - 3 (the tokens and weights of block v - 2).
             auto step = [&](int v, auto jc) __attribute__((always_inline)) {
                 constexpr int J = decltype(jc)::value;
-                wait_vm<kLoads>();
+                if constexpr (NW == 4) wait_vm<2 * kLoads>();
+                else wait_vm<kLoads>();
                 stage_barrier();
                 const int vt = v + 1 < kblocks ? v + 1 : kblocks - 1;
-                issue_tok(vt, slot(IntC<J + 1>{}));
-                issue_w(v < kblocks ? v : kblocks - 1, wset(IntC<J>{}));
-                if (v >= 2 && v - 2 < kblocks) compute(v - 2, slot(IntC<J + 2>{}), wset(IntC<J + 1>{}));
+                const int vw = v + NW - 3 < kblocks ? v + NW - 3 : kblocks - 1;
+                const bool mult = v >= 2 && v - 2 < kblocks;
+                // Steps without a multiply issue their token loads here, the
+                // others inside compute().
+                if (!mult || !CAEE_P8_SPREAD) issue_tok(vt, slot(IntC<J + 1>{}));
+                issue_w(vw, wset(IntC<J + NW - 3>{}));
+                if (mult)
+                    compute(v - 2, slot(IntC<J + 2>{}), wset(IntC<J + NW - 2>{}), vt, slot(IntC<J + 1>{}), vw,
+                            wset(IntC<J + NW - 3>{}));
             };
             // Whole groups of three steps; the twelve-step body (lcm of the
             // ring and the register sets) is entered at the group the
             // remaining step count needs, so at most two steps past the
             // first one without a multiply are run.
+            if constexpr (NW == 4) {
+                // Four-step body (the ring and the register sets both cycle
+                // by four), left after any pair of steps.
+                const int nsteps = (kblocks + 2 + 1) / 2 * 2;
+#pragma clang loop unroll(disable)
+                for (int v = 0; v < nsteps; v += 4) {
+                    step(v, IntC<0>{});
+                    step(v + 1, IntC<1>{});
+                    if (v + 2 >= nsteps) break;
+                    step(v + 2, IntC<2>{});
+                    step(v + 3, IntC<3>{});
+                }
+            } else {
             const int nsteps = (kblocks + 2 + 2) / 3 * 3;
 #pragma clang loop unroll(disable)
             for (int v = 0; v < nsteps; v += 12) {
@@ -338,6 +423,7 @@ __global__ __launch_bounds__(kP8Threads) void k_prefill8(FfnParams p) {
                 step(v + 9, IntC<9>{});
                 step(v + 10, IntC<10>{});
                 step(v + 11, IntC<11>{});
+            }
             }
             wait_vm<0>();   // the re-reads past the last block have landed
             // Every wave is done with the ring before the epilogue reuses
@@ -393,6 +479,7 @@ __global__ __launch_bounds__(kP8Threads) void k_prefill8(FfnParams p) {
                 }
             }
         };
+#if CAEE_P8_EVEN
         switch ((nb + 1) >> 1) {
             case 1: run(IntC<2>{}); break;
             case 2: run(IntC<4>{}); break;
@@ -403,6 +490,26 @@ __global__ __launch_bounds__(kP8Threads) void k_prefill8(FfnParams p) {
             case 7: run(IntC<14>{}); break;
             default: run(IntC<16>{}); break;
         }
+#else
+        switch (nb) {
+            case 1: run(IntC<1>{}); break;
+            case 2: run(IntC<2>{}); break;
+            case 3: run(IntC<3>{}); break;
+            case 4: run(IntC<4>{}); break;
+            case 5: run(IntC<5>{}); break;
+            case 6: run(IntC<6>{}); break;
+            case 7: run(IntC<7>{}); break;
+            case 8: run(IntC<8>{}); break;
+            case 9: run(IntC<9>{}); break;
+            case 10: run(IntC<10>{}); break;
+            case 11: run(IntC<11>{}); break;
+            case 12: run(IntC<12>{}); break;
+            case 13: run(IntC<13>{}); break;
+            case 14: run(IntC<14>{}); break;
+            case 15: run(IntC<15>{}); break;
+            default: run(IntC<16>{}); break;
+        }
+#endif
     }
 #endif
 }
