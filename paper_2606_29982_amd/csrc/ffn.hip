@@ -356,8 +356,11 @@ __global__ __launch_bounds__(256) void k_pack(const u32x4_t* __restrict__ src, u
 
 // One thread per W output features of one token: 4, or 8 when the expert
 // output rows are bf16 (one 16-byte load per row).  Slots are added in
-// order with fp32 fused multiply-adds, then the shared experts.
-template <int W>
+// order with fp32 fused multiply-adds, then the shared experts (expert
+// output rows are bf16 when W = 8, fp32 when W = 4).  The slot positions and
+// weights (up to KM slots) are all loaded first, then every row, so a thread
+// waits for two round trips to memory, not one per slot.
+template <int W, int KM>
 __global__ __launch_bounds__(256) void k_combine(FfnParams p) {
     const int per_tok = (p.d / W + 255) / 256;
     const int t = blockIdx.x / per_tok;
@@ -374,28 +377,39 @@ __global__ __launch_bounds__(256) void k_combine(FfnParams p) {
                 v[2 * i + 1] = __uint_as_float(u[i] & 0xFFFF0000u);
             }
         } else {
-            const float4 f = load_y4(p, (size_t)pos, c);
+            const float4 f = *(const float4*)((const float*)p.yperm + (size_t)pos * p.d + c);
             v[0] = f.x;
             v[1] = f.y;
             v[2] = f.z;
             v[3] = f.w;
         }
     };
-    float acc[W], v[W];
+    const int32_t* pp = p.perm_pos + (size_t)t * slots;
+    const float* pw = p.topk_w + (size_t)t * p.k;
+    int pos[KM];
+    float wt[KM];
+#pragma unroll
+    for (int j = 0; j < KM; ++j) {
+        pos[j] = j < p.k ? pp[j] : -1;
+        wt[j] = j < p.k ? pw[j] : 0.f;
+    }
+    // Every row load is issued (an empty slot reads row 0 and is not added).
+    float v[KM][W];
+#pragma unroll
+    for (int j = 0; j < KM; ++j) load(pos[j] >= 0 ? pos[j] : 0, v[j]);
+    float acc[W];
 #pragma unroll
     for (int i = 0; i < W; ++i) acc[i] = 0.f;
-    for (int j = 0; j < p.k; ++j) {
-        const int pos = p.perm_pos[t * slots + j];
-        if (pos < 0) continue;
-        const float w = p.topk_w[t * p.k + j];
-        load(pos, v);
 #pragma unroll
-        for (int i = 0; i < W; ++i) acc[i] = fmaf(w, v[i], acc[i]);
+    for (int j = 0; j < KM; ++j) {
+#pragma unroll
+        for (int i = 0; i < W; ++i) acc[i] = pos[j] >= 0 ? fmaf(wt[j], v[j][i], acc[i]) : acc[i];
     }
+    float vs[W];
     for (int s = 0; s < p.n_shared; ++s) {
-        load(p.perm_pos[t * slots + p.k + s], v);
+        load(pp[p.k + s], vs);
 #pragma unroll
-        for (int i = 0; i < W; ++i) acc[i] += v[i];
+        for (int i = 0; i < W; ++i) acc[i] += vs[i];
     }
     const size_t o = (size_t)t * p.d + c;
 #pragma unroll
@@ -497,8 +511,14 @@ hipError_t launch_pack(const void* src, void* dst, long long rows, long long row
 }
 
 hipError_t launch_combine(const FfnParams& p, hipStream_t s) {
-    if (p.y_half) hipLaunchKernelGGL(k_combine<8>, dim3(((p.d / 8 + 255) / 256) * p.T), dim3(256), 0, s, p);
-    else hipLaunchKernelGGL(k_combine<4>, dim3(((p.d / 4 + 255) / 256) * p.T), dim3(256), 0, s, p);
+    const dim3 g8(((p.d / 8 + 255) / 256) * p.T), g4(((p.d / 4 + 255) / 256) * p.T);
+    if (p.k <= 8) {
+        if (p.y_half) hipLaunchKernelGGL((k_combine<8, 8>), g8, dim3(256), 0, s, p);
+        else hipLaunchKernelGGL((k_combine<4, 8>), g4, dim3(256), 0, s, p);
+    } else {
+        if (p.y_half) hipLaunchKernelGGL((k_combine<8, kMaxK>), g8, dim3(256), 0, s, p);
+        else hipLaunchKernelGGL((k_combine<4, kMaxK>), g4, dim3(256), 0, s, p);
+    }
     return hipGetLastError();
 }
 
