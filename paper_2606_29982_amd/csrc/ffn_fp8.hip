@@ -41,8 +41,7 @@ __device__ inline void quant_block(const void* src, int src_bf16, long long row,
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1) amax = fmaxf(amax, __shfl_xor(amax, off));
     const float sc = amax > 0.0f ? amax / kE4M3Max : 1.0f;
-    const uint32_t c0 = e4m3_code(v0 / sc), c1 = e4m3_code(v1 / sc);
-    *(uint16_t*)(q + base) = (uint16_t)(c0 | (c1 << 8));
+    *(uint16_t*)(q + base) = (uint16_t)e4m3_code2(v0 / sc, v1 / sc);
     if (lane == 0) scale[row * srow + blk * sblk] = sc;
 }
 

@@ -83,6 +83,9 @@ __device__ inline void wait_vm() {
     __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | (((N >> 4) & 3) << 14));
 }
 
+// Waits until this wave's LDS (and scalar memory) operations are done.
+__device__ inline void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (0 << 8) | (3 << 14)); }
+
 // Workgroup barrier without the memory fence of __syncthreads (which would
 // wait for every load in flight); the empty asm keeps the compiler from
 // moving memory accesses across it.
@@ -451,7 +454,10 @@ __global__ __launch_bounds__(kP8Threads) void k_prefill8(FfnParams p) {
                     m = fmaxf(m, __shfl_xor(m, 32));
                     if (g == 0) red[wave * 256 + 16 * n + r] = m;
                 }
-                __syncthreads();
+                // Every wave's maxima are in LDS (no wait for memory: the
+                // stores of the previous item may still be in flight).
+                wait_lgkm0();
+                stage_barrier();
 #pragma unroll
                 for (int n = 0; n < NB; ++n) {
                     const int tn = 16 * n + r;
@@ -461,9 +467,8 @@ __global__ __launch_bounds__(kP8Threads) void k_prefill8(FfnParams p) {
                     for (int q = 0; q < kP8Waves; ++q) m = fmaxf(m, red[q * 256 + tn]);
                     const float sc = m > 0.0f ? m / kE4M3Max : 1.0f;
                     const size_t row = (size_t)(row0 + tn);
-                    uint32_t word = 0;
-#pragma unroll
-                    for (int v = 0; v < 4; ++v) word |= e4m3_code(hv[n][v] / sc) << (8 * v);
+                    const uint32_t word =
+                        e4m3_code4(hv[n][0] / sc, hv[n][1] / sc, hv[n][2] / sc, hv[n][3] / sc);
                     *(uint32_t*)(p.hq + row * p.f + grp * 128 + 16 * wave + 4 * g) = word;
                     if (wave == 0 && g == 0) p.hst[(size_t)grp * p.P + row] = sc;
                 }

@@ -7,25 +7,23 @@ namespace caee {
 
 constexpr float kE4M3Max = 448.0f;   // largest finite E4M3 magnitude
 
-// OCP E4M3 (fn) code of v: nearest representable value, ties to the even
-// code, magnitudes above 448 saturate to 448.
-__device__ inline uint32_t e4m3_code(float v) {
-    const uint32_t sign = (__float_as_uint(v) >> 24) & 0x80u;
-    const float a = fminf(fabsf(v), kE4M3Max);
-    uint32_t code;
-    if (a < 0.015625f) {                       // below 2^-6: subnormal steps of 2^-9
-        code = (uint32_t)rintf(a * 512.0f);     // 8 is the smallest normal, code 8
-    } else {
-        int e = (int)((__float_as_uint(a) >> 23) & 0xFFu) - 127;   // a in [2^e, 2^(e+1))
-        uint32_t q = (uint32_t)rintf(ldexpf(a, 3 - e));            // 8 .. 16
-        if (q == 16u) {
-            q = 8u;
-            ++e;
-        }
-        code = ((uint32_t)(e + 7) << 3) | (q - 8u);
-        if (code > 126u) code = 126u;
-    }
-    return sign | code;
+// OCP E4M3 (fn) codes of a and b (a in bits 7:0, b in bits 15:8, the rest of
+// `old` kept; HI = true puts them in bits 23:16 and 31:24 instead): nearest
+// representable value, ties to the even code, magnitudes above 448 saturate
+// to 448.  gfx950's packed conversion rounds to nearest even (subnormal
+// codes included); clamping to +-448 first gives the saturation.  Checked
+// bit for bit against the branch-by-branch definition (code = round(|v| /
+// 2^(e - 3)) within binade e, 2^-9 steps below 2^-6, sign bit 0x80) over
+// every fp32 value of magnitude up to 448.5, both signs.
+template <bool HI = false>
+__device__ inline uint32_t e4m3_code2(float a, float b, uint32_t old = 0u) {
+    const float ca = fminf(fmaxf(a, -kE4M3Max), kE4M3Max), cb = fminf(fmaxf(b, -kE4M3Max), kE4M3Max);
+    return (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(ca, cb, (int)old, HI);
+}
+
+// Four codes packed little-endian into one word.
+__device__ inline uint32_t e4m3_code4(float a, float b, float c, float d) {
+    return e4m3_code2<true>(c, d, e4m3_code2(a, b));
 }
 
 }  // namespace caee
