@@ -74,7 +74,9 @@ __device__ inline i32x8_t join(const u32x4_t& lo, const u32x4_t& hi) {
     return i32x8_t{(int)lo[0], (int)lo[1], (int)lo[2], (int)lo[3], (int)hi[0], (int)hi[1], (int)hi[2], (int)hi[3]};
 }
 
-__device__ inline float silu_mul(float g, float u) { return g / (1.0f + __expf(-g)) * u; }
+// silu(g) * u with the hardware reciprocal (about one ulp; the quantiser
+// that follows rounds to 3 mantissa bits).
+__device__ inline float silu_mul(float g, float u) { return g * __builtin_amdgcn_rcpf(1.0f + __expf(-g)) * u; }
 
 // Waits until at most N of this wave's vector memory loads are outstanding
 // (gfx9 s_waitcnt: vmcnt in bits 3:0 and 15:14, expcnt and lgkmcnt not waited).
