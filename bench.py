@@ -37,12 +37,33 @@ KERNEL_SOURCES = [os.path.join(ROOT, "paper_2606_29982_amd", "csrc", n)
                   for n in ("ffn.hip", "ffn_tile.h", "caee_internal.h")]
 
 
-def kernel_sources_sha256():
+# MFMA counters of the 8-bit prefill launches at T=4096, for the build of
+# these sources.
+MFMA_FILE = os.path.join(ROOT, "profiles", "prefill8_deepseek_r1_t4096_mfma.json")
+PREFILL_SOURCES = [os.path.join(ROOT, "paper_2606_29982_amd", "csrc", n)
+                   for n in ("ffn_prefill8.hip", "fp8_codec.h", "caee_internal.h")]
+
+
+def kernel_sources_sha256(paths=None):
     h = hashlib.sha256()
-    for path in KERNEL_SOURCES:
+    for path in paths or KERNEL_SOURCES:
         with open(path, "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()
+
+
+def mfma_counter_entry():
+    """MFMA busy share of the prefill launches (matrix-pipe busy cycles over
+    SIMD cycles) from a committed rocprofv3 counter run, or None when missing
+    or taken on a different kernel source."""
+    try:
+        with open(MFMA_FILE) as fh:
+            rec = json.load(fh)
+        if rec.get("sources_sha256") != kernel_sources_sha256(PREFILL_SOURCES):
+            return None
+        return {k: rec[k] for k in ("gate_up", "down")}
+    except (OSError, ValueError, KeyError):
+        return None
 
 
 def parse():
@@ -568,6 +589,9 @@ def main():
                              "hbm_frac": round(b / (m * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
                              "mfma_tflops": round(tflops, 1), "mfma_frac": round(tflops / FP8_PEAK_TFLOPS, 4),
                              "executed": s[5] + R1_FP8.n_shared, "pruned": s[4]})
+            if T == 4096:
+                # matrix-pipe busy share of the two prefill launches, from counters
+                fp8_rows[-1]["mfma_busy_counters"] = mfma_counter_entry()
             log(f"fp8 {fp8_rows[-1]}")
             del c
         result["fp8"] = fp8_rows

@@ -62,6 +62,14 @@ def test_e4m3_codes_match_oracle():
     rows[0, :128] = np.linspace(-448, 448, 128, dtype=np.float32)
     rows[1, :128] = 2.0 ** -np.arange(128, dtype=np.float32) * 0.5
     rows[2, :] = 0.0
+    # every tie of the codec: 448 (so the block scale is exactly 1) and the
+    # midpoint between each pair of consecutive codes, both signs; the
+    # midpoints have 5 significant bits, so the bf16 rows hold them exactly
+    from oracle import e4m3_decode as _dec
+    vals = _dec(np.arange(127, dtype=np.uint8))
+    ties = np.concatenate([[448.0], (vals[:-1] + vals[1:]) / 2, [vals[1] / 4]]).astype(np.float32)
+    rows[3, :128] = ties
+    rows[3, 128:] = -ties
     import synth_inputs
     bits = synth_inputs.bf16_bits_from_f32(rows)
     x = torch.from_numpy(bits.view(np.int16)).to(DEV).view(torch.bfloat16)
