@@ -157,7 +157,9 @@ def graph_protocol(case, warmup=10, iters=50, flush_mb=512):
         which evicts those dirty lines (written back before the timed call):
         the call starts from caches that hold neither its data nor dirty
         lines.
-    Returns the median and the 10th / 90th percentiles of both, in us."""
+    A third series runs the same flushed single calls eagerly (the layer's
+    launches issued one by one, no graph), the clean flush before each.
+    Returns the median and the 10th / 90th percentiles of all three, in us."""
     import torch
     case.step()
     torch.cuda.synchronize()
@@ -184,6 +186,18 @@ def graph_protocol(case, warmup=10, iters=50, flush_mb=512):
         res["us_p50" + key] = round(float(np.median(us)), 1)
         res["us_p10" + key] = round(float(np.percentile(us, 10)), 1)
         res["us_p90" + key] = round(float(np.percentile(us, 90)), 1)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(iters)]
+    for a, b in ev:
+        flush.fill_(1)
+        rd.sum()
+        a.record()
+        case.step()
+        b.record()
+    torch.cuda.synchronize()
+    us = np.array([a.elapsed_time(b) * 1e3 for a, b in ev])
+    res["us_p50_eager"] = round(float(np.median(us)), 1)
+    res["us_p10_eager"] = round(float(np.percentile(us, 10)), 1)
+    res["us_p90_eager"] = round(float(np.percentile(us, 90)), 1)
     del g, flush, rd
     return res
 
@@ -386,6 +400,7 @@ def run_case(args, dev):
         gp = graph_protocol(c)
         line["graph_protocol"] = gp
         line["weight_frac_flushed"] = round(b / (gp["us_p50"] * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4)
+        line["weight_frac_flushed_eager"] = round(b / (gp["us_p50_eager"] * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4)
     print(json.dumps(line), flush=True)
 
 
@@ -521,6 +536,7 @@ def main():
     gp = result["graph_protocol"]
     result["hbm_frac_flushed"] = round(b_layer / (gp["us_p50"] * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4)
     result["hbm_frac_flushed_write"] = round(b_layer / (gp["us_p50_write_flush"] * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4)
+    result["hbm_frac_flushed_eager"] = round(b_layer / (gp["us_p50_eager"] * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4)
     log(f"graph protocol {result['graph_protocol']}")
 
     link_model = None
@@ -562,6 +578,8 @@ def main():
                               "graph_write_flush_us_p50": gp["us_p50_write_flush"],
                               "hbm_frac_flushed_write": round(b / (gp["us_p50_write_flush"] * 1e-6) / 1e9
                                                               / HBM_PEAK_GBPS, 4),
+                              "eager_flushed_us_p50": gp["us_p50_eager"],
+                              "hbm_frac_flushed_eager": round(b / (gp["us_p50_eager"] * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),
                               "bin_loads_g": {"act": [round(v, 3) for v in loads[0]],
                                               "must": [round(v, 3) for v in loads[1]],
                                               "trans": [round(v, 3) for v in loads[2]]},
