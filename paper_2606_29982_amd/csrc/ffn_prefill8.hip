@@ -138,6 +138,12 @@ constexpr int kP8WSets(int nb) { return nb <= CAEE_P8_W4_MAX_NB ? 4 : 3; }
 #define CAEE_P8_SPREAD 1
 #endif
 
+// Workgroups of the launch per CU (one runs at a time: the ring takes most
+// of the LDS).
+#ifndef CAEE_P8_GRID_PER_CU
+#define CAEE_P8_GRID_PER_CU 2
+#endif
+
 // Token tiles an item is compiled for: its chunk's count rounded up to an
 // even number (1), or the count itself (0).
 #ifndef CAEE_P8_EVEN
@@ -571,7 +577,7 @@ hipError_t launch_prefill8(const FfnParams& p, bool gate_up, int max_chunks, hip
     // One workgroup per CU at a time (the ring takes most of the LDS); two
     // per CU in the grid, so that a CU whose items end early takes more.
     long long items = (long long)max_chunks * groups;
-    const long long cap = (long long)device_cu_count() * 2;
+    const long long cap = (long long)device_cu_count() * CAEE_P8_GRID_PER_CU;
     if (items > cap) items = cap;
     if (items < 1) items = 1;
     if (gate_up) ffn_launch(k_prefill8<true>, dim3((unsigned)items), dim3(kP8Threads), s, p);
