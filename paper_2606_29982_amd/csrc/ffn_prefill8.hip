@@ -7,10 +7,11 @@
 // one chunk over the whole contraction, one 128-deep block per pipeline
 // stage:
 //   * the chunk's token rows (and their block scales) go global -> LDS with
-//     direct-to-LDS buffer loads, in MFMA B-fragment order, three stages
-//     ahead of their multiply in a ring of four, issued among the multiplies
-//     of the stage before; every wave reads every token fragment of a stage
-//     from LDS;
+//     direct-to-LDS buffer loads, each load 8 whole 128-byte row blocks
+//     (16 half rows per load measured 5 % slower), three stages ahead of
+//     their multiply in a ring of four, issued among the multiplies of the
+//     stage before; every wave reads every token fragment of a stage from
+//     LDS;
 //   * each wave owns two 16-row weight tiles (32 rows), which nobody else
 //     reads: they go global -> registers, three stages ahead of their MFMAs
 //     (two for items of more than 12 token tiles, whose accumulators leave
@@ -65,8 +66,12 @@ constexpr int kXcds = 8;                  // accelerator complex dies, each with
 #define CAEE_P8_XCD 1
 #endif
 
+// One stage of the token ring: the chunk's rows' 128-byte blocks, row t at
+// f[t / 8][8 (t % 8) ..]: its 16-byte piece c in position c ^ (t % 8) (an
+// XOR swizzle, so that the 8 lanes of a fragment read that take one piece
+// each of 8 consecutive rows hit 8 different bank groups).
 struct P8Stage {
-    u32x4_t f[2 * kP8NT][kWave];          // token tile n, half h at [2n + h]: the B fragment of lane l
+    u32x4_t f[2 * kP8NT][kWave];
     float x[kP8Waves][kWave];             // row block scales: token n at [n / 32][n % 32]
 };
 
@@ -224,9 +229,9 @@ __global__ __launch_bounds__(kP8Threads) void k_prefill8(FfnParams p) {
         // count exactly.
         auto run = [&](auto nbc) __attribute__((always_inline)) {
             constexpr int NB = decltype(nbc)::value;
-            // Token fragments of a stage: 2 NB (tile n, half h at 2n + h),
-            // kTok per wave; fragments past 2 NB (when 8 kTok > 2 NB) read
-            // row 0 into stage slots nobody multiplies.
+            // Token loads of a stage: 2 NB of 8 rows each, kTok per wave;
+            // loads past 2 NB (when 8 kTok > 2 NB) read row 0 into stage
+            // slots nobody multiplies.
             constexpr int kTok = (2 * NB + kP8Waves - 1) / kP8Waves;
             constexpr int kLoads = kTok + 1 + 4;   // + row scales + two tiles x two halves of weights
             static_assert(kTok * kP8Waves <= 2 * kP8NT, "stage slots");
@@ -234,11 +239,15 @@ __global__ __launch_bounds__(kP8Threads) void k_prefill8(FfnParams p) {
 #pragma unroll
             for (int i = 0; i < kTok; ++i) {
                 const int j = kTok * wave + i;
-                int n = 16 * (j >> 1) + r;
+                int n = 8 * j + (lane >> 3);   // lane l: piece (l % 8) ^ (l / 8) of row 8j + l / 8
                 n = n < ntok ? n : 0;          // padded token columns read a valid row; results dropped
                 const uint32_t row = kGateUp ? (uint32_t)ffn_token(p, xs, row0 + n) : (uint32_t)(row0 + n);
-                toff[i] = (row * (uint32_t)row_units + (uint32_t)((j & 1) * 4 + g)) * 16u;
+                toff[i] = (row * (uint32_t)row_units + (uint32_t)((lane & 7) ^ (lane >> 3))) * 16u;
             }
+            // This lane's B fragment of token tile n: token 16n + r, pieces g
+            // and 4 + g of its block, at f[2n] + these offsets (16-byte units).
+            const int fo0 = (r >> 3) * kWave + (r & 7) * 8 + (g ^ (r & 7));
+            const int fo1 = (r >> 3) * kWave + (r & 7) * 8 + ((4 + g) ^ (r & 7));
 
             auto issue_tok = [&](int kb, P8Stage& s) __attribute__((always_inline)) {
 #pragma unroll
@@ -288,7 +297,8 @@ __global__ __launch_bounds__(kP8Threads) void k_prefill8(FfnParams p) {
                 const i32x8_t a0 = join(w.v[0][0], w.v[0][1]), a1 = join(w.v[1][0], w.v[1][1]);
                 const float wa = wsl[ws0][kb], wc = wsl[ws1][kb];
                 auto frag = [&](int n) __attribute__((always_inline)) {
-                    return join(s.f[2 * n][lane], s.f[2 * n + 1][lane]);
+                    const u32x4_t* b = &s.f[2 * n][0];
+                    return join(b[fo0], b[fo1]);
                 };
                 auto xsc = [&](int n) __attribute__((always_inline)) {
                     const int tok = 16 * n + r;
