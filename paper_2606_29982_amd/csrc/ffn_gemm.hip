@@ -54,8 +54,13 @@ constexpr int kFrags = 2 * (kTiles + kNT);
 constexpr int kLoads = kTiles / 4 + kNT / 4;   // fragment loads per wave and stage
 constexpr int kXcds = 8;              // accelerator complex dies, each with its own L2
 
+// One stage: [2 * tile + half] the weight fragments (lane order), then the
+// token rows' 128-byte blocks, row t at f[2 * kTiles + t / 8][8 (t % 8) ..],
+// its 16-byte piece c in position c ^ (t % 8) (an XOR swizzle: the 8 lanes of
+// a fragment read that take one piece each of 8 consecutive rows hit 8
+// different bank groups; each row load brings 8 whole blocks).
 struct GemmStage {
-    u32x4_t f[kFrags][kWave];         // [2 * tile + half] weights, then [2 * tiles + 2 * token tile + half] rows
+    u32x4_t f[kFrags][kWave];
 };
 
 __device__ inline float silu_mul(float g, float u) { return g / (1.0f + __expf(-g)) * u; }
@@ -138,11 +143,13 @@ __global__ __launch_bounds__(kGemmThreads) void k_gemm(FfnParams p) {
                 frag[i] = j;
                 stride[i] = 128;
             } else {
+                // Load j of the rows: 8 whole 128-byte blocks, lane l taking
+                // piece (l % 8) ^ (l / 8) of row 8j + l / 8 (see GemmStage).
                 const int j = (kLoads - na) * wave + i - na;
-                int n = 16 * (j >> 1) + r;
+                int n = 8 * j + (lane >> 3);
                 n = n < ntok ? n : 0;          // padded token columns read a valid row; results dropped
                 const int row = kGateUp ? ffn_token(p, xs, row0 + n) : row0 + n;
-                src[i] = (const u32x4_t*)(kGateUp ? p.x : p.h) + (size_t)row * row_units + (j & 1) * 4 + g;
+                src[i] = (const u32x4_t*)(kGateUp ? p.x : p.h) + (size_t)row * row_units + ((lane & 7) ^ (lane >> 3));
                 frag[i] = bbase + j;
                 stride[i] = 8;
             }
@@ -165,6 +172,10 @@ __global__ __launch_bounds__(kGemmThreads) void k_gemm(FfnParams p) {
 #pragma unroll
             for (int j = 0; j < kWaveNT; ++j) acc[i][j] = zero;
 
+        // This lane's B fragment of token tile n, half h: token 16n + r,
+        // piece 4h + g of its block, at f[bbase + 2n] + fo[h].
+        const int fo[2] = {(r >> 3) * kWave + (r & 7) * 8 + (g ^ (r & 7)),
+                           (r >> 3) * kWave + (r & 7) * 8 + ((4 + g) ^ (r & 7))};
         // Multiplies the stage's two 64-byte steps, two MFMAs deep.
         auto compute = [&](const GemmStage& s) __attribute__((always_inline)) {
 #pragma unroll
@@ -176,7 +187,7 @@ __global__ __launch_bounds__(kGemmThreads) void k_gemm(FfnParams p) {
                 for (int j = 0; j < kWaveNT; ++j) {
                     const int n = kWaveNT * wc + j;
                     if (n < nb) {
-                        const bf16x8_t bf = __builtin_bit_cast(bf16x8_t, s.f[bbase + 2 * n + h][lane]);
+                        const bf16x8_t bf = __builtin_bit_cast(bf16x8_t, (&s.f[bbase + 2 * n][0])[fo[h]]);
 #pragma unroll
                         for (int i = 0; i < 4; ++i)
                             acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bf, acc[i][j], 0, 0, 0);
