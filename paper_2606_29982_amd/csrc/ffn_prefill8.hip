@@ -27,12 +27,13 @@
 // all waves, and the multiplies of a stage are software-pipelined over the
 // token tiles (fragment reads two tiles ahead, scaling one tile behind).
 //
-// Work items: (chunk, weight group); gate/up groups are 128 features (the
-// gate and up rows of each; wave w takes feature tile w of both), down
-// groups 256 output rows (wave w takes tiles 2w, 2w + 1).  Gate/up ends in
+// Work items: (chunk, run of weight groups); gate/up groups are 128 features
+// (the gate and up rows of each; wave w takes feature tile w of both), down
+// groups 256 output rows (wave w takes tiles 2w, 2w + 1).  An item runs its
+// groups one after another through one pipeline.  Each gate/up group ends in
 // SwiGLU and quantises its 128 features per token (amax across the waves
 // through LDS) into e4m3 codes and a transposed block scale, the input of
-// the down product; down writes bf16 expert output rows.
+// the down product; each down group writes bf16 expert output rows.
 //
 // Per block: one scaled 16x16x128 MFMA (unit E8M0 scales) per (weight tile,
 // token tile), its partial sums times weight block scale x row block scale
@@ -136,6 +137,32 @@ constexpr int kP8Ahead(int nb) { return nb <= CAEE_P8_AHEAD_MAX_NB ? 2 : 1; }
 #endif
 constexpr int kP8WSets(int nb) { return nb <= CAEE_P8_W4_MAX_NB ? 4 : 3; }
 
+// Weight groups an item runs back to back over its chunk (gate/up, down).
+// The token ring and the weight stream carry on from one group into the
+// next, so only the item's first group waits for a filling pipeline, and a
+// group's epilogue runs while the next group's first blocks are in flight.
+// Contractions that are not a multiple of four blocks run one group per item.
+// Down (16-block contraction at d = 7168, f = 2048: short items) runs four;
+// gate/up one: with fewer items per chunk more chunks are in flight per XCD
+// and their token rows (7 KB each) no longer fit its L2 together (two groups:
+// gate/up 7 % slower; down with seven groups per item: uneven tail).
+#ifndef CAEE_P8_RUN_GU
+#define CAEE_P8_RUN_GU 1
+#endif
+#ifndef CAEE_P8_RUN_DN
+#define CAEE_P8_RUN_DN 4
+#endif
+constexpr int kP8MaxRun = 8;
+// Widest items (token tiles) whose groups run back to back; wider ones run
+// their groups one pipeline each (their accumulators leave no registers for
+// a group epilogue inside the stage loop).
+#ifndef CAEE_P8_RUN_MAX_NB
+#define CAEE_P8_RUN_MAX_NB 12
+#endif
+static_assert(CAEE_P8_RUN_GU >= 1 && CAEE_P8_RUN_GU <= kP8MaxRun && CAEE_P8_RUN_DN >= 1 &&
+                  CAEE_P8_RUN_DN <= kP8MaxRun,
+              "groups per item");
+
 // Token-row loads of a step issued among the multiplies of its tiles (1), or
 // all at once before them (0).  (Spreading the weight loads the same way
 // measured slower.)
@@ -162,7 +189,12 @@ __global__ __launch_bounds__(kP8Threads) void k_prefill8(FfnParams p) {
     // Four LDS objects, each named statically below, so that the compiler
     // can tell a read of one slot from the loads filling another.
     __shared__ P8Stage st0, st1, st2, st3;
-    __shared__ float wsl[2][kP8MaxKBlocks];   // weight block scales of the item's two 128-row scale rows
+    // Weight block scales of the item's groups: group q's two 128-row scale
+    // rows at wsl[2q], wsl[2q + 1].
+    constexpr int kRun = kGateUp ? CAEE_P8_RUN_GU : CAEE_P8_RUN_DN;
+    __shared__ float wsl[2 * kRun][kP8MaxKBlocks];
+    // Per-token maxima of the gate/up epilogue, [wave][token].
+    __shared__ float red[kGateUp ? kP8Waves * 256 : 1];
     const int tid = threadIdx.x, lane = tid & (kWave - 1);
     const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
     const int r = lane & 15, g = lane >> 4;
@@ -171,7 +203,14 @@ __global__ __launch_bounds__(kP8Threads) void k_prefill8(FfnParams p) {
     const size_t ksteps = (size_t)K / 64;          // 64-byte steps of a weight row (tiled layout)
     const size_t row_units = (size_t)K / 16;       // 16-byte pieces of a token row
     const int groups = kGateUp ? p.f / 128 : p.d / 256;
-    const int total = ffn_list_size(p) * groups;
+    // Groups per item (uniform): a run of up to G groups of one chunk.
+    const int G = kblocks % 4 == 0 ? kRun : 1;
+    const int runs = (groups + G - 1) / G;
+    const int total = ffn_list_size(p) * runs;
+    // Weight tiles from one group to the next (gate/up: 8 feature tiles of
+    // the gate rows and of the up rows; down: 16 row tiles), in 16-byte units
+    // (a run of groups spans less than 2^32 of them: K < 2^16).
+    const uint32_t gstride = (uint32_t)(kGateUp ? 8 : 16) * (uint32_t)ksteps * 64u;
     const size_t expert_bytes = kGateUp ? (size_t)2 * p.f * p.d : (size_t)p.d * p.f;
     const size_t scales_per_expert = (size_t)((kGateUp ? 2 * p.f : p.d) / 128) * kblocks;
     const f32x4_t zero = {0.f, 0.f, 0.f, 0.f};
@@ -185,15 +224,16 @@ __global__ __launch_bounds__(kP8Threads) void k_prefill8(FfnParams p) {
         __builtin_amdgcn_make_buffer_rsrc((void*)(kGateUp ? p.xst : p.hst), 0, (int)sbytes, kBufWord3);
 
     // Item order: plain (workgroup b takes items b, b + grid, ...), or by
-    // XCD (XCD x takes the chunks x, x + 8, ..., all groups of each, its
+    // XCD (XCD x takes the chunks x, x + 8, ..., all group runs of each, its
     // workgroups striding through that list).
     const bool by_xcd = CAEE_P8_XCD && gridDim.x % kXcds == 0;
     const int xcd = blockIdx.x % kXcds;
-    const int n_local = by_xcd ? (ffn_list_size(p) - xcd + kXcds - 1) / kXcds * groups : total;
+    const int n_local = by_xcd ? (ffn_list_size(p) - xcd + kXcds - 1) / kXcds * runs : total;
     for (int it = by_xcd ? blockIdx.x / kXcds : blockIdx.x; it < n_local;
          it += by_xcd ? gridDim.x / kXcds : gridDim.x) {
-        const int c = by_xcd ? xcd + kXcds * (it / groups) : it / groups;
-        const int grp = it % groups;
+        const int c = by_xcd ? xcd + kXcds * (it / runs) : it / runs;
+        const int g0 = (it % runs) * G;                 // the item's first group
+        const int gn = groups - g0 < G ? groups - g0 : G;
         const ChunkRef ck = ffn_chunk(p, c);
         const int xs = ck.xs;
         if (ffn_skip(p, xs)) continue;   // uniform over the workgroup
@@ -201,11 +241,10 @@ __global__ __launch_bounds__(kP8Threads) void k_prefill8(FfnParams p) {
         const int nb = (ntok + 15) >> 4;
         const u32x4_t* wb = (const u32x4_t*)ffn_weights(p, xs, !kGateUp, expert_bytes);
         const float* wsc = ffn_scales(p, xs, !kGateUp, scales_per_expert);
-        // This wave's weight tiles and the scale rows they fall in.
-        const int t0 = kGateUp ? grp * 8 + wave : grp * 16 + 2 * wave;
-        const int t1 = kGateUp ? p.f / 16 + grp * 8 + wave : t0 + 1;
-        const int srow0 = kGateUp ? grp : 2 * grp;                 // wsl[0]
-        const int srow1 = kGateUp ? p.f / 128 + grp : 2 * grp + 1; // wsl[1]
+        // This wave's weight tiles in the first group (group q's are gstride
+        // further) and which of a group's two scale rows they fall in.
+        const int t0 = kGateUp ? g0 * 8 + wave : g0 * 16 + 2 * wave;
+        const int t1 = kGateUp ? p.f / 16 + g0 * 8 + wave : t0 + 1;
         const int ws0 = kGateUp ? 0 : (wave >= 4 ? 1 : 0), ws1 = kGateUp ? 1 : ws0;
         const u32x4_t* wsrc[2] = {wb + (size_t)t0 * ksteps * 64 + lane, wb + (size_t)t1 * ksteps * 64 + lane};
         // Row scales, transposed and in permuted row order ([block][row]):
@@ -217,16 +256,18 @@ __global__ __launch_bounds__(kP8Threads) void k_prefill8(FfnParams p) {
         // compiler counts apart from the LDS reads of the multiply.
         const uint32_t xoff = (uint32_t)(row0 + xn) * 4u;
 
-        for (int q = tid; q < 2 * kblocks; q += kP8Threads) {
-            const int h = q >= kblocks, kb = q - h * kblocks;
-            wsl[h][kb] = wsc[(size_t)(h ? srow1 : srow0) * kblocks + kb];
+        for (int q = tid; q < 2 * gn * kblocks; q += kP8Threads) {
+            const int h = q / kblocks, kb = q - h * kblocks;   // group h / 2, its scale row h % 2
+            const int gq = g0 + (h >> 1);
+            const int srow = kGateUp ? ((h & 1) ? p.f / 128 + gq : gq) : 2 * gq + (h & 1);
+            wsl[h][kb] = wsc[(size_t)srow * kblocks + kb];
         }
         __syncthreads();
 
-        // The item for NB token tiles (the chunk's tile count rounded up to
-        // an even number): loads, multiplies and waits are all fixed by NB,
-        // so each stage is straight-line code whose waits the compiler can
-        // count exactly.
+        // The item for NB token tiles (the chunk's tile count, or that count
+        // rounded up to an even number): loads, multiplies and waits are all
+        // fixed by NB, so each stage is straight-line code whose waits the
+        // compiler can count exactly.
         auto run = [&](auto nbc) __attribute__((always_inline)) {
             constexpr int NB = decltype(nbc)::value;
             // Token loads of a stage: 2 NB of 8 rows each, kTok per wave;
@@ -256,19 +297,16 @@ __global__ __launch_bounds__(kP8Threads) void k_prefill8(FfnParams p) {
                                                              kb * 128, 0, 0);
                 __builtin_amdgcn_raw_ptr_buffer_load_lds(sbuf, (lds_void_t*)&s.x[wave][0], 4, xoff, kb * p.P * 4, 0, 0);
             };
-            auto issue_w = [&](int kb, WReg& w) __attribute__((always_inline)) {
+            // Weights of a block at offset wo (16-byte units) from each tile's start.
+            auto issue_w = [&](uint32_t wo, WReg& w) __attribute__((always_inline)) {
 #pragma unroll
                 for (int t = 0; t < 2; ++t)
 #pragma unroll
                     for (int h = 0; h < 2; ++h)
-                        w.v[t][h] = __builtin_nontemporal_load((g_u32x4_t*)(wsrc[t] + (size_t)(2 * kb + h) * 64));
+                        w.v[t][h] = __builtin_nontemporal_load((g_u32x4_t*)(wsrc[t] + (wo + (uint32_t)h * 64u)));
             };
 
             f32x4_t acc[2][NB];
-#pragma unroll
-            for (int t = 0; t < 2; ++t)
-#pragma unroll
-                for (int n = 0; n < NB; ++n) acc[t][n] = zero;
 
             // One stage: per token tile two MFMAs (one per weight tile) on its
             // fragment.  Software-pipelined over the tiles: while tile n's
@@ -279,7 +317,7 @@ __global__ __launch_bounds__(kP8Threads) void k_prefill8(FfnParams p) {
             // Load k of a step (kTok token fragments, the row scales, then the
             // four weight pieces): compute() can spread the token loads over
             // its tiles.
-            auto issue_one = [&](auto kc, int vt, P8Stage& st, int vw, WReg& w) __attribute__((always_inline)) {
+            auto issue_one = [&](auto kc, int vt, P8Stage& st, uint32_t vw, WReg& w) __attribute__((always_inline)) {
                 constexpr int k = decltype(kc)::value;
                 if constexpr (k < kTok) {
                     __builtin_amdgcn_raw_ptr_buffer_load_lds(tbuf, (lds_void_t*)&st.f[kTok * wave + k][0], 16, toff[k],
@@ -289,13 +327,13 @@ __global__ __launch_bounds__(kP8Threads) void k_prefill8(FfnParams p) {
                                                              0);
                 } else {
                     constexpr int q = k - kTok - 1, t = q >> 1, h = q & 1;
-                    w.v[t][h] = __builtin_nontemporal_load((g_u32x4_t*)(wsrc[t] + (size_t)(2 * vw + h) * 64));
+                    w.v[t][h] = __builtin_nontemporal_load((g_u32x4_t*)(wsrc[t] + (vw + (uint32_t)h * 64u)));
                 }
             };
-            auto compute = [&](int kb, const P8Stage& s, const WReg& w, int vt, P8Stage& st, int vw,
+            auto compute = [&](int q, int kb, const P8Stage& s, const WReg& w, int vt, P8Stage& st, uint32_t vw,
                                WReg& wn) __attribute__((always_inline)) {
                 const i32x8_t a0 = join(w.v[0][0], w.v[0][1]), a1 = join(w.v[1][0], w.v[1][1]);
-                const float wa = wsl[ws0][kb], wc = wsl[ws1][kb];
+                const float wa = wsl[2 * q + ws0][kb], wc = wsl[2 * q + ws1][kb];
                 auto frag = [&](int n) __attribute__((always_inline)) {
                     const u32x4_t* b = &s.f[2 * n][0];
                     return join(b[fo0], b[fo1]);
@@ -355,6 +393,93 @@ __global__ __launch_bounds__(kP8Threads) void k_prefill8(FfnParams p) {
                 acc[1][NB - 1] += pp1 * ps1;
             };
 
+            // Group outputs: the SwiGLU rows of group q (gate/up, quantised)
+            // or its expert output rows (down) from the accumulators.
+            auto epilogue = [&](int q) __attribute__((always_inline)) {
+                if constexpr (kGateUp) {
+                    // Lane (r, g) holds features 16 * wave + 4g .. + 3 of the
+                    // group for token 16n + r.  Per token: amax over the
+                    // group's 128 SwiGLU values (this lane's 4, the 4 lanes of
+                    // the column, the 8 waves through LDS), scale = amax / 448
+                    // (1 if zero), codes of value / scale: the activation
+                    // quantiser's arithmetic.  The SwiGLU values replace the
+                    // gate sums in place.
+                    const int grp = g0 + q;
+#pragma unroll
+                    for (int n = 0; n < NB; ++n) {
+                        float m = 0.0f;
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            acc[0][n][e] = silu_mul(acc[0][n][e], acc[1][n][e]);
+                            m = fmaxf(m, fabsf(acc[0][n][e]));
+                        }
+                        m = fmaxf(m, __shfl_xor(m, 16));
+                        m = fmaxf(m, __shfl_xor(m, 32));
+                        if (g == 0) red[wave * 256 + 16 * n + r] = m;
+                    }
+                    // Every wave's maxima are in LDS (no wait for memory: the
+                    // loads of the stages ahead and earlier stores stay in flight).
+                    wait_lgkm0();
+                    stage_barrier();
+#pragma unroll
+                    for (int n = 0; n < NB; ++n) {
+                        int tn = 16 * n + r;
+                        asm volatile("" : "+v"(tn));   // keeps the row arithmetic here, out of the stage loop
+                        if (n >= nb || tn >= ntok) continue;
+                        float m = 0.0f;
+#pragma unroll
+                        for (int w = 0; w < kP8Waves; ++w) m = fmaxf(m, red[w * 256 + tn]);
+                        const float sc = m > 0.0f ? m / kE4M3Max : 1.0f;
+                        const size_t row = (size_t)(row0 + tn);
+                        const uint32_t word = e4m3_code4(acc[0][n][0] / sc, acc[0][n][1] / sc, acc[0][n][2] / sc,
+                                                         acc[0][n][3] / sc);
+                        *(uint32_t*)(p.hq + row * p.f + grp * 128 + 16 * wave + 4 * g) = word;
+                        if (wave == 0 && g == 0) p.hst[(size_t)grp * p.P + row] = sc;
+                    }
+                } else {
+#pragma unroll
+                    for (int n = 0; n < NB; ++n) {
+                        int tn = 16 * n + r;
+                        asm volatile("" : "+v"(tn));   // keeps the row arithmetic here, out of the stage loop
+                        if (n >= nb || tn >= ntok) continue;
+#pragma unroll
+                        for (int t = 0; t < 2; ++t)
+                            store_y4(p, (size_t)(row0 + tn), (t ? t1 : t0) * 16 + 256 * q + 4 * g, acc[t][n][0],
+                                     acc[t][n][1], acc[t][n][2], acc[t][n][3]);
+                    }
+                }
+            };
+
+            // One pipeline over groups qbase .. qbase + qn - 1 of the item: its
+            // blocks u = 0 .. qn kblocks - 1 run group after group (block kb
+            // of group qbase + q is u = q kblocks + kb), the token ring cycling
+            // through the chunk's blocks once per group and the weights moving
+            // on to the group's tiles.  Items wider than the chained limit run
+            // one pipeline per group (qn = 1).
+            constexpr bool kChain = kRun > 1 && NB <= CAEE_P8_RUN_MAX_NB;
+            auto pipeline = [&](int qbase, int qn) __attribute__((always_inline)) {
+#pragma unroll
+            for (int t = 0; t < 2; ++t)
+#pragma unroll
+                for (int n = 0; n < NB; ++n) acc[t][n] = zero;
+            const int nblk = qn * kblocks;
+            auto split = [&](int u, int& q, int& kb) __attribute__((always_inline)) {
+                if constexpr (kChain) {
+                    q = 0;
+                    kb = u;
+#pragma unroll
+                    for (int i = 1; i < kRun; ++i)
+                        if (kb >= kblocks) {
+                            kb -= kblocks;
+                            ++q;
+                        }
+                } else {
+                    q = 0;
+                    kb = u;
+                }
+                q += qbase;
+            };
+
             // Token rows go three blocks ahead of their multiply (ring of
             // four), weights three (four register sets) or two (three sets):
             // step v issues the tokens of block v + 1 and the weights of
@@ -364,13 +489,11 @@ __global__ __launch_bounds__(kP8Threads) void k_prefill8(FfnParams p) {
             // v - 2 have landed: loads complete in order)
             // and passes a barrier that publishes every wave's token loads of
             // block v - 2 and guarantees that all waves are done with block
-            // v - 3, whose ring slot the tokens of v + 1 refill.  The steps run
-            // in whole groups (of two, or of three), so every step issues its loads
-            // unconditionally (steps past the last block re-read it, from L2,
-            // into a slot nobody multiplies) and the compiler's wait analysis
-            // sees the same loads per step on every path: the only waits in
-            // the loop are the kernel's own.  One code path for every step, so
-            // the accumulators live in one set of registers throughout.
+            // v - 3, whose ring slot the tokens of v + 1 refill.  Every step
+            // issues the same loads (steps past the last block re-read it,
+            // from L2, into a slot nobody multiplies), so the waits are
+            // constants (a group epilogue's stores only make them stricter),
+            // and the accumulators live in one set of registers throughout.
             constexpr int NW = kP8WSets(NB);
             WReg w0, w1, w2, w3;
             auto slot = [&](auto jc) -> P8Stage& {
@@ -387,119 +510,90 @@ __global__ __launch_bounds__(kP8Threads) void k_prefill8(FfnParams p) {
                 else if constexpr (J == 2) return w2;
                 else return w3;
             };
-            issue_tok(0, st0);
-            if constexpr (NW == 4) issue_w(0, w0);
-            // Step v = 12 m + J, or 4 m + J with four weight sets (J static:
-            // slot and register set are named).  With four sets step v
-            // loads the weights of block v + 1 and waits for the loads of
-            // step v - 3 (the tokens and weights of block v - 2).
-            auto step = [&](int v, auto jc) __attribute__((always_inline)) {
+            // Step v (J = v mod 12 static: slot and register set are named)
+            // issues the loads of block v + 1 (tokens) and v + NW - 3
+            // (weights) and, if kMult, multiplies block v - 2.  With four
+            // sets it waits for the loads of step v - 3 (the tokens and
+            // weights of block v - 2).
+            auto step = [&](int v, auto jc, auto mc) __attribute__((always_inline)) {
                 constexpr int J = decltype(jc)::value;
+                constexpr bool kMult = decltype(mc)::value;
                 if constexpr (NW == 4) wait_vm<2 * kLoads>();
                 else wait_vm<kLoads>();
                 stage_barrier();
-                const int vt = v + 1 < kblocks ? v + 1 : kblocks - 1;
-                const int vw = v + NW - 3 < kblocks ? v + NW - 3 : kblocks - 1;
-                const bool mult = v >= 2 && v - 2 < kblocks;
+                // A group other than the item's last ended with the previous
+                // step's multiply (block v - 3): its outputs leave the
+                // accumulators here, before this step's loads, while the
+                // loads of the next blocks are in flight.  (With kblocks a
+                // multiple of four that step is always v = 4 m + 2.)
+                if constexpr (kChain && kMult && (J & 3) == 2) {
+                    const int ub = v - 2;
+                    int qe, ke;
+                    split(ub, qe, ke);
+                    if (ke == 0 && qe > qbase) {
+                        epilogue(qe - 1);
+#pragma unroll
+                        for (int t = 0; t < 2; ++t)
+#pragma unroll
+                            for (int n = 0; n < NB; ++n) acc[t][n] = zero;
+                    }
+                }
+                const int ut = v + 1 < nblk ? v + 1 : nblk - 1;
+                const int uw = v + NW - 3 < nblk ? v + NW - 3 : nblk - 1;
+                int qt, vt, qw, kw;
+                split(ut, qt, vt);
+                split(uw, qw, kw);
+                const uint32_t vw = (uint32_t)qw * gstride + (uint32_t)kw * 128u;   // this step's weight block
+                (void)qt;
                 // Steps without a multiply issue their token loads here, the
                 // others inside compute().
-                if (!mult || !CAEE_P8_SPREAD) issue_tok(vt, slot(IntC<J + 1>{}));
+                if constexpr (!kMult || !CAEE_P8_SPREAD) issue_tok(vt, slot(IntC<J + 1>{}));
                 issue_w(vw, wset(IntC<J + NW - 3>{}));
-                if (mult)
-                    compute(v - 2, slot(IntC<J + 2>{}), wset(IntC<J + NW - 2>{}), vt, slot(IntC<J + 1>{}), vw,
+                if constexpr (kMult) {
+                    int qm, km;
+                    split(v - 2, qm, km);
+                    compute(qm, km, slot(IntC<J + 2>{}), wset(IntC<J + NW - 2>{}), vt, slot(IntC<J + 1>{}), vw,
                             wset(IntC<J + NW - 3>{}));
+                }
             };
-            // Whole groups of three steps; the twelve-step body (lcm of the
-            // ring and the register sets) is entered at the group the
-            // remaining step count needs, so at most two steps past the
-            // first one without a multiply are run.
-            if constexpr (NW == 4) {
-                // Four-step body (the ring and the register sets both cycle
-                // by four), left after any pair of steps.
-                const int nsteps = (kblocks + 2 + 1) / 2 * 2;
+            // Steps 0 and 1 only load; steps 2 .. nblk + 1 multiply blocks
+            // 0 .. nblk - 1: a loop over whole bodies of L steps (the lcm of
+            // the ring and the register sets), then the remaining steps one
+            // after another.  The loop body has a single path, so the
+            // compiler's count of the loads between a register load and its
+            // use is the real one and it adds no waits of its own.
+            constexpr int L = NW == 4 ? 4 : 12;
+            const int vend = nblk + 2;
+            issue_tok(0, st0);
+            if constexpr (NW == 4) issue_w((uint32_t)qbase * gstride, w0);
+            step(0, IntC<0>{}, std::false_type{});
+            step(1, IntC<1>{}, std::false_type{});
+            int v = 2;
 #pragma clang loop unroll(disable)
-                for (int v = 0; v < nsteps; v += 4) {
-                    step(v, IntC<0>{});
-                    step(v + 1, IntC<1>{});
-                    if (v + 2 >= nsteps) break;
-                    step(v + 2, IntC<2>{});
-                    step(v + 3, IntC<3>{});
-                }
-            } else {
-            const int nsteps = (kblocks + 2 + 2) / 3 * 3;
-#pragma clang loop unroll(disable)
-            for (int v = 0; v < nsteps; v += 12) {
-                step(v, IntC<0>{});
-                step(v + 1, IntC<1>{});
-                step(v + 2, IntC<2>{});
-                if (v + 3 >= nsteps) break;
-                step(v + 3, IntC<3>{});
-                step(v + 4, IntC<4>{});
-                step(v + 5, IntC<5>{});
-                if (v + 6 >= nsteps) break;
-                step(v + 6, IntC<6>{});
-                step(v + 7, IntC<7>{});
-                step(v + 8, IntC<8>{});
-                if (v + 9 >= nsteps) break;
-                step(v + 9, IntC<9>{});
-                step(v + 10, IntC<10>{});
-                step(v + 11, IntC<11>{});
-            }
-            }
-            wait_vm<0>();   // the re-reads past the last block have landed
-            // Every wave is done with the ring before the epilogue reuses
-            // st0 and the next item refills it.
-            stage_barrier();
-
-            if constexpr (kGateUp) {
-                // Lane (r, g) holds features 16 * wave + 4g .. + 3 of the group
-                // for token 16n + r.  Per token: amax over the group's 128
-                // SwiGLU values (this lane's 4, the 4 lanes of the column, the
-                // 8 waves through LDS), scale = amax / 448 (1 if zero), codes
-                // of value / scale: the activation quantiser's arithmetic.
-                float* red = reinterpret_cast<float*>(&st0);   // [wave][256 tokens]; the ring is idle
-                static_assert(sizeof(P8Stage) >= kP8Waves * 256 * sizeof(float), "epilogue buffer");
-                float hv[NB][4];
-#pragma unroll
-                for (int n = 0; n < NB; ++n) {
-                    float m = 0.0f;
-#pragma unroll
-                    for (int v = 0; v < 4; ++v) {
-                        hv[n][v] = silu_mul(acc[0][n][v], acc[1][n][v]);
-                        m = fmaxf(m, fabsf(hv[n][v]));
+            for (; v + L <= vend; v += L)
+                static_for<0, L>([&](auto ic) __attribute__((always_inline)) {
+                    constexpr int i = decltype(ic)::value;
+                    step(v + i, IntC<2 + i>{}, std::true_type{});
+                });
+            auto tail = [&](auto self, auto ic) __attribute__((always_inline)) {
+                constexpr int i = decltype(ic)::value;
+                if constexpr (i + 1 < L) {
+                    if (v + i < vend) {
+                        step(v + i, IntC<2 + i>{}, std::true_type{});
+                        self(self, IntC<i + 1>{});
                     }
-                    m = fmaxf(m, __shfl_xor(m, 16));
-                    m = fmaxf(m, __shfl_xor(m, 32));
-                    if (g == 0) red[wave * 256 + 16 * n + r] = m;
                 }
-                // Every wave's maxima are in LDS (no wait for memory: the
-                // stores of the previous item may still be in flight).
-                wait_lgkm0();
-                stage_barrier();
-#pragma unroll
-                for (int n = 0; n < NB; ++n) {
-                    const int tn = 16 * n + r;
-                    if (n >= nb || tn >= ntok) continue;
-                    float m = 0.0f;
-#pragma unroll
-                    for (int q = 0; q < kP8Waves; ++q) m = fmaxf(m, red[q * 256 + tn]);
-                    const float sc = m > 0.0f ? m / kE4M3Max : 1.0f;
-                    const size_t row = (size_t)(row0 + tn);
-                    const uint32_t word =
-                        e4m3_code4(hv[n][0] / sc, hv[n][1] / sc, hv[n][2] / sc, hv[n][3] / sc);
-                    *(uint32_t*)(p.hq + row * p.f + grp * 128 + 16 * wave + 4 * g) = word;
-                    if (wave == 0 && g == 0) p.hst[(size_t)grp * p.P + row] = sc;
-                }
+            };
+            tail(tail, IntC<0>{});
+            wait_vm<0>();   // the re-reads past the last block have landed
+            // Every wave is done with the ring before the next pipeline refills it.
+            stage_barrier();
+            epilogue(qbase + qn - 1);
+            };
+            if constexpr (kChain) {
+                pipeline(0, gn);
             } else {
-#pragma unroll
-                for (int n = 0; n < NB; ++n) {
-                    const int tn = 16 * n + r;
-                    if (n >= nb || tn >= ntok) continue;
-#pragma unroll
-                    for (int t = 0; t < 2; ++t)
-                        store_y4(p, (size_t)(row0 + tn), (t ? t1 : t0) * 16 + 4 * g, acc[t][n][0], acc[t][n][1],
-                                 acc[t][n][2], acc[t][n][3]);
-                }
+                for (int q = 0; q < gn; ++q) pipeline(q, 1);
             }
         };
 #if CAEE_P8_EVEN

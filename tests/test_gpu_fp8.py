@@ -15,8 +15,7 @@ DEV = torch.device("cuda:0")
 TINY_FP8 = TINY_F32.with_(name="tiny-fp8", w_dtype="fp8", x_dtype="bf16", y_dtype="bf16")
 
 
-def _tiny(seed, tau, n_bins, T=None, rule="max", tiled=False, zipf=None):
-    shape = TINY_FP8
+def _tiny(seed, tau, n_bins, T=None, rule="max", tiled=False, zipf=None, shape=TINY_FP8):
     inp = make_routing_inputs(shape, seed=seed, T=T, n_bins=n_bins, zipf_logit_s=zipf)
     W = make_expert_weights_np(shape, seed=seed)
     Wd = w_to_dev(W, DEV)
@@ -46,6 +45,20 @@ def test_tiny_fp8(seed, tiled):
 @pytest.mark.parametrize("T", [1, 5, 20, 40, 70, 130, 600, 1100])
 def test_tiny_fp8_batches(T):
     _tiny(7, 0.2, 4, T=T, tiled=True, zipf=1.1 if T > 100 else None)
+
+
+# d = f = 1024: both contractions are multiples of four 128-deep blocks, so
+# the prefill kernel runs several weight groups of a chunk back to back in
+# one item (8 gate/up groups of 128 features, 4 down groups of 256 rows).
+# 400 tokens: routed chunks of about 100 rows (7 token tiles) and the shared
+# expert's 400 rows in two chunks of 200 (13 tiles); every output compared.
+MID_FP8 = TINY_FP8.with_(name="mid-fp8", d=1024, f=1024)
+
+
+@pytest.mark.parametrize("seed", [11, 12])
+def test_mid_fp8_prefill(seed):
+    rel = _tiny(seed, 0.1, 4, T=400, tiled=True, shape=MID_FP8)
+    print(f"  max|err|/max|ref| = {rel:.3e}")
 
 
 def test_tiny_fp8_sum_rule():
