@@ -482,14 +482,13 @@ __global__ __launch_bounds__(kP8Threads) void k_prefill8(FfnParams p) {
 
             // Token rows go three blocks ahead of their multiply (ring of
             // four), weights three (four register sets) or two (three sets):
-            // step v issues the tokens of block v + 1 and the weights of
-            // block v + 1 (or v), and multiplies block v - 2.  It first waits
-            // until at most the loads of the previous two steps (one step)
-            // are outstanding (so this wave's tokens and weights of block
-            // v - 2 have landed: loads complete in order)
-            // and passes a barrier that publishes every wave's token loads of
-            // block v - 2 and guarantees that all waves are done with block
-            // v - 3, whose ring slot the tokens of v + 1 refill.  Every step
+            // step v issues the weights of block v + 1 (or v), then waits
+            // until this wave's tokens and weights of block v - 2 have
+            // landed (loads complete in order, so a constant count of later
+            // loads may stay outstanding), passes a barrier that publishes
+            // every wave's token loads of block v - 2 and guarantees that all
+            // waves are done with block v - 3, whose ring slot the tokens of
+            // block v + 1 then refill, and multiplies block v - 2.  Every step
             // issues the same loads (steps past the last block re-read it,
             // from L2, into a slot nobody multiplies), so the waits are
             // constants (a group epilogue's stores only make them stricter),
@@ -518,8 +517,19 @@ __global__ __launch_bounds__(kP8Threads) void k_prefill8(FfnParams p) {
             auto step = [&](int v, auto jc, auto mc) __attribute__((always_inline)) {
                 constexpr int J = decltype(jc)::value;
                 constexpr bool kMult = decltype(mc)::value;
-                if constexpr (NW == 4) wait_vm<2 * kLoads>();
-                else wait_vm<kLoads>();
+                // The weights first: their register set last held block
+                // v - 3, which this wave multiplied in the previous step, so
+                // they need no barrier and are in flight during the wait.
+                const int uw = v + NW - 3 < nblk ? v + NW - 3 : nblk - 1;
+                int qw, kw;
+                split(uw, qw, kw);
+                const uint32_t vw = (uint32_t)qw * gstride + (uint32_t)kw * 128u;   // this step's weight block
+                issue_w(vw, wset(IntC<J + NW - 3>{}));
+                // Block v - 2's tokens and weights have landed once at most
+                // the loads issued after its weights are outstanding: its
+                // tokens, the next steps' loads and these weights.
+                if constexpr (NW == 4) wait_vm<2 * kLoads + 4>();
+                else wait_vm<2 * kLoads>();
                 stage_barrier();
                 // A group other than the item's last ended with the previous
                 // step's multiply (block v - 3): its outputs leave the
@@ -539,16 +549,12 @@ __global__ __launch_bounds__(kP8Threads) void k_prefill8(FfnParams p) {
                     }
                 }
                 const int ut = v + 1 < nblk ? v + 1 : nblk - 1;
-                const int uw = v + NW - 3 < nblk ? v + NW - 3 : nblk - 1;
-                int qt, vt, qw, kw;
+                int qt, vt;
                 split(ut, qt, vt);
-                split(uw, qw, kw);
-                const uint32_t vw = (uint32_t)qw * gstride + (uint32_t)kw * 128u;   // this step's weight block
                 (void)qt;
                 // Steps without a multiply issue their token loads here, the
                 // others inside compute().
                 if constexpr (!kMult || !CAEE_P8_SPREAD) issue_tok(vt, slot(IntC<J + 1>{}));
-                issue_w(vw, wset(IntC<J + NW - 3>{}));
                 if constexpr (kMult) {
                     int qm, km;
                     split(v - 2, qm, km);
