@@ -15,14 +15,15 @@
 //   * each wave owns two 16-row weight tiles (32 rows), which nobody else
 //     reads: they go global -> registers, three stages ahead of their MFMAs
 //     (two for items of more than 12 token tiles, whose accumulators leave
-//     room for three register sets only), and never pass through LDS.
+//     room for three register sets only), issued before the stage's wait,
+//     and never pass through LDS.
 // So a chunk of up to 256 rows (every routed expert of a 4096-token batch of
 // the DeepSeek-R1 layer) streams each of its weight bytes once, and the
 // bytes in flight per CU are the token ring's plus every wave's register
 // stages.  An item is compiled for its chunk's token-tile count (1 .. 16),
 // so every stage is straight-line code:
-// per stage a wave issues the same loads (its share of the token fragments,
-// one row-scale load, four weight pieces) and waits for its oldest stage
+// per stage a wave issues the same loads (four weight pieces, its share of
+// the token fragments, one row-scale load) and waits for its oldest stage
 // with a constant vmcnt, one barrier per stage publishes the ring's stage to
 // all waves, and the multiplies of a stage are software-pipelined over the
 // token tiles (fragment reads two tiles ahead, scaling one tile behind).
