@@ -50,15 +50,18 @@ def test_tiny_fp8_batches(T):
 # d = f = 1024: both contractions are multiples of four 128-deep blocks, so
 # the prefill kernel runs several weight groups of a chunk back to back in
 # one item (8 gate/up groups of 128 features, 4 down groups of 256 rows).
+# d = 1280: five down groups, so a chunk's last run of groups is shorter
+# (and gate/up's ten-block contraction runs one group per item).
 # 400 tokens: routed chunks of about 100 rows (7 token tiles) and the shared
 # expert's 400 rows in two chunks of 200 (13 tiles); every output compared.
 MID_FP8 = TINY_FP8.with_(name="mid-fp8", d=1024, f=1024)
+MID_FP8_5 = TINY_FP8.with_(name="mid-fp8-5", d=1280, f=1024)
 
 
-@pytest.mark.parametrize("seed", [11, 12])
-def test_mid_fp8_prefill(seed):
-    rel = _tiny(seed, 0.1, 4, T=400, tiled=True, shape=MID_FP8)
-    print(f"  max|err|/max|ref| = {rel:.3e}")
+@pytest.mark.parametrize("seed,shape", [(11, MID_FP8), (12, MID_FP8), (13, MID_FP8_5)])
+def test_mid_fp8_prefill(seed, shape):
+    rel = _tiny(seed, 0.1, 4, T=400, tiled=True, shape=shape)
+    print(f"  {shape.name}: max|err|/max|ref| = {rel:.3e}")
 
 
 def test_tiny_fp8_sum_rule():
