@@ -83,7 +83,7 @@ def parse():
                     help="time one configuration only, DTYPE:T[:skewed] (e.g. bf16:128:skewed, fp8:4096), "
                          "and print its line instead of the headline")
     ap.add_argument("--graph", action="store_true",
-                    help="with --case: also time single flushed graph replays (the survey's protocol) and print them")
+                    help="with --case: also time single graph replays after a cache flush, and print them")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="finish with one device-to-device copy of this many bytes (a known-size "
                          "reference for HBM traffic counters)")
