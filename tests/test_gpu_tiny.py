@@ -201,10 +201,11 @@ def test_deterministic_repeat():
     assert np.array_equal(a["y"], b["y"]) and np.array_equal(a["topk_w"], b["topk_w"])
 
 
-@pytest.mark.parametrize("T", [300, 1100])
+@pytest.mark.parametrize("T", [300, 1100, 1101])
 def test_large_batches(T):
     # the shared expert has T > 128 rows, so it spans several FFN chunks;
-    # 1100 tokens also takes the permutation path used above 1024 tokens
+    # 1100 tokens also takes the permutation path used above 1024 tokens,
+    # and an odd count leaves the combine's last pair of tokens with one
     _run(TINY_F32, seed=21, tau=0.1, n_bins=4, T=T)
 
 
